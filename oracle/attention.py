@@ -1,0 +1,87 @@
+"""fp64 decode attention over the dequantized D-Quant cache (oracle).
+
+TEST INFRASTRUCTURE ONLY -- see the package header.
+
+What the paper fixes
+--------------------
+* App. A: a key channel is reconstructed as k_hat_tj = s_t v_{m_tj} + o_t + mu_j
+  (mu: windowed channel mean), a value channel as s_t v_{m_tj} + o_t, where the
+  reconstruction level v_m of symbol m is m itself on the affine grid of
+  Eq. (affine_token).
+* Eq. (fold-key): q . k_hat_t = s_t sum_j q_j v_{m_tj} + o_t sum_j q_j
+  + sum_j q_j mu_j.
+* Eq. (fold-value): sum_t a_t v_hat_tj = sum_t (a_t s_t) v_{m_tj} + sum_t a_t o_t.
+
+Readings
+--------
+* A1 the reconstruction lives in the rotated basis; with the unnormalized
+  Sylvester H (H H^T = d I) the original-basis key is H k_hat / d, so the logit
+  is (H q) . k_hat / d and the output is H (sum_t a_t v_hat_t) / d.
+* A2 a query head i reads KV head floor(i / G) (GQA); the logit is
+  softmax_scale * q . k (softmax_scale = 1/sqrt(d) by default) and the softmax
+  runs over the first seq_len[b] tokens of sequence b.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+from . import hadamard
+
+
+def dequantize(sym, s16, o16, mean_hat=None, window=128):
+    """Rotated-basis reconstruction [..., T, d] in fp64."""
+    x = s16.astype(np.float64)[..., None] * sym.astype(np.float64) + o16.astype(np.float64)[..., None]
+    if mean_hat is not None:
+        x = x + np.repeat(mean_hat, window, axis=-2)[..., : x.shape[-2], :]
+    return x
+
+
+def attention_direct(q, k_rot, v_rot, seq_lens, gqa, softmax_scale):
+    """Textbook softmax(q K^T * scale) V in the original basis, fp64.
+
+    q [B, Hq, d] fp64; k_rot, v_rot [B, Hkv, T, d] rotated reconstructions.
+    """
+    B, Hq, d = q.shape
+    H = hadamard.sylvester(d).astype(np.float64)
+    k = k_rot @ H / d
+    v = v_rot @ H / d
+    out = np.zeros((B, Hq, d), dtype=np.float64)
+    for b in range(B):
+        T = int(seq_lens[b])
+        for i in range(Hq):
+            h = i // gqa
+            s = (k[b, h, :T] @ q[b, i]) * softmax_scale
+            s = s - s.max()
+            a = np.exp(s)
+            a = a / a.sum()
+            out[b, i] = a @ v[b, h, :T]
+    return out
+
+
+def attention_folded(q, k_sym, k_s, k_o, k_mean_hat, v_sym, v_s, v_o, seq_lens,
+                     gqa, softmax_scale, window=128):
+    """Eq. (fold-key) / Eq. (fold-value) evaluated directly on the symbols, fp64.
+
+    k_mean_hat [B, Hkv, T/W, d] or None.
+    """
+    B, Hq, d = q.shape
+    q_rot = hadamard.fwht(q)
+    out = np.zeros((B, Hq, d), dtype=np.float64)
+    for b in range(B):
+        T = int(seq_lens[b])
+        for i in range(Hq):
+            h = i // gqa
+            qr = q_rot[b, i]
+            dot = k_sym[b, h, :T].astype(np.float64) @ qr
+            logit = k_s[b, h, :T].astype(np.float64) * dot + k_o[b, h, :T].astype(np.float64) * qr.sum()
+            if k_mean_hat is not None:
+                logit = logit + np.repeat(k_mean_hat[b, h] @ qr, window)[:T]
+            s = logit * (softmax_scale / d)
+            s = s - s.max()
+            a = np.exp(s)
+            a = a / a.sum()
+            acc = (a * v_s[b, h, :T].astype(np.float64)) @ v_sym[b, h, :T].astype(np.float64)
+            acc = acc + (a * v_o[b, h, :T].astype(np.float64)).sum()
+            out[b, i] = hadamard.fwht(acc) / d
+    return out

@@ -1,0 +1,75 @@
+"""Pins for the oracle's fp64 attention (CPU only)."""
+
+import numpy as np
+import pytest
+import scipy.linalg
+import scipy.special
+
+from oracle import attention
+
+
+def _random_cache(rng, B, Hkv, T, d, M, window):
+    k_sym = rng.integers(0, M, size=(B, Hkv, T, d))
+    v_sym = rng.integers(0, M, size=(B, Hkv, T, d))
+    k_s = rng.uniform(0.1, 2, size=(B, Hkv, T)).astype(np.float16)
+    k_o = rng.normal(size=(B, Hkv, T)).astype(np.float16)
+    v_s = rng.uniform(0.1, 2, size=(B, Hkv, T)).astype(np.float16)
+    v_o = rng.normal(size=(B, Hkv, T)).astype(np.float16)
+    mean = rng.normal(size=(B, Hkv, -(-T // window), d))
+    return k_sym, k_s, k_o, mean, v_sym, v_s, v_o
+
+
+def test_brute_force_tiny():
+    """B = 1, Hq = 2, Hkv = 1, d = 8, T = 3 against softmax(q K^T / sqrt d) V
+    built by hand from an explicit Hadamard matrix."""
+    rng = np.random.default_rng(0)
+    d, T, M, W = 8, 3, 5, 4
+    k_sym, k_s, k_o, mean, v_sym, v_s, v_o = _random_cache(rng, 1, 1, T, d, M, W)
+    q = rng.normal(size=(1, 2, d))
+    H = scipy.linalg.hadamard(d).astype(float)
+    k_rot = k_s[0, 0].astype(float)[:, None] * k_sym[0, 0] + k_o[0, 0].astype(float)[:, None] + mean[0, 0, 0]
+    v_rot = v_s[0, 0].astype(float)[:, None] * v_sym[0, 0] + v_o[0, 0].astype(float)[:, None]
+    K = np.linalg.solve(H, k_rot.T).T      # undo the rotation by solving, not by H/d
+    V = np.linalg.solve(H, v_rot.T).T
+    ref = scipy.special.softmax(q[0] @ K.T / np.sqrt(d), axis=-1) @ V
+    out = attention.attention_folded(q, k_sym, k_s, k_o, mean, v_sym, v_s, v_o, [T], 2, 1 / np.sqrt(d), window=W)
+    assert np.max(np.abs(out[0] - ref)) < 1e-12
+    krot = attention.dequantize(k_sym, k_s, k_o, mean, window=W)
+    vrot = attention.dequantize(v_sym, v_s, v_o)
+    out2 = attention.attention_direct(q, krot, vrot, [T], 2, 1 / np.sqrt(d))
+    assert np.max(np.abs(out2[0] - ref)) < 1e-12
+
+
+@pytest.mark.parametrize("G", [1, 4, 8])
+def test_folded_equals_direct(G):
+    """Eq. (fold-key) and Eq. (fold-value) are identities of the dequantized
+    attention."""
+    rng = np.random.default_rng(G)
+    B, Hkv, T, d, M, W = 2, 2, 256, 32, 9, 128
+    k_sym, k_s, k_o, mean, v_sym, v_s, v_o = _random_cache(rng, B, Hkv, T, d, M, W)
+    q = rng.normal(size=(B, Hkv * G, d)) * 3
+    lens = [256, 130]
+    krot = attention.dequantize(k_sym, k_s, k_o, mean, window=W)
+    vrot = attention.dequantize(v_sym, v_s, v_o)
+    a = attention.attention_direct(q, krot, vrot, lens, G, 0.1)
+    b = attention.attention_folded(q, k_sym, k_s, k_o, mean, v_sym, v_s, v_o, lens, G, 0.1, window=W)
+    assert np.max(np.abs(a - b)) < 1e-11 * np.max(np.abs(a))
+
+
+def test_gqa_mapping_and_lengths():
+    rng = np.random.default_rng(4)
+    B, Hkv, T, d, M = 1, 2, 8, 8, 4
+    k_sym, k_s, k_o, _, v_sym, v_s, v_o = _random_cache(rng, B, Hkv, T, d, M, 8)
+    q = rng.normal(size=(B, 4, d))
+    out = attention.attention_folded(q, k_sym, k_s, k_o, None, v_sym, v_s, v_o, [5], 2, 0.3, window=8)
+    # heads 2, 3 use kv head 1: recompute with kv head 1 copied into slot 0
+    k2 = [a.copy() for a in (k_sym, k_s, k_o, v_sym, v_s, v_o)]
+    for a in k2:
+        a[:, 0] = a[:, 1]
+    out2 = attention.attention_folded(q[:, 2:], k2[0], k2[1], k2[2], None, k2[3], k2[4], k2[5], [5], 2, 0.3, window=8)
+    assert np.max(np.abs(out[:, 2:] - out2)) < 1e-13
+    # tokens past the length do not matter
+    k3 = k_sym.copy()
+    k3[..., 5:, :] = 0
+    out3 = attention.attention_folded(q, k3, k_s, k_o, None, v_sym, v_s, v_o, [5], 2, 0.3, window=8)
+    assert np.array_equal(out, out3)
