@@ -1,0 +1,176 @@
+/*
+ * dq.h -- C ABI of the D-Quant hot path on MI355X (gfx950).
+ *
+ * D-Quant (arXiv 2609.19880) stores each token's key or value vector as a
+ * fixed-size record: Hadamard rotation, (keys) windowed channel-mean removal,
+ * a token-wise min-max affine grid with M levels, a rate-constrained
+ * assignment ("drift") that makes the entropy-coded length fit the record,
+ * and rANS with a static table derived from standard-normal CDF mass
+ * (Sec. 4, Alg. 1).  Decode attention reads the records at fixed stride,
+ * rANS-decodes them (Alg. 2) and attends with the affine folded into the
+ * contractions (App. A, Eq. fold-key / fold-value).
+ *
+ * One stream is one (token, KV head): n = head_dim values.  A record of C
+ * bytes is laid out as
+ *     [scale fp16 LE][offset fp16 LE][rANS state u32 LE][renorm bytes, in the
+ *     order the decoder reads them][zero padding]
+ * so its rANS budget (Eq. budget) is B = 8 (C - 4) - 32 bits.  The rANS state
+ * lives in [2^23, 2^31) and is renormalized one byte at a time.
+ *
+ * Conventions for every call:
+ *  - Device pointers are plain device addresses on the device that was current
+ *    when the tables were built; the caller owns every device buffer.
+ *  - Work is enqueued on `stream` (a hipStream_t, NULL = the null stream) and
+ *    is asynchronous: no call synchronizes, and device-side errors are reported
+ *    through the caller's `status` word (see DQ_STATUS_*), readable once the
+ *    stream has finished.
+ *  - Host-side validation failures return an error code before anything is
+ *    enqueued.  No C++ exception crosses this interface.
+ *  - bf16 and fp16 values are passed as their 16-bit patterns.
+ */
+#ifndef DQ_H
+#define DQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define DQ_OK 0
+#define DQ_ERR_INVALID_ARG 1 /* a size, pointer or layout is out of range    */
+#define DQ_ERR_INFEASIBLE 2  /* n * min cost exceeds the budget (Tab. 2 "--") */
+#define DQ_ERR_HIP 3         /* a HIP runtime call or a launch failed          */
+#define DQ_ERR_WORKSPACE 4   /* the workspace is missing or too small          */
+
+/* Bits OR-ed into the caller's device status word. */
+#define DQ_STATUS_RANGE 1u    /* encode: non-finite input, or scale/offset/mean overflowed fp16 */
+#define DQ_STATUS_OVERFLOW 2u /* encode: a stream could not be fitted into its record          */
+#define DQ_STATUS_CORRUPT 4u  /* decode: a record did not end in state 2^23 inside its C bytes  */
+
+/* Fixed parameters of the format. */
+#define DQ_MEAN_WINDOW 128 /* tokens per key-mean window (windows start at token 0) */
+#define DQ_MAX_LEVELS 64
+
+/*
+ * Coding parameters of one tensor (keys or values).  The per-token bit budget
+ * is given as the record size: bits per element = 8 * record_bytes / head_dim
+ * (Sec. 4.2 Eq. budget; Sec. 4.4 lets keys and values differ).
+ */
+typedef struct dq_config {
+    int32_t head_dim;       /* n: values per stream, a power of 2 in 64..1024;
+                               encode takes n <= 256, decode attention n = 128 */
+    int32_t levels;         /* M: quantization levels, 2..64 (Eq. affine_token) */
+    int32_t precision_bits; /* p: rANS precision, 8..12 (Eq. rans)              */
+    int32_t record_bytes;   /* C: record size in bytes, 9..2n+8                 */
+    double alpha;           /* sharpening exponent, >= 1 (Sec. 4.4; paper 1.4)  */
+} dq_config;
+
+typedef struct dq_table_info {
+    int32_t record_bytes;   /* C                                                 */
+    int32_t feasible;       /* 1 if n * min_cost_q16 <= budget_q16               */
+    int32_t cheapest;       /* lowest-index symbol of minimum cost               */
+    int32_t reserved;
+    int64_t budget_q16;     /* B = (8 (C - 4) - 32) * 2^16                       */
+    int64_t min_cost_q16;   /* n * min_m R_m                                     */
+    double expected_max;    /* a_n = E[max of n standard normals]                */
+} dq_table_info;
+
+/* Opaque coding tables: host copy plus a device copy, immutable once built. */
+typedef struct dq_tables dq_tables;
+
+/*
+ * Builds the entropy model on the host only (no GPU needed):
+ * level probabilities from normal CDF mass on the grid [-a_n, a_n] (Sec. 4.2,
+ * "Gaussian order statistics"), sharpened p^alpha (Sec. 4.4), apportioned to
+ * integers summing to 2^p (Eq. rans), Q16 costs R_m = round(2^16 (p - log2 f_m))
+ * (Alg. 1), the lambda grid 2^(k/512) as fp32, and the feasibility test.
+ * Output arrays may be NULL; sizes: freq, cum, cost_q16: levels entries;
+ * sym_of_z: 2^p entries; lambda512: 512 entries.
+ * Returns DQ_OK, DQ_ERR_INVALID_ARG, or DQ_ERR_INFEASIBLE (info is filled).
+ */
+int dq_compute_tables(const dq_config* cfg, dq_table_info* info, int32_t* freq,
+                      int32_t* cum, int32_t* cost_q16, uint8_t* sym_of_z,
+                      float* lambda512);
+
+/*
+ * Same tables, copied to the current HIP device.  On DQ_OK *out owns host and
+ * device memory until dq_free_tables.  An infeasible configuration returns
+ * DQ_ERR_INFEASIBLE with *out = NULL and info filled.
+ */
+int dq_build_tables(const dq_config* cfg, dq_tables** out, dq_table_info* info);
+void dq_free_tables(dq_tables* tables);
+
+/*
+ * Encodes new tokens into records (Fig. 1; Alg. 1 and the rANS coder).
+ *   kv:      bf16 [batch][tokens][kv_heads][head_dim] at element strides
+ *            (stride_b, stride_t, stride_h); channels contiguous.  Token i of
+ *            the input becomes cache token t0 + i.
+ *   records: u8 [batch][kv_heads][t_cap][C]; writes tokens [t0, t0 + n_new).
+ *   mean_q, mean_scale: keys only -- int8 [batch][kv_heads][t_cap/128][head_dim]
+ *            and fp16 [batch][kv_heads][t_cap/128]: the per-window INT8
+ *            channel mean of the rotated keys, which is removed before
+ *            quantization (Sec. 4.2).  Both NULL for values (no mean removal);
+ *            with them, t0 and n_new must be multiples of 128.
+ *   status:  device u32, may be NULL; DQ_STATUS_RANGE / DQ_STATUS_OVERFLOW.
+ * Every stream is rotated with the unnormalized Sylvester Hadamard matrix.
+ * The records are bit-identical to the reference definition of the format.
+ */
+int dq_encode_kv(const dq_tables* tables, const uint16_t* kv, int64_t stride_b,
+                 int64_t stride_t, int64_t stride_h, int32_t batch,
+                 int32_t kv_heads, int32_t t0, int32_t n_new, int32_t t_cap,
+                 uint8_t* records, int8_t* mean_q, uint16_t* mean_scale,
+                 uint32_t* status, void* stream);
+
+/* Workspace bytes dq_decode_attention needs for these sizes. */
+size_t dq_decode_workspace_bytes(int32_t batch, int32_t q_heads, int32_t kv_heads,
+                                 int32_t t_cap, int32_t head_dim);
+
+/*
+ * One decode step of attention over the compressed cache (Sec. 4.5 decoding,
+ * App. A): logits softmax_scale * q . k_hat over the first seq_lens[b] tokens,
+ * output sum_t a_t v_hat_t, with query head i reading KV head
+ * i / (q_heads / kv_heads).
+ *   q:        bf16 [batch][q_heads][head_dim]
+ *   k_records, v_records: u8 [batch][kv_heads][t_cap][C_k or C_v]
+ *   k_mean_q, k_mean_scale: as written by dq_encode_kv for the keys
+ *   seq_lens: device int32 [batch], each in [0, t_cap]
+ *   out:      fp32 [batch][q_heads][head_dim] (a sequence of length 0 gives 0)
+ *   workspace: device memory of dq_decode_workspace_bytes(...) bytes
+ *   status:   device u32, may be NULL; DQ_STATUS_CORRUPT for malformed records
+ * t_cap must be a multiple of 128; q_heads a multiple of kv_heads with
+ * q_heads / kv_heads <= 8.
+ */
+int dq_decode_attention(const dq_tables* k_tables, const dq_tables* v_tables,
+                        const uint16_t* q, int32_t batch, int32_t q_heads,
+                        int32_t kv_heads, const uint8_t* k_records,
+                        const int8_t* k_mean_q, const uint16_t* k_mean_scale,
+                        const uint8_t* v_records, const int32_t* seq_lens,
+                        int32_t t_cap, float softmax_scale, float* out,
+                        void* workspace, size_t workspace_bytes,
+                        uint32_t* status, void* stream);
+
+/*
+ * rANS-decodes records back to symbols (Alg. 2), for parity checks.
+ *   records: u8 [n_streams][C]; sym: u8 [n_streams][head_dim];
+ *   header:  u16 [n_streams][2] = (scale, offset) fp16 bits; may be NULL;
+ *   status:  DQ_STATUS_CORRUPT if a record is malformed; may be NULL.
+ */
+int dq_decode_symbols(const dq_tables* tables, const uint8_t* records,
+                      int64_t n_streams, uint8_t* sym, uint16_t* header,
+                      uint32_t* status, void* stream);
+
+/* Static description of a return code. */
+const char* dq_strerror(int code);
+
+/* The HIP call that last failed in this thread with DQ_ERR_HIP, and its HIP
+ * error name and text ("" if none).  Valid until the next failing call. */
+const char* dq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DQ_H */

@@ -73,8 +73,9 @@ def encode(sym: np.ndarray, tab: Tables):
 def decode(records: np.ndarray, tab: Tables, n: int):
     """Alg. 2 on records[S, C]: returns (sym [S, n], final x [S], ptr [S]).
 
-    Reads stop at the end of the record (a malformed record then shows up as a
-    final state different from L or a pointer past C).
+    Renormalization reads stop at the end of the C-byte record, so a
+    malformed record terminates and shows up as a final state different from L
+    (a well-formed record never reaches its end before the last symbol).
     """
     S, C = records.shape
     p = tab.p
@@ -93,12 +94,11 @@ def decode(records: np.ndarray, tab: Tables, n: int):
         c = tab.cum[m].astype(np.uint64)
         x = f * (x >> np.uint64(p)) + z.astype(np.uint64) - c
         while True:
-            need = x < np.uint64(RANS_L)
+            need = (x < np.uint64(RANS_L)) & (ptr < C)
             if not need.any():
                 break
             idx = rows[need]
-            byte = np.where(ptr[idx] < C, rec[idx, np.minimum(ptr[idx], C - 1)], np.uint64(0))
-            x[idx] = (x[idx] << np.uint64(8)) | byte
+            x[idx] = (x[idx] << np.uint64(8)) | rec[idx, ptr[idx]]
             ptr[idx] += 1
     return sym, x, ptr
 

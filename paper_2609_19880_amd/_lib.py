@@ -1,0 +1,271 @@
+"""ctypes binding of libdq.so (argument marshalling only)."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+# torch must be loaded first: libdq.so then binds to the HIP runtime torch
+# ships with (same soname), so both share one runtime, device context and
+# stream namespace.
+import torch  # noqa: F401  (load order matters)
+
+DQ_OK = 0
+DQ_ERR_INVALID_ARG = 1
+DQ_ERR_INFEASIBLE = 2
+DQ_ERR_HIP = 3
+DQ_ERR_WORKSPACE = 4
+
+DQ_STATUS_RANGE = 1
+DQ_STATUS_OVERFLOW = 2
+DQ_STATUS_CORRUPT = 4
+
+DQ_MEAN_WINDOW = 128
+LAMBDA_STEPS = 512
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, "libdq.so")
+
+
+class DqError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        detail = f" [{dq_last_error()}]" if code == DQ_ERR_HIP else ""
+        super().__init__(f"{where}: {dq_strerror(code)} (code {code}){detail}")
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [("head_dim", ctypes.c_int32), ("levels", ctypes.c_int32),
+                ("precision_bits", ctypes.c_int32), ("record_bytes", ctypes.c_int32),
+                ("alpha", ctypes.c_double)]
+
+
+class _Info(ctypes.Structure):
+    _fields_ = [("record_bytes", ctypes.c_int32), ("feasible", ctypes.c_int32),
+                ("cheapest", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("budget_q16", ctypes.c_int64), ("min_cost_q16", ctypes.c_int64),
+                ("expected_max", ctypes.c_double)]
+
+
+def _load():
+    path = library_path()
+    if not os.path.exists(path):
+        raise ImportError(f"libdq.so is not built ({path}); run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.dq_compute_tables.argtypes = [ctypes.POINTER(_Config), ctypes.POINTER(_Info), P, P, P, P, P]
+    lib.dq_compute_tables.restype = ctypes.c_int
+    lib.dq_build_tables.argtypes = [ctypes.POINTER(_Config), ctypes.POINTER(P), ctypes.POINTER(_Info)]
+    lib.dq_build_tables.restype = ctypes.c_int
+    lib.dq_free_tables.argtypes = [P]
+    lib.dq_free_tables.restype = None
+    lib.dq_encode_kv.argtypes = [P, P, I64, I64, I64, I32, I32, I32, I32, I32, P, P, P, P, P]
+    lib.dq_encode_kv.restype = ctypes.c_int
+    lib.dq_decode_workspace_bytes.argtypes = [I32, I32, I32, I32, I32]
+    lib.dq_decode_workspace_bytes.restype = SZ
+    lib.dq_decode_attention.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, ctypes.c_float,
+                                        P, P, SZ, P, P]
+    lib.dq_decode_attention.restype = ctypes.c_int
+    lib.dq_decode_symbols.argtypes = [P, P, I64, P, P, P, P]
+    lib.dq_decode_symbols.restype = ctypes.c_int
+    lib.dq_strerror.argtypes = [ctypes.c_int]
+    lib.dq_strerror.restype = ctypes.c_char_p
+    lib.dq_last_error.argtypes = []
+    lib.dq_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+_lib = _load()
+
+
+def dq_strerror(code: int) -> str:
+    return _lib.dq_strerror(int(code)).decode()
+
+
+def dq_last_error() -> str:
+    return _lib.dq_last_error().decode()
+
+
+@dataclass
+class TableInfo:
+    record_bytes: int
+    feasible: bool
+    cheapest: int
+    budget_q16: int
+    min_cost_q16: int
+    expected_max: float
+
+
+def _cfg(head_dim, levels, precision_bits, record_bytes, alpha) -> _Config:
+    return _Config(int(head_dim), int(levels), int(precision_bits), int(record_bytes), float(alpha))
+
+
+def _info(i: _Info) -> TableInfo:
+    return TableInfo(i.record_bytes, bool(i.feasible), i.cheapest, i.budget_q16, i.min_cost_q16,
+                     i.expected_max)
+
+
+def dq_compute_tables(head_dim: int, levels: int, precision_bits: int, record_bytes: int,
+                      alpha: float):
+    """Host-only table build.  Returns (info, dict of numpy arrays) or raises."""
+    cfg = _cfg(head_dim, levels, precision_bits, record_bytes, alpha)
+    info = _Info()
+    M, P = int(levels), 1 << int(precision_bits)
+    freq = np.zeros(M, np.int32)
+    cum = np.zeros(M, np.int32)
+    cost = np.zeros(M, np.int32)
+    sym = np.zeros(P, np.uint8)
+    lam = np.zeros(LAMBDA_STEPS, np.float32)
+    rc = _lib.dq_compute_tables(ctypes.byref(cfg), ctypes.byref(info), freq.ctypes.data,
+                                cum.ctypes.data, cost.ctypes.data, sym.ctypes.data, lam.ctypes.data)
+    if rc not in (DQ_OK, DQ_ERR_INFEASIBLE):
+        raise DqError(rc, "dq_compute_tables")
+    return _info(info), {"freq": freq, "cum": cum, "cost": cost, "sym_of_z": sym, "lambda": lam}
+
+
+class Tables:
+    """Owner of a dq_tables handle (host + device copy on the current device)."""
+
+    def __init__(self, head_dim: int, levels: int, precision_bits: int, record_bytes: int,
+                 alpha: float):
+        self.head_dim = int(head_dim)
+        self.levels = int(levels)
+        self.precision_bits = int(precision_bits)
+        self.record_bytes = int(record_bytes)
+        self.alpha = float(alpha)
+        cfg = _cfg(head_dim, levels, precision_bits, record_bytes, alpha)
+        handle = ctypes.c_void_p()
+        info = _Info()
+        self._handle = None
+        rc = _lib.dq_build_tables(ctypes.byref(cfg), ctypes.byref(handle), ctypes.byref(info))
+        self.info = _info(info)
+        if rc != DQ_OK:
+            raise DqError(rc, "dq_build_tables")
+        self._handle = handle
+
+    @property
+    def handle(self):
+        return self._handle
+
+    def __del__(self):
+        h = getattr(self, "_handle", None)
+        if h is not None and _lib is not None:
+            _lib.dq_free_tables(h)
+            self._handle = None
+
+
+def dq_build_tables(head_dim: int, levels: int, precision_bits: int, record_bytes: int,
+                    alpha: float) -> Tables:
+    return Tables(head_dim, levels, precision_bits, record_bytes, alpha)
+
+
+def smallest_feasible_alpha(head_dim: int, levels: int, precision_bits: int, record_bytes: int,
+                            start: float = 1.4, step: float = 0.1, stop: float = 64.0) -> float:
+    """Smallest alpha on the grid start + k * step for which the table fits."""
+    k = 0
+    while True:
+        a = round(start + k * step, 10)
+        if a > stop:
+            raise DqError(DQ_ERR_INFEASIBLE, "smallest_feasible_alpha")
+        info, _ = dq_compute_tables(head_dim, levels, precision_bits, record_bytes, a)
+        if info.feasible:
+            return a
+        k += 1
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _check(rc: int, where: str):
+    if rc != DQ_OK:
+        raise DqError(rc, where)
+
+
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def dq_encode_kv(tables: Tables, kv, t0: int, t_cap: int, records, mean_q=None, mean_scale=None,
+                 status=None, stream=None):
+    """Append kv (bf16 [B, T_new, H, d] on the GPU, channels contiguous) at
+    cache position t0.  records: uint8 [B, H, t_cap, C]; keys also pass
+    mean_q int8 [B, H, t_cap/128, d] and mean_scale int16/float16 [B, H, t_cap/128]."""
+    import torch
+    _need(kv.is_cuda and kv.dtype == torch.bfloat16 and kv.dim() == 4, "kv must be bf16 [B,T,H,d] on the GPU")
+    B, T, H, d = kv.shape
+    _need(kv.stride(3) == 1 and d == tables.head_dim, "kv channels must be contiguous and match head_dim")
+    _need(records.is_cuda and records.dtype == torch.uint8 and records.is_contiguous()
+          and tuple(records.shape) == (B, H, t_cap, tables.record_bytes), "records shape/dtype")
+    if mean_q is not None:
+        _need(mean_scale is not None, "mean_q and mean_scale go together")
+        _need(mean_q.dtype == torch.int8 and mean_q.is_contiguous()
+              and tuple(mean_q.shape) == (B, H, t_cap // DQ_MEAN_WINDOW, d), "mean_q shape/dtype")
+        _need(mean_scale.element_size() == 2 and mean_scale.is_contiguous()
+              and tuple(mean_scale.shape) == (B, H, t_cap // DQ_MEAN_WINDOW), "mean_scale shape/dtype")
+    if status is not None:
+        _need(status.is_cuda and status.element_size() == 4, "status must be a 4-byte device word")
+    rc = _lib.dq_encode_kv(tables.handle, _ptr(kv), kv.stride(0), kv.stride(1), kv.stride(2),
+                           B, H, int(t0), T, int(t_cap), _ptr(records), _ptr(mean_q), _ptr(mean_scale),
+                           _ptr(status), _stream(stream))
+    _check(rc, "dq_encode_kv")
+
+
+def dq_decode_workspace_bytes(batch: int, q_heads: int, kv_heads: int, t_cap: int,
+                              head_dim: int = 128) -> int:
+    return int(_lib.dq_decode_workspace_bytes(batch, q_heads, kv_heads, t_cap, head_dim))
+
+
+def dq_decode_attention(k_tables: Tables, v_tables: Tables, q, k_records, k_mean_q, k_mean_scale,
+                        v_records, seq_lens, out, workspace, softmax_scale=None, status=None,
+                        stream=None):
+    """One decode step: q bf16 [B, Hq, d] -> out fp32 [B, Hq, d]."""
+    import torch
+    _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3, "q")
+    B, Hq, d = q.shape
+    _need(k_records.dim() == 4 and k_records.is_contiguous() and k_records.dtype == torch.uint8, "k_records")
+    _, Hkv, t_cap, Ck = k_records.shape
+    _need(Ck == k_tables.record_bytes and k_records.shape[0] == B, "k_records shape")
+    _need(v_records.is_contiguous() and tuple(v_records.shape) == (B, Hkv, t_cap, v_tables.record_bytes),
+          "v_records shape")
+    _need(k_mean_q.is_contiguous() and tuple(k_mean_q.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW, d), "k_mean_q")
+    _need(k_mean_scale.is_contiguous() and tuple(k_mean_scale.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW),
+          "k_mean_scale")
+    _need(seq_lens.is_cuda and seq_lens.dtype == torch.int32 and seq_lens.numel() == B, "seq_lens")
+    _need(out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and tuple(out.shape) == (B, Hq, d),
+          "out")
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    rc = _lib.dq_decode_attention(k_tables.handle, v_tables.handle, _ptr(q), B, Hq, Hkv,
+                                  _ptr(k_records), _ptr(k_mean_q), _ptr(k_mean_scale), _ptr(v_records),
+                                  _ptr(seq_lens), t_cap, ctypes.c_float(scale), _ptr(out),
+                                  _ptr(workspace), ws_bytes, _ptr(status), _stream(stream))
+    _check(rc, "dq_decode_attention")
+
+
+def dq_decode_symbols(tables: Tables, records, sym, header=None, status=None, stream=None):
+    """records uint8 [..., C] -> sym uint8 [..., d] (+ header int16 [..., 2])."""
+    import torch
+    _need(records.is_contiguous() and records.dtype == torch.uint8 and records.shape[-1] == tables.record_bytes,
+          "records")
+    S = records.numel() // tables.record_bytes
+    _need(sym.is_contiguous() and sym.dtype == torch.uint8 and sym.numel() == S * tables.head_dim, "sym")
+    if header is not None:
+        _need(header.is_contiguous() and header.element_size() == 2 and header.numel() == 2 * S, "header")
+    rc = _lib.dq_decode_symbols(tables.handle, _ptr(records), S, _ptr(sym), _ptr(header), _ptr(status),
+                                _stream(stream))
+    _check(rc, "dq_decode_symbols")

@@ -1,0 +1,477 @@
+// Append path: bf16 K/V tokens -> fixed-size D-Quant records (Fig. 1, Alg. 1).
+//
+// Two kernels:
+//  * key_mean: one wavefront per (batch, head, 128-token window).  Rotates
+//    each token (Hadamard, Sec. 4.2), sums the window left to right in fp64,
+//    and stores the channel mean as INT8 with one fp16 scale (App. B,
+//    "windowed INT8 channel-mean removal").
+//  * encode: one workgroup per (batch, head, 64 consecutive tokens).  Each
+//    wavefront takes a stream at a time with its n values spread over the
+//    lanes and keeps them in registers through Alg. 1 (FitMinMax -> Drift ->
+//    Refit -> fp16 -> Drift); distortions are recomputed on the fly for every
+//    bisection step and the code length is reduced across the wavefront, as
+//    Sec. 4.5 describes for the encoder.  The symbols of the 64 streams then
+//    go through LDS to lane-per-stream backward rANS, and the 64 records are
+//    written as one contiguous span.
+//
+// Every floating-point step is fp64 in a fixed order without contraction
+// (this file is built with -ffp-contract=off), so the records are
+// bit-identical to the reference definition of the format.
+#include <float.h>
+
+#include "dq_common.h"
+
+namespace dq {
+namespace {
+
+constexpr int kEncStreams = 64;   // streams per workgroup
+constexpr int kEncWaves = 4;
+constexpr int kEncThreads = kEncWaves * kWave;
+
+// Unnormalized FWHT of n = 64 * VPL values; lane l holds elements
+// l + 64 k.  Stages run h = 1, 2, ..., n/2 as in the definition.
+template <int VPL>
+__device__ __forceinline__ void fwht_wave(double (&v)[VPL], int lane) {
+#pragma unroll
+    for (int h = 1; h < kWave; h <<= 1) {
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) {
+            double pv = __shfl_xor(v[k], h);
+            v[k] = (lane & h) ? (pv - v[k]) : (v[k] + pv);
+        }
+    }
+#pragma unroll
+    for (int s = 1; s < VPL; s <<= 1) {
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) {
+            if (!(k & s)) {
+                double a = v[k], b = v[k + s];
+                v[k] = a + b;
+                v[k + s] = a - b;
+            }
+        }
+    }
+}
+
+// Fold-in-halves sum of the n = 64 VPL values (v[i] += v[i + len/2] until
+// one is left); every lane ends with the total.
+template <int VPL>
+__device__ __forceinline__ double fold_sum(const double (&v)[VPL]) {
+    double w[VPL];
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) w[k] = v[k];
+#pragma unroll
+    for (int len = VPL; len > 1; len >>= 1) {
+#pragma unroll
+        for (int k = 0; k < len / 2; ++k) w[k] = w[k] + w[k + len / 2];
+    }
+    double s = w[0];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) s = s + __shfl_xor(s, off);
+    return s;
+}
+
+template <int VPL>
+__device__ __forceinline__ void load_rotated(const uint16_t* src, double (&v)[VPL], int lane) {
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) v[k] = (double)bf16_to_f32(src[lane + kWave * k]);
+    fwht_wave<VPL>(v, lane);
+}
+
+struct DriftCtx {
+    const double* rate;    // LDS [M]: R_m / 2^16
+    const int32_t* cost;   // LDS [M]
+    const float* lam;      // LDS [512]
+    int M;
+    int cheapest;
+    int rmin;
+};
+
+template <int VPL>
+__device__ __forceinline__ int assign_cost(const double (&x)[VPL], double s, double o, double lam,
+                                           const DriftCtx& c, int (&m)[VPL]) {
+    double best[VPL];
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) {
+        best[k] = DBL_MAX;
+        m[k] = 0;
+    }
+    for (int mm = 0; mm < c.M; ++mm) {
+        const double t = s * (double)mm;
+        const double u = o + t;
+        const double pen = lam * c.rate[mm];
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) {
+            const double e = x[k] - u;
+            const double J = e * e + pen;
+            if (J < best[k] || mm == 0) {
+                best[k] = J;
+                m[k] = mm;
+            }
+        }
+    }
+    int cst = 0;
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) cst += c.cost[m[k]];
+    return wave_sum_i32(cst);
+}
+
+// Drift(x, s, o, r, B) of Alg. 1: bisection on log2(lambda) over a
+// 40-octave bracket below hi = ceil(log2(8 (max D - min D))), lambda on the
+// 2^(U/512) grid, 12 steps, assignment at the final hi; nearest cheapest
+// symbol if even that overflows; cheapest symbol if all distortions are equal.
+template <int VPL>
+__device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget,
+                      const DriftCtx& c, int (&m)[VPL]) {
+    double dmax = -DBL_MAX, dmin = DBL_MAX;
+    for (int mm = 0; mm < c.M; ++mm) {
+        const double t = s * (double)mm;
+        const double u = o + t;
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) {
+            const double e = x[k] - u;
+            const double D = e * e;
+            dmax = fmax(dmax, D);
+            dmin = fmin(dmin, D);
+        }
+    }
+    dmax = wave_max(dmax);
+    dmin = wave_min(dmin);
+    if (dmax == dmin) {
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) m[k] = c.cheapest;
+        return;
+    }
+    int ex = 0;
+    const double mant = frexp(8.0 * (dmax - dmin), &ex);
+    const int hi = (mant == 0.5) ? ex - 1 : ex;
+    int u_hi = hi * kLambdaSteps;
+    int u_lo = u_hi - kBracketUnits;
+    for (int it = 0; it < kBisectSteps; ++it) {
+        const int u_mid = (u_lo + u_hi) >> 1;
+        const double lam = ldexp((double)c.lam[u_mid & (kLambdaSteps - 1)], u_mid >> 9);
+        int tmp[VPL];
+        const int cst = assign_cost<VPL>(x, s, o, lam, c, tmp);
+        if ((int64_t)cst <= budget)
+            u_hi = u_mid;
+        else
+            u_lo = u_mid;
+    }
+    const double lam = ldexp((double)c.lam[u_hi & (kLambdaSteps - 1)], u_hi >> 9);
+    const int cst = assign_cost<VPL>(x, s, o, lam, c, m);
+    if ((int64_t)cst > budget) {
+        double best[VPL];
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) best[k] = DBL_MAX;
+        for (int mm = 0; mm < c.M; ++mm) {
+            if (c.cost[mm] != c.rmin) continue;
+            const double t = s * (double)mm;
+            const double u = o + t;
+#pragma unroll
+            for (int k = 0; k < VPL; ++k) {
+                const double e = x[k] - u;
+                const double D = e * e;
+                if (D < best[k]) {
+                    best[k] = D;
+                    m[k] = mm;
+                }
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ uint16_t f64_to_half_bits(double v) {
+    return __half_as_ushort(__float2half_rn((float)v));
+}
+
+template <int VPL>
+__global__ __launch_bounds__(kWave) void key_mean_kernel(const uint16_t* __restrict__ kv,
+                                                         int64_t sb, int64_t st, int64_t sh, int H,
+                                                         int t0, int t_cap,
+                                                         int8_t* __restrict__ mean_q,
+                                                         uint16_t* __restrict__ mean_scale,
+                                                         uint32_t* status) {
+    constexpr int n = kWave * VPL;
+    const int w = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    const int lane = threadIdx.x;
+    double acc[VPL];
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) acc[k] = 0.0;
+    const uint16_t* base = kv + (int64_t)b * sb + (int64_t)h * sh;
+    const int tw = w * DQ_MEAN_WINDOW;
+    for (int t = 0; t < DQ_MEAN_WINDOW; ++t) {
+        double v[VPL];
+        load_rotated<VPL>(base + (int64_t)(tw + t) * st, v, lane);
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) acc[k] = acc[k] + v[k];
+    }
+    double mu[VPL];
+    double amax = 0.0;
+    bool finite = true;
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) {
+        mu[k] = acc[k] / (double)DQ_MEAN_WINDOW;
+        amax = fmax(amax, fabs(mu[k]));
+        finite = finite && isfinite(mu[k]);
+    }
+    amax = wave_max(amax);
+    const uint16_t sbits = f64_to_half_bits(amax / 127.0);
+    const double sc = (double)__half2float(__ushort_as_half(sbits));
+    const int win = t0 / DQ_MEAN_WINDOW + w;
+    const int nwin = t_cap / DQ_MEAN_WINDOW;
+    int8_t* dst = mean_q + ((int64_t)(b * H + h) * nwin + win) * n;
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) {
+        double qv = 0.0;
+        if (sc > 0.0) qv = fmin(127.0, fmax(-127.0, rint(mu[k] / sc)));
+        dst[lane + kWave * k] = (int8_t)qv;
+    }
+    if (lane == 0) mean_scale[(int64_t)(b * H + h) * nwin + win] = sbits;
+    const bool bad = __any(!finite) || !isfinite(sc);
+    if (bad && lane == 0 && status) atomicOr(status, DQ_STATUS_RANGE);
+}
+
+struct EncArgs {
+    TabArgs ta;
+    const uint16_t* kv;
+    int64_t sb, st, sh;
+    int H, t0, n_new, t_cap;
+    uint8_t* records;
+    const int8_t* mean_q;        // NULL for values
+    const uint16_t* mean_scale;
+    uint32_t* status;
+};
+
+// x = rotated stream of cache token t minus the dequantized window mean (keys).
+template <int VPL>
+__device__ __forceinline__ void stream_values(const EncArgs& a, int b, int h, int t,
+                                              double (&x)[VPL], int lane) {
+    const int64_t ti = t - a.t0;   // position in the input
+    load_rotated<VPL>(a.kv + (int64_t)b * a.sb + ti * a.st + (int64_t)h * a.sh, x, lane);
+    if (a.mean_q) {
+        constexpr int n = kWave * VPL;
+        const int nwin = a.t_cap / DQ_MEAN_WINDOW;
+        const int64_t wi = (int64_t)(b * a.H + h) * nwin + t / DQ_MEAN_WINDOW;
+        const double sc = (double)__half2float(__ushort_as_half(a.mean_scale[wi]));
+        const int8_t* mq = a.mean_q + wi * n;
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) x[k] = x[k] - sc * (double)mq[lane + kWave * k];
+    }
+}
+
+template <int VPL>
+__global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
+    constexpr int n = kWave * VPL;
+    extern __shared__ __align__(16) uint8_t smem[];
+    // layout: rate[64] f64 | cost[64] | lam[512] | budget[64] i64 | s16[64] | o16[64]
+    //         | flag[64] | sym[64][n] | rec[64][C]
+    double* s_rate = reinterpret_cast<double*>(smem);
+    int32_t* s_cost = reinterpret_cast<int32_t*>(s_rate + DQ_MAX_LEVELS);
+    float* s_lam = reinterpret_cast<float*>(s_cost + DQ_MAX_LEVELS);
+    int64_t* s_budget = reinterpret_cast<int64_t*>(s_lam + kLambdaSteps);
+    uint16_t* s_s16 = reinterpret_cast<uint16_t*>(s_budget + kEncStreams);
+    uint16_t* s_o16 = s_s16 + kEncStreams;
+    int32_t* s_flag = reinterpret_cast<int32_t*>(s_o16 + kEncStreams);
+    uint8_t* s_sym = reinterpret_cast<uint8_t*>(s_flag + kEncStreams);
+    uint8_t* s_rec = s_sym + kEncStreams * n;
+
+    const TabArgs& ta = a.ta;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int b = blockIdx.z, h = blockIdx.y;
+    const int first = a.t0 + blockIdx.x * kEncStreams;
+    const int active = min(kEncStreams, a.t0 + a.n_new - first);
+    const int C = ta.C;
+
+    for (int i = tid; i < ta.M; i += kEncThreads) {
+        s_cost[i] = ta.t.cost[i];
+        s_rate[i] = (double)ta.t.cost[i] * (1.0 / 65536.0);
+    }
+    for (int i = tid; i < kLambdaSteps; i += kEncThreads) s_lam[i] = ta.t.lam[i];
+    for (int i = tid; i < kEncStreams; i += kEncThreads) {
+        s_budget[i] = ta.budget;
+        s_flag[i] = 0;
+    }
+    __syncthreads();
+    DriftCtx dc{s_rate, s_cost, s_lam, ta.M, ta.cheapest, ta.rmin};
+
+    bool range_bad = false;
+    for (int pass = 0;; ++pass) {
+        // Drift, wavefront per stream.
+        for (int i = wave; i < active; i += kEncWaves) {
+            if (pass > 0 && !s_flag[i]) continue;
+            double x[VPL];
+            stream_values<VPL>(a, b, h, first + i, x, lane);
+            uint16_t sb16, ob16;
+            if (pass == 0) {
+                double mn = x[0], mx = x[0];
+                bool fin = true;
+#pragma unroll
+                for (int k = 0; k < VPL; ++k) {
+                    mn = fmin(mn, x[k]);
+                    mx = fmax(mx, x[k]);
+                    fin = fin && isfinite(x[k]);
+                }
+                mn = wave_min(mn);
+                mx = wave_max(mx);
+                const double s0 = (mx - mn) / (double)(ta.M - 1);
+                const double o0 = mn;
+                int m1[VPL];
+                drift<VPL>(x, s0, o0, ta.budget, dc, m1);
+                // least-squares refit
+                int sm = 0, smm = 0;
+                double mx_[VPL];
+#pragma unroll
+                for (int k = 0; k < VPL; ++k) {
+                    sm += m1[k];
+                    smm += m1[k] * m1[k];
+                    mx_[k] = (double)m1[k] * x[k];
+                }
+                sm = wave_sum_i32(sm);
+                smm = wave_sum_i32(smm);
+                const double Sx = fold_sum<VPL>(x);
+                const double Smx = fold_sum<VPL>(mx_);
+                const int64_t den_i = (int64_t)n * smm - (int64_t)sm * sm;
+                double s1 = s0, o1 = o0;
+                if (den_i != 0) {
+                    const double den = (double)den_i;
+                    const double smf = (double)sm;
+                    const double s = ((double)n * Smx - smf * Sx) / den;
+                    const double o = (Sx - s * smf) / (double)n;
+                    if (isfinite(s) && s > 0.0) {
+                        s1 = s;
+                        o1 = o;
+                    }
+                }
+                sb16 = f64_to_half_bits(s1);
+                ob16 = f64_to_half_bits(o1);
+                const float sf = __half2float(__ushort_as_half(sb16));
+                const float of = __half2float(__ushort_as_half(ob16));
+                if (__any(!fin) || !isfinite(sf) || !isfinite(of)) range_bad = true;
+                if (lane == 0) {
+                    s_s16[i] = sb16;
+                    s_o16[i] = ob16;
+                }
+            } else {
+                sb16 = s_s16[i];
+                ob16 = s_o16[i];
+            }
+            const double s16 = (double)__half2float(__ushort_as_half(sb16));
+            const double o16 = (double)__half2float(__ushort_as_half(ob16));
+            int m2[VPL];
+            drift<VPL>(x, s16, o16, s_budget[i], dc, m2);
+#pragma unroll
+            for (int k = 0; k < VPL; ++k) s_sym[i * n + lane + kWave * k] = (uint8_t)m2[k];
+        }
+        __syncthreads();
+
+        // Backward rANS, lane per stream (Eq. rans, encoded in reverse).
+        if (tid < active && (pass == 0 || s_flag[tid])) {
+            const int i = tid;
+            uint8_t* rec = s_rec + i * C;
+            const int cap = C - kPayloadOffset;
+            const uint32_t xmax_unit = (kRansL >> ta.p) << 8;
+            uint32_t xs = kRansL;
+            int emitted = 0;
+            for (int j = n - 1; j >= 0; --j) {
+                const int m = s_sym[i * n + j];
+                const uint32_t f = (uint32_t)ta.t.freq[m];
+                const uint32_t c = (uint32_t)ta.t.cum[m];
+                const uint32_t xmax = xmax_unit * f;
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    if (xs >= xmax) {
+                        if (emitted < cap) rec[C - 1 - emitted] = (uint8_t)(xs & 0xFF);
+                        ++emitted;
+                        xs >>= 8;
+                    }
+                }
+                xs = (xs / f) * (1u << ta.p) + (xs % f) + c;
+            }
+            if (emitted > cap) {
+                s_flag[i] = 1;
+                s_budget[i] -= (int64_t)8 * 65536;
+                if (s_budget[i] < (int64_t)n * ta.rmin) {
+                    s_flag[i] = 0;
+                    if (a.status) atomicOr(a.status, DQ_STATUS_OVERFLOW);
+                }
+            } else {
+                s_flag[i] = 0;
+                // move the payload from the end of the record to offset 8
+                const int src = C - emitted;
+                for (int k = 0; k < emitted; ++k) rec[kPayloadOffset + k] = rec[src + k];
+                for (int k = kPayloadOffset + emitted; k < C; ++k) rec[k] = 0;
+                const uint16_t sb = s_s16[i], ob = s_o16[i];
+                rec[0] = (uint8_t)(sb & 0xFF);
+                rec[1] = (uint8_t)(sb >> 8);
+                rec[2] = (uint8_t)(ob & 0xFF);
+                rec[3] = (uint8_t)(ob >> 8);
+                rec[4] = (uint8_t)(xs & 0xFF);
+                rec[5] = (uint8_t)((xs >> 8) & 0xFF);
+                rec[6] = (uint8_t)((xs >> 16) & 0xFF);
+                rec[7] = (uint8_t)(xs >> 24);
+            }
+        }
+        const int again = __syncthreads_or(tid < active ? s_flag[tid] : 0);
+        if (!again) break;
+    }
+    if (range_bad && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_RANGE);
+
+    // Write the records of the active streams: one contiguous span.
+    uint8_t* dst = a.records + ((int64_t)(b * a.H + h) * a.t_cap + first) * C;
+    const int total = active * C;
+    if ((((uintptr_t)dst) & 3) == 0 && (total & 3) == 0) {
+        uint32_t* d32 = reinterpret_cast<uint32_t*>(dst);
+        const uint32_t* s32 = reinterpret_cast<const uint32_t*>(s_rec);
+        for (int k = tid; k < total / 4; k += kEncThreads) d32[k] = s32[k];
+    } else {
+        for (int k = tid; k < total; k += kEncThreads) dst[k] = s_rec[k];
+    }
+}
+
+}  // namespace
+
+int launch_encode(const dq_tables* tab, const uint16_t* kv, int64_t sb, int64_t st, int64_t sh,
+                  int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
+                  uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status,
+                  hipStream_t stream) {
+    const int n = tab->cfg.head_dim;
+    const int vpl = n / kWave;
+    if (mean_q) {
+        dim3 grid(n_new / DQ_MEAN_WINDOW, H, B);
+        switch (vpl) {
+            case 1: key_mean_kernel<1><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, mean_q, mean_scale, status); break;
+            case 2: key_mean_kernel<2><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, mean_q, mean_scale, status); break;
+            case 4: key_mean_kernel<4><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, mean_q, mean_scale, status); break;
+            default: return DQ_ERR_INVALID_ARG;
+        }
+        if (int rc = hip_check("key_mean launch", hipGetLastError())) return rc;
+    }
+    EncArgs a;
+    a.ta = tab_args(tab);
+    a.kv = kv;
+    a.sb = sb;
+    a.st = st;
+    a.sh = sh;
+    a.H = H;
+    a.t0 = t0;
+    a.n_new = n_new;
+    a.t_cap = t_cap;
+    a.records = records;
+    a.mean_q = mean_q;
+    a.mean_scale = mean_scale;
+    a.status = status;
+    const size_t smem = sizeof(double) * DQ_MAX_LEVELS + sizeof(int32_t) * DQ_MAX_LEVELS +
+                        sizeof(float) * kLambdaSteps + sizeof(int64_t) * kEncStreams +
+                        2 * sizeof(uint16_t) * kEncStreams + sizeof(int32_t) * kEncStreams +
+                        (size_t)kEncStreams * n + (size_t)kEncStreams * a.ta.C;
+    dim3 grid((n_new + kEncStreams - 1) / kEncStreams, H, B);
+    switch (vpl) {
+        case 1: encode_kernel<1><<<grid, kEncThreads, smem, stream>>>(a); break;
+        case 2: encode_kernel<2><<<grid, kEncThreads, smem, stream>>>(a); break;
+        case 4: encode_kernel<4><<<grid, kEncThreads, smem, stream>>>(a); break;
+        default: return DQ_ERR_INVALID_ARG;
+    }
+    return hip_check("kernel launch", hipGetLastError());
+}
+
+}  // namespace dq

@@ -1,0 +1,96 @@
+// Internal definitions shared by the host library and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dq.h"
+
+namespace dq {
+
+constexpr uint32_t kRansL = 1u << 23;       // rANS lower bound; state in [L, 256 L)
+constexpr int kLambdaSteps = 512;           // lambda grid points per octave
+constexpr int kPayloadOffset = 8;           // fp16 scale, fp16 offset, u32 state
+constexpr int kBisectSteps = 12;            // T of Alg. 1
+constexpr int kBracketUnits = 40 * kLambdaSteps;  // hi - lo = 40 octaves
+
+// Device-resident tables, one allocation.
+//   lut[z], z in [0, 2^p):  bias (z - c_m) in bits 0..11, f_m in bits 12..23,
+//                           m in bits 24..29.
+struct DevTables {
+    const uint32_t* lut;
+    const int32_t* freq;
+    const int32_t* cum;
+    const int32_t* cost;   // Q16
+    const float* lam;      // [512]
+};
+
+// Everything a kernel needs about one coding configuration (by value).
+struct TabArgs {
+    DevTables t;
+    int32_t n;          // values per stream
+    int32_t M;          // levels
+    int32_t p;          // precision bits
+    int32_t C;          // record bytes
+    int32_t cheapest;   // lowest-index minimum-cost symbol
+    int32_t rmin;       // minimum cost (Q16)
+    int64_t budget;     // Q16 budget
+};
+
+}  // namespace dq
+
+struct dq_tables {
+    dq_config cfg;
+    dq_table_info info;
+    int32_t freq[DQ_MAX_LEVELS];
+    int32_t cum[DQ_MAX_LEVELS];
+    int32_t cost[DQ_MAX_LEVELS];
+    int device;
+    void* dev_block;
+    dq::DevTables dev;
+};
+
+namespace dq {
+
+inline TabArgs tab_args(const dq_tables* t) {
+    TabArgs a;
+    a.t = t->dev;
+    a.n = t->cfg.head_dim;
+    a.M = t->cfg.levels;
+    a.p = t->cfg.precision_bits;
+    a.C = t->cfg.record_bytes;
+    a.cheapest = t->info.cheapest;
+    int32_t rmin = t->cost[0];
+    for (int m = 1; m < t->cfg.levels; ++m) rmin = t->cost[m] < rmin ? t->cost[m] : rmin;
+    a.rmin = rmin;
+    a.budget = t->info.budget_q16;
+    return a;
+}
+
+// Records the failing HIP call for dq_last_error(); returns DQ_ERR_HIP.
+int hip_fail(const char* where, hipError_t err);
+
+// DQ_OK if err is hipSuccess, else records it and returns DQ_ERR_HIP.
+inline int hip_check(const char* where, hipError_t err) {
+    return err == hipSuccess ? DQ_OK : hip_fail(where, err);
+}
+
+// Launchers implemented in the .hip files.  Return DQ_OK or DQ_ERR_HIP.
+int launch_encode(const dq_tables* tab, const uint16_t* kv, int64_t sb, int64_t st,
+                  int64_t sh, int32_t B, int32_t H, int32_t t0, int32_t n_new,
+                  int32_t t_cap, uint8_t* records, int8_t* mean_q,
+                  uint16_t* mean_scale, uint32_t* status, hipStream_t stream);
+
+int launch_decode_symbols(const dq_tables* tab, const uint8_t* records, int64_t n_streams,
+                          uint8_t* sym, uint16_t* header, uint32_t* status,
+                          hipStream_t stream);
+
+size_t attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d);
+
+int launch_attention(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
+                     int32_t Hq, int32_t Hkv, const uint8_t* krec, const int8_t* kmq,
+                     const uint16_t* kms, const uint8_t* vrec, const int32_t* seq_lens,
+                     int32_t t_cap, float scale, float* out, void* ws, size_t ws_bytes,
+                     uint32_t* status, hipStream_t stream);
+
+}  // namespace dq

@@ -99,3 +99,9 @@ def test_corrupted_record_is_detected():
     bad[:, 5] ^= 0x5A
     _, x, _ = rans.decode(bad, t, 128)
     assert np.mean(x != rans.RANS_L) > 0.9
+
+
+def test_all_zero_record_terminates():
+    t = tables.build_tables(128, 6, 12, 1.4, 36)
+    _, x, ptr = rans.decode(np.zeros((3, 36), np.uint8), t, 128)
+    assert np.all(x != rans.RANS_L) and np.all(ptr <= 36)
