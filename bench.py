@@ -1,0 +1,229 @@
+"""Decode-attention throughput of the D-Quant hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 100] [--warmup 10] [--workload b16_t32k]
+                    [--variant paper|literal] [--bpe 2.26] [--no-cpu-baseline]
+
+A step is one decode-attention pass over the whole compressed cache of the
+workload: batch 16 x 32768 tokens x 8 KV heads (32 query heads, head_dim 128)
+with 36-byte key and value records (2.25 bits per element).  The cache is
+filled once by the encoder (timed separately and reported), the raw K/V are
+freed, and the timed region holds only the decode-attention steps with the
+compressed cache resident in HBM.  Prints one JSON line.
+
+Other modes (for the profiles under profiles/):
+    --copy-calibration BYTES   time a plain device copy of BYTES bytes
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "KV tokens/s + achieved HBM GB/s, D-Quant decode attention at 2.26 bits/elem"
+HBM_PEAK_GBS = 8000.0
+
+
+def _args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="b16_t32k")
+    ap.add_argument("--variant", default="paper", choices=["paper", "literal"])
+    ap.add_argument("--bpe", type=float, default=None)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0)
+    return ap.parse_args()
+
+
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def copy_calibration(nbytes: int, steps: int):
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    print(json.dumps({"mode": "copy_calibration", "bytes": nbytes, "ms_per_copy": ms,
+                      "gbs_read_plus_write": 2 * nbytes / ms / 1e6}))
+
+
+def cpu_baseline(wl, seed: int):
+    """The CPU oracle's decode attention, timed on one (sequence, KV head)
+    slice of the workload at full context and scaled to a whole step."""
+    import numpy as np
+    import dq_workloads as wlmod
+    from oracle import attention, kmean, kv, tables
+
+    T = wl.context
+    otk = tables.build_tables(wl.head_dim, wl.k.levels, wl.k.precision, wl.k.alpha, wl.k.record_bytes)
+    otv = tables.build_tables(wl.head_dim, wl.v.levels, wl.v.precision, wl.v.alpha, wl.v.record_bytes)
+    one = wl.with_context(T, batch=1)
+    k = wlmod.bf16_bits(wlmod.make_k(one, seed + 100))[:, :, :1]      # one KV head
+    v = wlmod.bf16_bits(wlmod.make_v(one, seed + 100))[:, :, :1]
+    q = wlmod.bf16_bits(wlmod.make_q(one, seed + 100))[:, : wl.gqa]
+    krec, mq, ms, _ = kv.encode_keys(k, otk)
+    vrec, _ = kv.encode_values(v, otv)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        ksym, ks, ko, _ = kv.decode_records(krec, otk, wl.head_dim)
+        vsym, vs, vo, _ = kv.decode_records(vrec, otv, wl.head_dim)
+        attention.attention_folded(kv.bf16_to_f64(q), ksym, ks, ko, kmean.dequantize_mean(mq, ms),
+                                   vsym, vs, vo, [T], wl.gqa, 1 / np.sqrt(wl.head_dim))
+        reps += 1
+        if time.perf_counter() - t0 > 10.0:
+            break
+    per_slice = (time.perf_counter() - t0) / reps
+    slices = wl.batch * wl.kv_heads
+    step_s = per_slice * slices
+    return {"value": wl.batch * T / step_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"oracle rANS decode of the K and V records plus fp64 folded attention for one "
+                      f"(sequence, KV head) slice: {T} tokens, {wl.gqa} query heads; {reps} repetitions, "
+                      f"{per_slice:.3f} s each, scaled x{slices} to the {wl.batch}x{wl.kv_heads} slices of a "
+                      f"step; single-threaded numpy on {_cpu_model()} ({os.cpu_count()} host cores)"}
+
+
+def main():
+    a = _args()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only: the decode-attention path has no multi-GPU leg "
+              f"(asked for --gpus {a.gpus})", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    if a.copy_calibration:
+        copy_calibration(a.copy_calibration, a.steps)
+        return
+
+    import dq_workloads as wlmod
+    import paper_2609_19880_amd as dq
+
+    wl = wlmod.workload(a.workload, a.variant, a.bpe) if a.workload == "b1_t128k" else \
+        wlmod.workload(a.workload, a.variant)
+    dev = torch.device("cuda")
+    B, T, Hq, Hkv, d = wl.batch, wl.context, wl.q_heads, wl.kv_heads, wl.head_dim
+    tk = dq.Tables(d, wl.k.levels, wl.k.precision, wl.k.record_bytes, wl.k.alpha)
+    tv = dq.Tables(d, wl.v.levels, wl.v.precision, wl.v.record_bytes, wl.v.alpha)
+    cache = dq.KVCache(B, Hkv, Hq, T, tk, tv, device=dev)
+
+    # fill the cache, one sequence at a time (encode throughput is reported too)
+    enc_ms = 0.0
+    for b in range(B):
+        k = wlmod.make_k(wl, a.seed * 1000 + b, device=dev, batch=1)
+        v = wlmod.make_v(wl, a.seed * 1000 + b, device=dev, batch=1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dq.dq_encode_kv(tk, k, 0, T, cache.k_records[b:b + 1], cache.k_mean_q[b:b + 1],
+                        cache.k_mean_scale[b:b + 1], cache.status)
+        dq.dq_encode_kv(tv, v, 0, T, cache.v_records[b:b + 1], None, None, cache.status)
+        e1.record()
+        torch.cuda.synchronize()
+        enc_ms += e0.elapsed_time(e1)
+        del k, v
+    status = int(cache.status.item())
+    if status:
+        raise RuntimeError(f"encoder status {status}")
+    torch.cuda.empty_cache()
+
+    q = wlmod.make_q(wl, a.seed, device=dev)
+    seq = torch.full((B,), T, dtype=torch.int32, device=dev)
+    out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
+    ws = cache.workspace
+
+    def step():
+        dq.dq_decode_attention_partial(tk, tv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
+                                       cache.v_records, seq, ws, status=cache.status)
+        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 * a.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(a.steps):
+        ev[3 * i].record()
+        dq.dq_decode_attention_partial(tk, tv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
+                                       cache.v_records, seq, ws, status=cache.status)
+        ev[3 * i + 1].record()
+        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
+        ev[3 * i + 2].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    if int(cache.status.item()):
+        raise RuntimeError(f"decode status {int(cache.status.item())}")
+    partial_ms = sum(ev[3 * i].elapsed_time(ev[3 * i + 1]) for i in range(a.steps)) / a.steps
+    merge_ms = sum(ev[3 * i + 1].elapsed_time(ev[3 * i + 2]) for i in range(a.steps)) / a.steps
+    step_ms = ev[0].elapsed_time(ev[-1]) / a.steps
+
+    # algorithmic bytes of one partial launch: per (token, KV head) the two
+    # records plus the amortized INT8 key mean and its fp16 scale
+    per_unit = wl.k.record_bytes + wl.v.record_bytes + (d + 2) / 128.0
+    units = B * T * Hkv
+    alg_bytes = per_unit * units
+    achieved = alg_bytes / (partial_ms * 1e-3) / 1e9
+    tokens_s = B * T / (step_ms * 1e-3)
+
+    rec = {
+        "metric": METRIC,
+        "value": tokens_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: batch {B} x context {T}, {Hq} query / {Hkv} KV heads, "
+                               f"head_dim {d}, K {wl.k.record_bytes} B / V {wl.v.record_bytes} B records "
+                               f"({8 * wl.k.record_bytes / d:.2f}/{8 * wl.v.record_bytes / d:.2f} bits/elem), "
+                               f"{wl.k.levels}/{wl.v.levels} levels, alpha {wl.k.alpha}/{wl.v.alpha}, p 12",
+                   "variant": a.variant, "batch": B, "context": T, "q_heads": Hq, "kv_heads": Hkv,
+                   "head_dim": d, "k_record_bytes": wl.k.record_bytes, "v_record_bytes": wl.v.record_bytes,
+                   "k_levels": wl.k.levels, "v_levels": wl.v.levels},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "attn_partial_kernel", "alg_bytes_per_launch": alg_bytes,
+                     "kernel_ms": partial_ms},
+        "merge_ms": merge_ms,
+        "wall_ms_per_step": wall * 1e3 / a.steps,
+        "symbols_per_s": 2 * units * d / (step_ms * 1e-3),
+        "encode": {"ms": enc_ms, "tokens_per_s": B * T / (enc_ms * 1e-3),
+                   "input_gbs": 2 * B * T * Hkv * d * 2 / (enc_ms * 1e-3) / 1e9},
+    }
+    if not a.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(wl, a.seed)
+    print(json.dumps(rec))
+
+
+if __name__ == "__main__":
+    main()

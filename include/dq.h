@@ -153,6 +153,27 @@ int dq_decode_attention(const dq_tables* k_tables, const dq_tables* v_tables,
                         uint32_t* status, void* stream);
 
 /*
+ * The two halves of dq_decode_attention, for callers that merge partial
+ * results themselves (e.g. context split over devices) or time them apart.
+ * _partial writes one (max, sum, accumulator) triple per (sequence, query
+ * head, context chunk) into the workspace (online-softmax state over the
+ * chunk); _merge combines the chunks by log-sum-exp, undoes the value
+ * rotation and writes `out`.  Arguments mean what they mean above; the chunk
+ * size is a function of (batch, kv_heads, t_cap), so both halves must be
+ * called with the same sizes and workspace.
+ */
+int dq_decode_attention_partial(const dq_tables* k_tables, const dq_tables* v_tables,
+                                const uint16_t* q, int32_t batch, int32_t q_heads,
+                                int32_t kv_heads, const uint8_t* k_records,
+                                const int8_t* k_mean_q, const uint16_t* k_mean_scale,
+                                const uint8_t* v_records, const int32_t* seq_lens,
+                                int32_t t_cap, float softmax_scale, void* workspace,
+                                size_t workspace_bytes, uint32_t* status, void* stream);
+int dq_decode_attention_merge(int32_t batch, int32_t q_heads, int32_t kv_heads,
+                              const int32_t* seq_lens, int32_t t_cap, const void* workspace,
+                              size_t workspace_bytes, float* out, void* stream);
+
+/*
  * rANS-decodes records back to symbols (Alg. 2), for parity checks.
  *   records: u8 [n_streams][C]; sym: u8 [n_streams][head_dim];
  *   header:  u16 [n_streams][2] = (scale, offset) fp16 bits; may be NULL;

@@ -7,7 +7,8 @@ raises if the library has not been built (``__graft_entry__.build()``).
 
 Entry points (same names as the C ABI in ``include/dq.h``):
     dq_compute_tables, dq_build_tables, dq_encode_kv,
-    dq_decode_workspace_bytes, dq_decode_attention, dq_decode_symbols,
+    dq_decode_workspace_bytes, dq_decode_attention, dq_decode_attention_partial,
+    dq_decode_attention_merge, dq_decode_symbols,
     dq_strerror, dq_last_error
 """
 
@@ -16,7 +17,7 @@ from ._lib import (  # noqa: F401
     DQ_STATUS_RANGE, DQ_STATUS_OVERFLOW, DQ_STATUS_CORRUPT, DQ_MEAN_WINDOW,
     DqError, Tables, TableInfo, library_path,
     dq_compute_tables, dq_build_tables, dq_encode_kv, dq_decode_workspace_bytes,
-    dq_decode_attention, dq_decode_symbols, dq_strerror, dq_last_error,
-    smallest_feasible_alpha,
+    dq_decode_attention, dq_decode_attention_partial, dq_decode_attention_merge,
+    dq_decode_symbols, dq_strerror, dq_last_error, smallest_feasible_alpha,
 )
 from .cache import KVCache  # noqa: F401

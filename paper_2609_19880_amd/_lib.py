@@ -72,6 +72,11 @@ def _load():
     lib.dq_decode_attention.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, ctypes.c_float,
                                         P, P, SZ, P, P]
     lib.dq_decode_attention.restype = ctypes.c_int
+    lib.dq_decode_attention_partial.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32,
+                                                ctypes.c_float, P, SZ, P, P]
+    lib.dq_decode_attention_partial.restype = ctypes.c_int
+    lib.dq_decode_attention_merge.argtypes = [I32, I32, I32, P, I32, P, SZ, P, P]
+    lib.dq_decode_attention_merge.restype = ctypes.c_int
     lib.dq_decode_symbols.argtypes = [P, P, I64, P, P, P, P]
     lib.dq_decode_symbols.restype = ctypes.c_int
     lib.dq_strerror.argtypes = [ctypes.c_int]
@@ -230,10 +235,7 @@ def dq_decode_workspace_bytes(batch: int, q_heads: int, kv_heads: int, t_cap: in
     return int(_lib.dq_decode_workspace_bytes(batch, q_heads, kv_heads, t_cap, head_dim))
 
 
-def dq_decode_attention(k_tables: Tables, v_tables: Tables, q, k_records, k_mean_q, k_mean_scale,
-                        v_records, seq_lens, out, workspace, softmax_scale=None, status=None,
-                        stream=None):
-    """One decode step: q bf16 [B, Hq, d] -> out fp32 [B, Hq, d]."""
+def _attention_args(k_tables, v_tables, q, k_records, k_mean_q, k_mean_scale, v_records, seq_lens, workspace):
     import torch
     _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3, "q")
     B, Hq, d = q.shape
@@ -246,10 +248,44 @@ def dq_decode_attention(k_tables: Tables, v_tables: Tables, q, k_records, k_mean
     _need(k_mean_scale.is_contiguous() and tuple(k_mean_scale.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW),
           "k_mean_scale")
     _need(seq_lens.is_cuda and seq_lens.dtype == torch.int32 and seq_lens.numel() == B, "seq_lens")
+    return B, Hq, Hkv, t_cap, d, workspace.numel() * workspace.element_size()
+
+
+def dq_decode_attention_partial(k_tables: Tables, v_tables: Tables, q, k_records, k_mean_q, k_mean_scale,
+                                v_records, seq_lens, workspace, softmax_scale=None, status=None, stream=None):
+    """First half of a decode step: per-chunk softmax partials into the workspace."""
+    B, Hq, Hkv, t_cap, d, ws_bytes = _attention_args(k_tables, v_tables, q, k_records, k_mean_q,
+                                                     k_mean_scale, v_records, seq_lens, workspace)
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    rc = _lib.dq_decode_attention_partial(k_tables.handle, v_tables.handle, _ptr(q), B, Hq, Hkv,
+                                          _ptr(k_records), _ptr(k_mean_q), _ptr(k_mean_scale),
+                                          _ptr(v_records), _ptr(seq_lens), t_cap, ctypes.c_float(scale),
+                                          _ptr(workspace), ws_bytes, _ptr(status), _stream(stream))
+    _check(rc, "dq_decode_attention_partial")
+
+
+def dq_decode_attention_merge(batch: int, q_heads: int, kv_heads: int, seq_lens, t_cap: int, workspace, out,
+                              stream=None):
+    """Second half: log-sum-exp merge of the chunk partials into out fp32 [B, Hq, d]."""
+    import torch
+    _need(out.is_cuda and out.dtype == torch.float32 and out.is_contiguous()
+          and tuple(out.shape) == (batch, q_heads, 128), "out")
+    ws_bytes = workspace.numel() * workspace.element_size()
+    rc = _lib.dq_decode_attention_merge(batch, q_heads, kv_heads, _ptr(seq_lens), t_cap, _ptr(workspace),
+                                        ws_bytes, _ptr(out), _stream(stream))
+    _check(rc, "dq_decode_attention_merge")
+
+
+def dq_decode_attention(k_tables: Tables, v_tables: Tables, q, k_records, k_mean_q, k_mean_scale,
+                        v_records, seq_lens, out, workspace, softmax_scale=None, status=None,
+                        stream=None):
+    """One decode step: q bf16 [B, Hq, d] -> out fp32 [B, Hq, d]."""
+    import torch
+    B, Hq, Hkv, t_cap, d, ws_bytes = _attention_args(k_tables, v_tables, q, k_records, k_mean_q,
+                                                     k_mean_scale, v_records, seq_lens, workspace)
     _need(out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and tuple(out.shape) == (B, Hq, d),
           "out")
     scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
-    ws_bytes = workspace.numel() * workspace.element_size()
     rc = _lib.dq_decode_attention(k_tables.handle, v_tables.handle, _ptr(q), B, Hq, Hkv,
                                   _ptr(k_records), _ptr(k_mean_q), _ptr(k_mean_scale), _ptr(v_records),
                                   _ptr(seq_lens), t_cap, ctypes.c_float(scale), _ptr(out),

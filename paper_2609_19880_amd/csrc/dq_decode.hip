@@ -253,6 +253,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(AttnArgs a) 
         float acc[G];
 #pragma unroll
         for (int g = 0; g < G; ++g) acc[g] = 0.f;
+#pragma unroll 2
         for (int j = 0; j < kD; ++j) {
             const float lv = (float)rans_step(x, ptr, lutk, maskk, pk, rk, Ck);
             const float* qj = qr + j * G;
@@ -289,9 +290,11 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(AttnArgs a) 
         const int ch = lane & (kVSlice - 1), half = lane / kVSlice;
 #pragma unroll
         for (int s = 0; s < kD / kVSlice; ++s) {
+#pragma unroll 2
             for (int jj = 0; jj < kVSlice; ++jj)
                 vt[lane * kVSlice + jj] = (uint8_t)rans_step(xv, ptrv, lutv, maskv, pvb, rv, Cv);
             wave_sync();
+#pragma unroll 4
             for (int tt = 0; tt < kTile / 2; ++tt) {
                 const int tok = half * (kTile / 2) + tt;
                 const float lv = (float)vt[tok * kVSlice + ch];
@@ -430,12 +433,26 @@ static int launch_g(AttnArgs& a, dim3 grid, hipStream_t stream) {
     return hip_check("kernel launch", hipGetLastError());
 }
 
-int launch_attention(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
-                     int32_t Hq, int32_t Hkv, const uint8_t* krec, const int8_t* kmq,
-                     const uint16_t* kms, const uint8_t* vrec, const int32_t* seq_lens,
-                     int32_t t_cap, float scale, float* out, void* ws, size_t ws_bytes,
-                     uint32_t* status, hipStream_t stream) {
+struct ChunkPlan {
+    int chunk, nchunks;
+    int64_t slots;
+};
+
+static ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap) {
+    ChunkPlan p;
+    p.chunk = choose_chunk(B, Hkv, t_cap);
+    p.nchunks = (t_cap + p.chunk - 1) / p.chunk;
+    p.slots = (int64_t)B * Hq * p.nchunks;
+    return p;
+}
+
+int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
+                             int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
+                             const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
+                             const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
+                             uint32_t* status, hipStream_t stream) {
     const int G = Hq / Hkv;
+    const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap);
     AttnArgs a;
     a.tk = tab_args(tk);
     a.tv = tab_args(tv);
@@ -443,39 +460,43 @@ int launch_attention(const dq_tables* tk, const dq_tables* tv, const uint16_t* q
     a.Hq = Hq;
     a.Hkv = Hkv;
     a.t_cap = t_cap;
-    a.chunk = choose_chunk(B, Hkv, t_cap);
-    a.nchunks = (t_cap + a.chunk - 1) / a.chunk;
+    a.chunk = plan.chunk;
+    a.nchunks = plan.nchunks;
     a.krec = krec;
     a.kmq = kmq;
     a.kms = kms;
     a.vrec = vrec;
     a.seq_lens = seq_lens;
     a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
-    const int64_t slots = (int64_t)B * Hq * a.nchunks;
     a.ws_acc = static_cast<float*>(ws);
-    a.ws_m = a.ws_acc + slots * kD;
-    a.ws_l = a.ws_m + slots;
+    a.ws_m = a.ws_acc + plan.slots * kD;
+    a.ws_l = a.ws_m + plan.slots;
     a.status = status;
     a.L = attn_layout(a.tk.p, a.tv.p, a.tk.C, a.tv.C, G, a.chunk);
     if (a.L.total > 160 * 1024) return DQ_ERR_INVALID_ARG;
-    (void)ws_bytes;
     dim3 grid(a.nchunks, Hkv, B);
-    int rc;
     switch (G) {
-        case 1: rc = launch_g<1>(a, grid, stream); break;
-        case 2: rc = launch_g<2>(a, grid, stream); break;
-        case 3: rc = launch_g<3>(a, grid, stream); break;
-        case 4: rc = launch_g<4>(a, grid, stream); break;
-        case 5: rc = launch_g<5>(a, grid, stream); break;
-        case 6: rc = launch_g<6>(a, grid, stream); break;
-        case 7: rc = launch_g<7>(a, grid, stream); break;
-        case 8: rc = launch_g<8>(a, grid, stream); break;
+        case 1: return launch_g<1>(a, grid, stream);
+        case 2: return launch_g<2>(a, grid, stream);
+        case 3: return launch_g<3>(a, grid, stream);
+        case 4: return launch_g<4>(a, grid, stream);
+        case 5: return launch_g<5>(a, grid, stream);
+        case 6: return launch_g<6>(a, grid, stream);
+        case 7: return launch_g<7>(a, grid, stream);
+        case 8: return launch_g<8>(a, grid, stream);
         default: return DQ_ERR_INVALID_ARG;
     }
-    if (rc != DQ_OK) return rc;
-    attn_merge_kernel<<<dim3(Hq, B), kD, 0, stream>>>(a.ws_m, a.ws_l, a.ws_acc, seq_lens, Hq,
-                                                      t_cap, a.chunk, a.nchunks, out);
-    return hip_check("kernel launch", hipGetLastError());
+}
+
+int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
+                           int32_t t_cap, const void* ws, float* out, hipStream_t stream) {
+    const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap);
+    const float* acc = static_cast<const float*>(ws);
+    const float* m = acc + plan.slots * kD;
+    const float* l = m + plan.slots;
+    attn_merge_kernel<<<dim3(Hq, B), kD, 0, stream>>>(m, l, acc, seq_lens, Hq, t_cap, plan.chunk,
+                                                      plan.nchunks, out);
+    return hip_check("attn_merge launch", hipGetLastError());
 }
 
 }  // namespace dq

@@ -310,22 +310,54 @@ size_t dq_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_c
     return dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, d);
 }
 
+static int check_attention(const dq_tables* tk, const dq_tables* tv, int32_t B, int32_t Hq,
+                           int32_t Hkv, int32_t t_cap) {
+    if (!table_args_ok(tk) || !table_args_ok(tv)) return DQ_ERR_INVALID_ARG;
+    if (tk->cfg.head_dim != 128 || tv->cfg.head_dim != 128) return DQ_ERR_INVALID_ARG;
+    if (B <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 8) return DQ_ERR_INVALID_ARG;
+    if (B > 65535 || Hkv > 65535) return DQ_ERR_INVALID_ARG;
+    if (t_cap <= 0 || t_cap % DQ_MEAN_WINDOW) return DQ_ERR_INVALID_ARG;
+    return DQ_OK;
+}
+
+int dq_decode_attention_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
+                                int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
+                                const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
+                                const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
+                                size_t ws_bytes, uint32_t* status, void* stream) {
+    int rc = check_attention(tk, tv, B, Hq, Hkv, t_cap);
+    if (rc != DQ_OK) return rc;
+    if (!q || !krec || !kmq || !kms || !vrec || !seq_lens) return DQ_ERR_INVALID_ARG;
+    if (!std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128))
+        return DQ_ERR_WORKSPACE;
+    return dq::launch_attention_partial(tk, tv, q, B, Hq, Hkv, krec, kmq, kms, vrec, seq_lens,
+                                        t_cap, scale, ws, status,
+                                        static_cast<hipStream_t>(stream));
+}
+
+int dq_decode_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
+                              int32_t t_cap, const void* ws, size_t ws_bytes, float* out,
+                              void* stream) {
+    if (B <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 8 || B > 65535)
+        return DQ_ERR_INVALID_ARG;
+    if (t_cap <= 0 || t_cap % DQ_MEAN_WINDOW || !seq_lens || !out) return DQ_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128))
+        return DQ_ERR_WORKSPACE;
+    return dq::launch_attention_merge(B, Hq, Hkv, seq_lens, t_cap, ws, out,
+                                      static_cast<hipStream_t>(stream));
+}
+
 int dq_decode_attention(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
                         int32_t Hq, int32_t Hkv, const uint8_t* krec, const int8_t* kmq,
                         const uint16_t* kms, const uint8_t* vrec, const int32_t* seq_lens,
                         int32_t t_cap, float scale, float* out, void* ws, size_t ws_bytes,
                         uint32_t* status, void* stream) {
-    if (!table_args_ok(tk) || !table_args_ok(tv)) return DQ_ERR_INVALID_ARG;
-    if (!q || !krec || !kmq || !kms || !vrec || !seq_lens || !out) return DQ_ERR_INVALID_ARG;
-    if (tk->cfg.head_dim != 128 || tv->cfg.head_dim != 128) return DQ_ERR_INVALID_ARG;
-    if (B <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 8) return DQ_ERR_INVALID_ARG;
-    if (t_cap <= 0 || t_cap % DQ_MEAN_WINDOW) return DQ_ERR_INVALID_ARG;
-    if (!std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
-    size_t need = dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128);
-    if (!ws || ws_bytes < need) return DQ_ERR_WORKSPACE;
-    return dq::launch_attention(tk, tv, q, B, Hq, Hkv, krec, kmq, kms, vrec, seq_lens, t_cap,
-                                scale, out, ws, ws_bytes, status,
-                                static_cast<hipStream_t>(stream));
+    if (!out) return DQ_ERR_INVALID_ARG;
+    int rc = dq_decode_attention_partial(tk, tv, q, B, Hq, Hkv, krec, kmq, kms, vrec, seq_lens,
+                                         t_cap, scale, ws, ws_bytes, status, stream);
+    if (rc != DQ_OK) return rc;
+    return dq_decode_attention_merge(B, Hq, Hkv, seq_lens, t_cap, ws, ws_bytes, out, stream);
 }
 
 int dq_decode_symbols(const dq_tables* t, const uint8_t* records, int64_t n_streams, uint8_t* sym,

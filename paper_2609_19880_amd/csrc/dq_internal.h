@@ -87,10 +87,13 @@ int launch_decode_symbols(const dq_tables* tab, const uint8_t* records, int64_t 
 
 size_t attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d);
 
-int launch_attention(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
-                     int32_t Hq, int32_t Hkv, const uint8_t* krec, const int8_t* kmq,
-                     const uint16_t* kms, const uint8_t* vrec, const int32_t* seq_lens,
-                     int32_t t_cap, float scale, float* out, void* ws, size_t ws_bytes,
-                     uint32_t* status, hipStream_t stream);
+int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
+                             int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
+                             const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
+                             const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
+                             uint32_t* status, hipStream_t stream);
+
+int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
+                           int32_t t_cap, const void* ws, float* out, hipStream_t stream);
 
 }  // namespace dq
