@@ -18,17 +18,22 @@
 //    head), then the inverse rotation of the value basis and the 1/d scale.
 #include <math.h>
 
+#include <algorithm>
+
 #include "dq_common.h"
 
 namespace dq {
 namespace {
 
-constexpr int kD = 128;         // head_dim of the attention kernels
-constexpr int kTile = 64;       // tokens per wavefront tile
-constexpr int kAttnWaves = 4;
-constexpr int kAttnThreads = kAttnWaves * kWave;
-constexpr int kVSlice = 32;     // value channels decoded between two PV passes
-constexpr int kTargetGroups = 2048;
+constexpr int kD = 128;          // head_dim of the attention kernels
+constexpr int kTile = 64;        // tokens per wavefront tile (one per lane)
+constexpr int kMaxWaves = 12;    // wavefronts per workgroup (LDS permitting)
+constexpr int kVSlice = 64;      // value channels per PV pass
+constexpr int kVRow = 68;        // bytes per channel row of the value tile (64 + pad)
+constexpr int kMaxRecDwords = 16;
+constexpr int kMaxLds = 160 * 1024;
+constexpr int kMinChunk = 512;
+constexpr int kWsHeader = 256;   // workspace header: chunk size, chunk count
 
 // ---------------------------------------------------------------- symbols
 
@@ -61,120 +66,187 @@ __global__ void decode_symbols_kernel(TabArgs ta, const uint8_t* __restrict__ re
 }
 
 // -------------------------------------------------------------- attention
+//
+// Work split.  One workgroup per (context chunk, KV head, sequence); each
+// wavefront takes 64-token tiles, one token per lane, and decodes that
+// token's key stream then its value stream (Alg. 2), 128 steps each.
+//
+// Decode step.  The table is staged in LDS as 8-byte entries
+// (f_m | m << 24, z - c_m), so the state update x' = f (x >> p) + (z - c) is a
+// single 24-bit multiply-add.  Renormalization bytes are staged per lane as
+// overlapping big-endian byte pairs P[k] = (b_k << 8) | b_{k+1}: one aligned
+// 16-bit LDS read yields the next 16 bits wherever the lane's byte pointer
+// stands, and with the leading-zero count of x' (x' >= 2^11 when p <= 12) the
+// number of bytes Alg. 2 reads, 0, 1 or 2, is sh/8 with sh = (clz(x') - 1) & 24:
+//     x = (x' << sh) | (P[ptr] >> (16 - sh)),   ptr += sh / 8.
+//
+// Contractions (Eq. fold-key / fold-value) run on the matrix cores with
+// v_mfma_i32_4x4x4_16b_i8 (16 blocks of 4x4x4; lane l is column l % 4 of
+// block l / 4).  Decoded levels are bytes and enter as they are; the rotated
+// query and the softmax weights (with the value scale folded in) enter as
+// three signed 8-bit digits of a 22-bit fixed-point value, accumulated exactly
+// in int32 and recombined in fp32.
+//   q . k:  block = 4 tokens, K = 4 channels.  A = the query digits of head
+//           l % 4, B = the 4 levels the lane just decoded, D = the lane's own
+//           token's dot products for 4 heads.
+//   P . v:  block = 4 channels, K = 4 tokens.  Levels go through a 4x4 byte
+//           transpose inside each lane quad and a channel-major LDS tile;
+//           D = 4 heads of channel l of the 64-channel slice.
 
 struct AttnLayout {
-    int lutk, lutv, qr, qsum, qmu, waves, wave_stride;
-    int krec, vrec, vt, pv;   // offsets inside a wave region
+    int nw;             // wavefronts per workgroup
+    int lut_k, lut_v;   // 8-byte tables (the same offset when K and V share one)
+    int qlimb;          // [32 channel groups][GP heads] x 16 B (three digit words)
+    int qscale, qsum;   // float [GP]
+    int qmu;            // float [windows][GP]
+    int waves;          // first wavefront region
+    int wave_stride;
+    int p16, p16_stride;    // byte pairs, per lane
+    int vtile;              // [64 channels][kVRow] bytes
+    int plimb;              // [HG][3 digits][4 heads][64 tokens] bytes
     int total;
 };
 
-__host__ __device__ inline int align16(int v) { return (v + 15) & ~15; }
+__host__ inline int align16(int v) { return (v + 15) & ~15; }
 
-__host__ __device__ inline AttnLayout attn_layout(int pk, int pv_bits, int Ck, int Cv, int G,
-                                                  int chunk) {
-    AttnLayout L;
-    int off = 0;
-    L.lutk = off;
-    off += align16(4 << pk);
-    L.lutv = off;
-    off += align16(4 << pv_bits);
-    // the merge at the end reuses [0, ...) : make it large enough
-    const int merge = kAttnWaves * (2 * G + G * kD) * 4;
-    if (off < merge) off = align16(merge);
-    L.qr = off;
-    off += align16(kD * G * 4);
-    L.qsum = off;
-    off += align16(G * 4);
-    L.qmu = off;
-    off += align16((chunk / DQ_MEAN_WINDOW) * G * 4);
-    L.waves = off;
-    int w = 0;
-    L.krec = w;
-    w += align16(kTile * Ck);
-    L.vrec = w;
-    w += align16(kTile * Cv);
-    L.vt = w;
-    w += align16(kTile * kVSlice);
-    L.pv = w;
-    w += align16(kTile * G * 4);
-    // the query rotation before the main loop uses the wave regions as scratch
-    if (w * kAttnWaves < G * kD * 4) w = align16((G * kD * 4 + kAttnWaves - 1) / kAttnWaves);
-    L.wave_stride = w;
-    off += kAttnWaves * w;
-    L.total = off;
-    return L;
+__host__ inline int p16_stride_for(int C) {
+    int s = (2 * (C - kPayloadOffset) + 3) & ~3;   // 2 bytes per byte position
+    if (((s / 4) & 1) == 0) s += 4;                 // odd dword stride: no bank conflicts
+    return s;
 }
 
 struct AttnArgs {
     TabArgs tk, tv;
     const uint16_t* q;
-    int Hq, Hkv, t_cap, chunk, nchunks;
+    int Hq, Hkv, G, t_cap, chunk, nchunks;
     const uint8_t* krec;
     const int8_t* kmq;
     const uint16_t* kms;
     const uint8_t* vrec;
     const int32_t* seq_lens;
     float scale_log2;            // softmax_scale * log2(e) / d
+    int32_t* ws_hdr;             // [0] chunk, [1] chunk count
     float* ws_m;                 // [B][Hq][NC]
     float* ws_l;                 // [B][Hq][NC]
     float* ws_acc;               // [B][Hq][NC][d]
     uint32_t* status;
+    int shared_lut;
     AttnLayout L;
 };
 
-__device__ __forceinline__ uint32_t rd_u32(const uint8_t* p) {
-    return (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16) | ((uint32_t)p[3] << 24);
+__device__ __forceinline__ float half_lo(uint32_t w) { return half_bits_to_f32((uint16_t)(w & 0xFFFFu)); }
+__device__ __forceinline__ float half_hi(uint32_t w) { return half_bits_to_f32((uint16_t)(w >> 16)); }
+
+// One step of Alg. 2.  Returns the table word (level in its top byte).
+__device__ __forceinline__ uint32_t dstep(uint32_t& x, uint32_t& pq, const uint8_t* lds,
+                                          uint32_t lut_off, uint32_t mask8, int p) {
+    const uint2 e = *reinterpret_cast<const uint2*>(lds + lut_off + ((x << 3) & mask8));
+    const uint32_t pair = *reinterpret_cast<const uint16_t*>(lds + pq);
+    const uint32_t xp = __umul24(e.x, x >> p) + e.y;
+    const uint32_t sh = ((uint32_t)__clz(xp) - 1u) & 24u;
+    x = (xp << sh) | (pair >> (16u - sh));
+    pq += sh >> 2;
+    return e.x;
 }
 
-__device__ __forceinline__ float rd_half(const uint8_t* p) {
-    return half_bits_to_f32((uint16_t)(p[0] | (p[1] << 8)));
+// Levels of four consecutive steps (top bytes of the table words) as one word.
+__device__ __forceinline__ uint32_t pack4(uint32_t e0, uint32_t e1, uint32_t e2, uint32_t e3) {
+    const uint32_t lo = __builtin_amdgcn_perm(e1, e0, 0x0c0c0703u);
+    const uint32_t hi = __builtin_amdgcn_perm(e3, e2, 0x07030c0cu);
+    return lo | hi;
 }
 
-// One step of Alg. 2 on an LDS-resident record: table lookup, state update
-// and up to two renormalization bytes (x >= 2^23 and p <= 12 need no more).
-__device__ __forceinline__ uint32_t rans_step(uint32_t& x, int& ptr, const uint32_t* lut,
-                                              uint32_t mask, int p, const uint8_t* rb, int C) {
-    const uint32_t e = lut[x & mask];
-    x = ((e >> 12) & 0xFFFu) * (x >> p) + (e & 0xFFFu);
+// 4x4 byte transpose inside each lane quad: lane 4q+i holds row i on input
+// and column i on output.
+__device__ __forceinline__ uint32_t quad_transpose(uint32_t w, uint32_t sel1, uint32_t sel2) {
+    const uint32_t p1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)w, 0xB1, 0xF, 0xF, false);
+    const uint32_t r = __builtin_amdgcn_perm(p1, w, sel1);
+    const uint32_t p2 = (uint32_t)__builtin_amdgcn_mov_dpp((int)r, 0x4E, 0xF, 0xF, false);
+    return __builtin_amdgcn_perm(p2, r, sel2);
+}
+
+// Three signed 8-bit digits of v in [-2^22, 2^22]: v = d2 2^16 + d1 2^8 + d0.
+__device__ __forceinline__ void digits3(int v, int& d0, int& d1, int& d2) {
+    d0 = ((v + 128) & 255) - 128;
+    const int v1 = (v - d0) >> 8;
+    d1 = ((v1 + 128) & 255) - 128;
+    d2 = (v1 - d1) >> 8;
+}
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4i mfma(uint32_t a, uint32_t b, v4i c) {
+    return __builtin_amdgcn_mfma_i32_4x4x4i8((int)a, (int)b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float combine(const v4i& d0, const v4i& d1, const v4i& d2, int r) {
+    return (float)d2[r] * 65536.0f + (float)d1[r] * 256.0f + (float)d0[r];
+}
+
+// Record dwords of the lane's token (C % 4 == 0, C <= 64).
+__device__ __forceinline__ void load_record(uint32_t (&r)[kMaxRecDwords], const uint8_t* recs,
+                                            int64_t tok, int CW) {
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(recs + tok * (CW * 4));
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-        const bool need = x < kRansL;
-        const uint32_t byte = rb[min(ptr, C - 1)];
-        x = need ? ((x << 8) | byte) : x;
-        ptr += need ? 1 : 0;
-    }
-    return e >> 24;
+    for (int k = 0; k < kMaxRecDwords; ++k)
+        if (k < CW) r[k] = src[k];
 }
 
-template <int G>
-__global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(AttnArgs a) {
+// Payload bytes of a record -> the lane's byte-pair array.
+__device__ __forceinline__ void build_pairs(const uint32_t (&r)[kMaxRecDwords], int CW, uint8_t* dst) {
+#pragma unroll
+    for (int k = 2; k < kMaxRecDwords; ++k) {
+        if (k < CW) {
+            const uint32_t w = r[k];
+            const uint32_t wn = (k + 1 < CW) ? r[(k + 1) & (kMaxRecDwords - 1)] : 0u;
+            uint32_t* d = reinterpret_cast<uint32_t*>(dst + 8 * (k - 2));
+            d[0] = __builtin_amdgcn_perm(w, w, 0x01020001u);
+            d[1] = __builtin_amdgcn_perm(wn, w, 0x03040203u);
+        }
+    }
+}
+
+// Wavefronts per workgroup: 12 (3 per SIMD) for up to 4 query heads per KV
+// head; 8 for up to 8, whose accumulators need more registers.
+__host__ __device__ constexpr int max_waves(int HG) { return HG == 1 ? kMaxWaves : 8; }
+
+template <int HG>
+__global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(AttnArgs a) {
+    constexpr int GP = 4 * HG;
     extern __shared__ __align__(16) uint8_t smem[];
     const AttnLayout& L = a.L;
-    uint32_t* lutk = reinterpret_cast<uint32_t*>(smem + L.lutk);
-    uint32_t* lutv = reinterpret_cast<uint32_t*>(smem + L.lutv);
-    float* qr = reinterpret_cast<float*>(smem + L.qr);        // [d][G]
-    float* qsum = reinterpret_cast<float*>(smem + L.qsum);    // [G]
-    float* qmu = reinterpret_cast<float*>(smem + L.qmu);      // [chunk/128][G]
-
+    const int G = a.G;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int nthr = L.nw * kWave;
     const int c = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    if ((c | h | b) == 0 && tid == 0) {
+        a.ws_hdr[0] = a.chunk;
+        a.ws_hdr[1] = a.nchunks;
+    }
     const int T = min(a.seq_lens[b], a.t_cap);
     const int start = c * a.chunk;
     if (start >= T) return;   // the merge ignores chunks past the length
 
-    const int Ck = a.tk.C, Cv = a.tv.C;
-    const int pk = a.tk.p, pvb = a.tv.p;
-    for (int i = tid; i < (1 << pk); i += kAttnThreads) lutk[i] = a.tk.t.lut[i];
-    for (int i = tid; i < (1 << pvb); i += kAttnThreads) lutv[i] = a.tv.t.lut[i];
-
-    // Rotate the G query heads: unnormalized FWHT in fp32 (scratch in the wave regions).
-    float* qt = reinterpret_cast<float*>(smem + L.waves);     // [G][d]
+    // ---- prologue: tables, rotated query, its digits, q . mu per window
+    {
+        const int Pk = 1 << a.tk.p, Pv = 1 << a.tv.p;
+        uint2* lk = reinterpret_cast<uint2*>(smem + L.lut_k);
+        for (int i = tid; i < Pk; i += nthr) lk[i] = a.tk.t.lut64[i];
+        if (!a.shared_lut) {
+            uint2* lv = reinterpret_cast<uint2*>(smem + L.lut_v);
+            for (int i = tid; i < Pv; i += nthr) lv[i] = a.tv.t.lut64[i];
+        }
+    }
+    float* qt = reinterpret_cast<float*>(smem + L.waves);          // [G][d] scratch
+    float* qscale = reinterpret_cast<float*>(smem + L.qscale);
+    float* qsum = reinterpret_cast<float*>(smem + L.qsum);
+    float* qmu = reinterpret_cast<float*>(smem + L.qmu);
+    uint8_t* qlimb = smem + L.qlimb;
     const int hq0 = h * G;
-    for (int i = tid; i < G * kD; i += kAttnThreads)
-        qt[i] = bf16_to_f32(a.q[((int64_t)b * a.Hq + hq0) * kD + i]);
+    for (int i = tid; i < G * kD; i += nthr) qt[i] = bf16_to_f32(a.q[((int64_t)b * a.Hq + hq0) * kD + i]);
     __syncthreads();
     for (int hh = 1; hh < kD; hh <<= 1) {
-        for (int i = tid; i < G * (kD / 2); i += kAttnThreads) {
+        for (int i = tid; i < G * (kD / 2); i += nthr) {
             const int g = i / (kD / 2), r = i % (kD / 2);
             const int lo = (r / hh) * 2 * hh + (r % hh);
             const float x0 = qt[g * kD + lo], x1 = qt[g * kD + lo + hh];
@@ -183,171 +255,238 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(AttnArgs a) 
         }
         __syncthreads();
     }
-    for (int i = tid; i < G * kD; i += kAttnThreads) {
-        const int g = i / kD, j = i % kD;
-        qr[j * G + g] = qt[i];
+    if (tid < GP) {
+        float mx = 0.f, sm = 0.f;
+        if (tid < G) {
+            for (int j = 0; j < kD; ++j) {
+                mx = fmaxf(mx, fabsf(qt[tid * kD + j]));
+                sm += qt[tid * kD + j];
+            }
+        }
+        qscale[tid] = mx * (1.0f / 4194304.0f);
+        qsum[tid] = sm;
     }
     __syncthreads();
-    if (tid < G) {
-        float s = 0.f;
-        for (int j = 0; j < kD; ++j) s += qr[j * G + tid];
-        qsum[tid] = s;
+    for (int i = tid; i < GP * kD; i += nthr) {
+        const int g = i / kD, j = i % kD;
+        int v = 0;
+        if (g < G && qscale[g] > 0.f) {
+            v = (int)rintf(qt[g * kD + j] / qscale[g]);
+            v = max(-4194304, min(4194304, v));
+        }
+        int d0, d1, d2;
+        digits3(v, d0, d1, d2);
+        uint8_t* dst = qlimb + ((j / 4) * GP + g) * 16 + (j % 4);
+        dst[0] = (uint8_t)d0;
+        dst[4] = (uint8_t)d1;
+        dst[8] = (uint8_t)d2;
+        dst[12] = 0;
     }
-    // q . mu_hat for every key-mean window of the chunk
     const int nwin_total = a.t_cap / DQ_MEAN_WINDOW;
     const int w0 = start / DQ_MEAN_WINDOW;
-    const int nwin = a.chunk / DQ_MEAN_WINDOW;
-    for (int i = tid; i < nwin * G; i += kAttnThreads) {
-        const int wi = i / G, g = i % G;
+    const int nwin = (a.chunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1;
+    for (int i = tid; i < nwin * GP; i += nthr) {
+        const int wi = i / GP, g = i % GP;
         float s = 0.f;
-        if (w0 + wi < nwin_total) {
+        if (g < G && w0 + wi < nwin_total) {
             const int64_t widx = (int64_t)(b * a.Hkv + h) * nwin_total + w0 + wi;
             const float sc = half_bits_to_f32(a.kms[widx]);
             const int8_t* mq = a.kmq + widx * kD;
-            for (int j = 0; j < kD; ++j) s += qr[j * G + g] * (sc * (float)mq[j]);
+            for (int j = 0; j < kD; ++j) s += qt[g * kD + j] * (sc * (float)mq[j]);
         }
         qmu[i] = s;
     }
     __syncthreads();
 
+    // ---- per-wavefront state
     uint8_t* wreg = smem + L.waves + wave * L.wave_stride;
-    uint8_t* krs = wreg + L.krec;
-    uint8_t* vrs = wreg + L.vrec;
-    uint8_t* vt = wreg + L.vt;
-    float* pvw = reinterpret_cast<float*>(wreg + L.pv);
+    const uint32_t p16_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.p16 + lane * L.p16_stride);
+    uint8_t* vtile = wreg + L.vtile;
+    uint8_t* plimb = wreg + L.plimb;
+    const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
+    const uint32_t sel2 = (lane & 2) ? 0x03020706u : 0x05040100u;
+    const int Ck = a.tk.C, Cv = a.tv.C, CWk = Ck / 4, CWv = Cv / 4;
+    const int pk = a.tk.p, pvb = a.tv.p;
+    const uint32_t mask8k = ((1u << pk) - 1u) << 3, mask8v = ((1u << pvb) - 1u) << 3;
+    const uint32_t lutk_off = (uint32_t)L.lut_k, lutv_off = (uint32_t)L.lut_v;
+    const int64_t bh = (int64_t)b * a.Hkv + h;
 
-    float m_run[G], l_part[G], acco[G], accv[kD / kVSlice][G];
+    float m_run[GP], l_part[GP], acco[GP], accf[2][GP];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
+    for (int g = 0; g < GP; ++g) {
         m_run[g] = -INFINITY;
         l_part[g] = 0.f;
         acco[g] = 0.f;
-#pragma unroll
-        for (int s = 0; s < kD / kVSlice; ++s) accv[s][g] = 0.f;
+        accf[0][g] = 0.f;
+        accf[1][g] = 0.f;
     }
-    const uint32_t maskk = (1u << pk) - 1u, maskv = (1u << pvb) - 1u;
-    const int64_t bh = (int64_t)b * a.Hkv + h;
     bool corrupt = false;
+    const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
+    uint32_t kr[kMaxRecDwords], vr[kMaxRecDwords];
+    if (wave < ntiles) {
+        const int64_t tok = bh * a.t_cap + start + wave * kTile + lane;
+        load_record(kr, a.krec, tok, CWk);
+        load_record(vr, a.vrec, tok, CWv);
+    }
 
-    const int ntiles = a.chunk / kTile;
-    for (int tile = wave; tile < ntiles; tile += kAttnWaves) {
+    for (int tile = wave; tile < ntiles; tile += L.nw) {
         const int t_base = start + tile * kTile;
-        if (t_base >= T) break;
-        {
-            const uint4* src = reinterpret_cast<const uint4*>(a.krec + (bh * a.t_cap + t_base) * Ck);
-            uint4* dst = reinterpret_cast<uint4*>(krs);
-            for (int i = lane; i < 4 * Ck; i += kWave) dst[i] = src[i];
-            const uint4* srcv = reinterpret_cast<const uint4*>(a.vrec + (bh * a.t_cap + t_base) * Cv);
-            uint4* dstv = reinterpret_cast<uint4*>(vrs);
-            for (int i = lane; i < 4 * Cv; i += kWave) dstv[i] = srcv[i];
-        }
-        wave_sync();
         const int t = t_base + lane;
         const bool valid = t < T;
+        const bool more = tile + L.nw < ntiles;
+        const int64_t next_tok = bh * a.t_cap + t_base + L.nw * kTile + lane;
 
-        // keys: Eq. (fold-key)
-        const uint8_t* rk = krs + lane * Ck;
-        const float sk = rd_half(rk), ok = rd_half(rk + 2);
-        uint32_t x = rd_u32(rk + 4);
-        int ptr = kPayloadOffset;
-        float acc[G];
+        // ---- keys
+        build_pairs(kr, CWk, smem + p16_lane);
+        const float sk = half_lo(kr[0]), ok = half_hi(kr[0]);
+        uint32_t x = kr[1];
+        uint32_t pq = p16_lane;
+        if (more) load_record(kr, a.krec, next_tok, CWk);
+        v4i dk[HG][3];
 #pragma unroll
-        for (int g = 0; g < G; ++g) acc[g] = 0.f;
+        for (int hg = 0; hg < HG; ++hg)
+#pragma unroll
+            for (int d = 0; d < 3; ++d) dk[hg][d] = v4i{0, 0, 0, 0};
 #pragma unroll 2
-        for (int j = 0; j < kD; ++j) {
-            const float lv = (float)rans_step(x, ptr, lutk, maskk, pk, rk, Ck);
-            const float* qj = qr + j * G;
+        for (int grp = 0; grp < kD / 4; ++grp) {
+            const uint32_t e0 = dstep(x, pq, smem, lutk_off, mask8k, pk);
+            const uint32_t e1 = dstep(x, pq, smem, lutk_off, mask8k, pk);
+            const uint32_t e2 = dstep(x, pq, smem, lutk_off, mask8k, pk);
+            const uint32_t e3 = dstep(x, pq, smem, lutk_off, mask8k, pk);
+            const uint32_t lv = pack4(e0, e1, e2, e3);
 #pragma unroll
-            for (int g = 0; g < G; ++g) acc[g] = fmaf(qj[g], lv, acc[g]);
+            for (int hg = 0; hg < HG; ++hg) {
+                const uint4 ql = *reinterpret_cast<const uint4*>(qlimb + ((grp * GP) + hg * 4 + (lane & 3)) * 16);
+                dk[hg][0] = mfma(ql.x, lv, dk[hg][0]);
+                dk[hg][1] = mfma(ql.y, lv, dk[hg][1]);
+                dk[hg][2] = mfma(ql.z, lv, dk[hg][2]);
+            }
         }
-        corrupt |= valid && (x != kRansL || ptr > Ck);
-        const float* qm = qmu + ((t / DQ_MEAN_WINDOW) - w0) * G;
-        float score[G];
+        corrupt |= valid && (x != kRansL || pq > p16_lane + 2u * (uint32_t)(Ck - kPayloadOffset));
+        const float* qm = qmu + ((t / DQ_MEAN_WINDOW) - w0) * GP;
+        float score[GP];
 #pragma unroll
-        for (int g = 0; g < G; ++g)
-            score[g] = valid ? (sk * acc[g] + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
+        for (int hg = 0; hg < HG; ++hg)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int g = 4 * hg + r;
+                const float dot = combine(dk[hg][0], dk[hg][1], dk[hg][2], r) * qscale[g];
+                score[g] = (valid && g < G) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
+            }
 
-        // online softmax; value scale folded into the weight (Eq. fold-value)
-        const uint8_t* rv = vrs + lane * Cv;
-        const float sv = rd_half(rv), ov = rd_half(rv + 2);
-        uint32_t xv = rd_u32(rv + 4);
-        int ptrv = kPayloadOffset;
+        // ---- online softmax; the value scale is folded into the weight
+        build_pairs(vr, CWv, smem + p16_lane);
+        const float sv = half_lo(vr[0]), ov = half_hi(vr[0]);
+        uint32_t xv = vr[1];
+        uint32_t pv = p16_lane;
+        if (more) load_record(vr, a.vrec, next_tok, CWv);
+        float pscale[GP];
+        int pint[GP];
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
+        for (int g = 0; g < GP; ++g) {
             const float tmax = wave_max(score[g]);
             const float mn = fmaxf(m_run[g], tmax);
-            const float corr = (m_run[g] == -INFINITY) ? 0.f : exp2f(m_run[g] - mn);
-            const float p = valid ? exp2f(score[g] - mn) : 0.f;
+            const float corr = (m_run[g] == -INFINITY || mn == -INFINITY) ? (m_run[g] == mn ? 1.f : 0.f)
+                                                                           : exp2f(m_run[g] - mn);
+            const float p = (score[g] == -INFINITY) ? 0.f : exp2f(score[g] - mn);
             l_part[g] = l_part[g] * corr + p;
             acco[g] = acco[g] * corr + p * ov;
-#pragma unroll
-            for (int s = 0; s < kD / kVSlice; ++s) accv[s][g] *= corr;
+            accf[0][g] *= corr;
+            accf[1][g] *= corr;
             m_run[g] = mn;
-            pvw[lane * G + g] = p * sv;
+            const float pw = p * sv;
+            const float smax = wave_max(pw);
+            pscale[g] = smax * (1.0f / 4194304.0f);
+            pint[g] = smax > 0.f ? min(4194304, (int)rintf(pw / pscale[g])) : 0;
+        }
+        // weight digits -> LDS [hg][digit][head][token] via the quad transpose
+#pragma unroll
+        for (int hg = 0; hg < HG; ++hg) {
+            int dd[4][3];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) digits3(pint[4 * hg + r], dd[r][0], dd[r][1], dd[r][2]);
+#pragma unroll
+            for (int d = 0; d < 3; ++d) {
+                const uint32_t w = ((uint32_t)dd[0][d] & 0xFFu) | (((uint32_t)dd[1][d] & 0xFFu) << 8) |
+                                   (((uint32_t)dd[2][d] & 0xFFu) << 16) | ((uint32_t)dd[3][d] << 24);
+                const uint32_t wt = quad_transpose(w, sel1, sel2);
+                *reinterpret_cast<uint32_t*>(plimb + ((hg * 3 + d) * 4 + (lane & 3)) * kTile + (lane >> 2) * 4) = wt;
+            }
         }
 
-        // values: decode a slice of channels into LDS, then accumulate it
-        const int ch = lane & (kVSlice - 1), half = lane / kVSlice;
+        // ---- values, two slices of 64 channels
 #pragma unroll
-        for (int s = 0; s < kD / kVSlice; ++s) {
+        for (int s = 0; s < 2; ++s) {
 #pragma unroll 2
-            for (int jj = 0; jj < kVSlice; ++jj)
-                vt[lane * kVSlice + jj] = (uint8_t)rans_step(xv, ptrv, lutv, maskv, pvb, rv, Cv);
-            wave_sync();
-#pragma unroll 4
-            for (int tt = 0; tt < kTile / 2; ++tt) {
-                const int tok = half * (kTile / 2) + tt;
-                const float lv = (float)vt[tok * kVSlice + ch];
-                const float* pw = pvw + tok * G;
-#pragma unroll
-                for (int g = 0; g < G; ++g) accv[s][g] = fmaf(pw[g], lv, accv[s][g]);
+            for (int grp = 0; grp < kVSlice / 4; ++grp) {
+                const uint32_t e0 = dstep(xv, pv, smem, lutv_off, mask8v, pvb);
+                const uint32_t e1 = dstep(xv, pv, smem, lutv_off, mask8v, pvb);
+                const uint32_t e2 = dstep(xv, pv, smem, lutv_off, mask8v, pvb);
+                const uint32_t e3 = dstep(xv, pv, smem, lutv_off, mask8v, pvb);
+                const uint32_t wt = quad_transpose(pack4(e0, e1, e2, e3), sel1, sel2);
+                *reinterpret_cast<uint32_t*>(vtile + (grp * 4 + (lane & 3)) * kVRow + (lane >> 2) * 4) = wt;
             }
             wave_sync();
+            v4i dv[HG][3];
+#pragma unroll
+            for (int hg = 0; hg < HG; ++hg)
+#pragma unroll
+                for (int d = 0; d < 3; ++d) dv[hg][d] = v4i{0, 0, 0, 0};
+#pragma unroll 4
+            for (int qd = 0; qd < kTile / 4; ++qd) {
+                const uint32_t bv = *reinterpret_cast<const uint32_t*>(vtile + lane * kVRow + qd * 4);
+#pragma unroll
+                for (int hg = 0; hg < HG; ++hg) {
+                    const uint8_t* pl = plimb + (hg * 12 + (lane & 3)) * kTile + qd * 4;
+                    dv[hg][0] = mfma(*reinterpret_cast<const uint32_t*>(pl), bv, dv[hg][0]);
+                    dv[hg][1] = mfma(*reinterpret_cast<const uint32_t*>(pl + 4 * kTile), bv, dv[hg][1]);
+                    dv[hg][2] = mfma(*reinterpret_cast<const uint32_t*>(pl + 8 * kTile), bv, dv[hg][2]);
+                }
+            }
+#pragma unroll
+            for (int hg = 0; hg < HG; ++hg)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    accf[s][4 * hg + r] += combine(dv[hg][0], dv[hg][1], dv[hg][2], r) * pscale[4 * hg + r];
+            wave_sync();
         }
-        corrupt |= valid && (xv != kRansL || ptrv > Cv);
+        corrupt |= valid && (xv != kRansL || pv > p16_lane + 2u * (uint32_t)(Cv - kPayloadOffset));
     }
     if (__any(corrupt) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_CORRUPT);
 
-    // combine the two token halves, then the four wavefronts
-    float l_tot[G], o_tot[G];
+    // ---- merge the wavefronts of the workgroup
+    float l_tot[GP], o_tot[GP];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-#pragma unroll
-        for (int s = 0; s < kD / kVSlice; ++s) accv[s][g] += __shfl_xor(accv[s][g], 32);
+    for (int g = 0; g < GP; ++g) {
         l_tot[g] = wave_sum_f32(l_part[g]);
         o_tot[g] = wave_sum_f32(acco[g]);
     }
-    __syncthreads();   // every wavefront is done with the tables
-    float* mw = reinterpret_cast<float*>(smem);               // [waves][G]
-    float* lw = mw + kAttnWaves * G;                          // [waves][G]
-    float* aw = lw + kAttnWaves * G;                          // [waves][G][d]
+    __syncthreads();   // every wavefront is done with LDS
+    float* mw = reinterpret_cast<float*>(smem);        // [nw][GP]
+    float* lw = mw + L.nw * GP;                        // [nw][GP]
+    float* aw = lw + L.nw * GP;                        // [nw][GP][d]
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
+    for (int g = 0; g < GP; ++g) {
         if (lane == 0) {
-            mw[wave * G + g] = m_run[g];
-            lw[wave * G + g] = l_tot[g];
+            mw[wave * GP + g] = m_run[g];
+            lw[wave * GP + g] = l_tot[g];
         }
-        if (lane < kVSlice) {
-#pragma unroll
-            for (int s = 0; s < kD / kVSlice; ++s)
-                aw[(wave * G + g) * kD + s * kVSlice + lane] = accv[s][g] + o_tot[g];
-        }
+        aw[(wave * GP + g) * kD + lane] = accf[0][g] + o_tot[g];
+        aw[(wave * GP + g) * kD + kVSlice + lane] = accf[1][g] + o_tot[g];
     }
     __syncthreads();
     const int NC = a.nchunks;
-    for (int i = tid; i < G * kD; i += kAttnThreads) {
+    for (int i = tid; i < G * kD; i += nthr) {
         const int g = i / kD, j = i % kD;
         float M = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, mw[w * G + g]);
+        for (int w = 0; w < L.nw; ++w) M = fmaxf(M, mw[w * GP + g]);
         float acc = 0.f, l = 0.f;
-#pragma unroll
-        for (int w = 0; w < kAttnWaves; ++w) {
-            const float mv = mw[w * G + g];
+        for (int w = 0; w < L.nw; ++w) {
+            const float mv = mw[w * GP + g];
             if (mv == -INFINITY) continue;
             const float e = exp2f(mv - M);
-            acc += aw[(w * G + g) * kD + j] * e;
-            l += lw[w * G + g] * e;
+            acc += aw[(w * GP + g) * kD + j] * e;
+            l += lw[w * GP + g] * e;
         }
         const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * NC + c;
         a.ws_acc[slot * kD + j] = acc;
@@ -358,21 +497,22 @@ __global__ __launch_bounds__(kAttnThreads) void attn_partial_kernel(AttnArgs a) 
     }
 }
 
-__global__ __launch_bounds__(kD) void attn_merge_kernel(const float* __restrict__ ws_m,
+__global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restrict__ ws_hdr,
+                                                        const float* __restrict__ ws_m,
                                                         const float* __restrict__ ws_l,
                                                         const float* __restrict__ ws_acc,
                                                         const int32_t* __restrict__ seq_lens,
-                                                        int Hq, int t_cap, int chunk, int NC,
-                                                        float* __restrict__ out) {
+                                                        int Hq, int t_cap, float* __restrict__ out) {
     __shared__ float o[kD];
     const int hq = blockIdx.x, b = blockIdx.y, j = threadIdx.x;
+    const int chunk = ws_hdr[0], NC = ws_hdr[1];
     const int T = min(seq_lens[b], t_cap);
     float* dst = out + ((int64_t)b * Hq + hq) * kD;
     if (T <= 0) {
         dst[j] = 0.f;
         return;
     }
-    const int nc = (T + chunk - 1) / chunk;
+    const int nc = min(NC, (T + chunk - 1) / chunk);
     const int64_t base = ((int64_t)b * Hq + hq) * NC;
     float M = -INFINITY;
     for (int c = 0; c < nc; ++c) M = fmaxf(M, ws_m[base + c]);
@@ -386,7 +526,7 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const float* __restrict_
     __syncthreads();
     // inverse rotation of the value basis: H v / d
     for (int hh = 1; hh < kD; hh <<= 1) {
-        float mine = o[j], other = o[j ^ hh];
+        const float mine = o[j], other = o[j ^ hh];
         __syncthreads();
         o[j] = (j & hh) ? (other - mine) : (mine + other);
         __syncthreads();
@@ -394,13 +534,69 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const float* __restrict_
     dst[j] = o[j] * (1.0f / kD);
 }
 
-int choose_chunk(int B, int Hkv, int t_cap) {
-    const int units = (t_cap + 255) / 256;
-    long long k = ((long long)B * Hkv * units) / kTargetGroups;
-    if (k < 1) k = 1;
-    if (k > 16) k = 16;
-    if (k > units) k = units;
-    return 256 * (int)k;
+// LDS layout for given coding sizes; picks the largest wavefront count that fits.
+AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut) {
+    const int GP = G <= 4 ? 4 : 8, HG = GP / 4;
+    AttnLayout L;
+    int off = 0;
+    L.lut_k = off;
+    off += align16(8 << pk);
+    if (shared_lut) {
+        L.lut_v = L.lut_k;
+    } else {
+        L.lut_v = off;
+        off += align16(8 << pvb);
+    }
+    L.qlimb = off;
+    off += align16((kD / 4) * GP * 16);
+    L.qscale = off;
+    off += align16(GP * 4);
+    L.qsum = off;
+    off += align16(GP * 4);
+    L.qmu = off;
+    off += align16(((4096 + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1) * GP * 4);
+    L.waves = off;
+    L.p16_stride = std::max(p16_stride_for(Ck), p16_stride_for(Cv));
+    int w = 0;
+    L.p16 = w;
+    w += align16(kTile * L.p16_stride);
+    L.vtile = w;
+    w += align16(kVSlice * kVRow);
+    L.plimb = w;
+    w += align16(HG * 3 * 4 * kTile);
+    L.wave_stride = w;
+    int nw = (kMaxLds - off) / w;
+    if (nw > max_waves(HG)) nw = max_waves(HG);
+    // the query rotation scratch and the final merge must fit as well
+    while (nw > 0 && (nw * w < G * kD * 4 ||
+                      off + nw * w < nw * (2 * GP + GP * kD) * 4))
+        --nw;
+    L.nw = nw;
+    L.total = off + nw * w;
+    return L;
+}
+
+struct ChunkPlan {
+    int chunk, nchunks;
+    int64_t slots_max;
+};
+
+int64_t max_chunks(int t_cap) { return (t_cap + kMinChunk - 1) / kMinChunk; }
+
+// Chunk = a whole number of passes of the workgroup (nw x 64 tokens), at
+// least kMinChunk tokens, sized for about two thousand workgroups.
+ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap, int nw) {
+    ChunkPlan p;
+    const int pass = nw * kTile;
+    int k = (int)(((int64_t)B * Hkv * t_cap) / ((int64_t)pass * 2048));
+    k = std::max(k, (kMinChunk + pass - 1) / pass);
+    k = std::min(k, std::max(1, 4096 / pass));
+    p.chunk = pass * k;
+    if (p.chunk > t_cap) p.chunk = ((t_cap + pass - 1) / pass) * pass;
+    if (p.chunk < kMinChunk) p.chunk = kMinChunk;
+    p.nchunks = (t_cap + p.chunk - 1) / p.chunk;
+    p.slots_max = (int64_t)B * Hq * max_chunks(t_cap);
+    return p;
 }
 
 }  // namespace
@@ -413,37 +609,31 @@ int launch_decode_symbols(const dq_tables* tab, const uint8_t* records, int64_t 
     if (blocks > 0x7FFFFFFF) return DQ_ERR_INVALID_ARG;
     decode_symbols_kernel<<<dim3((unsigned)blocks), threads, 0, stream>>>(ta, records, n_streams,
                                                                          sym, header, status);
-    return hip_check("kernel launch", hipGetLastError());
+    return hip_check("decode_symbols launch", hipGetLastError());
 }
 
 size_t attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d) {
-    const int chunk = choose_chunk(B, Hkv, t_cap);
-    const int64_t NC = (t_cap + chunk - 1) / chunk;
-    const int64_t slots = (int64_t)B * Hq * NC;
-    return (size_t)(slots * d + 2 * slots) * sizeof(float) + 256;
+    (void)Hkv;
+    const int64_t slots = (int64_t)B * Hq * max_chunks(t_cap);
+    return (size_t)kWsHeader + (size_t)(slots * d + 2 * slots) * sizeof(float);
 }
 
-template <int G>
-static int launch_g(AttnArgs& a, dim3 grid, hipStream_t stream) {
+bool attention_supports(const dq_tables* tk, const dq_tables* tv) {
+    for (const dq_tables* t : {tk, tv}) {
+        const int C = t->cfg.record_bytes;
+        if (C % 4 || C < 12 || C > 4 * kMaxRecDwords) return false;
+    }
+    return true;
+}
+
+template <int HG>
+static int launch_hg(AttnArgs& a, dim3 grid, hipStream_t stream) {
     if (int rc = hip_check("hipFuncSetAttribute",
-                           hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_partial_kernel<G>),
+                           hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_partial_kernel<HG>),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
         return rc;
-    attn_partial_kernel<G><<<grid, kAttnThreads, a.L.total, stream>>>(a);
-    return hip_check("kernel launch", hipGetLastError());
-}
-
-struct ChunkPlan {
-    int chunk, nchunks;
-    int64_t slots;
-};
-
-static ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap) {
-    ChunkPlan p;
-    p.chunk = choose_chunk(B, Hkv, t_cap);
-    p.nchunks = (t_cap + p.chunk - 1) / p.chunk;
-    p.slots = (int64_t)B * Hq * p.nchunks;
-    return p;
+    attn_partial_kernel<HG><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
+    return hip_check("attn_partial launch", hipGetLastError());
 }
 
 int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
@@ -451,14 +641,22 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uin
                              const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                              const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
                              uint32_t* status, hipStream_t stream) {
+    if (!attention_supports(tk, tv)) return DQ_ERR_INVALID_ARG;
     const int G = Hq / Hkv;
-    const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap);
     AttnArgs a;
     a.tk = tab_args(tk);
     a.tv = tab_args(tv);
+    a.shared_lut = (tk == tv || (tk->cfg.levels == tv->cfg.levels &&
+                                 tk->cfg.precision_bits == tv->cfg.precision_bits &&
+                                 tk->cfg.alpha == tv->cfg.alpha && tk->cfg.head_dim == tv->cfg.head_dim))
+                       ? 1 : 0;
+    a.L = attn_layout(a.tk.p, a.tv.p, a.tk.C, a.tv.C, G, a.shared_lut != 0);
+    if (a.L.nw < 1) return DQ_ERR_INVALID_ARG;
+    const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap, a.L.nw);
     a.q = q;
     a.Hq = Hq;
     a.Hkv = Hkv;
+    a.G = G;
     a.t_cap = t_cap;
     a.chunk = plan.chunk;
     a.nchunks = plan.nchunks;
@@ -468,34 +666,24 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uin
     a.vrec = vrec;
     a.seq_lens = seq_lens;
     a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
-    a.ws_acc = static_cast<float*>(ws);
-    a.ws_m = a.ws_acc + plan.slots * kD;
-    a.ws_l = a.ws_m + plan.slots;
+    a.ws_hdr = static_cast<int32_t*>(ws);
+    a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
+    a.ws_m = a.ws_acc + plan.slots_max * kD;
+    a.ws_l = a.ws_m + plan.slots_max;
     a.status = status;
-    a.L = attn_layout(a.tk.p, a.tv.p, a.tk.C, a.tv.C, G, a.chunk);
-    if (a.L.total > 160 * 1024) return DQ_ERR_INVALID_ARG;
     dim3 grid(a.nchunks, Hkv, B);
-    switch (G) {
-        case 1: return launch_g<1>(a, grid, stream);
-        case 2: return launch_g<2>(a, grid, stream);
-        case 3: return launch_g<3>(a, grid, stream);
-        case 4: return launch_g<4>(a, grid, stream);
-        case 5: return launch_g<5>(a, grid, stream);
-        case 6: return launch_g<6>(a, grid, stream);
-        case 7: return launch_g<7>(a, grid, stream);
-        case 8: return launch_g<8>(a, grid, stream);
-        default: return DQ_ERR_INVALID_ARG;
-    }
+    return G <= 4 ? launch_hg<1>(a, grid, stream) : launch_hg<2>(a, grid, stream);
 }
 
 int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
                            int32_t t_cap, const void* ws, float* out, hipStream_t stream) {
-    const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap);
-    const float* acc = static_cast<const float*>(ws);
-    const float* m = acc + plan.slots * kD;
-    const float* l = m + plan.slots;
-    attn_merge_kernel<<<dim3(Hq, B), kD, 0, stream>>>(m, l, acc, seq_lens, Hq, t_cap, plan.chunk,
-                                                      plan.nchunks, out);
+    (void)Hkv;
+    const int64_t slots = (int64_t)B * Hq * max_chunks(t_cap);
+    const int32_t* hdr = static_cast<const int32_t*>(ws);
+    const float* acc = reinterpret_cast<const float*>(static_cast<const uint8_t*>(ws) + kWsHeader);
+    const float* m = acc + slots * kD;
+    const float* l = m + slots;
+    attn_merge_kernel<<<dim3(Hq, B), kD, 0, stream>>>(hdr, m, l, acc, seq_lens, Hq, t_cap, out);
     return hip_check("attn_merge launch", hipGetLastError());
 }
 

@@ -235,15 +235,20 @@ int dq_build_tables(const dq_config* cfg, dq_tables** out, dq_table_info* info) 
     if (rc != DQ_OK) return rc;
 
     const int M = cfg->levels, P = 1 << cfg->precision_bits;
-    // device block: lut[P] u32 | freq[64] | cum[64] | cost[64] | lam[512]
-    const size_t lut_bytes = sizeof(uint32_t) * P;
+    // device block: lut64[P] | lut[P] u32 | freq[64] | cum[64] | cost[64] | lam[512]
+    const size_t lut64_bytes = sizeof(uint32_t) * 2 * P;
+    const size_t lut_bytes = lut64_bytes + sizeof(uint32_t) * P;
     const size_t small = sizeof(int32_t) * DQ_MAX_LEVELS;
     const size_t bytes = lut_bytes + 3 * small + sizeof(float) * dq::kLambdaSteps;
     std::vector<uint8_t> host(bytes, 0);
-    uint32_t* lut = reinterpret_cast<uint32_t*>(host.data());
+    uint32_t* lut64 = reinterpret_cast<uint32_t*>(host.data());
+    uint32_t* lut = reinterpret_cast<uint32_t*>(host.data() + lut64_bytes);
     for (int m = 0; m < M; ++m)
-        for (int z = b.cum[m]; z < b.cum[m] + b.freq[m]; ++z)
+        for (int z = b.cum[m]; z < b.cum[m] + b.freq[m]; ++z) {
             lut[z] = (uint32_t)(z - b.cum[m]) | ((uint32_t)b.freq[m] << 12) | ((uint32_t)m << 24);
+            lut64[2 * z] = (uint32_t)b.freq[m] | ((uint32_t)m << 24);
+            lut64[2 * z + 1] = (uint32_t)(z - b.cum[m]);
+        }
     std::memcpy(host.data() + lut_bytes, b.freq, sizeof(int32_t) * M);
     std::memcpy(host.data() + lut_bytes + small, b.cum, sizeof(int32_t) * M);
     std::memcpy(host.data() + lut_bytes + 2 * small, b.cost, sizeof(int32_t) * M);
@@ -272,7 +277,8 @@ int dq_build_tables(const dq_config* cfg, dq_tables** out, dq_table_info* info) 
         return rc;
     }
     uint8_t* base = static_cast<uint8_t*>(t->dev_block);
-    t->dev.lut = reinterpret_cast<const uint32_t*>(base);
+    t->dev.lut64 = reinterpret_cast<const uint2*>(base);
+    t->dev.lut = reinterpret_cast<const uint32_t*>(base + lut64_bytes);
     t->dev.freq = reinterpret_cast<const int32_t*>(base + lut_bytes);
     t->dev.cum = reinterpret_cast<const int32_t*>(base + lut_bytes + small);
     t->dev.cost = reinterpret_cast<const int32_t*>(base + lut_bytes + 2 * small);

@@ -17,8 +17,10 @@ constexpr int kBracketUnits = 40 * kLambdaSteps;  // hi - lo = 40 octaves
 // Device-resident tables, one allocation.
 //   lut[z], z in [0, 2^p):  bias (z - c_m) in bits 0..11, f_m in bits 12..23,
 //                           m in bits 24..29.
+//   lut64[z]: x = f_m | m << 24 (so a 24-bit multiply reads f_m), y = z - c_m.
 struct DevTables {
     const uint32_t* lut;
+    const uint2* lut64;
     const int32_t* freq;
     const int32_t* cum;
     const int32_t* cost;   // Q16
