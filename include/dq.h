@@ -15,7 +15,7 @@
  *     [scale fp16 LE][offset fp16 LE][rANS state u32 LE][renorm bytes, in the
  *     order the decoder reads them][zero padding]
  * so its rANS budget (Eq. budget) is B = 8 (C - 4) - 32 bits.  The rANS state
- * lives in [2^23, 2^31) and is renormalized one byte at a time.
+ * lives in [2^21, 2^29) and is renormalized one byte at a time.
  *
  * Conventions for every call:
  *  - Device pointers are plain device addresses on the device that was current
@@ -48,7 +48,7 @@ extern "C" {
 /* Bits OR-ed into the caller's device status word. */
 #define DQ_STATUS_RANGE 1u    /* encode: non-finite input, or scale/offset/mean overflowed fp16 */
 #define DQ_STATUS_OVERFLOW 2u /* encode: a stream could not be fitted into its record          */
-#define DQ_STATUS_CORRUPT 4u  /* decode: a record did not end in state 2^23 inside its C bytes  */
+#define DQ_STATUS_CORRUPT 4u  /* decode: a record did not end in state 2^21 inside its C bytes  */
 
 /* Fixed parameters of the format. */
 #define DQ_MEAN_WINDOW 128 /* tokens per key-mean window (windows start at token 0) */

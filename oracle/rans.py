@@ -15,8 +15,11 @@ What the paper fixes
 
 Readings
 --------
-* R1 L = 2**23, the state is 32 bits (sigma = 32).  For p <= 12 a decode step
-  reads at most two bytes.
+* R1 L = 2**21: the state lives in [2**21, 2**29) and is stored as 32 bits
+  (sigma = 32).  For p <= 12 a decode step reads at most two bytes.  The
+  number of emitted bytes does not depend on L (the stored state always
+  carries log2 L bits of the initial value); 2**21 leaves room to keep the
+  state scaled by 8 in a 32-bit register.
 * R2 the encoder starts from x = L and, before encoding symbol m, emits the low
   byte and shifts while x >= ((L >> p) << 8) f_m, which keeps x in [L, 256 L).
 * R3 record layout (C bytes): fp16 scale (LE), fp16 offset (LE), final state
@@ -29,7 +32,7 @@ import numpy as np
 
 from .tables import Tables, HEADER_BYTES
 
-RANS_L = 1 << 23
+RANS_L = 1 << 21
 STATE_BYTES = 4
 PAYLOAD_OFFSET = HEADER_BYTES + STATE_BYTES
 

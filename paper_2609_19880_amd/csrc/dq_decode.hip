@@ -71,14 +71,16 @@ __global__ void decode_symbols_kernel(TabArgs ta, const uint8_t* __restrict__ re
 // wavefront takes 64-token tiles, one token per lane, and decodes that
 // token's key stream then its value stream (Alg. 2), 128 steps each.
 //
-// Decode step.  The table is staged in LDS as 8-byte entries
-// (f_m | m << 24, z - c_m), so the state update x' = f (x >> p) + (z - c) is a
-// single 24-bit multiply-add.  Renormalization bytes are staged per lane as
-// overlapping big-endian byte pairs P[k] = (b_k << 8) | b_{k+1}: one aligned
-// 16-bit LDS read yields the next 16 bits wherever the lane's byte pointer
-// stands, and with the leading-zero count of x' (x' >= 2^11 when p <= 12) the
-// number of bytes Alg. 2 reads, 0, 1 or 2, is sh/8 with sh = (clz(x') - 1) & 24:
-//     x = (x' << sh) | (P[ptr] >> (16 - sh)),   ptr += sh / 8.
+// Decode step.  The state is kept as X = 8 x (its low three bits are never
+// read), which with 8-byte table entries (8 f_m | m << 24, 8 (z - c_m)) in LDS
+// makes the table address one mask of X and the state update
+// x' = f (x >> p) + (z - c) one 24-bit multiply-add.  Renormalization bytes
+// are staged per lane as overlapping big-endian byte pairs
+// P[k] = (b_k << 8) | b_{k+1}: one aligned 16-bit LDS read yields the next
+// 16 bits wherever the lane's byte pointer stands.  Since x' >= 2^9 for
+// p <= 12, the number of bytes Alg. 2 reads (0, 1 or 2) is sh / 8 with
+// sh = clz(8 x') & 24, and
+//     X = (8 x' << sh) | ((P[ptr] << 16) >> (29 - sh)),   ptr += sh / 8.
 //
 // Contractions (Eq. fold-key / fold-value) run on the matrix cores with
 // v_mfma_i32_4x4x4_16b_i8 (16 blocks of 4x4x4; lane l is column l % 4 of
@@ -102,8 +104,8 @@ struct AttnLayout {
     int waves;          // first wavefront region
     int wave_stride;
     int p16, p16_stride;    // byte pairs, per lane
-    int vtile;              // [64 channels][kVRow] bytes
-    int plimb;              // [HG][3 digits][4 heads][64 tokens] bytes
+    int vtile;              // [64 channels][kVRow] bytes, over the pair arrays
+    int plimb;              // [HG][4 heads][16 token quads] x 16 B (three digit words)
     int total;
 };
 
@@ -137,16 +139,27 @@ struct AttnArgs {
 __device__ __forceinline__ float half_lo(uint32_t w) { return half_bits_to_f32((uint16_t)(w & 0xFFFFu)); }
 __device__ __forceinline__ float half_hi(uint32_t w) { return half_bits_to_f32((uint16_t)(w >> 16)); }
 
-// One step of Alg. 2.  Returns the table word (level in its top byte).
-__device__ __forceinline__ uint32_t dstep(uint32_t& x, uint32_t& pq, const uint8_t* lds,
-                                          uint32_t lut_off, uint32_t mask8, int p) {
-    const uint2 e = *reinterpret_cast<const uint2*>(lds + lut_off + ((x << 3) & mask8));
-    const uint32_t pair = *reinterpret_cast<const uint16_t*>(lds + pq);
-    const uint32_t xp = __umul24(e.x, x >> p) + e.y;
-    const uint32_t sh = ((uint32_t)__clz(xp) - 1u) & 24u;
-    x = (xp << sh) | (pair >> (16u - sh));
+// LDS access through a plain byte offset (no symbol relocation in the address).
+#define LDS_PTR(T, off) reinterpret_cast<__attribute__((address_space(3))) T*>((uintptr_t)(off))
+
+// One step of Alg. 2 on the state kept as X = 8 x (+ up to 7 in the low bits,
+// which nothing reads).  Returns the table word (level in its top byte).
+//   table address = X & (2^p - 1) << 3          (8-byte entries at lut_off)
+//   Y = 8 f (X >> (p + 3)) + 8 (z - c) = 8 x'   (one 24-bit multiply-add)
+//   sh = clz(Y) & 24: 0, 8 or 16 bits to shift in (x' >= 2^9 for p <= 12)
+//   X = (Y << sh) | ((pair << 16) >> (29 - sh)),  29 - sh = sh ^ 29
+template <uint32_t LUT_OFF>
+__device__ __forceinline__ uint32_t dstep(uint32_t& X, uint32_t& pq, uint32_t mask8, int p3) {
+    const uint64_t e = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
+    const uint32_t ex = (uint32_t)e, ey = (uint32_t)(e >> 32);
+    const uint32_t r = (uint32_t)*LDS_PTR(const uint16_t, pq) << 16;
+    const uint32_t y = __umul24(ex, X >> p3) + ey;
+    const uint32_t sh = (uint32_t)__builtin_clz(y) & 24u;
+    const uint32_t q = r >> (sh ^ 29u);
+    // one v_lshl_or_b32, so that the next table address stays a single mask
+    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(y), "v"(sh), "v"(q));
     pq += sh >> 2;
-    return e.x;
+    return ex;
 }
 
 // Levels of four consecutive steps (top bytes of the table words) as one word.
@@ -210,7 +223,11 @@ __device__ __forceinline__ void build_pairs(const uint32_t (&r)[kMaxRecDwords], 
 // head; 8 for up to 8, whose accumulators need more registers.
 __host__ __device__ constexpr int max_waves(int HG) { return HG == 1 ? kMaxWaves : 8; }
 
-template <int HG>
+constexpr uint32_t kLutVOffset = 8u << 12;   // value table when it differs from the key table
+
+// RW: record length in dwords when keys and values share it (compile-time
+// record loads), 0 for the general case.
+template <int HG, uint32_t LUTV, int RW>
 __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(AttnArgs a) {
     constexpr int GP = 4 * HG;
     extern __shared__ __align__(16) uint8_t smem[];
@@ -232,8 +249,8 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
         const int Pk = 1 << a.tk.p, Pv = 1 << a.tv.p;
         uint2* lk = reinterpret_cast<uint2*>(smem + L.lut_k);
         for (int i = tid; i < Pk; i += nthr) lk[i] = a.tk.t.lut64[i];
-        if (!a.shared_lut) {
-            uint2* lv = reinterpret_cast<uint2*>(smem + L.lut_v);
+        if (LUTV != 0) {
+            uint2* lv = reinterpret_cast<uint2*>(smem + LUTV);
             for (int i = tid; i < Pv; i += nthr) lv[i] = a.tv.t.lut64[i];
         }
     }
@@ -300,15 +317,15 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
 
     // ---- per-wavefront state
     uint8_t* wreg = smem + L.waves + wave * L.wave_stride;
-    const uint32_t p16_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.p16 + lane * L.p16_stride);
-    uint8_t* vtile = wreg + L.vtile;
+    const uint32_t pk_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.p16 + lane * L.p16_stride);
+    const uint32_t pv_lane = pk_lane + (uint32_t)(kTile * L.p16_stride);
+    uint8_t* vtile = wreg + L.vtile;     // overlays the pair arrays once both streams are decoded
     uint8_t* plimb = wreg + L.plimb;
     const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
     const uint32_t sel2 = (lane & 2) ? 0x03020706u : 0x05040100u;
-    const int Ck = a.tk.C, Cv = a.tv.C, CWk = Ck / 4, CWv = Cv / 4;
-    const int pk = a.tk.p, pvb = a.tv.p;
-    const uint32_t mask8k = ((1u << pk) - 1u) << 3, mask8v = ((1u << pvb) - 1u) << 3;
-    const uint32_t lutk_off = (uint32_t)L.lut_k, lutv_off = (uint32_t)L.lut_v;
+    const int Ck = RW ? 4 * RW : a.tk.C, Cv = RW ? 4 * RW : a.tv.C, CWk = Ck / 4, CWv = Cv / 4;
+    const int pk3 = a.tk.p + 3, pv3 = a.tv.p + 3;
+    const uint32_t mask8k = ((1u << a.tk.p) - 1u) << 3, mask8v = ((1u << a.tv.p) - 1u) << 3;
     const int64_t bh = (int64_t)b * a.Hkv + h;
 
     float m_run[GP], l_part[GP], acco[GP], accf[2][GP];
@@ -322,108 +339,121 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
     }
     bool corrupt = false;
     const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
-    uint32_t kr[kMaxRecDwords], vr[kMaxRecDwords];
-    if (wave < ntiles) {
-        const int64_t tok = bh * a.t_cap + start + wave * kTile + lane;
-        load_record(kr, a.krec, tok, CWk);
-        load_record(vr, a.vrec, tok, CWv);
-    }
 
     for (int tile = wave; tile < ntiles; tile += L.nw) {
         const int t_base = start + tile * kTile;
         const int t = t_base + lane;
         const bool valid = t < T;
-        const bool more = tile + L.nw < ntiles;
-        const int64_t next_tok = bh * a.t_cap + t_base + L.nw * kTile + lane;
+        const int64_t tok = bh * a.t_cap + t_base + lane;
 
-        // ---- keys
-        build_pairs(kr, CWk, smem + p16_lane);
-        const float sk = half_lo(kr[0]), ok = half_hi(kr[0]);
-        uint32_t x = kr[1];
-        uint32_t pq = p16_lane;
-        if (more) load_record(kr, a.krec, next_tok, CWk);
+        // ---- both records of the lane's token -> headers + byte-pair arrays
+        uint32_t hk0, xk, hv0, xv;
+        {
+            uint32_t r[kMaxRecDwords];
+            load_record(r, a.krec, tok, CWk);
+            hk0 = r[0];
+            xk = r[1] << 3;
+            build_pairs(r, CWk, smem + pk_lane);
+            load_record(r, a.vrec, tok, CWv);
+            hv0 = r[0];
+            xv = r[1] << 3;
+            build_pairs(r, CWv, smem + pv_lane);
+        }
+        // the pair arrays are read back by this lane only: order the reads
+        // after the writes (LDS keeps a wavefront's accesses in order)
+        asm volatile("" ::: "memory");
+        uint32_t pq = pk_lane, pv = pv_lane;
+
+        // ---- keys and values decoded together: two independent rANS chains
+        //      per lane.  Key levels go straight into the q . k products; value
+        //      levels wait in registers until the softmax weights are known.
         v4i dk[HG][3];
 #pragma unroll
         for (int hg = 0; hg < HG; ++hg)
 #pragma unroll
             for (int d = 0; d < 3; ++d) dk[hg][d] = v4i{0, 0, 0, 0};
-#pragma unroll 2
+        uint32_t vlev[kD / 4];
+#pragma unroll
         for (int grp = 0; grp < kD / 4; ++grp) {
-            const uint32_t e0 = dstep(x, pq, smem, lutk_off, mask8k, pk);
-            const uint32_t e1 = dstep(x, pq, smem, lutk_off, mask8k, pk);
-            const uint32_t e2 = dstep(x, pq, smem, lutk_off, mask8k, pk);
-            const uint32_t e3 = dstep(x, pq, smem, lutk_off, mask8k, pk);
-            const uint32_t lv = pack4(e0, e1, e2, e3);
+            const uint32_t k0 = dstep<0>(xk, pq, mask8k, pk3);
+            const uint32_t v0 = dstep<LUTV>(xv, pv, mask8v, pv3);
+            const uint32_t k1 = dstep<0>(xk, pq, mask8k, pk3);
+            const uint32_t v1 = dstep<LUTV>(xv, pv, mask8v, pv3);
+            const uint32_t k2 = dstep<0>(xk, pq, mask8k, pk3);
+            const uint32_t v2 = dstep<LUTV>(xv, pv, mask8v, pv3);
+            const uint32_t k3 = dstep<0>(xk, pq, mask8k, pk3);
+            const uint32_t v3 = dstep<LUTV>(xv, pv, mask8v, pv3);
+            const uint32_t lk = pack4(k0, k1, k2, k3);
+            vlev[grp] = pack4(v0, v1, v2, v3);
+            // pack now: left alone, the packing sinks to the value pass and the
+            // four table words stay live until then
+            asm volatile("" : "+v"(vlev[grp]));
 #pragma unroll
             for (int hg = 0; hg < HG; ++hg) {
                 const uint4 ql = *reinterpret_cast<const uint4*>(qlimb + ((grp * GP) + hg * 4 + (lane & 3)) * 16);
-                dk[hg][0] = mfma(ql.x, lv, dk[hg][0]);
-                dk[hg][1] = mfma(ql.y, lv, dk[hg][1]);
-                dk[hg][2] = mfma(ql.z, lv, dk[hg][2]);
+                dk[hg][0] = mfma(ql.x, lk, dk[hg][0]);
+                dk[hg][1] = mfma(ql.y, lk, dk[hg][1]);
+                dk[hg][2] = mfma(ql.z, lk, dk[hg][2]);
             }
+            // keep the scheduler inside one group: live ranges stay short
+            __builtin_amdgcn_sched_barrier(0);
         }
-        corrupt |= valid && (x != kRansL || pq > p16_lane + 2u * (uint32_t)(Ck - kPayloadOffset));
+        corrupt |= valid && ((xk >> 3) != kRansL || pq > pk_lane + 2u * (uint32_t)(Ck - kPayloadOffset));
+        corrupt |= valid && ((xv >> 3) != kRansL || pv > pv_lane + 2u * (uint32_t)(Cv - kPayloadOffset));
+
+        // ---- scores (Eq. fold-key) and online softmax; the value scale is
+        //      folded into the weight (Eq. fold-value)
+        const float sk = half_lo(hk0), ok = half_hi(hk0);
+        const float sv = half_lo(hv0), ov = half_hi(hv0);
         const float* qm = qmu + ((t / DQ_MEAN_WINDOW) - w0) * GP;
-        float score[GP];
+        float pscale[GP];
+        int pint[GP];
 #pragma unroll
         for (int hg = 0; hg < HG; ++hg)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int g = 4 * hg + r;
                 const float dot = combine(dk[hg][0], dk[hg][1], dk[hg][2], r) * qscale[g];
-                score[g] = (valid && g < G) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
+                const float score = (valid && g < G) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
+                const float tmax = wave_max(score);
+                const float mn = fmaxf(m_run[g], tmax);
+                const float corr = (m_run[g] == -INFINITY || mn == -INFINITY) ? (m_run[g] == mn ? 1.f : 0.f)
+                                                                               : exp2f(m_run[g] - mn);
+                const float p = (score == -INFINITY) ? 0.f : exp2f(score - mn);
+                l_part[g] = l_part[g] * corr + p;
+                acco[g] = acco[g] * corr + p * ov;
+                accf[0][g] *= corr;
+                accf[1][g] *= corr;
+                m_run[g] = mn;
+                const float pw = p * sv;
+                const float smax = wave_max(pw);
+                pscale[g] = smax * (1.0f / 4194304.0f);
+                pint[g] = smax > 0.f ? min(4194304, (int)rintf(pw / pscale[g])) : 0;
             }
-
-        // ---- online softmax; the value scale is folded into the weight
-        build_pairs(vr, CWv, smem + p16_lane);
-        const float sv = half_lo(vr[0]), ov = half_hi(vr[0]);
-        uint32_t xv = vr[1];
-        uint32_t pv = p16_lane;
-        if (more) load_record(vr, a.vrec, next_tok, CWv);
-        float pscale[GP];
-        int pint[GP];
-#pragma unroll
-        for (int g = 0; g < GP; ++g) {
-            const float tmax = wave_max(score[g]);
-            const float mn = fmaxf(m_run[g], tmax);
-            const float corr = (m_run[g] == -INFINITY || mn == -INFINITY) ? (m_run[g] == mn ? 1.f : 0.f)
-                                                                           : exp2f(m_run[g] - mn);
-            const float p = (score[g] == -INFINITY) ? 0.f : exp2f(score[g] - mn);
-            l_part[g] = l_part[g] * corr + p;
-            acco[g] = acco[g] * corr + p * ov;
-            accf[0][g] *= corr;
-            accf[1][g] *= corr;
-            m_run[g] = mn;
-            const float pw = p * sv;
-            const float smax = wave_max(pw);
-            pscale[g] = smax * (1.0f / 4194304.0f);
-            pint[g] = smax > 0.f ? min(4194304, (int)rintf(pw / pscale[g])) : 0;
-        }
-        // weight digits -> LDS [hg][digit][head][token] via the quad transpose
+        // weight digits -> LDS [hg][head][token quad] x (d0, d1, d2) words
 #pragma unroll
         for (int hg = 0; hg < HG; ++hg) {
             int dd[4][3];
 #pragma unroll
             for (int r = 0; r < 4; ++r) digits3(pint[4 * hg + r], dd[r][0], dd[r][1], dd[r][2]);
+            uint32_t wt[3];
 #pragma unroll
             for (int d = 0; d < 3; ++d) {
                 const uint32_t w = ((uint32_t)dd[0][d] & 0xFFu) | (((uint32_t)dd[1][d] & 0xFFu) << 8) |
                                    (((uint32_t)dd[2][d] & 0xFFu) << 16) | ((uint32_t)dd[3][d] << 24);
-                const uint32_t wt = quad_transpose(w, sel1, sel2);
-                *reinterpret_cast<uint32_t*>(plimb + ((hg * 3 + d) * 4 + (lane & 3)) * kTile + (lane >> 2) * 4) = wt;
+                wt[d] = quad_transpose(w, sel1, sel2);
             }
+            *reinterpret_cast<uint4*>(plimb + ((hg * 4 + (lane & 3)) * (kTile / 4) + (lane >> 2)) * 16) =
+                uint4{wt[0], wt[1], wt[2], 0u};
         }
 
-        // ---- values, two slices of 64 channels
+        // ---- P . v over two slices of 64 channels
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
-#pragma unroll 2
+            wave_sync();   // pair arrays (first slice) or the previous slice are no longer read
+#pragma unroll
             for (int grp = 0; grp < kVSlice / 4; ++grp) {
-                const uint32_t e0 = dstep(xv, pv, smem, lutv_off, mask8v, pvb);
-                const uint32_t e1 = dstep(xv, pv, smem, lutv_off, mask8v, pvb);
-                const uint32_t e2 = dstep(xv, pv, smem, lutv_off, mask8v, pvb);
-                const uint32_t e3 = dstep(xv, pv, smem, lutv_off, mask8v, pvb);
-                const uint32_t wt = quad_transpose(pack4(e0, e1, e2, e3), sel1, sel2);
+                const uint32_t wt = quad_transpose(vlev[s * (kVSlice / 4) + grp], sel1, sel2);
                 *reinterpret_cast<uint32_t*>(vtile + (grp * 4 + (lane & 3)) * kVRow + (lane >> 2) * 4) = wt;
             }
             wave_sync();
@@ -437,10 +467,11 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
                 const uint32_t bv = *reinterpret_cast<const uint32_t*>(vtile + lane * kVRow + qd * 4);
 #pragma unroll
                 for (int hg = 0; hg < HG; ++hg) {
-                    const uint8_t* pl = plimb + (hg * 12 + (lane & 3)) * kTile + qd * 4;
-                    dv[hg][0] = mfma(*reinterpret_cast<const uint32_t*>(pl), bv, dv[hg][0]);
-                    dv[hg][1] = mfma(*reinterpret_cast<const uint32_t*>(pl + 4 * kTile), bv, dv[hg][1]);
-                    dv[hg][2] = mfma(*reinterpret_cast<const uint32_t*>(pl + 8 * kTile), bv, dv[hg][2]);
+                    const uint4 pl = *reinterpret_cast<const uint4*>(
+                        plimb + ((hg * 4 + (lane & 3)) * (kTile / 4) + qd) * 16);
+                    dv[hg][0] = mfma(pl.x, bv, dv[hg][0]);
+                    dv[hg][1] = mfma(pl.y, bv, dv[hg][1]);
+                    dv[hg][2] = mfma(pl.z, bv, dv[hg][2]);
                 }
             }
 #pragma unroll
@@ -448,9 +479,8 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
                     accf[s][4 * hg + r] += combine(dv[hg][0], dv[hg][1], dv[hg][2], r) * pscale[4 * hg + r];
-            wave_sync();
         }
-        corrupt |= valid && (xv != kRansL || pv > p16_lane + 2u * (uint32_t)(Cv - kPayloadOffset));
+        wave_sync();   // the next tile rewrites the pair arrays over the value tile
     }
     if (__any(corrupt) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_CORRUPT);
 
@@ -539,13 +569,14 @@ AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut) 
     const int GP = G <= 4 ? 4 : 8, HG = GP / 4;
     AttnLayout L;
     int off = 0;
-    L.lut_k = off;
-    off += align16(8 << pk);
+    // key table at 0; a distinct value table at a fixed 32 KB (the DS offset field)
+    L.lut_k = 0;
     if (shared_lut) {
-        L.lut_v = L.lut_k;
+        L.lut_v = 0;
+        off = align16(8 << pk);
     } else {
-        L.lut_v = off;
-        off += align16(8 << pvb);
+        L.lut_v = (int)kLutVOffset;
+        off = (int)kLutVOffset + align16(8 << pvb);
     }
     L.qlimb = off;
     off += align16((kD / 4) * GP * 16);
@@ -558,12 +589,11 @@ AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut) 
     L.waves = off;
     L.p16_stride = std::max(p16_stride_for(Ck), p16_stride_for(Cv));
     int w = 0;
-    L.p16 = w;
-    w += align16(kTile * L.p16_stride);
-    L.vtile = w;
-    w += align16(kVSlice * kVRow);
+    L.p16 = w;                                     // key pairs, then value pairs
+    L.vtile = w;                                   // reuses the pair arrays
+    w += std::max(align16(2 * kTile * L.p16_stride), align16(kVSlice * kVRow));
     L.plimb = w;
-    w += align16(HG * 3 * 4 * kTile);
+    w += align16(HG * 4 * (kTile / 4) * 16);
     L.wave_stride = w;
     int nw = (kMaxLds - off) / w;
     if (nw > max_waves(HG)) nw = max_waves(HG);
@@ -584,11 +614,11 @@ struct ChunkPlan {
 int64_t max_chunks(int t_cap) { return (t_cap + kMinChunk - 1) / kMinChunk; }
 
 // Chunk = a whole number of passes of the workgroup (nw x 64 tokens), at
-// least kMinChunk tokens, sized for about two thousand workgroups.
+// least kMinChunk tokens, sized for about a thousand workgroups (four per CU).
 ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap, int nw) {
     ChunkPlan p;
     const int pass = nw * kTile;
-    int k = (int)(((int64_t)B * Hkv * t_cap) / ((int64_t)pass * 2048));
+    int k = (int)(((int64_t)B * Hkv * t_cap) / ((int64_t)pass * 1024));
     k = std::max(k, (kMinChunk + pass - 1) / pass);
     k = std::min(k, std::max(1, 4096 / pass));
     p.chunk = pass * k;
@@ -626,14 +656,28 @@ bool attention_supports(const dq_tables* tk, const dq_tables* tv) {
     return true;
 }
 
-template <int HG>
-static int launch_hg(AttnArgs& a, dim3 grid, hipStream_t stream) {
+template <int HG, uint32_t LUTV, int RW>
+static int launch_rw(AttnArgs& a, dim3 grid, hipStream_t stream) {
     if (int rc = hip_check("hipFuncSetAttribute",
-                           hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_partial_kernel<HG>),
+                           hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_partial_kernel<HG, LUTV, RW>),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
         return rc;
-    attn_partial_kernel<HG><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
+    attn_partial_kernel<HG, LUTV, RW><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
     return hip_check("attn_partial launch", hipGetLastError());
+}
+
+// Record lengths of the 2.0 / 2.25 / 3.0 / 4.0 bits-per-element budgets at
+// head_dim 128 get their own instantiation; other lengths take the general one.
+template <int HG, uint32_t LUTV>
+static int launch_hg(AttnArgs& a, dim3 grid, hipStream_t stream) {
+    const int rw = a.tk.C == a.tv.C ? a.tk.C / 4 : 0;
+    switch (rw) {
+        case 8: return launch_rw<HG, LUTV, 8>(a, grid, stream);
+        case 9: return launch_rw<HG, LUTV, 9>(a, grid, stream);
+        case 12: return launch_rw<HG, LUTV, 12>(a, grid, stream);
+        case 16: return launch_rw<HG, LUTV, 16>(a, grid, stream);
+        default: return launch_rw<HG, LUTV, 0>(a, grid, stream);
+    }
 }
 
 int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
@@ -672,7 +716,8 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uin
     a.ws_l = a.ws_m + plan.slots_max;
     a.status = status;
     dim3 grid(a.nchunks, Hkv, B);
-    return G <= 4 ? launch_hg<1>(a, grid, stream) : launch_hg<2>(a, grid, stream);
+    if (a.shared_lut) return G <= 4 ? launch_hg<1, 0>(a, grid, stream) : launch_hg<2, 0>(a, grid, stream);
+    return G <= 4 ? launch_hg<1, kLutVOffset>(a, grid, stream) : launch_hg<2, kLutVOffset>(a, grid, stream);
 }
 
 int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,

@@ -246,8 +246,8 @@ int dq_build_tables(const dq_config* cfg, dq_tables** out, dq_table_info* info) 
     for (int m = 0; m < M; ++m)
         for (int z = b.cum[m]; z < b.cum[m] + b.freq[m]; ++z) {
             lut[z] = (uint32_t)(z - b.cum[m]) | ((uint32_t)b.freq[m] << 12) | ((uint32_t)m << 24);
-            lut64[2 * z] = (uint32_t)b.freq[m] | ((uint32_t)m << 24);
-            lut64[2 * z + 1] = (uint32_t)(z - b.cum[m]);
+            lut64[2 * z] = 8u * (uint32_t)b.freq[m] | ((uint32_t)m << 24);
+            lut64[2 * z + 1] = 8u * (uint32_t)(z - b.cum[m]);
         }
     std::memcpy(host.data() + lut_bytes, b.freq, sizeof(int32_t) * M);
     std::memcpy(host.data() + lut_bytes + small, b.cum, sizeof(int32_t) * M);

@@ -8,7 +8,7 @@
 
 namespace dq {
 
-constexpr uint32_t kRansL = 1u << 23;       // rANS lower bound; state in [L, 256 L)
+constexpr uint32_t kRansL = 1u << 21;       // rANS lower bound; state in [L, 256 L)
 constexpr int kLambdaSteps = 512;           // lambda grid points per octave
 constexpr int kPayloadOffset = 8;           // fp16 scale, fp16 offset, u32 state
 constexpr int kBisectSteps = 12;            // T of Alg. 1
@@ -17,7 +17,7 @@ constexpr int kBracketUnits = 40 * kLambdaSteps;  // hi - lo = 40 octaves
 // Device-resident tables, one allocation.
 //   lut[z], z in [0, 2^p):  bias (z - c_m) in bits 0..11, f_m in bits 12..23,
 //                           m in bits 24..29.
-//   lut64[z]: x = f_m | m << 24 (so a 24-bit multiply reads f_m), y = z - c_m.
+//   lut64[z]: x = 8 f_m | m << 24 (a 24-bit multiply reads 8 f_m), y = 8 (z - c_m).
 struct DevTables {
     const uint32_t* lut;
     const uint2* lut64;

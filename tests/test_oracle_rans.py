@@ -64,7 +64,7 @@ def test_uniform_alphabet_packs_exact_bits():
 
 
 def test_decoder_reads_at_most_two_bytes_per_symbol():
-    # reading R1: x in [2^23, 2^31) and f >= 1 give x' >= 2^11 after a step
+    # reading R1: x in [2^21, 2^29) and f >= 1 give x' >= 2^9 after a step
     t = tables.build_tables(128, 64, 12, 7.8, 64)
     sym = np.zeros((1, 128), dtype=np.int64)       # rarest symbol, f = 1
     _, _, length = rans.encode(sym, t)
