@@ -29,6 +29,12 @@ if ROOT not in sys.path:
 
 METRIC = "KV tokens/s + achieved HBM GB/s, D-Quant decode attention at 2.26 bits/elem"
 HBM_PEAK_GBS = 8000.0
+# VALU issue peak: 256 CUs x 4 SIMDs, a wave64 instruction occupies a 16-lane
+# SIMD for 4 cycles, 2.4 GHz
+VALU_PEAK_GINST = 256 * 4 / 4 * 2.4
+COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "attn_partial_b16_t32k_pmc.md")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_19880_amd", "csrc", f)
+                  for f in ("dq_decode.hip", "dq_common.h", "dq_internal.h")]
 
 
 def _args():
@@ -74,6 +80,26 @@ def copy_calibration(nbytes: int, steps: int):
                       "gbs_read_plus_write": 2 * nbytes / ms / 1e6}))
 
 
+def counter_figures(workload: str, variant: str):
+    """HBM bytes and VALU instructions per partial launch from the committed
+    rocprofv3 counter summary, if it was taken on this workload from the
+    kernel sources as they are now (else None)."""
+    import hashlib
+    import re
+    if (workload, variant) != ("b16_t32k", "paper") or not os.path.exists(COUNTER_SUMMARY):
+        return None
+    text = open(COUNTER_SUMMARY).read()
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    m_tr = re.search(r"traffic_bytes_per_launch:\s*(\d+)", text)
+    m_valu = re.search(r"\|\s*SQ_INSTS_VALU\s*\|\s*([\d,]+)", text)
+    if not (m_sha and m_tr and m_valu) or m_sha.group(1) != h.hexdigest():
+        return None
+    return int(m_tr.group(1)), int(m_valu.group(1).replace(",", ""))
+
+
 def cpu_baseline(wl, seed: int):
     """The CPU oracle's decode attention, timed on one (sequence, KV head)
     slice of the workload at full context and scaled to a whole step."""
@@ -90,15 +116,17 @@ def cpu_baseline(wl, seed: int):
     q = wlmod.bf16_bits(wlmod.make_q(one, seed + 100))[:, : wl.gqa]
     krec, mq, ms, _ = kv.encode_keys(k, otk)
     vrec, _ = kv.encode_values(v, otv)
+    from threadpoolctl import threadpool_limits
     reps, t0 = 0, time.perf_counter()
-    while True:
-        ksym, ks, ko, _ = kv.decode_records(krec, otk, wl.head_dim)
-        vsym, vs, vo, _ = kv.decode_records(vrec, otv, wl.head_dim)
-        attention.attention_folded(kv.bf16_to_f64(q), ksym, ks, ko, kmean.dequantize_mean(mq, ms),
-                                   vsym, vs, vo, [T], wl.gqa, 1 / np.sqrt(wl.head_dim))
-        reps += 1
-        if time.perf_counter() - t0 > 10.0:
-            break
+    with threadpool_limits(limits=1):      # the one core the figure is quoted on
+        while True:
+            ksym, ks, ko, _ = kv.decode_records(krec, otk, wl.head_dim)
+            vsym, vs, vo, _ = kv.decode_records(vrec, otv, wl.head_dim)
+            attention.attention_folded(kv.bf16_to_f64(q), ksym, ks, ko, kmean.dequantize_mean(mq, ms),
+                                       vsym, vs, vo, [T], wl.gqa, 1 / np.sqrt(wl.head_dim))
+            reps += 1
+            if time.perf_counter() - t0 > 10.0:
+                break
     per_slice = (time.perf_counter() - t0) / reps
     slices = wl.batch * wl.kv_heads
     step_s = per_slice * slices
@@ -107,6 +135,53 @@ def cpu_baseline(wl, seed: int):
                       f"(sequence, KV head) slice: {T} tokens, {wl.gqa} query heads; {reps} repetitions, "
                       f"{per_slice:.3f} s each, scaled x{slices} to the {wl.batch}x{wl.kv_heads} slices of a "
                       f"step; single-threaded numpy on {_cpu_model()} ({os.cpu_count()} host cores)"}
+
+
+def fill_cache(wl, seed: int, dev):
+    """Tables and a compressed cache holding the whole workload, encoded one
+    sequence at a time from the seeded generators (sequence b uses seed
+    1000 seed + b on the device).  Returns (tk, tv, cache, encode_ms)."""
+    import torch
+    import dq_workloads as wlmod
+    import paper_2609_19880_amd as dq
+
+    B, T, Hq, Hkv, d = wl.batch, wl.context, wl.q_heads, wl.kv_heads, wl.head_dim
+    tk = dq.Tables(d, wl.k.levels, wl.k.precision, wl.k.record_bytes, wl.k.alpha)
+    tv = dq.Tables(d, wl.v.levels, wl.v.precision, wl.v.record_bytes, wl.v.alpha)
+    cache = dq.KVCache(B, Hkv, Hq, T, tk, tv, device=dev)
+    enc_ms = 0.0
+    for b in range(B):
+        k = wlmod.make_k(wl, seed * 1000 + b, device=dev, batch=1)
+        v = wlmod.make_v(wl, seed * 1000 + b, device=dev, batch=1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dq.dq_encode_kv(tk, k, 0, T, cache.k_records[b:b + 1], cache.k_mean_q[b:b + 1],
+                        cache.k_mean_scale[b:b + 1], cache.status)
+        dq.dq_encode_kv(tv, v, 0, T, cache.v_records[b:b + 1], None, None, cache.status)
+        e1.record()
+        torch.cuda.synchronize()
+        enc_ms += e0.elapsed_time(e1)
+        del k, v
+    return tk, tv, cache, enc_ms
+
+
+def step_inputs(wl, seed: int, dev):
+    """Query (seeded), full-length sequence lengths and the output buffer."""
+    import torch
+    import dq_workloads as wlmod
+    q = wlmod.make_q(wl, seed, device=dev)
+    seq = torch.full((wl.batch,), wl.context, dtype=torch.int32, device=dev)
+    out = torch.empty((wl.batch, wl.q_heads, wl.head_dim), dtype=torch.float32, device=dev)
+    return q, seq, out
+
+
+def decode_step(tk, tv, cache, q, seq, out):
+    """One step: split-K partials over the whole cache, then the merge."""
+    import paper_2609_19880_amd as dq
+    dq.dq_decode_attention_partial(tk, tv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
+                                   cache.v_records, seq, cache.workspace, status=cache.status)
+    dq.dq_decode_attention_merge(cache.batch, cache.q_heads, cache.kv_heads, seq, cache.t_cap,
+                                 cache.workspace, out)
 
 
 def main():
@@ -128,38 +203,15 @@ def main():
         wlmod.workload(a.workload, a.variant)
     dev = torch.device("cuda")
     B, T, Hq, Hkv, d = wl.batch, wl.context, wl.q_heads, wl.kv_heads, wl.head_dim
-    tk = dq.Tables(d, wl.k.levels, wl.k.precision, wl.k.record_bytes, wl.k.alpha)
-    tv = dq.Tables(d, wl.v.levels, wl.v.precision, wl.v.record_bytes, wl.v.alpha)
-    cache = dq.KVCache(B, Hkv, Hq, T, tk, tv, device=dev)
-
-    # fill the cache, one sequence at a time (encode throughput is reported too)
-    enc_ms = 0.0
-    for b in range(B):
-        k = wlmod.make_k(wl, a.seed * 1000 + b, device=dev, batch=1)
-        v = wlmod.make_v(wl, a.seed * 1000 + b, device=dev, batch=1)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        dq.dq_encode_kv(tk, k, 0, T, cache.k_records[b:b + 1], cache.k_mean_q[b:b + 1],
-                        cache.k_mean_scale[b:b + 1], cache.status)
-        dq.dq_encode_kv(tv, v, 0, T, cache.v_records[b:b + 1], None, None, cache.status)
-        e1.record()
-        torch.cuda.synchronize()
-        enc_ms += e0.elapsed_time(e1)
-        del k, v
+    tk, tv, cache, enc_ms = fill_cache(wl, a.seed, dev)
     status = int(cache.status.item())
     if status:
         raise RuntimeError(f"encoder status {status}")
     torch.cuda.empty_cache()
-
-    q = wlmod.make_q(wl, a.seed, device=dev)
-    seq = torch.full((B,), T, dtype=torch.int32, device=dev)
-    out = torch.empty((B, Hq, d), dtype=torch.float32, device=dev)
-    ws = cache.workspace
+    q, seq, out = step_inputs(wl, a.seed, dev)
 
     def step():
-        dq.dq_decode_attention_partial(tk, tv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
-                                       cache.v_records, seq, ws, status=cache.status)
-        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
+        decode_step(tk, tv, cache, q, seq, out)
 
     for _ in range(a.warmup):
         step()
@@ -170,9 +222,9 @@ def main():
     for i in range(a.steps):
         ev[3 * i].record()
         dq.dq_decode_attention_partial(tk, tv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
-                                       cache.v_records, seq, ws, status=cache.status)
+                                       cache.v_records, seq, cache.workspace, status=cache.status)
         ev[3 * i + 1].record()
-        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
+        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, cache.workspace, out)
         ev[3 * i + 2].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -189,6 +241,8 @@ def main():
     alg_bytes = per_unit * units
     achieved = alg_bytes / (partial_ms * 1e-3) / 1e9
     tokens_s = B * T / (step_ms * 1e-3)
+    counters = counter_figures(wl.name, a.variant)
+    traffic = counters[0] if counters else None
 
     rec = {
         "metric": METRIC,
@@ -211,9 +265,16 @@ def main():
                    "head_dim": d, "k_record_bytes": wl.k.record_bytes, "v_record_bytes": wl.v.record_bytes,
                    "k_levels": wl.k.levels, "v_levels": wl.v.levels},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "kernel": "attn_partial_kernel", "alg_bytes_per_launch": alg_bytes,
                      "kernel_ms": partial_ms},
+        "valu_issue": None if counters is None else {
+            "bound": "alu", "achieved": counters[1] / (partial_ms * 1e-3) / 1e9,
+            "peak": VALU_PEAK_GINST, "unit": "G wave64 VALU instructions/s",
+            "frac": counters[1] / (partial_ms * 1e-3) / 1e9 / VALU_PEAK_GINST,
+            "valu_insts_per_launch": counters[1],
+            "valu_lane_ops_per_symbol": counters[1] * 64 / (2 * units * d)},
         "merge_ms": merge_ms,
         "wall_ms_per_step": wall * 1e3 / a.steps,
         "symbols_per_s": 2 * units * d / (step_ms * 1e-3),
