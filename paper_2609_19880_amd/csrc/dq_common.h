@@ -26,30 +26,68 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Wavefront reductions on the DPP network (no LDS traffic).  Quad
+// permutations and row mirrors reduce each row of 16 lanes; two row broadcasts
+// carry the row results up to lane 63, which is read back as a uniform value.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, ROW_MASK, 0xF, false);
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_step(float v) {
+    return __uint_as_float(dpp_u32<CTRL, ROW_MASK>(__float_as_uint(v)));
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_step(int v) {
+    return (int)dpp_u32<CTRL, ROW_MASK>((uint32_t)v);
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_step(double v) {
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const uint64_t lo = dpp_u32<CTRL, ROW_MASK>((uint32_t)u);
+    const uint64_t hi = dpp_u32<CTRL, ROW_MASK>((uint32_t)(u >> 32));
+    return __longlong_as_double((long long)(lo | (hi << 32)));
+}
+
+__device__ __forceinline__ float lane63(float v) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ __forceinline__ int lane63(int v) { return __builtin_amdgcn_readlane(v, 63); }
+__device__ __forceinline__ double lane63(double v) {
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const uint64_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 63);
+    const uint64_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
+    return __longlong_as_double((long long)(lo | (hi << 32)));
+}
+
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce(T v, Op op) {
+    v = op(v, dpp_step<0xB1, 0xF>(v));    // quad_perm [1, 0, 3, 2]
+    v = op(v, dpp_step<0x4E, 0xF>(v));    // quad_perm [2, 3, 0, 1]
+    v = op(v, dpp_step<0x141, 0xF>(v));   // row_half_mirror
+    v = op(v, dpp_step<0x140, 0xF>(v));   // row_mirror: every lane holds its row's result
+    v = op(v, dpp_step<0x142, 0xA>(v));   // row_bcast:15 into rows 1 and 3
+    v = op(v, dpp_step<0x143, 0xC>(v));   // row_bcast:31 into rows 2 and 3
+    return lane63(v);
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_max(T v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = max(v, __shfl_xor(v, off));
-    return v;
+    return wave_reduce(v, [](T a, T b) { return a > b ? a : b; });
 }
 
 template <typename T>
 __device__ __forceinline__ T wave_min(T v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = min(v, __shfl_xor(v, off));
-    return v;
+    return wave_reduce(v, [](T a, T b) { return a < b ? a : b; });
 }
 
 __device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-    return v;
+    return wave_reduce(v, [](int a, int b) { return a + b; });
 }
 
 __device__ __forceinline__ float wave_sum_f32(float v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-    return v;
+    return wave_reduce(v, [](float a, float b) { return a + b; });
 }
 
 }  // namespace dq

@@ -2,18 +2,16 @@
 // attention over them (Sec. 4.5 "Decoding", App. A Eq. fold-key/fold-value).
 //
 // decode_attention is split-K over context chunks:
-//  * attn_partial: one workgroup per (chunk, KV head, sequence), four
-//    wavefronts.  The workgroup stages both rANS lookup tables in LDS and
-//    rotates the G query heads that share the KV head (one FWHT in LDS).  Each
-//    wavefront then takes 64-token tiles: the tile's 64 K and 64 V records are
-//    copied to LDS with 16-byte coalesced loads (fixed stride: the address of a
-//    record follows from its token index), and every lane decodes one token's
-//    stream.  Keys: the decoded level feeds sum_j q_j m_j directly and the
-//    affine terms are applied once per token (Eq. fold-key).  Values: levels go
-//    to a 64 x 32 byte tile in LDS, the softmax weight is folded with the
-//    token's scale (Eq. fold-value) and each lane accumulates one output channel.
-//    Online softmax state stays per wavefront; the four wavefronts are merged
-//    in LDS at the end.
+//  * attn_partial: one workgroup per (chunk, KV head, sequence), up to 12
+//    wavefronts.  The workgroup stages the rANS tables in LDS and rotates the
+//    G query heads that share the KV head (one FWHT in LDS).  Each wavefront
+//    then takes 64-token tiles, one token per lane: the lane stages its key
+//    and value payloads in LDS and runs the two rANS chains interleaved.  Key
+//    levels feed the q . k products on the matrix cores as they are decoded
+//    (Eq. fold-key); value levels wait in registers until the tile's softmax
+//    weights are known, then meet them on the matrix cores (Eq. fold-value).
+//    Online softmax state stays per wavefront; the wavefronts are merged in
+//    LDS at the end.
 //  * attn_merge: log-sum-exp merge of the chunk partials per (sequence, query
 //    head), then the inverse rotation of the value basis and the 1/d scale.
 #include <math.h>
@@ -33,6 +31,7 @@ constexpr int kVRow = 68;        // bytes per channel row of the value tile (64 
 constexpr int kMaxRecDwords = 16;
 constexpr int kMaxLds = 160 * 1024;
 constexpr int kMinChunk = 512;
+constexpr int kMaxChunk = 16384;  // bounds the per-window q . mu table in LDS
 constexpr int kWsHeader = 256;   // workspace header: chunk size, chunk count
 
 // ---------------------------------------------------------------- symbols
@@ -103,7 +102,7 @@ struct AttnLayout {
     int qmu;            // float [windows][GP]
     int waves;          // first wavefront region
     int wave_stride;
-    int p16, p16_stride;    // byte pairs, per lane
+    int pk, pv;             // key / value byte-pair arrays: [position][64 lanes] x 2 B
     int vtile;              // [64 channels][kVRow] bytes, over the pair arrays
     int plimb;              // [HG][4 heads][16 token quads] x 16 B (three digit words)
     int total;
@@ -111,11 +110,9 @@ struct AttnLayout {
 
 __host__ inline int align16(int v) { return (v + 15) & ~15; }
 
-__host__ inline int p16_stride_for(int C) {
-    int s = (2 * (C - kPayloadOffset) + 3) & ~3;   // 2 bytes per byte position
-    if (((s / 4) & 1) == 0) s += 4;                 // odd dword stride: no bank conflicts
-    return s;
-}
+constexpr int kPairRow = 2 * kTile;     // bytes per payload position: one pair per lane
+constexpr int kPairSlack = 4096;         // LDS above the last array that a corrupt stream may read
+constexpr int kClampGroups = 4;          // pointers are clamped every 4 x 4 decode steps
 
 struct AttnArgs {
     TabArgs tk, tv;
@@ -158,7 +155,9 @@ __device__ __forceinline__ uint32_t dstep(uint32_t& X, uint32_t& pq, uint32_t ma
     const uint32_t q = r >> (sh ^ 29u);
     // one v_lshl_or_b32, so that the next table address stays a single mask
     asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(y), "v"(sh), "v"(q));
-    pq += sh >> 2;
+    // pq += (sh / 8) positions of kPairRow bytes, as one v_lshl_add_u32 (left
+    // to itself the compiler keeps a running sum and adds it to the base)
+    asm("v_lshl_add_u32 %0, %1, 4, %2" : "=v"(pq) : "v"(sh), "v"(pq));
     return ex;
 }
 
@@ -205,16 +204,23 @@ __device__ __forceinline__ void load_record(uint32_t (&r)[kMaxRecDwords], const 
         if (k < CW) r[k] = src[k];
 }
 
-// Payload bytes of a record -> the lane's byte-pair array.
+// Payload bytes of a record -> the lane's column of a byte-pair array: the
+// big-endian pair (b_k << 8) | b_{k+1} of position k goes to dst + k * 128.
+// A lane's pairs share one LDS bank whatever position it has reached, so the
+// lanes of a wavefront conflict at most two-way.
 __device__ __forceinline__ void build_pairs(const uint32_t (&r)[kMaxRecDwords], int CW, uint8_t* dst) {
 #pragma unroll
     for (int k = 2; k < kMaxRecDwords; ++k) {
         if (k < CW) {
             const uint32_t w = r[k];
             const uint32_t wn = (k + 1 < CW) ? r[(k + 1) & (kMaxRecDwords - 1)] : 0u;
-            uint32_t* d = reinterpret_cast<uint32_t*>(dst + 8 * (k - 2));
-            d[0] = __builtin_amdgcn_perm(w, w, 0x01020001u);
-            d[1] = __builtin_amdgcn_perm(wn, w, 0x03040203u);
+            const uint32_t d0 = __builtin_amdgcn_perm(w, w, 0x01020001u);
+            const uint32_t d1 = __builtin_amdgcn_perm(wn, w, 0x03040203u);
+            uint8_t* p = dst + 4 * (k - 2) * kPairRow;
+            *reinterpret_cast<uint16_t*>(p) = (uint16_t)d0;
+            *reinterpret_cast<uint16_t*>(p + kPairRow) = (uint16_t)(d0 >> 16);
+            *reinterpret_cast<uint16_t*>(p + 2 * kPairRow) = (uint16_t)d1;
+            *reinterpret_cast<uint16_t*>(p + 3 * kPairRow) = (uint16_t)(d1 >> 16);
         }
     }
 }
@@ -317,8 +323,8 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
 
     // ---- per-wavefront state
     uint8_t* wreg = smem + L.waves + wave * L.wave_stride;
-    const uint32_t pk_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.p16 + lane * L.p16_stride);
-    const uint32_t pv_lane = pk_lane + (uint32_t)(kTile * L.p16_stride);
+    const uint32_t pk_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.pk + 2 * lane);
+    const uint32_t pv_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.pv + 2 * lane);
     uint8_t* vtile = wreg + L.vtile;     // overlays the pair arrays once both streams are decoded
     uint8_t* plimb = wreg + L.plimb;
     const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
@@ -363,6 +369,9 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
         // after the writes (LDS keeps a wavefront's accesses in order)
         asm volatile("" ::: "memory");
         uint32_t pq = pk_lane, pv = pv_lane;
+        // one past the last payload position: a valid stream never reads beyond
+        const uint32_t pk_end = pk_lane + (uint32_t)((Ck - kPayloadOffset) * kPairRow);
+        const uint32_t pv_end = pv_lane + (uint32_t)((Cv - kPayloadOffset) * kPairRow);
 
         // ---- keys and values decoded together: two independent rANS chains
         //      per lane.  Key levels go straight into the q . k products; value
@@ -395,11 +404,18 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
                 dk[hg][1] = mfma(ql.y, lk, dk[hg][1]);
                 dk[hg][2] = mfma(ql.z, lk, dk[hg][2]);
             }
+            // a corrupt stream may run past its array: clamp often enough that
+            // it cannot leave the workgroup's LDS (kPairSlack above the arrays)
+            if ((grp % kClampGroups) == kClampGroups - 1) {
+                pq = min(pq, pk_end);
+                pv = min(pv, pv_end);
+            }
             // keep the scheduler inside one group: live ranges stay short
             __builtin_amdgcn_sched_barrier(0);
         }
-        corrupt |= valid && ((xk >> 3) != kRansL || pq > pk_lane + 2u * (uint32_t)(Ck - kPayloadOffset));
-        corrupt |= valid && ((xv >> 3) != kRansL || pv > pv_lane + 2u * (uint32_t)(Cv - kPayloadOffset));
+        // every stream ends at x = L having read at most its C - 8 payload bytes
+        corrupt |= valid && ((xk >> 3) != kRansL || pq > pk_end);
+        corrupt |= valid && ((xv >> 3) != kRansL || pv > pv_end);
 
         // ---- scores (Eq. fold-key) and online softmax; the value scale is
         //      folded into the weight (Eq. fold-value)
@@ -585,24 +601,24 @@ AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut) 
     L.qsum = off;
     off += align16(GP * 4);
     L.qmu = off;
-    off += align16(((4096 + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1) * GP * 4);
+    off += align16(((kMaxChunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1) * GP * 4);
     L.waves = off;
-    L.p16_stride = std::max(p16_stride_for(Ck), p16_stride_for(Cv));
     int w = 0;
-    L.p16 = w;                                     // key pairs, then value pairs
+    L.pk = w;                                      // key pairs, then value pairs
+    L.pv = w + align16((Ck - kPayloadOffset) * kPairRow);
     L.vtile = w;                                   // reuses the pair arrays
-    w += std::max(align16(2 * kTile * L.p16_stride), align16(kVSlice * kVRow));
+    w += std::max(L.pv + align16((Cv - kPayloadOffset) * kPairRow), align16(kVSlice * kVRow));
     L.plimb = w;
     w += align16(HG * 4 * (kTile / 4) * 16);
     L.wave_stride = w;
-    int nw = (kMaxLds - off) / w;
+    int nw = (kMaxLds - kPairSlack - off) / w;
     if (nw > max_waves(HG)) nw = max_waves(HG);
     // the query rotation scratch and the final merge must fit as well
     while (nw > 0 && (nw * w < G * kD * 4 ||
                       off + nw * w < nw * (2 * GP + GP * kD) * 4))
         --nw;
     L.nw = nw;
-    L.total = off + nw * w;
+    L.total = off + nw * w + kPairSlack;
     return L;
 }
 
@@ -613,20 +629,36 @@ struct ChunkPlan {
 
 int64_t max_chunks(int t_cap) { return (t_cap + kMinChunk - 1) / kMinChunk; }
 
-// Chunk = a whole number of passes of the workgroup (nw x 64 tokens), at
-// least kMinChunk tokens, sized for about a thousand workgroups (four per CU).
-ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap, int nw) {
+// Few, large chunks: one workgroup fits per CU (LDS), so the grid is sized to
+// about one workgroup per CU (more when the batch has more (sequence, KV head)
+// pairs than there are CUs), with chunks of kMinChunk..kMaxChunk tokens in
+// whole 64-token tiles.  Every workgroup then runs its waves over many tiles
+// and the grid ends in whole rounds of the CUs.
+ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap, int num_cus) {
     ChunkPlan p;
-    const int pass = nw * kTile;
-    int k = (int)(((int64_t)B * Hkv * t_cap) / ((int64_t)pass * 1024));
-    k = std::max(k, (kMinChunk + pass - 1) / pass);
-    k = std::min(k, std::max(1, 4096 / pass));
-    p.chunk = pass * k;
-    if (p.chunk > t_cap) p.chunk = ((t_cap + pass - 1) / pass) * pass;
-    if (p.chunk < kMinChunk) p.chunk = kMinChunk;
-    p.nchunks = (t_cap + p.chunk - 1) / p.chunk;
+    const int64_t pairs = (int64_t)B * Hkv;
+    int64_t nc = std::max<int64_t>((t_cap + kMaxChunk - 1) / kMaxChunk, (num_cus + pairs - 1) / pairs);
+    int chunk = (int)((t_cap + nc - 1) / nc);
+    chunk = ((chunk + kTile - 1) / kTile) * kTile;
+    chunk = std::max(chunk, kMinChunk);
+    chunk = std::min(chunk, kMaxChunk);
+    p.chunk = chunk;
+    p.nchunks = (t_cap + chunk - 1) / chunk;
     p.slots_max = (int64_t)B * Hq * max_chunks(t_cap);
     return p;
+}
+
+int cu_count() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cached[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        cached[dev] = n;
+    }
+    return cached[dev];
 }
 
 }  // namespace
@@ -696,7 +728,7 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uin
                        ? 1 : 0;
     a.L = attn_layout(a.tk.p, a.tv.p, a.tk.C, a.tv.C, G, a.shared_lut != 0);
     if (a.L.nw < 1) return DQ_ERR_INVALID_ARG;
-    const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap, a.L.nw);
+    const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap, cu_count());
     a.q = q;
     a.Hq = Hq;
     a.Hkv = Hkv;

@@ -272,7 +272,7 @@ def test_attention_ragged_lengths(dq):
     assert _rel_err(got[1:], ref) < TOL
 
 
-@pytest.mark.parametrize("G", [1, 2, 8])
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
 def test_attention_gqa_groups(dq, G):
     wl = wlmod.workload("b32_t32k_g8")     # keys 48 B / values 32 B
     gtk, otk = _tabs(dq, wl.k)
@@ -288,6 +288,26 @@ def test_attention_gqa_groups(dq, G):
     lens = [1024, 700]
     ref = _oracle_attention(wlmod.bf16_bits(q), krec, mq, ms, vrec, otk, otv, lens, G)
     got, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl2, krec, mq, ms, vrec), lens, Hq)
+    assert st == 0
+    assert _rel_err(got, ref) < TOL
+
+
+@pytest.mark.parametrize("C,G", [(32, 4), (36, 8), (48, 4), (64, 4), (64, 8)])
+def test_attention_record_lengths(dq, C, G):
+    """Equal key/value record lengths of the 2.0 / 2.25 / 3.0 / 4.0 bits-per-
+    element budgets (paper level counts), 4 and 8 query heads per KV head."""
+    coding = wlmod.Coding(levels=wlmod.PAPER_LEVELS[C], record_bytes=C, alpha=1.4)
+    gtk, otk = _tabs(dq, coding)
+    B, T, Hkv = 2, 1536, 2
+    wl = wlmod.Workload("r", B, T, Hkv * G, Hkv, 4, coding, coding)
+    k = wlmod.bf16_bits(wlmod.make_k(wl, 15))
+    v = wlmod.bf16_bits(wlmod.make_v(wl, 15))
+    q = wlmod.make_q(wl, 15)
+    krec, mq, ms, _ = kv.encode_keys(k, otk)
+    vrec, _ = kv.encode_values(v, otk)
+    lens = [1536, 1000]
+    ref = _oracle_attention(wlmod.bf16_bits(q), krec, mq, ms, vrec, otk, otk, lens, G)
+    got, st = _gpu_attention(dq, gtk, gtk, q, *_upload_cache(dq, wl, krec, mq, ms, vrec), lens, Hkv * G)
     assert st == 0
     assert _rel_err(got, ref) < TOL
 
