@@ -346,25 +346,29 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
     bool corrupt = false;
     const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
 
+    // records of the wavefront's next tile are loaded while it decodes this one
+    uint32_t rk[kMaxRecDwords], rv[kMaxRecDwords];
+    if (wave < ntiles) {
+        const int64_t tok = bh * a.t_cap + start + wave * kTile + lane;
+        load_record(rk, a.krec, tok, CWk);
+        load_record(rv, a.vrec, tok, CWv);
+    }
     for (int tile = wave; tile < ntiles; tile += L.nw) {
         const int t_base = start + tile * kTile;
         const int t = t_base + lane;
         const bool valid = t < T;
-        const int64_t tok = bh * a.t_cap + t_base + lane;
 
         // ---- both records of the lane's token -> headers + byte-pair arrays
-        uint32_t hk0, xk, hv0, xv;
-        {
-            uint32_t r[kMaxRecDwords];
-            load_record(r, a.krec, tok, CWk);
-            hk0 = r[0];
-            xk = r[1] << 3;
-            build_pairs(r, CWk, smem + pk_lane);
-            load_record(r, a.vrec, tok, CWv);
-            hv0 = r[0];
-            xv = r[1] << 3;
-            build_pairs(r, CWv, smem + pv_lane);
+        const uint32_t hk0 = rk[0], xk0 = rk[1] << 3;
+        const uint32_t hv0 = rv[0], xv0 = rv[1] << 3;
+        build_pairs(rk, CWk, smem + pk_lane);
+        build_pairs(rv, CWv, smem + pv_lane);
+        if (tile + L.nw < ntiles) {
+            const int64_t tok = bh * a.t_cap + t_base + L.nw * kTile + lane;
+            load_record(rk, a.krec, tok, CWk);
+            load_record(rv, a.vrec, tok, CWv);
         }
+        uint32_t xk = xk0, xv = xv0;
         // the pair arrays are read back by this lane only: order the reads
         // after the writes (LDS keeps a wavefront's accesses in order)
         asm volatile("" ::: "memory");
@@ -433,18 +437,22 @@ __global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(Att
                 const float score = (valid && g < G) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
                 const float tmax = wave_max(score);
                 const float mn = fmaxf(m_run[g], tmax);
+                // v_exp_f32 directly: arguments are <= 0 and results that would
+                // be denormal may flush to zero
                 const float corr = (m_run[g] == -INFINITY || mn == -INFINITY) ? (m_run[g] == mn ? 1.f : 0.f)
-                                                                               : exp2f(m_run[g] - mn);
-                const float p = (score == -INFINITY) ? 0.f : exp2f(score - mn);
+                                                                               : __builtin_amdgcn_exp2f(m_run[g] - mn);
+                const float p = (score == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(score - mn);
                 l_part[g] = l_part[g] * corr + p;
                 acco[g] = acco[g] * corr + p * ov;
                 accf[0][g] *= corr;
                 accf[1][g] *= corr;
                 m_run[g] = mn;
-                const float pw = p * sv;
+                const float pw = p * sv;                 // >= 0: scales are non-negative
                 const float smax = wave_max(pw);
                 pscale[g] = smax * (1.0f / 4194304.0f);
-                pint[g] = smax > 0.f ? min(4194304, (int)rintf(pw / pscale[g])) : 0;
+                // 22-bit fixed point of pw relative to the tile maximum
+                const float inv = smax > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax) : 0.f;
+                pint[g] = min(4194304, (int)rintf(pw * inv));
             }
         // weight digits -> LDS [hg][head][token quad] x (d0, d1, d2) words
 #pragma unroll
