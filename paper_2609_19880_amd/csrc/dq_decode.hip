@@ -25,7 +25,7 @@ namespace {
 
 constexpr int kD = 128;          // head_dim of the attention kernels
 constexpr int kTile = 64;        // tokens per wavefront tile (one per lane)
-constexpr int kMaxWaves = 12;    // wavefronts per workgroup (LDS permitting)
+constexpr int kMaxWaves = 16;    // wavefronts per workgroup (LDS permitting)
 constexpr int kVSlice = 64;      // value channels per PV pass
 constexpr int kVRow = 68;        // bytes per channel row of the value tile (64 + pad)
 constexpr int kMaxRecDwords = 16;
@@ -225,16 +225,20 @@ __device__ __forceinline__ void build_pairs(const uint32_t (&r)[kMaxRecDwords], 
     }
 }
 
-// Wavefronts per workgroup: 12 (3 per SIMD) for up to 4 query heads per KV
-// head; 8 for up to 8, whose accumulators need more registers.
-__host__ __device__ constexpr int max_waves(int HG) { return HG == 1 ? kMaxWaves : 8; }
+// Wavefronts per workgroup.  Up to 4 query heads per KV head: 16 (4 per SIMD,
+// at most 128 VGPRs) for records of up to 36 bytes, 12 for longer or
+// run-time-length records, whose prefetched record words need more
+// registers.  Up to 8 query heads: 8, for the larger accumulators.
+__host__ __device__ constexpr int max_waves(int HG, int RW) {
+    return HG == 1 ? ((RW == 8 || RW == 9) ? kMaxWaves : 12) : 8;
+}
 
 constexpr uint32_t kLutVOffset = 8u << 12;   // value table when it differs from the key table
 
 // RW: record length in dwords when keys and values share it (compile-time
 // record loads), 0 for the general case.
 template <int HG, uint32_t LUTV, int RW>
-__global__ __launch_bounds__(max_waves(HG) * kWave) void attn_partial_kernel(AttnArgs a) {
+__global__ __launch_bounds__(max_waves(HG, RW) * kWave) void attn_partial_kernel(AttnArgs a) {
     constexpr int GP = 4 * HG;
     extern __shared__ __align__(16) uint8_t smem[];
     const AttnLayout& L = a.L;
@@ -589,7 +593,17 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
 }
 
 // LDS layout for given coding sizes; picks the largest wavefront count that fits.
-AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut) {
+// Record length in dwords of the instantiation that serves (Ck, Cv); 0 = the
+// general kernel.
+int compiled_rw(int Ck, int Cv) {
+    if (Ck != Cv) return 0;
+    switch (Ck / 4) {
+        case 8: case 9: case 12: case 16: return Ck / 4;
+        default: return 0;
+    }
+}
+
+AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut, int rw) {
     const int GP = G <= 4 ? 4 : 8, HG = GP / 4;
     AttnLayout L;
     int off = 0;
@@ -615,12 +629,12 @@ AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut) 
     L.pk = w;                                      // key pairs, then value pairs
     L.pv = w + align16((Ck - kPayloadOffset) * kPairRow);
     L.vtile = w;                                   // reuses the pair arrays
-    w += std::max(L.pv + align16((Cv - kPayloadOffset) * kPairRow), align16(kVSlice * kVRow));
-    L.plimb = w;
-    w += align16(HG * 4 * (kTile / 4) * 16);
+    L.plimb = w + align16(kVSlice * kVRow);        // so do the weight digits
+    w = std::max(L.pv + align16((Cv - kPayloadOffset) * kPairRow),
+                 L.plimb + align16(HG * 4 * (kTile / 4) * 16));
     L.wave_stride = w;
     int nw = (kMaxLds - kPairSlack - off) / w;
-    if (nw > max_waves(HG)) nw = max_waves(HG);
+    if (nw > max_waves(HG, rw)) nw = max_waves(HG, rw);
     // the query rotation scratch and the final merge must fit as well
     while (nw > 0 && (nw * w < G * kD * 4 ||
                       off + nw * w < nw * (2 * GP + GP * kD) * 4))
@@ -710,8 +724,7 @@ static int launch_rw(AttnArgs& a, dim3 grid, hipStream_t stream) {
 // head_dim 128 get their own instantiation; other lengths take the general one.
 template <int HG, uint32_t LUTV>
 static int launch_hg(AttnArgs& a, dim3 grid, hipStream_t stream) {
-    const int rw = a.tk.C == a.tv.C ? a.tk.C / 4 : 0;
-    switch (rw) {
+    switch (compiled_rw(a.tk.C, a.tv.C)) {
         case 8: return launch_rw<HG, LUTV, 8>(a, grid, stream);
         case 9: return launch_rw<HG, LUTV, 9>(a, grid, stream);
         case 12: return launch_rw<HG, LUTV, 12>(a, grid, stream);
@@ -734,7 +747,7 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uin
                                  tk->cfg.precision_bits == tv->cfg.precision_bits &&
                                  tk->cfg.alpha == tv->cfg.alpha && tk->cfg.head_dim == tv->cfg.head_dim))
                        ? 1 : 0;
-    a.L = attn_layout(a.tk.p, a.tv.p, a.tk.C, a.tv.C, G, a.shared_lut != 0);
+    a.L = attn_layout(a.tk.p, a.tv.p, a.tk.C, a.tv.C, G, a.shared_lut != 0, compiled_rw(a.tk.C, a.tv.C));
     if (a.L.nw < 1) return DQ_ERR_INVALID_ARG;
     const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap, cu_count());
     a.q = q;
