@@ -206,8 +206,7 @@ __device__ __forceinline__ void load_record(uint32_t (&r)[kMaxRecDwords], const 
 
 // Payload bytes of a record -> the lane's column of a byte-pair array: the
 // big-endian pair (b_k << 8) | b_{k+1} of position k goes to dst + k * 128.
-// A lane's pairs share one LDS bank whatever position it has reached, so the
-// lanes of a wavefront conflict at most two-way.
+// A lane's pairs stay in one LDS bank whatever position it has reached.
 __device__ __forceinline__ void build_pairs(const uint32_t (&r)[kMaxRecDwords], int CW, uint8_t* dst) {
 #pragma unroll
     for (int k = 2; k < kMaxRecDwords; ++k) {
@@ -327,8 +326,11 @@ __global__ __launch_bounds__(max_waves(HG, RW) * kWave) void attn_partial_kernel
 
     // ---- per-wavefront state
     uint8_t* wreg = smem + L.waves + wave * L.wave_stride;
-    const uint32_t pk_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.pk + 2 * lane);
-    const uint32_t pv_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.pv + 2 * lane);
+    // lane l's column in a row of 64 pairs: lanes l and l + 32 share a dword,
+    // so each half-wavefront reads 32 different banks
+    const uint32_t col = (uint32_t)(4 * (lane & 31) + 2 * (lane >> 5));
+    const uint32_t pk_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.pk) + col;
+    const uint32_t pv_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.pv) + col;
     uint8_t* vtile = wreg + L.vtile;     // overlays the pair arrays once both streams are decoded
     uint8_t* plimb = wreg + L.plimb;
     const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
