@@ -8,11 +8,13 @@
 //  * encode: one workgroup per (batch, head, 64 consecutive tokens).  Each
 //    wavefront takes a stream at a time with its n values spread over the
 //    lanes and keeps them in registers through Alg. 1 (FitMinMax -> Drift ->
-//    Refit -> fp16 -> Drift); distortions are recomputed on the fly for every
-//    bisection step and the code length is reduced across the wavefront, as
-//    Sec. 4.5 describes for the encoder.  The symbols of the 64 streams then
-//    go through LDS to lane-per-stream backward rANS, and the 64 records are
-//    written as one contiguous span.
+//    Refit -> fp16 -> Drift); no n x M distortion matrix goes to memory (the
+//    distortions of up to 8 or 16 levels stay in registers for the 13
+//    assignments of a drift, more levels are recomputed on the fly) and the
+//    code length is reduced across the wavefront, as Sec. 4.5 describes for
+//    the encoder.  The symbols of the 64 streams then go through LDS to
+//    lane-per-stream backward rANS (divisions by f as exact multiply-high
+//    reciprocals), and the 64 records are written as one contiguous span.
 //
 // Every floating-point step is fp64 in a fixed order without contraction
 // (this file is built with -ffp-contract=off), so the records are
@@ -87,26 +89,52 @@ struct DriftCtx {
     int rmin;
 };
 
-template <int VPL>
-__device__ __forceinline__ int assign_cost(const double (&x)[VPL], double s, double o, double lam,
-                                           const DriftCtx& c, int (&m)[VPL]) {
+// Assignment at one lambda: each value takes argmin_m D_im + lambda r_m (ties to
+// the smallest m); returns the wavefront's total Q16 cost.  MB > 0: the
+// distortions D[k][m] of the M <= MB levels were computed once per drift;
+// MB = 0: they are recomputed here (t = s m, u = o + t, e = x - u, D = e e).
+template <int VPL, int MB>
+__device__ __forceinline__ int assign_cost(const double (&x)[VPL], const double (&D)[VPL][MB > 0 ? MB : 1],
+                                           double s, double o, double lam, const DriftCtx& c,
+                                           int (&m)[VPL]) {
     double best[VPL];
-#pragma unroll
-    for (int k = 0; k < VPL; ++k) {
-        best[k] = DBL_MAX;
-        m[k] = 0;
-    }
-    for (int mm = 0; mm < c.M; ++mm) {
-        const double t = s * (double)mm;
-        const double u = o + t;
-        const double pen = lam * c.rate[mm];
+    if (MB > 0) {
+        const double pen0 = lam * c.rate[0];
 #pragma unroll
         for (int k = 0; k < VPL; ++k) {
-            const double e = x[k] - u;
-            const double J = e * e + pen;
-            if (J < best[k] || mm == 0) {
-                best[k] = J;
-                m[k] = mm;
+            best[k] = D[k][0] + pen0;
+            m[k] = 0;
+        }
+#pragma unroll
+        for (int mm = 1; mm < (MB > 0 ? MB : 1); ++mm) {
+            if (mm < c.M) {
+                const double pen = lam * c.rate[mm];
+#pragma unroll
+                for (int k = 0; k < VPL; ++k) {
+                    const double J = D[k][mm] + pen;
+                    m[k] = J < best[k] ? mm : m[k];
+                    best[k] = fmin(best[k], J);
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) {
+            best[k] = DBL_MAX;
+            m[k] = 0;
+        }
+        for (int mm = 0; mm < c.M; ++mm) {
+            const double t = s * (double)mm;
+            const double u = o + t;
+            const double pen = lam * c.rate[mm];
+#pragma unroll
+            for (int k = 0; k < VPL; ++k) {
+                const double e = x[k] - u;
+                const double J = e * e + pen;
+                if (J < best[k] || mm == 0) {
+                    best[k] = J;
+                    m[k] = mm;
+                }
             }
         }
     }
@@ -120,19 +148,37 @@ __device__ __forceinline__ int assign_cost(const double (&x)[VPL], double s, dou
 // 40-octave bracket below hi = ceil(log2(8 (max D - min D))), lambda on the
 // 2^(U/512) grid, 12 steps, assignment at the final hi; nearest cheapest
 // symbol if even that overflows; cheapest symbol if all distortions are equal.
-template <int VPL>
+template <int VPL, int MB>
 __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget,
                       const DriftCtx& c, int (&m)[VPL]) {
+    double D[VPL][MB > 0 ? MB : 1];
     double dmax = -DBL_MAX, dmin = DBL_MAX;
-    for (int mm = 0; mm < c.M; ++mm) {
-        const double t = s * (double)mm;
-        const double u = o + t;
+    if (MB > 0) {
 #pragma unroll
-        for (int k = 0; k < VPL; ++k) {
-            const double e = x[k] - u;
-            const double D = e * e;
-            dmax = fmax(dmax, D);
-            dmin = fmin(dmin, D);
+        for (int mm = 0; mm < (MB > 0 ? MB : 1); ++mm) {
+            const double t = s * (double)mm;
+            const double u = o + t;
+#pragma unroll
+            for (int k = 0; k < VPL; ++k) {
+                const double e = x[k] - u;
+                D[k][mm] = e * e;
+                if (mm < c.M) {
+                    dmax = fmax(dmax, D[k][mm]);
+                    dmin = fmin(dmin, D[k][mm]);
+                }
+            }
+        }
+    } else {
+        for (int mm = 0; mm < c.M; ++mm) {
+            const double t = s * (double)mm;
+            const double u = o + t;
+#pragma unroll
+            for (int k = 0; k < VPL; ++k) {
+                const double e = x[k] - u;
+                const double Dv = e * e;
+                dmax = fmax(dmax, Dv);
+                dmin = fmin(dmin, Dv);
+            }
         }
     }
     dmax = wave_max(dmax);
@@ -151,14 +197,14 @@ __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget
         const int u_mid = (u_lo + u_hi) >> 1;
         const double lam = ldexp((double)c.lam[u_mid & (kLambdaSteps - 1)], u_mid >> 9);
         int tmp[VPL];
-        const int cst = assign_cost<VPL>(x, s, o, lam, c, tmp);
+        const int cst = assign_cost<VPL, MB>(x, D, s, o, lam, c, tmp);
         if ((int64_t)cst <= budget)
             u_hi = u_mid;
         else
             u_lo = u_mid;
     }
     const double lam = ldexp((double)c.lam[u_hi & (kLambdaSteps - 1)], u_hi >> 9);
-    const int cst = assign_cost<VPL>(x, s, o, lam, c, m);
+    const int cst = assign_cost<VPL, MB>(x, D, s, o, lam, c, m);
     if ((int64_t)cst > budget) {
         double best[VPL];
 #pragma unroll
@@ -170,9 +216,9 @@ __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget
 #pragma unroll
             for (int k = 0; k < VPL; ++k) {
                 const double e = x[k] - u;
-                const double D = e * e;
-                if (D < best[k]) {
-                    best[k] = D;
+                const double Dv = e * e;
+                if (Dv < best[k]) {
+                    best[k] = Dv;
                     m[k] = mm;
                 }
             }
@@ -259,12 +305,12 @@ __device__ __forceinline__ void stream_values(const EncArgs& a, int b, int h, in
     }
 }
 
-template <int VPL>
+template <int VPL, int MB>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     constexpr int n = kWave * VPL;
     extern __shared__ __align__(16) uint8_t smem[];
     // layout: rate[64] f64 | cost[64] | lam[512] | budget[64] i64 | s16[64] | o16[64]
-    //         | flag[64] | sym[64][n] | rec[64][C]
+    //         | flag[64] | rcp[64] | rsh[64] | sym[64][n] | rec[64][C]
     double* s_rate = reinterpret_cast<double*>(smem);
     int32_t* s_cost = reinterpret_cast<int32_t*>(s_rate + DQ_MAX_LEVELS);
     float* s_lam = reinterpret_cast<float*>(s_cost + DQ_MAX_LEVELS);
@@ -272,7 +318,9 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     uint16_t* s_s16 = reinterpret_cast<uint16_t*>(s_budget + kEncStreams);
     uint16_t* s_o16 = s_s16 + kEncStreams;
     int32_t* s_flag = reinterpret_cast<int32_t*>(s_o16 + kEncStreams);
-    uint8_t* s_sym = reinterpret_cast<uint8_t*>(s_flag + kEncStreams);
+    uint32_t* s_rcp = reinterpret_cast<uint32_t*>(s_flag + kEncStreams);
+    uint32_t* s_rsh = s_rcp + DQ_MAX_LEVELS;
+    uint8_t* s_sym = reinterpret_cast<uint8_t*>(s_rsh + DQ_MAX_LEVELS);
     uint8_t* s_rec = s_sym + kEncStreams * n;
 
     const TabArgs& ta = a.ta;
@@ -285,6 +333,12 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     for (int i = tid; i < ta.M; i += kEncThreads) {
         s_cost[i] = ta.t.cost[i];
         s_rate[i] = (double)ta.t.cost[i] * (1.0 / 65536.0);
+        // floor(x / f) = mulhi(x, rcp) >> (sh - 1) for x < 2^31, where
+        // sh = ceil(log2 f) and rcp = ceil(2^(31 + sh) / f) (f = 1: x itself)
+        const uint32_t f = (uint32_t)ta.t.freq[i];
+        const uint32_t sh = f > 1 ? 32u - (uint32_t)__builtin_clz(f - 1u) : 0u;
+        s_rcp[i] = f > 1 ? (uint32_t)(((1ull << (31 + sh)) + f - 1) / f) : 0u;
+        s_rsh[i] = f > 1 ? sh - 1u : 0u;
     }
     for (int i = tid; i < kLambdaSteps; i += kEncThreads) s_lam[i] = ta.t.lam[i];
     for (int i = tid; i < kEncStreams; i += kEncThreads) {
@@ -316,7 +370,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
                 const double s0 = (mx - mn) / (double)(ta.M - 1);
                 const double o0 = mn;
                 int m1[VPL];
-                drift<VPL>(x, s0, o0, ta.budget, dc, m1);
+                drift<VPL, MB>(x, s0, o0, ta.budget, dc, m1);
                 // least-squares refit
                 int sm = 0, smm = 0;
                 double mx_[VPL];
@@ -358,7 +412,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
             const double s16 = (double)__half2float(__ushort_as_half(sb16));
             const double o16 = (double)__half2float(__ushort_as_half(ob16));
             int m2[VPL];
-            drift<VPL>(x, s16, o16, s_budget[i], dc, m2);
+            drift<VPL, MB>(x, s16, o16, s_budget[i], dc, m2);
 #pragma unroll
             for (int k = 0; k < VPL; ++k) s_sym[i * n + lane + kWave * k] = (uint8_t)m2[k];
         }
@@ -372,10 +426,12 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
             const uint32_t xmax_unit = (kRansL >> ta.p) << 8;
             uint32_t xs = kRansL;
             int emitted = 0;
+            const uint32_t P = 1u << ta.p;
             for (int j = n - 1; j >= 0; --j) {
                 const int m = s_sym[i * n + j];
                 const uint32_t f = (uint32_t)ta.t.freq[m];
                 const uint32_t c = (uint32_t)ta.t.cum[m];
+                const uint32_t rcp = s_rcp[m], rsh = s_rsh[m];
                 const uint32_t xmax = xmax_unit * f;
 #pragma unroll
                 for (int r = 0; r < 2; ++r) {
@@ -385,7 +441,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
                         xs >>= 8;
                     }
                 }
-                xs = (xs / f) * (1u << ta.p) + (xs % f) + c;
+                // Enc(x, m) = floor(x / f) 2^p + (x mod f) + c = x + q (2^p - f) + c;
+                // after renormalization x < 256 L = 2^29
+                const uint32_t q = f > 1 ? __umulhi(xs, rcp) >> rsh : xs;
+                xs = xs + q * (P - f) + c;
             }
             if (emitted > cap) {
                 s_flag[i] = 1;
@@ -463,14 +522,25 @@ int launch_encode(const dq_tables* tab, const uint16_t* kv, int64_t sb, int64_t 
     const size_t smem = sizeof(double) * DQ_MAX_LEVELS + sizeof(int32_t) * DQ_MAX_LEVELS +
                         sizeof(float) * kLambdaSteps + sizeof(int64_t) * kEncStreams +
                         2 * sizeof(uint16_t) * kEncStreams + sizeof(int32_t) * kEncStreams +
+                        2 * sizeof(uint32_t) * DQ_MAX_LEVELS +
                         (size_t)kEncStreams * n + (size_t)kEncStreams * a.ta.C;
     dim3 grid((n_new + kEncStreams - 1) / kEncStreams, H, B);
-    switch (vpl) {
-        case 1: encode_kernel<1><<<grid, kEncThreads, smem, stream>>>(a); break;
-        case 2: encode_kernel<2><<<grid, kEncThreads, smem, stream>>>(a); break;
-        case 4: encode_kernel<4><<<grid, kEncThreads, smem, stream>>>(a); break;
+    // distortions held in registers for up to 8 levels (16 with two values per lane)
+    const int M = tab->cfg.levels;
+    const int mb = M <= 8 ? 8 : (M <= 16 && vpl <= 2) ? 16 : 0;
+#define DQ_ENC(V, MB) encode_kernel<V, MB><<<grid, kEncThreads, smem, stream>>>(a)
+    switch (vpl * 100 + mb) {
+        case 108: DQ_ENC(1, 8); break;
+        case 116: DQ_ENC(1, 16); break;
+        case 100: DQ_ENC(1, 0); break;
+        case 208: DQ_ENC(2, 8); break;
+        case 216: DQ_ENC(2, 16); break;
+        case 200: DQ_ENC(2, 0); break;
+        case 408: DQ_ENC(4, 8); break;
+        case 400: DQ_ENC(4, 0); break;
         default: return DQ_ERR_INVALID_ARG;
     }
+#undef DQ_ENC
     return hip_check("kernel launch", hipGetLastError());
 }
 
