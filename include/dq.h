@@ -117,6 +117,11 @@ void dq_free_tables(dq_tables* tables);
  *   status:  device u32, may be NULL; DQ_STATUS_RANGE / DQ_STATUS_OVERFLOW.
  * Every stream is rotated with the unnormalized Sylvester Hadamard matrix.
  * The records are bit-identical to the reference definition of the format.
+ * Requires head_dim <= 256, 1 <= kv_heads <= 65535, 0 <= batch <= 65535,
+ * t0 >= 0, n_new >= 0, t0 + n_new <= t_cap and non-negative strides; with the
+ * mean buffers also t0, n_new and t_cap multiples of 128.  Returns DQ_OK
+ * (nothing is launched when batch or n_new is 0), DQ_ERR_INVALID_ARG, or
+ * DQ_ERR_HIP if a launch fails.
  */
 int dq_encode_kv(const dq_tables* tables, const uint16_t* kv, int64_t stride_b,
                  int64_t stride_t, int64_t stride_h, int32_t batch,
@@ -140,8 +145,11 @@ size_t dq_decode_workspace_bytes(int32_t batch, int32_t q_heads, int32_t kv_head
  *   out:      fp32 [batch][q_heads][head_dim] (a sequence of length 0 gives 0)
  *   workspace: device memory of dq_decode_workspace_bytes(...) bytes
  *   status:   device u32, may be NULL; DQ_STATUS_CORRUPT for malformed records
- * t_cap must be a multiple of 128; q_heads a multiple of kv_heads with
- * q_heads / kv_heads <= 8.
+ * Requires head_dim = 128 for both tables, record lengths C_k and C_v that
+ * are multiples of 4 in [12, 64], t_cap a positive multiple of 128,
+ * 1 <= batch <= 65535, 1 <= kv_heads <= 65535, q_heads a multiple of kv_heads
+ * with q_heads / kv_heads <= 8.  Returns DQ_OK, DQ_ERR_INVALID_ARG (nothing
+ * launched), DQ_ERR_WORKSPACE (workspace missing or too small) or DQ_ERR_HIP.
  */
 int dq_decode_attention(const dq_tables* k_tables, const dq_tables* v_tables,
                         const uint16_t* q, int32_t batch, int32_t q_heads,
@@ -159,8 +167,9 @@ int dq_decode_attention(const dq_tables* k_tables, const dq_tables* v_tables,
  * head, context chunk) into the workspace (online-softmax state over the
  * chunk); _merge combines the chunks by log-sum-exp, undoes the value
  * rotation and writes `out`.  Arguments mean what they mean above; the chunk
- * size is a function of (batch, kv_heads, t_cap), so both halves must be
- * called with the same sizes and workspace.
+ * size is chosen from (batch, kv_heads, t_cap) and the device's CU count and
+ * recorded in the workspace, so both halves must be called with the same
+ * sizes and workspace, on the same device and stream.
  */
 int dq_decode_attention_partial(const dq_tables* k_tables, const dq_tables* v_tables,
                                 const uint16_t* q, int32_t batch, int32_t q_heads,

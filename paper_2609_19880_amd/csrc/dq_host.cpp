@@ -301,6 +301,7 @@ int dq_encode_kv(const dq_tables* t, const uint16_t* kv, int64_t sb, int64_t st,
     if (t->cfg.head_dim > 256) return DQ_ERR_INVALID_ARG;
     if (B < 0 || H <= 0 || t0 < 0 || n_new < 0 || t_cap <= 0 || t0 + n_new > t_cap)
         return DQ_ERR_INVALID_ARG;
+    if (B > 65535 || H > 65535) return DQ_ERR_INVALID_ARG;   // grid dimensions
     if (sb < 0 || st < 0 || sh < 0) return DQ_ERR_INVALID_ARG;
     const bool keys = mean_q != nullptr;
     if (keys != (mean_scale != nullptr)) return DQ_ERR_INVALID_ARG;
