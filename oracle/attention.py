@@ -20,6 +20,10 @@ Readings
 * A2 a query head i reads KV head floor(i / G) (GQA); the logit is
   softmax_scale * q . k (softmax_scale = 1/sqrt(d) by default) and the softmax
   runs over the first seq_len[b] tokens of sequence b.
+* A3 residual window: Sec. 5.1 keeps the most recent tokens in BF16.  A
+  sequence is then seq_len[b] compressed tokens followed by res_len[b] raw
+  tokens (original basis, no rotation, no mean removal), and the softmax runs
+  over all of them; a sequence with no tokens at all gives 0.
 """
 
 from __future__ import annotations
@@ -84,4 +88,33 @@ def attention_folded(q, k_sym, k_s, k_o, k_mean_hat, v_sym, v_s, v_o, seq_lens,
             acc = (a * v_s[b, h, :T].astype(np.float64)) @ v_sym[b, h, :T].astype(np.float64)
             acc = acc + (a * v_o[b, h, :T].astype(np.float64)).sum()
             out[b, i] = hadamard.fwht(acc) / d
+    return out
+
+
+def attention_with_residual(q, k_rot, v_rot, seq_lens, res_k, res_v, res_lens, gqa, softmax_scale):
+    """Decode attention over compressed tokens and a raw residual window, fp64.
+
+    q [B, Hq, d]; k_rot, v_rot [B, Hkv, T, d] rotated reconstructions of the
+    compressed tokens; res_k, res_v [B, Hkv, R, d] raw residual tokens, of
+    which the first res_lens[b] are in use.  Textbook softmax over the union
+    of the two sets in the original basis (reading A3).
+    """
+    B, Hq, d = q.shape
+    H = hadamard.sylvester(d).astype(np.float64)
+    k = k_rot @ H / d
+    v = v_rot @ H / d
+    out = np.zeros((B, Hq, d), dtype=np.float64)
+    for b in range(B):
+        T, R = int(seq_lens[b]), int(res_lens[b])
+        for i in range(Hq):
+            h = i // gqa
+            keys = np.concatenate([k[b, h, :T], res_k[b, h, :R]], axis=0)
+            vals = np.concatenate([v[b, h, :T], res_v[b, h, :R]], axis=0)
+            if keys.shape[0] == 0:
+                continue
+            s = (keys @ q[b, i]) * softmax_scale
+            s = s - s.max()
+            a = np.exp(s)
+            a = a / a.sum()
+            out[b, i] = a @ vals
     return out

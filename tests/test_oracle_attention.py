@@ -73,3 +73,68 @@ def test_gqa_mapping_and_lengths():
     k3[..., 5:, :] = 0
     out3 = attention.attention_folded(q, k3, k_s, k_o, None, v_sym, v_s, v_o, [5], 2, 0.3, window=8)
     assert np.array_equal(out, out3)
+
+
+# ---------------------------------------------------------------- residual window
+
+def test_residual_only_is_plain_attention():
+    """With no compressed tokens the residual window is plain softmax attention
+    over the raw tokens (scipy's softmax as the reference)."""
+    rng = np.random.default_rng(11)
+    B, Hkv, G, R, d = 2, 2, 3, 17, 16
+    q = rng.normal(size=(B, Hkv * G, d))
+    rk = rng.normal(size=(B, Hkv, R, d))
+    rv = rng.normal(size=(B, Hkv, R, d))
+    lens = [R, 5]
+    empty = np.zeros((B, Hkv, 0, d))
+    out = attention.attention_with_residual(q, empty, empty, [0, 0], rk, rv, lens, G, 0.3)
+    for b in range(B):
+        for i in range(Hkv * G):
+            h = i // G
+            ref = scipy.special.softmax(0.3 * rk[b, h, :lens[b]] @ q[b, i]) @ rv[b, h, :lens[b]]
+            assert np.max(np.abs(out[b, i] - ref)) < 1e-13
+
+
+def test_residual_empty_equals_compressed_attention():
+    rng = np.random.default_rng(12)
+    B, Hkv, G, T, d, M, W = 2, 1, 4, 200, 32, 6, 128
+    k_sym, k_s, k_o, mean, v_sym, v_s, v_o = _random_cache(rng, B, Hkv, T, d, M, W)
+    q = rng.normal(size=(B, Hkv * G, d))
+    krot = attention.dequantize(k_sym, k_s, k_o, mean, window=W)
+    vrot = attention.dequantize(v_sym, v_s, v_o)
+    rk = rng.normal(size=(B, Hkv, 8, d))
+    a = attention.attention_with_residual(q, krot, vrot, [T, 77], rk, rk, [0, 0], G, 0.2)
+    b = attention.attention_direct(q, krot, vrot, [T, 77], G, 0.2)
+    assert np.max(np.abs(a - b)) < 1e-13 * np.max(np.abs(b))
+
+
+def test_residual_split_point_is_invisible():
+    """Raw tokens stored as exact rotated reconstructions (k_rot = k H) give
+    the same result whichever of them are called compressed: the basis change
+    and the union of the two sets are both right."""
+    rng = np.random.default_rng(13)
+    B, Hkv, G, N, d = 1, 2, 2, 40, 16
+    H = scipy.linalg.hadamard(d).astype(float)
+    k = rng.normal(size=(B, Hkv, N, d))
+    v = rng.normal(size=(B, Hkv, N, d))
+    q = rng.normal(size=(B, Hkv * G, d))
+    full = attention.attention_with_residual(q, np.zeros((B, Hkv, 0, d)), np.zeros((B, Hkv, 0, d)), [0],
+                                             k, v, [N], G, 0.25)
+    for T in (1, 13, 39, N):
+        out = attention.attention_with_residual(q, k[:, :, :T] @ H, v[:, :, :T] @ H, [T],
+                                                k[:, :, T:], v[:, :, T:], [N - T], G, 0.25)
+        assert np.max(np.abs(out - full)) < 1e-12
+
+
+def test_residual_order_and_empty_sequence():
+    rng = np.random.default_rng(14)
+    B, Hkv, G, R, d = 2, 1, 2, 9, 8
+    q = rng.normal(size=(B, Hkv * G, d))
+    rk = rng.normal(size=(B, Hkv, R, d))
+    rv = rng.normal(size=(B, Hkv, R, d))
+    e = np.zeros((B, Hkv, 0, d))
+    perm = rng.permutation(R)
+    a = attention.attention_with_residual(q, e, e, [0, 0], rk, rv, [R, 0], G, 0.5)
+    b = attention.attention_with_residual(q, e, e, [0, 0], rk[:, :, perm], rv[:, :, perm], [R, 0], G, 0.5)
+    assert np.max(np.abs(a - b)) < 1e-13
+    assert np.all(a[1] == 0.0)        # a sequence with no tokens gives 0
