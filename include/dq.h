@@ -49,6 +49,7 @@ extern "C" {
 #define DQ_STATUS_RANGE 1u    /* encode: non-finite input, or scale/offset/mean overflowed fp16 */
 #define DQ_STATUS_OVERFLOW 2u /* encode: a stream could not be fitted into its record          */
 #define DQ_STATUS_CORRUPT 4u  /* decode: a record did not end in state 2^21 inside its C bytes  */
+#define DQ_STATUS_WINDOW 8u   /* residual window: append to a full ring, or commit more than it holds */
 
 /* Fixed parameters of the format. */
 #define DQ_MEAN_WINDOW 128 /* tokens per key-mean window (windows start at token 0) */
@@ -181,6 +182,54 @@ int dq_decode_attention_partial(const dq_tables* k_tables, const dq_tables* v_ta
 int dq_decode_attention_merge(int32_t batch, int32_t q_heads, int32_t kv_heads,
                               const int32_t* seq_lens, int32_t t_cap, const void* workspace,
                               size_t workspace_bytes, float* out, void* stream);
+
+/*
+ * Residual window (Sec. 5.1 keeps the most recent tokens in BF16).  The raw
+ * keys and values of a sequence's newest tokens live in a ring:
+ *   res_k, res_v: bf16 [batch][kv_heads][r_cap][head_dim], 16-byte aligned,
+ *            r_cap <= 256; residual token i of sequence b sits in slot
+ *            (seq_lens[b] + i) mod r_cap, in the original basis (no
+ *            rotation, no mean removal).
+ *   seq_lens: device int32 [batch], the compressed tokens of each sequence;
+ *   res_lens: device int32 [batch], its residual tokens (<= r_cap).
+ * With r_cap a multiple of 128 and seq_lens[b] a multiple of 128, the oldest
+ * 128 residual tokens are the contiguous slots [seq_lens[b] mod r_cap, + 128):
+ * encode them with dq_encode_kv at t0 = seq_lens[b] (element strides
+ * r_cap * head_dim between heads and head_dim between tokens), then call
+ * dq_residual_commit(..., 128).
+ *
+ * dq_decode_attention_residual writes the residual window's softmax partial
+ * into the workspace: call it after dq_decode_attention_partial and before
+ * dq_decode_attention_merge, with the same sizes and workspace; the merge then
+ * attends over the compressed tokens and the residual tokens together
+ * (a sequence with neither gives 0).  head_dim is 128; q_heads / kv_heads <= 8.
+ * Returns DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_WORKSPACE or DQ_ERR_HIP.
+ */
+int dq_decode_attention_residual(const uint16_t* q, int32_t batch, int32_t q_heads,
+                                 int32_t kv_heads, const uint16_t* res_k,
+                                 const uint16_t* res_v, const int32_t* seq_lens,
+                                 const int32_t* res_lens, int32_t r_cap, int32_t t_cap,
+                                 float softmax_scale, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/*
+ * Appends one token per sequence to its ring: k_new, v_new bf16
+ * [batch][kv_heads][head_dim] go to slot (seq_lens[b] + res_lens[b]) mod
+ * r_cap, and res_lens[b] grows by one.  A full ring is left unchanged and
+ * sets DQ_STATUS_WINDOW.  Returns DQ_OK, DQ_ERR_INVALID_ARG or DQ_ERR_HIP.
+ */
+int dq_residual_append(const uint16_t* k_new, const uint16_t* v_new, int32_t batch,
+                       int32_t kv_heads, int32_t head_dim, uint16_t* res_k, uint16_t* res_v,
+                       const int32_t* seq_lens, int32_t* res_lens, int32_t r_cap,
+                       uint32_t* status, void* stream);
+
+/*
+ * The oldest n residual tokens of every sequence have been encoded:
+ * seq_lens[b] += n, res_lens[b] -= n.  A sequence holding fewer than n is
+ * left unchanged and sets DQ_STATUS_WINDOW.
+ */
+int dq_residual_commit(int32_t* seq_lens, int32_t* res_lens, int32_t batch, int32_t n,
+                       uint32_t* status, void* stream);
 
 /*
  * rANS-decodes records back to symbols (Alg. 2), for parity checks.

@@ -22,6 +22,7 @@ DQ_ERR_WORKSPACE = 4
 DQ_STATUS_RANGE = 1
 DQ_STATUS_OVERFLOW = 2
 DQ_STATUS_CORRUPT = 4
+DQ_STATUS_WINDOW = 8
 
 DQ_MEAN_WINDOW = 128
 LAMBDA_STEPS = 512
@@ -77,6 +78,13 @@ def _load():
     lib.dq_decode_attention_partial.restype = ctypes.c_int
     lib.dq_decode_attention_merge.argtypes = [I32, I32, I32, P, I32, P, SZ, P, P]
     lib.dq_decode_attention_merge.restype = ctypes.c_int
+    lib.dq_decode_attention_residual.argtypes = [P, I32, I32, I32, P, P, P, P, I32, I32, ctypes.c_float,
+                                                 P, SZ, P]
+    lib.dq_decode_attention_residual.restype = ctypes.c_int
+    lib.dq_residual_append.argtypes = [P, P, I32, I32, I32, P, P, P, P, I32, P, P]
+    lib.dq_residual_append.restype = ctypes.c_int
+    lib.dq_residual_commit.argtypes = [P, P, I32, I32, P, P]
+    lib.dq_residual_commit.restype = ctypes.c_int
     lib.dq_decode_symbols.argtypes = [P, P, I64, P, P, P, P]
     lib.dq_decode_symbols.restype = ctypes.c_int
     lib.dq_strerror.argtypes = [ctypes.c_int]
@@ -274,6 +282,53 @@ def dq_decode_attention_merge(batch: int, q_heads: int, kv_heads: int, seq_lens,
     rc = _lib.dq_decode_attention_merge(batch, q_heads, kv_heads, _ptr(seq_lens), t_cap, _ptr(workspace),
                                         ws_bytes, _ptr(out), _stream(stream))
     _check(rc, "dq_decode_attention_merge")
+
+
+def _ring_args(res_k, res_v, seq_lens, res_lens):
+    import torch
+    _need(res_k.is_cuda and res_k.dtype == torch.bfloat16 and res_k.is_contiguous() and res_k.dim() == 4,
+          "res_k must be bf16 [B, Hkv, r_cap, d]")
+    _need(res_v.is_cuda and res_v.dtype == torch.bfloat16 and res_v.is_contiguous()
+          and res_v.shape == res_k.shape, "res_v must match res_k")
+    B = res_k.shape[0]
+    for t, name in ((seq_lens, "seq_lens"), (res_lens, "res_lens")):
+        _need(t.is_cuda and t.dtype == torch.int32 and t.is_contiguous() and t.numel() == B, name)
+    return res_k.shape
+
+
+def dq_decode_attention_residual(q, res_k, res_v, seq_lens, res_lens, t_cap: int, workspace,
+                                 softmax_scale=None, stream=None):
+    """Residual window's partial: between dq_decode_attention_partial and _merge."""
+    import torch
+    B, Hkv, r_cap, d = _ring_args(res_k, res_v, seq_lens, res_lens)
+    _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3
+          and q.shape[0] == B and q.shape[2] == d, "q")
+    Hq = q.shape[1]
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    rc = _lib.dq_decode_attention_residual(_ptr(q), B, Hq, Hkv, _ptr(res_k), _ptr(res_v), _ptr(seq_lens),
+                                           _ptr(res_lens), r_cap, int(t_cap), ctypes.c_float(scale),
+                                           _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                           _stream(stream))
+    _check(rc, "dq_decode_attention_residual")
+
+
+def dq_residual_append(k_new, v_new, res_k, res_v, seq_lens, res_lens, status=None, stream=None):
+    """One token per sequence (bf16 [B, Hkv, d]) into the residual ring."""
+    import torch
+    B, Hkv, r_cap, d = _ring_args(res_k, res_v, seq_lens, res_lens)
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        _need(t.is_cuda and t.dtype == torch.bfloat16 and t.is_contiguous() and tuple(t.shape) == (B, Hkv, d),
+              name)
+    rc = _lib.dq_residual_append(_ptr(k_new), _ptr(v_new), B, Hkv, d, _ptr(res_k), _ptr(res_v), _ptr(seq_lens),
+                                 _ptr(res_lens), r_cap, _ptr(status), _stream(stream))
+    _check(rc, "dq_residual_append")
+
+
+def dq_residual_commit(seq_lens, res_lens, n: int, status=None, stream=None):
+    """The oldest n residual tokens were encoded: move them to the compressed side."""
+    rc = _lib.dq_residual_commit(_ptr(seq_lens), _ptr(res_lens), seq_lens.numel(), int(n), _ptr(status),
+                                 _stream(stream))
+    _check(rc, "dq_residual_commit")
 
 
 def dq_decode_attention(k_tables: Tables, v_tables: Tables, q, k_records, k_mean_q, k_mean_scale,

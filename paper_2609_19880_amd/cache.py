@@ -48,3 +48,86 @@ class KVCache:
         per_tok = self.k_tables.record_bytes + self.v_tables.record_bytes
         mean = (self.head_dim + 2) * ((tokens + _lib.DQ_MEAN_WINDOW - 1) // _lib.DQ_MEAN_WINDOW)
         return self.batch * self.kv_heads * (per_tok * tokens + mean)
+
+
+class StreamingKVCache:
+    """A compressed cache plus the BF16 residual window of the newest tokens.
+
+    Sec. 5.1 keeps the most recent tokens in BF16.  Here the newest tokens of
+    every sequence sit raw in a ring of 2 x 128 slots (the library's residual
+    window); when the ring is full its oldest 128 tokens are encoded as one
+    key-mean window and leave it, so at least the 128 most recent tokens are
+    always raw.  Decode attention runs over both parts in one step.  All
+    sequences of the batch advance together (same length).
+    """
+
+    WINDOW = _lib.DQ_MEAN_WINDOW
+
+    def __init__(self, batch: int, kv_heads: int, q_heads: int, t_cap: int, k_tables, v_tables,
+                 device="cuda", r_cap: int = 256):
+        if r_cap % self.WINDOW or not (2 * self.WINDOW <= r_cap <= 256):
+            raise ValueError("r_cap must be 256 (two mean windows)")
+        self.cache = KVCache(batch, kv_heads, q_heads, t_cap, k_tables, v_tables, device=device)
+        d = k_tables.head_dim
+        self.r_cap = r_cap
+        self.res_k = torch.zeros((batch, kv_heads, r_cap, d), dtype=torch.bfloat16, device=device)
+        self.res_v = torch.zeros_like(self.res_k)
+        self.seq_lens = torch.zeros(batch, dtype=torch.int32, device=device)   # compressed tokens
+        self.res_lens = torch.zeros(batch, dtype=torch.int32, device=device)   # residual tokens
+        self.n_comp = 0
+        self.n_res = 0
+
+    @property
+    def status(self):
+        return self.cache.status
+
+    def __len__(self) -> int:
+        return self.n_comp + self.n_res
+
+    def prefill(self, k, v):
+        """k, v bf16 [B, T, H, d] into an empty cache: whole windows are encoded,
+        the last 128..255 tokens (all of them if T < 128) stay raw."""
+        if len(self):
+            raise RuntimeError("prefill needs an empty cache")
+        T = k.shape[1]
+        n_enc = max(0, (T - self.WINDOW) // self.WINDOW * self.WINDOW)
+        if n_enc:
+            self.cache.append(k[:, :n_enc], v[:, :n_enc], 0)
+            self.seq_lens += n_enc
+            self.n_comp = n_enc
+        for t in range(n_enc, T):
+            self.append(k[:, t].contiguous(), v[:, t].contiguous())
+
+    def append(self, k1, v1):
+        """One decode token per sequence: k1, v1 bf16 [B, H, d]."""
+        if self.n_res == self.r_cap:
+            self._flush()
+        _lib.dq_residual_append(k1, v1, self.res_k, self.res_v, self.seq_lens, self.res_lens, self.status)
+        self.n_res += 1
+        if self.n_res == self.r_cap:
+            self._flush()
+
+    def _flush(self):
+        W = self.WINDOW
+        if self.n_comp + W > self.cache.t_cap:
+            raise RuntimeError("compressed cache is full")
+        s = self.n_comp % self.r_cap
+        k = self.res_k[:, :, s:s + W].permute(0, 2, 1, 3)     # [B, W, H, d] view of the ring
+        v = self.res_v[:, :, s:s + W].permute(0, 2, 1, 3)
+        self.cache.append(k, v, self.n_comp)
+        _lib.dq_residual_commit(self.seq_lens, self.res_lens, W, self.status)
+        self.n_comp += W
+        self.n_res -= W
+
+    def attend(self, q, out=None, softmax_scale=None):
+        """q bf16 [B, Hq, d] -> out fp32 [B, Hq, d] over every token so far."""
+        c = self.cache
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        _lib.dq_decode_attention_partial(c.k_tables, c.v_tables, q, c.k_records, c.k_mean_q, c.k_mean_scale,
+                                         c.v_records, self.seq_lens, c.workspace, softmax_scale=softmax_scale,
+                                         status=c.status)
+        _lib.dq_decode_attention_residual(q, self.res_k, self.res_v, self.seq_lens, self.res_lens, c.t_cap,
+                                          c.workspace, softmax_scale=softmax_scale)
+        _lib.dq_decode_attention_merge(c.batch, c.q_heads, c.kv_heads, self.seq_lens, c.t_cap, c.workspace, out)
+        return out

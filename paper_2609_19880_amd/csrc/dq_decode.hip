@@ -124,10 +124,10 @@ struct AttnArgs {
     const uint8_t* vrec;
     const int32_t* seq_lens;
     float scale_log2;            // softmax_scale * log2(e) / d
-    int32_t* ws_hdr;             // [0] chunk, [1] chunk count
-    float* ws_m;                 // [B][Hq][NC]
-    float* ws_l;                 // [B][Hq][NC]
-    float* ws_acc;               // [B][Hq][NC][d]
+    int32_t* ws_hdr;             // [0] chunk, [1] chunk count NC, [2] residual slot written
+    float* ws_m;                 // [B][Hq][NC + 1]   (slot NC: the residual window)
+    float* ws_l;                 // [B][Hq][NC + 1]
+    float* ws_acc;               // [B][Hq][NC + 1][d]
     uint32_t* status;
     int shared_lut;
     AttnLayout L;
@@ -248,6 +248,7 @@ __global__ __launch_bounds__(max_waves(HG, RW) * kWave) void attn_partial_kernel
     if ((c | h | b) == 0 && tid == 0) {
         a.ws_hdr[0] = a.chunk;
         a.ws_hdr[1] = a.nchunks;
+        a.ws_hdr[2] = 0;          // set by the residual kernel when it runs
     }
     const int T = min(a.seq_lens[b], a.t_cap);
     const int start = c * a.chunk;
@@ -548,7 +549,7 @@ __global__ __launch_bounds__(max_waves(HG, RW) * kWave) void attn_partial_kernel
             acc += aw[(w * GP + g) * kD + j] * e;
             l += lw[w * GP + g] * e;
         }
-        const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * NC + c;
+        const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * (NC + 1) + c;
         a.ws_acc[slot * kD + j] = acc;
         if (j == 0) {
             a.ws_m[slot] = M;
@@ -565,22 +566,30 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
                                                         int Hq, int t_cap, float* __restrict__ out) {
     __shared__ float o[kD];
     const int hq = blockIdx.x, b = blockIdx.y, j = threadIdx.x;
-    const int chunk = ws_hdr[0], NC = ws_hdr[1];
-    const int T = min(seq_lens[b], t_cap);
+    const int chunk = ws_hdr[0], NC = ws_hdr[1], residual = ws_hdr[2];
+    const int T = max(0, min(seq_lens[b], t_cap));
     float* dst = out + ((int64_t)b * Hq + hq) * kD;
-    if (T <= 0) {
+    // the chunks that hold tokens, then the residual window's slot (an empty
+    // window wrote m = -inf)
+    const int nc = min(NC, (T + chunk - 1) / chunk);
+    const int64_t base = ((int64_t)b * Hq + hq) * (NC + 1);
+    float M = -INFINITY;
+    for (int c = 0; c < nc; ++c) M = fmaxf(M, ws_m[base + c]);
+    if (residual) M = fmaxf(M, ws_m[base + NC]);
+    if (M == -INFINITY) {      // no token at all
         dst[j] = 0.f;
         return;
     }
-    const int nc = min(NC, (T + chunk - 1) / chunk);
-    const int64_t base = ((int64_t)b * Hq + hq) * NC;
-    float M = -INFINITY;
-    for (int c = 0; c < nc; ++c) M = fmaxf(M, ws_m[base + c]);
     float acc = 0.f, l = 0.f;
     for (int c = 0; c < nc; ++c) {
         const float e = exp2f(ws_m[base + c] - M);
         acc += ws_acc[(base + c) * kD + j] * e;
         l += ws_l[base + c] * e;
+    }
+    if (residual) {
+        const float e = exp2f(ws_m[base + NC] - M);
+        acc += ws_acc[(base + NC) * kD + j] * e;
+        l += ws_l[base + NC] * e;
     }
     o[j] = acc / l;
     __syncthreads();
@@ -594,7 +603,169 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
     dst[j] = o[j] * (1.0f / kD);
 }
 
-// LDS layout for given coding sizes; picks the largest wavefront count that fits.
+// ------------------------------------------------------- residual window
+//
+// The most recent tokens of a sequence stay in bf16 (Sec. 5.1).  They live in
+// a ring of r_cap slots per (sequence, KV head): residual token i of sequence
+// b is slot (seq_lens[b] + i) mod r_cap, so the oldest tokens are contiguous
+// whenever the compressed length is a multiple of the window being flushed.
+
+constexpr int kResThreads = 256;
+constexpr int kMaxResidual = 256;
+constexpr int kMaxGroup = 8;
+
+struct ResArgs {
+    const uint16_t* q;
+    const uint16_t* rk;          // [B][Hkv][r_cap][d] bf16
+    const uint16_t* rv;
+    const int32_t* seq_lens;     // compressed tokens per sequence
+    const int32_t* res_lens;     // residual tokens per sequence
+    int r_cap, Hq, Hkv, G;
+    float scale_log2;            // softmax_scale * log2(e): logits of raw keys
+    int32_t* ws_hdr;
+    float* ws_m;
+    float* ws_l;
+    float* ws_acc;
+};
+
+// One workgroup per (KV head, sequence): logits of the G query heads against
+// the raw keys, softmax statistics, the weighted sum of the raw values, and
+// the rotation H of that sum so that the merge's inverse rotation H / d
+// returns it (H H = d I).  The result is one more split-K partial, in slot NC.
+__global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
+    __shared__ float qs[kMaxGroup][kD];
+    __shared__ float sc[kMaxGroup][kMaxResidual];
+    __shared__ float part[2][kMaxGroup][kD];
+    __shared__ float stat[2][kMaxGroup];
+    const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int lane = tid & (kWave - 1), wave = tid / kWave;
+    const int G = a.G, NC = a.ws_hdr[1];
+    if ((h | b) == 0 && tid == 0) a.ws_hdr[2] = 1;
+    const int r = max(0, min(a.res_lens[b], a.r_cap));
+    const int first = max(0, a.seq_lens[b]) % a.r_cap;
+    const int hq0 = h * G;
+    for (int i = tid; i < G * kD; i += kResThreads)
+        qs[i / kD][i % kD] = bf16_to_f32(a.q[((int64_t)b * a.Hq + hq0) * kD + i]);
+    __syncthreads();
+    const int64_t row0 = ((int64_t)b * a.Hkv + h) * a.r_cap;
+    if (tid < r) {
+        const int slot = (first + tid) % a.r_cap;
+        const uint4* kp = reinterpret_cast<const uint4*>(a.rk + (row0 + slot) * kD);
+        float dot[kMaxGroup];
+#pragma unroll
+        for (int g = 0; g < kMaxGroup; ++g) dot[g] = 0.f;
+        for (int c8 = 0; c8 < kD / 8; ++c8) {
+            const uint4 w = kp[c8];
+            const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float kv = __uint_as_float((e & 1) ? (ww[e >> 1] & 0xFFFF0000u) : (ww[e >> 1] << 16));
+#pragma unroll
+                for (int g = 0; g < kMaxGroup; ++g)
+                    if (g < G) dot[g] += qs[g][c8 * 8 + e] * kv;
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < kMaxGroup; ++g)
+            if (g < G) sc[g][tid] = dot[g] * a.scale_log2;
+    }
+    __syncthreads();
+    for (int g = wave; g < G; g += kResThreads / kWave) {
+        float mx = -INFINITY;
+        for (int t = lane; t < r; t += kWave) mx = fmaxf(mx, sc[g][t]);
+        mx = wave_max(mx);
+        float sum = 0.f;
+        for (int t = lane; t < r; t += kWave) {
+            const float p = exp2f(sc[g][t] - mx);
+            sc[g][t] = p;
+            sum += p;
+        }
+        sum = wave_sum_f32(sum);
+        if (lane == 0) {
+            stat[0][g] = mx;
+            stat[1][g] = sum;
+        }
+    }
+    __syncthreads();
+    {
+        const int j = tid % kD, half = tid / kD;
+        float acc[kMaxGroup];
+#pragma unroll
+        for (int g = 0; g < kMaxGroup; ++g) acc[g] = 0.f;
+        for (int t = half; t < r; t += 2) {
+            const int slot = (first + t) % a.r_cap;
+            const float v = bf16_to_f32(a.rv[(row0 + slot) * kD + j]);
+#pragma unroll
+            for (int g = 0; g < kMaxGroup; ++g)
+                if (g < G) acc[g] += sc[g][t] * v;
+        }
+#pragma unroll
+        for (int g = 0; g < kMaxGroup; ++g)
+            if (g < G) part[half][g][j] = acc[g];
+    }
+    __syncthreads();
+    for (int i = tid; i < G * kD; i += kResThreads) part[0][i / kD][i % kD] += part[1][i / kD][i % kD];
+    __syncthreads();
+    for (int hh = 1; hh < kD; hh <<= 1) {
+        for (int i = tid; i < G * (kD / 2); i += kResThreads) {
+            const int g = i / (kD / 2), x = i % (kD / 2);
+            const int lo = (x / hh) * 2 * hh + (x % hh);
+            const float x0 = part[0][g][lo], x1 = part[0][g][lo + hh];
+            part[0][g][lo] = x0 + x1;
+            part[0][g][lo + hh] = x0 - x1;
+        }
+        __syncthreads();
+    }
+    for (int i = tid; i < G * kD; i += kResThreads) {
+        const int g = i / kD, j = i % kD;
+        const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * (NC + 1) + NC;
+        a.ws_acc[slot * kD + j] = part[0][g][j];
+        if (j == 0) {
+            a.ws_m[slot] = stat[0][g];
+            a.ws_l[slot] = stat[1][g];
+        }
+    }
+}
+
+// One new token per sequence into its ring slot; block per sequence.
+__global__ __launch_bounds__(kResThreads) void residual_append_kernel(const uint16_t* __restrict__ k_new,
+                                                                      const uint16_t* __restrict__ v_new,
+                                                                      int Hkv, uint16_t* __restrict__ rk,
+                                                                      uint16_t* __restrict__ rv,
+                                                                      const int32_t* __restrict__ seq_lens,
+                                                                      int32_t* __restrict__ res_lens,
+                                                                      int r_cap, uint32_t* status) {
+    const int b = blockIdx.x, tid = threadIdx.x;
+    const int r = res_lens[b];
+    if (r < 0 || r >= r_cap) {
+        if (tid == 0 && status) atomicOr(status, DQ_STATUS_WINDOW);
+        return;
+    }
+    const int slot = (max(0, seq_lens[b]) + r) % r_cap;
+    for (int i = tid; i < Hkv * kD; i += kResThreads) {
+        const int h = i / kD, j = i % kD;
+        const int64_t dst = (((int64_t)b * Hkv + h) * r_cap + slot) * kD + j;
+        rk[dst] = k_new[(int64_t)b * Hkv * kD + i];
+        rv[dst] = v_new[(int64_t)b * Hkv * kD + i];
+    }
+    __syncthreads();
+    if (tid == 0) res_lens[b] = r + 1;
+}
+
+// After the oldest n residual tokens were encoded: they become compressed.
+__global__ void residual_commit_kernel(int32_t* __restrict__ seq_lens, int32_t* __restrict__ res_lens,
+                                       int B, int n, uint32_t* status) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= B) return;
+    const int r = res_lens[b];
+    if (r < n) {
+        if (status) atomicOr(status, DQ_STATUS_WINDOW);
+        return;
+    }
+    seq_lens[b] += n;
+    res_lens[b] = r - n;
+}
+
 // Record length in dwords of the instantiation that serves (Ck, Cv); 0 = the
 // general kernel.
 int compiled_rw(int Ck, int Cv) {
@@ -605,6 +776,7 @@ int compiled_rw(int Ck, int Cv) {
     }
 }
 
+// LDS layout for given coding sizes; picks the largest wavefront count that fits.
 AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut, int rw) {
     const int GP = G <= 4 ? 4 : 8, HG = GP / 4;
     AttnLayout L;
@@ -668,7 +840,7 @@ ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap, int num_cus) {
     chunk = std::min(chunk, kMaxChunk);
     p.chunk = chunk;
     p.nchunks = (t_cap + chunk - 1) / chunk;
-    p.slots_max = (int64_t)B * Hq * max_chunks(t_cap);
+    p.slots_max = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
     return p;
 }
 
@@ -700,7 +872,7 @@ int launch_decode_symbols(const dq_tables* tab, const uint8_t* records, int64_t 
 
 size_t attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d) {
     (void)Hkv;
-    const int64_t slots = (int64_t)B * Hq * max_chunks(t_cap);
+    const int64_t slots = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
     return (size_t)kWsHeader + (size_t)(slots * d + 2 * slots) * sizeof(float);
 }
 
@@ -778,13 +950,51 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uin
 int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
                            int32_t t_cap, const void* ws, float* out, hipStream_t stream) {
     (void)Hkv;
-    const int64_t slots = (int64_t)B * Hq * max_chunks(t_cap);
+    const int64_t slots = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
     const int32_t* hdr = static_cast<const int32_t*>(ws);
     const float* acc = reinterpret_cast<const float*>(static_cast<const uint8_t*>(ws) + kWsHeader);
     const float* m = acc + slots * kD;
     const float* l = m + slots;
     attn_merge_kernel<<<dim3(Hq, B), kD, 0, stream>>>(hdr, m, l, acc, seq_lens, Hq, t_cap, out);
     return hip_check("attn_merge launch", hipGetLastError());
+}
+
+int launch_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                              const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
+                              const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
+                              void* ws, hipStream_t stream) {
+    const int64_t slots = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
+    ResArgs a;
+    a.q = q;
+    a.rk = res_k;
+    a.rv = res_v;
+    a.seq_lens = seq_lens;
+    a.res_lens = res_lens;
+    a.r_cap = r_cap;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.G = Hq / Hkv;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.ws_hdr = static_cast<int32_t*>(ws);
+    a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
+    a.ws_m = a.ws_acc + slots * kD;
+    a.ws_l = a.ws_m + slots;
+    attn_residual_kernel<<<dim3(Hkv, B), kResThreads, 0, stream>>>(a);
+    return hip_check("attn_residual launch", hipGetLastError());
+}
+
+int launch_residual_append(const uint16_t* k_new, const uint16_t* v_new, int32_t B, int32_t Hkv,
+                           uint16_t* res_k, uint16_t* res_v, const int32_t* seq_lens, int32_t* res_lens,
+                           int32_t r_cap, uint32_t* status, hipStream_t stream) {
+    residual_append_kernel<<<B, kResThreads, 0, stream>>>(k_new, v_new, Hkv, res_k, res_v, seq_lens, res_lens,
+                                                          r_cap, status);
+    return hip_check("residual_append launch", hipGetLastError());
+}
+
+int launch_residual_commit(int32_t* seq_lens, int32_t* res_lens, int32_t B, int32_t n, uint32_t* status,
+                           hipStream_t stream) {
+    residual_commit_kernel<<<(B + 255) / 256, 256, 0, stream>>>(seq_lens, res_lens, B, n, status);
+    return hip_check("residual_commit launch", hipGetLastError());
 }
 
 }  // namespace dq

@@ -367,6 +367,36 @@ int dq_decode_attention(const dq_tables* tk, const dq_tables* tv, const uint16_t
     return dq_decode_attention_merge(B, Hq, Hkv, seq_lens, t_cap, ws, ws_bytes, out, stream);
 }
 
+int dq_decode_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                                 const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
+                                 const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
+                                 void* ws, size_t ws_bytes, void* stream) {
+    if (B <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 8 || B > 65535 || Hkv > 65535)
+        return DQ_ERR_INVALID_ARG;
+    if (t_cap <= 0 || t_cap % DQ_MEAN_WINDOW || r_cap <= 0 || r_cap > 256) return DQ_ERR_INVALID_ARG;
+    if (!q || !res_k || !res_v || !seq_lens || !res_lens || !std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(res_k) | reinterpret_cast<uintptr_t>(res_v)) & 15) return DQ_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128)) return DQ_ERR_WORKSPACE;
+    return dq::launch_attention_residual(q, B, Hq, Hkv, res_k, res_v, seq_lens, res_lens, r_cap, t_cap, scale,
+                                         ws, static_cast<hipStream_t>(stream));
+}
+
+int dq_residual_append(const uint16_t* k_new, const uint16_t* v_new, int32_t B, int32_t Hkv, int32_t d,
+                       uint16_t* res_k, uint16_t* res_v, const int32_t* seq_lens, int32_t* res_lens,
+                       int32_t r_cap, uint32_t* status, void* stream) {
+    if (B <= 0 || Hkv <= 0 || d != 128 || r_cap <= 0 || B > 0x7FFFFFFF / 2) return DQ_ERR_INVALID_ARG;
+    if (!k_new || !v_new || !res_k || !res_v || !seq_lens || !res_lens) return DQ_ERR_INVALID_ARG;
+    return dq::launch_residual_append(k_new, v_new, B, Hkv, res_k, res_v, seq_lens, res_lens, r_cap, status,
+                                      static_cast<hipStream_t>(stream));
+}
+
+int dq_residual_commit(int32_t* seq_lens, int32_t* res_lens, int32_t B, int32_t n, uint32_t* status,
+                       void* stream) {
+    if (B <= 0 || n < 0 || !seq_lens || !res_lens) return DQ_ERR_INVALID_ARG;
+    if (n == 0) return DQ_OK;
+    return dq::launch_residual_commit(seq_lens, res_lens, B, n, status, static_cast<hipStream_t>(stream));
+}
+
 int dq_decode_symbols(const dq_tables* t, const uint8_t* records, int64_t n_streams, uint8_t* sym,
                       uint16_t* header, uint32_t* status, void* stream) {
     if (!table_args_ok(t) || n_streams < 0 || (n_streams > 0 && (!records || !sym)))
