@@ -48,6 +48,8 @@ def _args():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0)
+    ap.add_argument("--residual", type=int, default=0,
+                    help="also attend over this many raw BF16 tokens per sequence (residual window, <= 255)")
     return ap.parse_args()
 
 
@@ -175,11 +177,14 @@ def step_inputs(wl, seed: int, dev):
     return q, seq, out
 
 
-def decode_step(tk, tv, cache, q, seq, out):
-    """One step: split-K partials over the whole cache, then the merge."""
+def decode_step(tk, tv, cache, q, seq, out, ring=None):
+    """One step: split-K partials over the whole cache (and the residual
+    window's partial, if a ring is given), then the merge."""
     import paper_2609_19880_amd as dq
     dq.dq_decode_attention_partial(tk, tv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
                                    cache.v_records, seq, cache.workspace, status=cache.status)
+    if ring is not None:
+        dq.dq_decode_attention_residual(q, ring[0], ring[1], seq, ring[2], cache.t_cap, cache.workspace)
     dq.dq_decode_attention_merge(cache.batch, cache.q_heads, cache.kv_heads, seq, cache.t_cap,
                                  cache.workspace, out)
 
@@ -210,28 +215,45 @@ def main():
     torch.cuda.empty_cache()
     q, seq, out = step_inputs(wl, a.seed, dev)
 
+    ring = None
+    if a.residual:
+        if not 0 < a.residual < 256:
+            raise SystemExit("--residual must be in 1..255")
+        # the newest tokens of every sequence, raw, in the ring slots that follow
+        # the compressed ones
+        g = torch.Generator(device=dev)
+        g.manual_seed(a.seed * 7 + 5)
+        rk = torch.randn((B, Hkv, 256, d), generator=g, device=dev).to(torch.bfloat16)
+        rv = torch.randn((B, Hkv, 256, d), generator=g, device=dev).to(torch.bfloat16)
+        rl = torch.full((B,), a.residual, dtype=torch.int32, device=dev)
+        ring = (rk, rv, rl)
+
     def step():
-        decode_step(tk, tv, cache, q, seq, out)
+        decode_step(tk, tv, cache, q, seq, out, ring)
 
     for _ in range(a.warmup):
         step()
     torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 * a.steps)]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4 * a.steps)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     for i in range(a.steps):
-        ev[3 * i].record()
+        ev[4 * i].record()
         dq.dq_decode_attention_partial(tk, tv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
                                        cache.v_records, seq, cache.workspace, status=cache.status)
-        ev[3 * i + 1].record()
+        ev[4 * i + 1].record()
+        if ring is not None:
+            dq.dq_decode_attention_residual(q, ring[0], ring[1], seq, ring[2], T, cache.workspace)
+        ev[4 * i + 2].record()
         dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, cache.workspace, out)
-        ev[3 * i + 2].record()
+        ev[4 * i + 3].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     if int(cache.status.item()):
         raise RuntimeError(f"decode status {int(cache.status.item())}")
-    partial_ms = sum(ev[3 * i].elapsed_time(ev[3 * i + 1]) for i in range(a.steps)) / a.steps
-    merge_ms = sum(ev[3 * i + 1].elapsed_time(ev[3 * i + 2]) for i in range(a.steps)) / a.steps
+    partial_ms = sum(ev[4 * i].elapsed_time(ev[4 * i + 1]) for i in range(a.steps)) / a.steps
+    residual_ms = sum(ev[4 * i + 1].elapsed_time(ev[4 * i + 2]) for i in range(a.steps)) / a.steps
+    merge_ms = sum(ev[4 * i + 2].elapsed_time(ev[4 * i + 3]) for i in range(a.steps)) / a.steps
     step_ms = ev[0].elapsed_time(ev[-1]) / a.steps
 
     # algorithmic bytes of one partial launch: per (token, KV head) the two
@@ -240,7 +262,7 @@ def main():
     units = B * T * Hkv
     alg_bytes = per_unit * units
     achieved = alg_bytes / (partial_ms * 1e-3) / 1e9
-    tokens_s = B * T / (step_ms * 1e-3)
+    tokens_s = B * (T + a.residual) / (step_ms * 1e-3)
     counters = counter_figures(wl.name, a.variant)
     traffic = counters[0] if counters else None
 
@@ -263,7 +285,7 @@ def main():
                                f"{wl.k.levels}/{wl.v.levels} levels, alpha {wl.k.alpha}/{wl.v.alpha}, p 12",
                    "variant": a.variant, "batch": B, "context": T, "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": d, "k_record_bytes": wl.k.record_bytes, "v_record_bytes": wl.v.record_bytes,
-                   "k_levels": wl.k.levels, "v_levels": wl.v.levels},
+                   "k_levels": wl.k.levels, "v_levels": wl.v.levels, "residual_tokens": a.residual},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
@@ -276,6 +298,9 @@ def main():
             "valu_insts_per_launch": counters[1],
             "valu_lane_ops_per_symbol": counters[1] * 64 / (2 * units * d)},
         "merge_ms": merge_ms,
+        "residual": None if ring is None else {
+            "tokens_per_sequence": a.residual, "ms": residual_ms,
+            "gbs": B * Hkv * a.residual * d * 2 * 2 / (residual_ms * 1e-3) / 1e9},
         "wall_ms_per_step": wall * 1e3 / a.steps,
         "symbols_per_s": 2 * units * d / (step_ms * 1e-3),
         "encode": {"ms": enc_ms, "tokens_per_s": B * T / (enc_ms * 1e-3),

@@ -32,7 +32,7 @@ constexpr int kMaxRecDwords = 16;
 constexpr int kMaxLds = 160 * 1024;
 constexpr int kMinChunk = 512;
 constexpr int kMaxChunk = 16384;  // bounds the per-window q . mu table in LDS
-constexpr int kWsHeader = 256;   // workspace header: chunk size, chunk count
+constexpr int kWsHeader = 256;   // workspace header: chunk size, chunk count, residual flag
 
 // ---------------------------------------------------------------- symbols
 
@@ -565,6 +565,7 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
                                                         const int32_t* __restrict__ seq_lens,
                                                         int Hq, int t_cap, float* __restrict__ out) {
     __shared__ float o[kD];
+    __shared__ float red[kD];
     const int hq = blockIdx.x, b = blockIdx.y, j = threadIdx.x;
     const int chunk = ws_hdr[0], NC = ws_hdr[1], residual = ws_hdr[2];
     const int T = max(0, min(seq_lens[b], t_cap));
@@ -573,23 +574,40 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
     // window wrote m = -inf)
     const int nc = min(NC, (T + chunk - 1) / chunk);
     const int64_t base = ((int64_t)b * Hq + hq) * (NC + 1);
+    // partials in use: chunks 0..nc-1, then the residual slot NC
+    const int np = nc + (residual ? 1 : 0);
     float M = -INFINITY;
-    for (int c = 0; c < nc; ++c) M = fmaxf(M, ws_m[base + c]);
-    if (residual) M = fmaxf(M, ws_m[base + NC]);
+    for (int i = j; i < np; i += kD) M = fmaxf(M, ws_m[base + (i < nc ? i : NC)]);
+    red[j] = M;
+    __syncthreads();
+    for (int s2 = kD / 2; s2 > 0; s2 >>= 1) {
+        if (j < s2) red[j] = fmaxf(red[j], red[j + s2]);
+        __syncthreads();
+    }
+    M = red[0];
     if (M == -INFINITY) {      // no token at all
         dst[j] = 0.f;
         return;
     }
     float acc = 0.f, l = 0.f;
-    for (int c = 0; c < nc; ++c) {
-        const float e = exp2f(ws_m[base + c] - M);
-        acc += ws_acc[(base + c) * kD + j] * e;
-        l += ws_l[base + c] * e;
-    }
-    if (residual) {
-        const float e = exp2f(ws_m[base + NC] - M);
-        acc += ws_acc[(base + NC) * kD + j] * e;
-        l += ws_l[base + NC] * e;
+    // batches of 8 partials, loads unconditional on a clamped index so that
+    // they are in flight together; partials past np get weight 0
+    for (int i0 = 0; i0 < np; i0 += 8) {
+        float av[8], mv[8], lv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = min(i0 + u, np - 1);
+            const int c = i < nc ? i : NC;          // same for every thread of the block
+            av[u] = ws_acc[(base + c) * kD + j];
+            mv[u] = ws_m[base + c];
+            lv[u] = ws_l[base + c];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const float e = i0 + u < np ? exp2f(mv[u] - M) : 0.f;
+            acc += av[u] * e;
+            l += lv[u] * e;
+        }
     }
     o[j] = acc / l;
     __syncthreads();
@@ -633,9 +651,10 @@ struct ResArgs {
 // the rotation H of that sum so that the merge's inverse rotation H / d
 // returns it (H H = d I).  The result is one more split-K partial, in slot NC.
 __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
-    __shared__ float qs[kMaxGroup][kD];
+    __shared__ __align__(16) float qs[kMaxGroup][kD];
     __shared__ float sc[kMaxGroup][kMaxResidual];
-    __shared__ float part[2][kMaxGroup][kD];
+    __shared__ float part[1][kMaxGroup][kD];
+    __shared__ float pq[4][kMaxGroup][kD];
     __shared__ float stat[2][kMaxGroup];
     const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const int lane = tid & (kWave - 1), wave = tid / kWave;
@@ -649,20 +668,28 @@ __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
     __syncthreads();
     const int64_t row0 = ((int64_t)b * a.Hkv + h) * a.r_cap;
     if (tid < r) {
-        const int slot = (first + tid) % a.r_cap;
+        const int slot = first + tid < a.r_cap ? first + tid : first + tid - a.r_cap;
         const uint4* kp = reinterpret_cast<const uint4*>(a.rk + (row0 + slot) * kD);
+        // the whole 256-byte key row in flight at once
+        uint4 row[kD / 8];
+#pragma unroll
+        for (int c8 = 0; c8 < kD / 8; ++c8) row[c8] = kp[c8];
         float dot[kMaxGroup];
 #pragma unroll
         for (int g = 0; g < kMaxGroup; ++g) dot[g] = 0.f;
+#pragma unroll
         for (int c8 = 0; c8 < kD / 8; ++c8) {
-            const uint4 w = kp[c8];
-            const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+            const uint32_t ww[4] = {row[c8].x, row[c8].y, row[c8].z, row[c8].w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float kv = __uint_as_float((e & 1) ? (ww[e >> 1] & 0xFFFF0000u) : (ww[e >> 1] << 16));
+            for (int g = 0; g < kMaxGroup; ++g) {
+                if (g < G) {
+                    const float4 qa = *reinterpret_cast<const float4*>(&qs[g][c8 * 8]);
+                    const float4 qb = *reinterpret_cast<const float4*>(&qs[g][c8 * 8 + 4]);
+                    const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
 #pragma unroll
-                for (int g = 0; g < kMaxGroup; ++g)
-                    if (g < G) dot[g] += qs[g][c8 * 8 + e] * kv;
+                    for (int e = 0; e < 8; ++e)
+                        dot[g] += qv[e] * __uint_as_float((e & 1) ? (ww[e >> 1] & 0xFFFF0000u) : (ww[e >> 1] << 16));
+                }
             }
         }
 #pragma unroll
@@ -688,23 +715,49 @@ __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
     }
     __syncthreads();
     {
-        const int j = tid % kD, half = tid / kD;
-        float acc[kMaxGroup];
+        // thread (channel pair jp, quarter): channels 2 jp, 2 jp + 1 of tokens
+        // quarter, quarter + 4, ...; all of its value loads are issued before
+        // any is used (loads on a clamped token; tokens past r are skipped)
+        const int jp = tid % (kD / 2), quarter = tid / (kD / 2);
+        constexpr int kPer = kMaxResidual / 4;
+        uint32_t vw[kPer];
 #pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g) acc[g] = 0.f;
-        for (int t = half; t < r; t += 2) {
-            const int slot = (first + t) % a.r_cap;
-            const float v = bf16_to_f32(a.rv[(row0 + slot) * kD + j]);
+        for (int u = 0; u < kPer; ++u) {
+            const int tc = min(quarter + 4 * u, max(r - 1, 0));
+            const int slot = first + tc < a.r_cap ? first + tc : first + tc - a.r_cap;
+            // every slot of the ring is allocated, so the clamped load is in bounds even for r = 0
+            vw[u] = *reinterpret_cast<const uint32_t*>(a.rv + (row0 + slot) * kD + 2 * jp);
+        }
+        float acc0[kMaxGroup], acc1[kMaxGroup];
 #pragma unroll
-            for (int g = 0; g < kMaxGroup; ++g)
-                if (g < G) acc[g] += sc[g][t] * v;
+        for (int g = 0; g < kMaxGroup; ++g) acc0[g] = acc1[g] = 0.f;
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int t = quarter + 4 * u;
+            if (t < r) {
+                const float v0 = __uint_as_float(vw[u] << 16), v1 = __uint_as_float(vw[u] & 0xFFFF0000u);
+#pragma unroll
+                for (int g = 0; g < kMaxGroup; ++g) {
+                    if (g < G) {
+                        acc0[g] += sc[g][t] * v0;
+                        acc1[g] += sc[g][t] * v1;
+                    }
+                }
+            }
         }
 #pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g)
-            if (g < G) part[half][g][j] = acc[g];
+        for (int g = 0; g < kMaxGroup; ++g) {
+            if (g < G) {
+                pq[quarter][g][2 * jp] = acc0[g];
+                pq[quarter][g][2 * jp + 1] = acc1[g];
+            }
+        }
     }
     __syncthreads();
-    for (int i = tid; i < G * kD; i += kResThreads) part[0][i / kD][i % kD] += part[1][i / kD][i % kD];
+    for (int i = tid; i < G * kD; i += kResThreads) {
+        const int g = i / kD, j = i % kD;
+        part[0][g][j] = pq[0][g][j] + pq[1][g][j] + pq[2][g][j] + pq[3][g][j];
+    }
     __syncthreads();
     for (int hh = 1; hh < kD; hh <<= 1) {
         for (int i = tid; i < G * (kD / 2); i += kResThreads) {
