@@ -224,20 +224,26 @@ __device__ __forceinline__ void build_pairs(const uint32_t (&r)[kMaxRecDwords], 
     }
 }
 
-// Wavefronts per workgroup.  Up to 4 query heads per KV head: 16 (4 per SIMD,
-// at most 128 VGPRs) for records of up to 36 bytes, 12 for longer or
-// run-time-length records, whose prefetched record words need more
-// registers.  Up to 8 query heads: 8, for the larger accumulators.
-__host__ __device__ constexpr int max_waves(int HG, int RW) {
-    return HG == 1 ? ((RW == 8 || RW == 9) ? kMaxWaves : 12) : 8;
+// Wavefronts per workgroup (LDS permitting).  Up to 4 query heads per KV
+// head: 16 (4 per SIMD, at most 128 VGPRs) for records of up to 36 bytes, 12
+// for longer or run-time-length records, whose prefetched record words need
+// more registers.  Up to 8 query heads: 12 (at most 168 VGPRs), without the
+// record prefetch, whose registers the larger accumulators need; 8 for
+// run-time record lengths.
+// RWP packs the compile-time record lengths in dwords, keys << 8 | values
+// (0: run-time lengths).
+__host__ __device__ constexpr int rw_pair(int rwk, int rwv) { return (rwk << 8) | rwv; }
+__host__ __device__ constexpr int max_waves(int HG, int RWP) {
+    return HG == 1 ? ((RWP == rw_pair(8, 8) || RWP == rw_pair(9, 9)) ? kMaxWaves : 12) : (RWP ? 12 : 8);
 }
 
 constexpr uint32_t kLutVOffset = 8u << 12;   // value table when it differs from the key table
 
-// RW: record length in dwords when keys and values share it (compile-time
-// record loads), 0 for the general case.
-template <int HG, uint32_t LUTV, int RW>
-__global__ __launch_bounds__(max_waves(HG, RW) * kWave) void attn_partial_kernel(AttnArgs a) {
+// RWP: compile-time key and value record lengths (rw_pair), 0 for run-time
+// lengths.
+template <int HG, uint32_t LUTV, int RWP>
+__global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kernel(AttnArgs a) {
+    constexpr int RWK = RWP >> 8, RWV = RWP & 0xFF;
     constexpr int GP = 4 * HG;
     extern __shared__ __align__(16) uint8_t smem[];
     const AttnLayout& L = a.L;
@@ -336,7 +342,7 @@ __global__ __launch_bounds__(max_waves(HG, RW) * kWave) void attn_partial_kernel
     uint8_t* plimb = wreg + L.plimb;
     const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
     const uint32_t sel2 = (lane & 2) ? 0x03020706u : 0x05040100u;
-    const int Ck = RW ? 4 * RW : a.tk.C, Cv = RW ? 4 * RW : a.tv.C, CWk = Ck / 4, CWv = Cv / 4;
+    const int Ck = RWK ? 4 * RWK : a.tk.C, Cv = RWV ? 4 * RWV : a.tv.C, CWk = Ck / 4, CWv = Cv / 4;
     const int pk3 = a.tk.p + 3, pv3 = a.tv.p + 3;
     const uint32_t mask8k = ((1u << a.tk.p) - 1u) << 3, mask8v = ((1u << a.tv.p) - 1u) << 3;
     const int64_t bh = (int64_t)b * a.Hkv + h;
@@ -354,8 +360,10 @@ __global__ __launch_bounds__(max_waves(HG, RW) * kWave) void attn_partial_kernel
     const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
 
     // records of the wavefront's next tile are loaded while it decodes this one
+    // (up to 4 query heads per KV head; with 8 the registers go to accumulators)
+    constexpr bool kPrefetch = HG == 1;
     uint32_t rk[kMaxRecDwords], rv[kMaxRecDwords];
-    if (wave < ntiles) {
+    if (kPrefetch && wave < ntiles) {
         const int64_t tok = bh * a.t_cap + start + wave * kTile + lane;
         load_record(rk, a.krec, tok, CWk);
         load_record(rv, a.vrec, tok, CWv);
@@ -364,13 +372,18 @@ __global__ __launch_bounds__(max_waves(HG, RW) * kWave) void attn_partial_kernel
         const int t_base = start + tile * kTile;
         const int t = t_base + lane;
         const bool valid = t < T;
+        if (!kPrefetch) {
+            const int64_t tok = bh * a.t_cap + t_base + lane;
+            load_record(rk, a.krec, tok, CWk);
+            load_record(rv, a.vrec, tok, CWv);
+        }
 
         // ---- both records of the lane's token -> headers + byte-pair arrays
         const uint32_t hk0 = rk[0], xk0 = rk[1] << 3;
         const uint32_t hv0 = rv[0], xv0 = rv[1] << 3;
         build_pairs(rk, CWk, smem + pk_lane);
         build_pairs(rv, CWv, smem + pv_lane);
-        if (tile + L.nw < ntiles) {
+        if (kPrefetch && tile + L.nw < ntiles) {
             const int64_t tok = bh * a.t_cap + t_base + L.nw * kTile + lane;
             load_record(rk, a.krec, tok, CWk);
             load_record(rv, a.vrec, tok, CWv);
@@ -822,10 +835,13 @@ __global__ void residual_commit_kernel(int32_t* __restrict__ seq_lens, int32_t* 
 // Record length in dwords of the instantiation that serves (Ck, Cv); 0 = the
 // general kernel.
 int compiled_rw(int Ck, int Cv) {
-    if (Ck != Cv) return 0;
-    switch (Ck / 4) {
-        case 8: case 9: case 12: case 16: return Ck / 4;
-        default: return 0;
+    const int p = (Ck % 4 || Cv % 4) ? 0 : rw_pair(Ck / 4, Cv / 4);
+    switch (p) {
+        case rw_pair(8, 8): case rw_pair(9, 9): case rw_pair(12, 12): case rw_pair(16, 16):
+        case rw_pair(12, 8):
+            return p;
+        default:
+            return 0;
     }
 }
 
@@ -862,6 +878,9 @@ AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut, 
     L.wave_stride = w;
     int nw = (kMaxLds - kPairSlack - off) / w;
     if (nw > max_waves(HG, rw)) nw = max_waves(HG, rw);
+    // whole wavefronts per SIMD: tiles go round-robin over the wavefronts, so
+    // an uneven split would leave two SIMDs with half again the work
+    if (nw > 4) nw &= ~3;
     // the query rotation scratch and the final merge must fit as well
     while (nw > 0 && (nw * w < G * kD * 4 ||
                       off + nw * w < nw * (2 * GP + GP * kD) * 4))
@@ -937,25 +956,27 @@ bool attention_supports(const dq_tables* tk, const dq_tables* tv) {
     return true;
 }
 
-template <int HG, uint32_t LUTV, int RW>
+template <int HG, uint32_t LUTV, int RWP>
 static int launch_rw(AttnArgs& a, dim3 grid, hipStream_t stream) {
     if (int rc = hip_check("hipFuncSetAttribute",
-                           hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_partial_kernel<HG, LUTV, RW>),
+                           hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_partial_kernel<HG, LUTV, RWP>),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
         return rc;
-    attn_partial_kernel<HG, LUTV, RW><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
+    attn_partial_kernel<HG, LUTV, RWP><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
     return hip_check("attn_partial launch", hipGetLastError());
 }
 
 // Record lengths of the 2.0 / 2.25 / 3.0 / 4.0 bits-per-element budgets at
-// head_dim 128 get their own instantiation; other lengths take the general one.
+// head_dim 128 (equal for keys and values, or 3.0 / 2.0) get their own
+// instantiation; other lengths take the general one.
 template <int HG, uint32_t LUTV>
 static int launch_hg(AttnArgs& a, dim3 grid, hipStream_t stream) {
     switch (compiled_rw(a.tk.C, a.tv.C)) {
-        case 8: return launch_rw<HG, LUTV, 8>(a, grid, stream);
-        case 9: return launch_rw<HG, LUTV, 9>(a, grid, stream);
-        case 12: return launch_rw<HG, LUTV, 12>(a, grid, stream);
-        case 16: return launch_rw<HG, LUTV, 16>(a, grid, stream);
+        case rw_pair(8, 8): return launch_rw<HG, LUTV, rw_pair(8, 8)>(a, grid, stream);
+        case rw_pair(9, 9): return launch_rw<HG, LUTV, rw_pair(9, 9)>(a, grid, stream);
+        case rw_pair(12, 12): return launch_rw<HG, LUTV, rw_pair(12, 12)>(a, grid, stream);
+        case rw_pair(16, 16): return launch_rw<HG, LUTV, rw_pair(16, 16)>(a, grid, stream);
+        case rw_pair(12, 8): return launch_rw<HG, LUTV, rw_pair(12, 8)>(a, grid, stream);
         default: return launch_rw<HG, LUTV, 0>(a, grid, stream);
     }
 }
