@@ -48,6 +48,8 @@ def _args():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0)
+    ap.add_argument("--compare-bf16", action="store_true",
+                    help="also time the BF16 comparator (uncompressed cache of the same shape)")
     ap.add_argument("--residual", type=int, default=0,
                     help="also attend over this many raw BF16 tokens per sequence (residual window, <= 255)")
     return ap.parse_args()
@@ -189,6 +191,39 @@ def decode_step(tk, tv, cache, q, seq, out, ring=None):
                                  cache.workspace, out)
 
 
+def bf16_comparator(wl, a, q, seq, out, ws):
+    """The same decode step over an uncompressed BF16 cache of the same shape
+    (random contents), timed like the compressed one."""
+    import torch
+    import paper_2609_19880_amd as dq
+    B, T, Hq, Hkv, d = wl.batch, wl.context, wl.q_heads, wl.kv_heads, wl.head_dim
+    g = torch.Generator(device="cuda")
+    g.manual_seed(a.seed * 7 + 11)
+    k = torch.randn((B, Hkv, T, d), generator=g, device="cuda").to(torch.bfloat16)
+    v = torch.randn((B, Hkv, T, d), generator=g, device="cuda").to(torch.bfloat16)
+    for _ in range(a.warmup):
+        dq.dq_bf16_decode_attention_partial(q, k, v, seq, ws)
+        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 * a.steps)]
+    for i in range(a.steps):
+        ev[3 * i].record()
+        dq.dq_bf16_decode_attention_partial(q, k, v, seq, ws)
+        ev[3 * i + 1].record()
+        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
+        ev[3 * i + 2].record()
+    torch.cuda.synchronize()
+    pms = sum(ev[3 * i].elapsed_time(ev[3 * i + 1]) for i in range(a.steps)) / a.steps
+    sms = ev[0].elapsed_time(ev[-1]) / a.steps
+    nbytes = 2 * B * Hkv * T * d * 2
+    del k, v
+    torch.cuda.empty_cache()
+    return {"ms_per_step": sms, "tokens_per_s": B * T / (sms * 1e-3), "partial_ms": pms,
+            "bytes_per_step": nbytes, "gbs": nbytes / (pms * 1e-3) / 1e9,
+            "hbm_frac": nbytes / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "kv_bytes_ratio": nbytes / (B * T * Hkv * (wl.k.record_bytes + wl.v.record_bytes + (d + 2) / 128))}
+
+
 def main():
     a = _args()
     if a.gpus != 1:
@@ -306,6 +341,8 @@ def main():
         "encode": {"ms": enc_ms, "tokens_per_s": B * T / (enc_ms * 1e-3),
                    "input_gbs": 2 * B * T * Hkv * d * 2 / (enc_ms * 1e-3) / 1e9},
     }
+    if a.compare_bf16:
+        rec["bf16_decode"] = bf16_comparator(wl, a, q, seq, out, cache.workspace)
     if not a.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, a.seed)
     print(json.dumps(rec))

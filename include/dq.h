@@ -232,6 +232,21 @@ int dq_residual_commit(int32_t* seq_lens, int32_t* res_lens, int32_t batch, int3
                        uint32_t* status, void* stream);
 
 /*
+ * Comparator: the same decode step over an uncompressed BF16 cache.
+ *   k, v: bf16 [batch][kv_heads][t_cap][head_dim], 16-byte aligned, original
+ *         basis; the first seq_lens[b] tokens of sequence b are attended.
+ * Writes split-K partials into the workspace (same size rule as above);
+ * finish with dq_decode_attention_merge, with the same sizes and workspace.
+ * head_dim is 128; t_cap a positive multiple of 128; q_heads / kv_heads <= 8.
+ * Returns DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_WORKSPACE or DQ_ERR_HIP.
+ */
+int dq_bf16_decode_attention_partial(const uint16_t* q, int32_t batch, int32_t q_heads,
+                                     int32_t kv_heads, const uint16_t* k, const uint16_t* v,
+                                     const int32_t* seq_lens, int32_t t_cap,
+                                     float softmax_scale, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
+/*
  * rANS-decodes records back to symbols (Alg. 2), for parity checks.
  *   records: u8 [n_streams][C]; sym: u8 [n_streams][head_dim];
  *   header:  u16 [n_streams][2] = (scale, offset) fp16 bits; may be NULL;

@@ -9,7 +9,8 @@ Entry points (same names as the C ABI in ``include/dq.h``):
     dq_compute_tables, dq_build_tables, dq_encode_kv,
     dq_decode_workspace_bytes, dq_decode_attention, dq_decode_attention_partial,
     dq_decode_attention_merge, dq_decode_attention_residual, dq_residual_append,
-    dq_residual_commit, dq_decode_symbols, dq_strerror, dq_last_error
+    dq_residual_commit, dq_bf16_decode_attention_partial, dq_decode_symbols,
+    dq_strerror, dq_last_error
 """
 
 from ._lib import (  # noqa: F401
@@ -19,6 +20,7 @@ from ._lib import (  # noqa: F401
     dq_compute_tables, dq_build_tables, dq_encode_kv, dq_decode_workspace_bytes,
     dq_decode_attention, dq_decode_attention_partial, dq_decode_attention_merge,
     dq_decode_attention_residual, dq_residual_append, dq_residual_commit,
+    dq_bf16_decode_attention_partial,
     dq_decode_symbols, dq_strerror, dq_last_error, smallest_feasible_alpha,
 )
 from .cache import KVCache, StreamingKVCache  # noqa: F401

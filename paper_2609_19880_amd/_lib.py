@@ -81,6 +81,8 @@ def _load():
     lib.dq_decode_attention_residual.argtypes = [P, I32, I32, I32, P, P, P, P, I32, I32, ctypes.c_float,
                                                  P, SZ, P]
     lib.dq_decode_attention_residual.restype = ctypes.c_int
+    lib.dq_bf16_decode_attention_partial.argtypes = [P, I32, I32, I32, P, P, P, I32, ctypes.c_float, P, SZ, P]
+    lib.dq_bf16_decode_attention_partial.restype = ctypes.c_int
     lib.dq_residual_append.argtypes = [P, P, I32, I32, I32, P, P, P, P, I32, P, P]
     lib.dq_residual_append.restype = ctypes.c_int
     lib.dq_residual_commit.argtypes = [P, P, I32, I32, P, P]
@@ -310,6 +312,24 @@ def dq_decode_attention_residual(q, res_k, res_v, seq_lens, res_lens, t_cap: int
                                            _ptr(workspace), workspace.numel() * workspace.element_size(),
                                            _stream(stream))
     _check(rc, "dq_decode_attention_residual")
+
+
+def dq_bf16_decode_attention_partial(q, k, v, seq_lens, workspace, softmax_scale=None, stream=None):
+    """Comparator: split-K partials of plain BF16 attention over k, v bf16
+    [B, Hkv, t_cap, d]; finish with dq_decode_attention_merge."""
+    import torch
+    for t, name in ((k, "k"), (v, "v")):
+        _need(t.is_cuda and t.dtype == torch.bfloat16 and t.is_contiguous() and t.dim() == 4, name)
+    _need(v.shape == k.shape, "v must match k")
+    B, Hkv, t_cap, d = k.shape
+    _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3
+          and q.shape[0] == B and q.shape[2] == d, "q")
+    _need(seq_lens.is_cuda and seq_lens.dtype == torch.int32 and seq_lens.numel() == B, "seq_lens")
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    rc = _lib.dq_bf16_decode_attention_partial(_ptr(q), B, q.shape[1], Hkv, _ptr(k), _ptr(v), _ptr(seq_lens),
+                                               t_cap, ctypes.c_float(scale), _ptr(workspace),
+                                               workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(rc, "dq_bf16_decode_attention_partial")
 
 
 def dq_residual_append(k_new, v_new, res_k, res_v, seq_lens, res_lens, status=None, stream=None):

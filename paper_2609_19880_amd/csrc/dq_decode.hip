@@ -30,9 +30,7 @@ constexpr int kVSlice = 64;      // value channels per PV pass
 constexpr int kVRow = 68;        // bytes per channel row of the value tile (64 + pad)
 constexpr int kMaxRecDwords = 16;
 constexpr int kMaxLds = 160 * 1024;
-constexpr int kMinChunk = 512;
 constexpr int kMaxChunk = 16384;  // bounds the per-window q . mu table in LDS
-constexpr int kWsHeader = 256;   // workspace header: chunk size, chunk count, residual flag
 
 // ---------------------------------------------------------------- symbols
 
@@ -895,7 +893,6 @@ struct ChunkPlan {
     int64_t slots_max;
 };
 
-int64_t max_chunks(int t_cap) { return (t_cap + kMinChunk - 1) / kMinChunk; }
 
 // Few, large chunks: one workgroup fits per CU (LDS), so the grid is sized to
 // about one workgroup per CU (more when the batch has more (sequence, KV head)
@@ -916,18 +913,6 @@ ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap, int num_cus) {
     return p;
 }
 
-int cu_count() {
-    static int cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cached[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-            n = 256;
-        cached[dev] = n;
-    }
-    return cached[dev];
-}
 
 }  // namespace
 
@@ -1069,6 +1054,19 @@ int launch_residual_commit(int32_t* seq_lens, int32_t* res_lens, int32_t B, int3
                            hipStream_t stream) {
     residual_commit_kernel<<<(B + 255) / 256, 256, 0, stream>>>(seq_lens, res_lens, B, n, status);
     return hip_check("residual_commit launch", hipGetLastError());
+}
+
+int cu_count() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cached[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        cached[dev] = n;
+    }
+    return cached[dev];
 }
 
 }  // namespace dq

@@ -381,6 +381,19 @@ int dq_decode_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32
                                          ws, static_cast<hipStream_t>(stream));
 }
 
+int dq_bf16_decode_attention_partial(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, const uint16_t* k,
+                                     const uint16_t* v, const int32_t* seq_lens, int32_t t_cap, float scale,
+                                     void* ws, size_t ws_bytes, void* stream) {
+    if (B <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 8 || B > 65535 || Hkv > 65535)
+        return DQ_ERR_INVALID_ARG;
+    if (t_cap <= 0 || t_cap % DQ_MEAN_WINDOW) return DQ_ERR_INVALID_ARG;
+    if (!q || !k || !v || !seq_lens || !std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(k) | reinterpret_cast<uintptr_t>(v)) & 15) return DQ_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128)) return DQ_ERR_WORKSPACE;
+    return dq::launch_bf16_partial(q, B, Hq, Hkv, k, v, seq_lens, t_cap, scale, ws,
+                                   static_cast<hipStream_t>(stream));
+}
+
 int dq_residual_append(const uint16_t* k_new, const uint16_t* v_new, int32_t B, int32_t Hkv, int32_t d,
                        uint16_t* res_k, uint16_t* res_v, const int32_t* seq_lens, int32_t* res_lens,
                        int32_t r_cap, uint32_t* status, void* stream) {

@@ -14,6 +14,15 @@ constexpr int kPayloadOffset = 8;           // fp16 scale, fp16 offset, u32 stat
 constexpr int kBisectSteps = 12;            // T of Alg. 1
 constexpr int kBracketUnits = 40 * kLambdaSteps;  // hi - lo = 40 octaves
 
+// Split-K attention workspace: a 256-byte header (chunk size, chunk count NC,
+// residual slot written), then fp32 acc [B][Hq][NC + 1][d], m and l
+// [B][Hq][NC + 1], sized for chunks of at least kMinChunk tokens.
+constexpr int kWsHeader = 256;
+constexpr int kMinChunk = 512;
+inline int64_t max_chunks(int t_cap) { return (t_cap + kMinChunk - 1) / kMinChunk; }
+inline int64_t ws_slots(int B, int Hq, int t_cap) { return (int64_t)B * Hq * (max_chunks(t_cap) + 1); }
+int cu_count();   // CUs of the current device
+
 // Device-resident tables, one allocation.
 //   lut[z], z in [0, 2^p):  bias (z - c_m) in bits 0..11, f_m in bits 12..23,
 //                           m in bits 24..29.
@@ -104,6 +113,9 @@ int launch_residual_append(const uint16_t* k_new, const uint16_t* v_new, int32_t
                            int32_t r_cap, uint32_t* status, hipStream_t stream);
 int launch_residual_commit(int32_t* seq_lens, int32_t* res_lens, int32_t B, int32_t n, uint32_t* status,
                            hipStream_t stream);
+int launch_bf16_partial(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, const uint16_t* k,
+                        const uint16_t* v, const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
+                        hipStream_t stream);
 int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
                            int32_t t_cap, const void* ws, float* out, hipStream_t stream);
 
