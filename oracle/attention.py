@@ -53,6 +53,8 @@ def attention_direct(q, k_rot, v_rot, seq_lens, gqa, softmax_scale):
     out = np.zeros((B, Hq, d), dtype=np.float64)
     for b in range(B):
         T = int(seq_lens[b])
+        if T == 0:
+            continue            # no tokens: the output stays 0 (reading A3)
         for i in range(Hq):
             h = i // gqa
             s = (k[b, h, :T] @ q[b, i]) * softmax_scale
@@ -74,6 +76,8 @@ def attention_folded(q, k_sym, k_s, k_o, k_mean_hat, v_sym, v_s, v_o, seq_lens,
     out = np.zeros((B, Hq, d), dtype=np.float64)
     for b in range(B):
         T = int(seq_lens[b])
+        if T == 0:
+            continue            # no tokens: the output stays 0 (reading A3)
         for i in range(Hq):
             h = i // gqa
             qr = q_rot[b, i]

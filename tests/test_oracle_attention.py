@@ -138,3 +138,17 @@ def test_residual_order_and_empty_sequence():
     b = attention.attention_with_residual(q, e, e, [0, 0], rk[:, :, perm], rv[:, :, perm], [R, 0], G, 0.5)
     assert np.max(np.abs(a - b)) < 1e-13
     assert np.all(a[1] == 0.0)        # a sequence with no tokens gives 0
+
+
+def test_empty_sequence_gives_zero():
+    """Reading A3: a sequence with no tokens gives 0, in every form."""
+    rng = np.random.default_rng(15)
+    B, Hkv, T, d, M, W = 2, 1, 128, 16, 5, 128
+    k_sym, k_s, k_o, mean, v_sym, v_s, v_o = _random_cache(rng, B, Hkv, T, d, M, W)
+    q = rng.normal(size=(B, 2, d))
+    krot = attention.dequantize(k_sym, k_s, k_o, mean, window=W)
+    vrot = attention.dequantize(v_sym, v_s, v_o)
+    a = attention.attention_direct(q, krot, vrot, [T, 0], 2, 0.3)
+    b = attention.attention_folded(q, k_sym, k_s, k_o, mean, v_sym, v_s, v_o, [T, 0], 2, 0.3, window=W)
+    assert np.all(a[1] == 0.0) and np.all(b[1] == 0.0)
+    assert np.max(np.abs(a[0] - b[0])) < 1e-12 * np.max(np.abs(a[0]))
