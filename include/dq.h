@@ -50,6 +50,7 @@ extern "C" {
 #define DQ_STATUS_OVERFLOW 2u /* encode: a stream could not be fitted into its record          */
 #define DQ_STATUS_CORRUPT 4u  /* decode: a record did not end in state 2^21 inside its C bytes  */
 #define DQ_STATUS_WINDOW 8u   /* residual window: append to a full ring, or commit more than it holds */
+#define DQ_STATUS_PAGE 16u    /* paged layout: a block-table entry outside the page pool (skipped)     */
 
 /* Fixed parameters of the format. */
 #define DQ_MEAN_WINDOW 128 /* tokens per key-mean window (windows start at token 0) */
@@ -230,6 +231,37 @@ int dq_residual_append(const uint16_t* k_new, const uint16_t* v_new, int32_t bat
  */
 int dq_residual_commit(int32_t* seq_lens, int32_t* res_lens, int32_t batch, int32_t n,
                        uint32_t* status, void* stream);
+
+/*
+ * Paged layout, for serving engines that allocate the cache in pages.  The
+ * records and key means of every sequence live in fixed-size pages of a pool:
+ *   record pools:    u8 [num_pages][kv_heads][page_tokens][C]
+ *   mean_q pool:     int8 [num_pages][kv_heads][page_tokens/128][head_dim]
+ *   mean_scale pool: fp16 [num_pages][kv_heads][page_tokens/128]
+ *   block_table:     device int32 [batch][max_pages]; logical page i of
+ *                    sequence b (tokens [i page_tokens, (i+1) page_tokens)) is
+ *                    pool page block_table[b * max_pages + i].
+ * page_tokens is a power of two in [128, 2^20]; the logical capacity t_cap =
+ * max_pages * page_tokens takes the place of t_cap above (workspace size,
+ * the merge).  Otherwise the calls mean what their contiguous forms mean.  A
+ * block-table entry outside [0, num_pages) sets DQ_STATUS_PAGE: the encoder
+ * writes nothing through it, the attention reads page 0 in its place.
+ */
+int dq_encode_kv_paged(const dq_tables* tables, const uint16_t* kv, int64_t stride_b,
+                       int64_t stride_t, int64_t stride_h, int32_t batch, int32_t kv_heads,
+                       int32_t t0, int32_t n_new, const int32_t* block_table,
+                       int32_t max_pages, int32_t page_tokens, int32_t num_pages,
+                       uint8_t* record_pool, int8_t* mean_q_pool, uint16_t* mean_scale_pool,
+                       uint32_t* status, void* stream);
+int dq_decode_attention_paged_partial(const dq_tables* k_tables, const dq_tables* v_tables,
+                                      const uint16_t* q, int32_t batch, int32_t q_heads,
+                                      int32_t kv_heads, const uint8_t* k_pool,
+                                      const int8_t* mean_q_pool, const uint16_t* mean_scale_pool,
+                                      const uint8_t* v_pool, const int32_t* block_table,
+                                      int32_t max_pages, int32_t page_tokens, int32_t num_pages,
+                                      const int32_t* seq_lens, float softmax_scale,
+                                      void* workspace, size_t workspace_bytes, uint32_t* status,
+                                      void* stream);
 
 /*
  * Comparator: the same decode step over an uncompressed BF16 cache.

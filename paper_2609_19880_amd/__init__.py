@@ -9,18 +9,18 @@ Entry points (same names as the C ABI in ``include/dq.h``):
     dq_compute_tables, dq_build_tables, dq_encode_kv,
     dq_decode_workspace_bytes, dq_decode_attention, dq_decode_attention_partial,
     dq_decode_attention_merge, dq_decode_attention_residual, dq_residual_append,
-    dq_residual_commit, dq_bf16_decode_attention_partial, dq_decode_symbols,
-    dq_strerror, dq_last_error
+    dq_residual_commit, dq_bf16_decode_attention_partial, dq_encode_kv_paged,
+    dq_decode_attention_paged_partial, dq_decode_symbols, dq_strerror, dq_last_error
 """
 
 from ._lib import (  # noqa: F401
     DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_INFEASIBLE, DQ_ERR_HIP, DQ_ERR_WORKSPACE,
-    DQ_STATUS_RANGE, DQ_STATUS_OVERFLOW, DQ_STATUS_CORRUPT, DQ_STATUS_WINDOW, DQ_MEAN_WINDOW,
+    DQ_STATUS_RANGE, DQ_STATUS_OVERFLOW, DQ_STATUS_CORRUPT, DQ_STATUS_WINDOW, DQ_STATUS_PAGE, DQ_MEAN_WINDOW,
     DqError, Tables, TableInfo, library_path,
     dq_compute_tables, dq_build_tables, dq_encode_kv, dq_decode_workspace_bytes,
     dq_decode_attention, dq_decode_attention_partial, dq_decode_attention_merge,
     dq_decode_attention_residual, dq_residual_append, dq_residual_commit,
-    dq_bf16_decode_attention_partial,
+    dq_bf16_decode_attention_partial, dq_encode_kv_paged, dq_decode_attention_paged_partial,
     dq_decode_symbols, dq_strerror, dq_last_error, smallest_feasible_alpha,
 )
 from .cache import KVCache, StreamingKVCache  # noqa: F401

@@ -23,6 +23,7 @@ DQ_STATUS_RANGE = 1
 DQ_STATUS_OVERFLOW = 2
 DQ_STATUS_CORRUPT = 4
 DQ_STATUS_WINDOW = 8
+DQ_STATUS_PAGE = 16
 
 DQ_MEAN_WINDOW = 128
 LAMBDA_STEPS = 512
@@ -81,6 +82,11 @@ def _load():
     lib.dq_decode_attention_residual.argtypes = [P, I32, I32, I32, P, P, P, P, I32, I32, ctypes.c_float,
                                                  P, SZ, P]
     lib.dq_decode_attention_residual.restype = ctypes.c_int
+    lib.dq_encode_kv_paged.argtypes = [P, P, I64, I64, I64, I32, I32, I32, I32, P, I32, I32, I32, P, P, P, P, P]
+    lib.dq_encode_kv_paged.restype = ctypes.c_int
+    lib.dq_decode_attention_paged_partial.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, I32, I32, P,
+                                                      ctypes.c_float, P, SZ, P, P]
+    lib.dq_decode_attention_paged_partial.restype = ctypes.c_int
     lib.dq_bf16_decode_attention_partial.argtypes = [P, I32, I32, I32, P, P, P, I32, ctypes.c_float, P, SZ, P]
     lib.dq_bf16_decode_attention_partial.restype = ctypes.c_int
     lib.dq_residual_append.argtypes = [P, P, I32, I32, I32, P, P, P, P, I32, P, P]
@@ -312,6 +318,59 @@ def dq_decode_attention_residual(q, res_k, res_v, seq_lens, res_lens, t_cap: int
                                            _ptr(workspace), workspace.numel() * workspace.element_size(),
                                            _stream(stream))
     _check(rc, "dq_decode_attention_residual")
+
+
+def _pool_args(tables, record_pool, block_table, mean_q_pool=None, mean_scale_pool=None):
+    import torch
+    _need(record_pool.is_cuda and record_pool.dtype == torch.uint8 and record_pool.is_contiguous()
+          and record_pool.dim() == 4 and record_pool.shape[3] == tables.record_bytes, "record pool")
+    num_pages, H, page, _ = record_pool.shape
+    _need(block_table.is_cuda and block_table.dtype == torch.int32 and block_table.is_contiguous()
+          and block_table.dim() == 2, "block_table must be int32 [batch, max_pages]")
+    if mean_q_pool is not None:
+        _need(mean_q_pool.dtype == torch.int8 and mean_q_pool.is_contiguous()
+              and tuple(mean_q_pool.shape) == (num_pages, H, page // DQ_MEAN_WINDOW, tables.head_dim), "mean_q pool")
+        _need(mean_scale_pool is not None and mean_scale_pool.element_size() == 2 and mean_scale_pool.is_contiguous()
+              and tuple(mean_scale_pool.shape) == (num_pages, H, page // DQ_MEAN_WINDOW), "mean_scale pool")
+    return num_pages, H, page, block_table.shape[1]
+
+
+def dq_encode_kv_paged(tables: Tables, kv, t0: int, block_table, record_pool, mean_q_pool=None,
+                       mean_scale_pool=None, status=None, stream=None):
+    """dq_encode_kv into a paged pool: record_pool uint8 [num_pages, H, page, C];
+    block_table int32 [B, max_pages]; keys also pass the mean pools."""
+    import torch
+    _need(kv.is_cuda and kv.dtype == torch.bfloat16 and kv.dim() == 4 and kv.stride(3) == 1, "kv")
+    B, T, H, d = kv.shape
+    num_pages, Hp, page, max_pages = _pool_args(tables, record_pool, block_table, mean_q_pool, mean_scale_pool)
+    _need(Hp == H and block_table.shape[0] == B and d == tables.head_dim, "pool/kv shapes")
+    rc = _lib.dq_encode_kv_paged(tables.handle, _ptr(kv), kv.stride(0), kv.stride(1), kv.stride(2), B, H,
+                                 int(t0), T, _ptr(block_table), max_pages, page, num_pages, _ptr(record_pool),
+                                 _ptr(mean_q_pool), _ptr(mean_scale_pool), _ptr(status), _stream(stream))
+    _check(rc, "dq_encode_kv_paged")
+
+
+def dq_decode_attention_paged_partial(k_tables: Tables, v_tables: Tables, q, k_pool, mean_q_pool, mean_scale_pool,
+                                      v_pool, block_table, seq_lens, workspace, softmax_scale=None, status=None,
+                                      stream=None):
+    """dq_decode_attention_partial over paged pools; finish with
+    dq_decode_attention_merge(..., t_cap = max_pages * page_tokens, ...)."""
+    import torch
+    num_pages, Hkv, page, max_pages = _pool_args(k_tables, k_pool, block_table, mean_q_pool, mean_scale_pool)
+    _need(v_pool.is_cuda and v_pool.dtype == torch.uint8 and v_pool.is_contiguous()
+          and tuple(v_pool.shape) == (num_pages, Hkv, page, v_tables.record_bytes), "v pool")
+    _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3, "q")
+    B, Hq, d = q.shape
+    _need(block_table.shape[0] == B and seq_lens.is_cuda and seq_lens.dtype == torch.int32
+          and seq_lens.numel() == B, "block_table / seq_lens")
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    rc = _lib.dq_decode_attention_paged_partial(k_tables.handle, v_tables.handle, _ptr(q), B, Hq, Hkv, _ptr(k_pool),
+                                                _ptr(mean_q_pool), _ptr(mean_scale_pool), _ptr(v_pool),
+                                                _ptr(block_table), max_pages, page, num_pages, _ptr(seq_lens),
+                                                ctypes.c_float(scale), _ptr(workspace),
+                                                workspace.numel() * workspace.element_size(), _ptr(status),
+                                                _stream(stream))
+    _check(rc, "dq_decode_attention_paged_partial")
 
 
 def dq_bf16_decode_attention_partial(q, k, v, seq_lens, workspace, softmax_scale=None, stream=None):

@@ -128,6 +128,7 @@ struct AttnArgs {
     float* ws_acc;               // [B][Hq][NC + 1][d]
     uint32_t* status;
     int shared_lut;
+    Pages pg;                    // records and key means: contiguous or paged
     AttnLayout L;
 };
 
@@ -316,11 +317,12 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
     const int nwin_total = a.t_cap / DQ_MEAN_WINDOW;
     const int w0 = start / DQ_MEAN_WINDOW;
     const int nwin = (a.chunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1;
+    bool bad_page = false;
     for (int i = tid; i < nwin * GP; i += nthr) {
         const int wi = i / GP, g = i % GP;
         float s = 0.f;
         if (g < G && w0 + wi < nwin_total) {
-            const int64_t widx = (int64_t)(b * a.Hkv + h) * nwin_total + w0 + wi;
+            const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + wi, bad_page);
             const float sc = half_bits_to_f32(a.kms[widx]);
             const int8_t* mq = a.kmq + widx * kD;
             for (int j = 0; j < kD; ++j) s += qt[g * kD + j] * (sc * (float)mq[j]);
@@ -362,7 +364,7 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
     constexpr bool kPrefetch = HG == 1;
     uint32_t rk[kMaxRecDwords], rv[kMaxRecDwords];
     if (kPrefetch && wave < ntiles) {
-        const int64_t tok = bh * a.t_cap + start + wave * kTile + lane;
+        const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, start + wave * kTile, bad_page) + lane;
         load_record(rk, a.krec, tok, CWk);
         load_record(rv, a.vrec, tok, CWv);
     }
@@ -371,7 +373,7 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
         const int t = t_base + lane;
         const bool valid = t < T;
         if (!kPrefetch) {
-            const int64_t tok = bh * a.t_cap + t_base + lane;
+            const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, t_base, bad_page) + lane;
             load_record(rk, a.krec, tok, CWk);
             load_record(rv, a.vrec, tok, CWv);
         }
@@ -382,7 +384,7 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
         build_pairs(rk, CWk, smem + pk_lane);
         build_pairs(rv, CWv, smem + pv_lane);
         if (kPrefetch && tile + L.nw < ntiles) {
-            const int64_t tok = bh * a.t_cap + t_base + L.nw * kTile + lane;
+            const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, t_base + L.nw * kTile, bad_page) + lane;
             load_record(rk, a.krec, tok, CWk);
             load_record(rv, a.vrec, tok, CWv);
         }
@@ -525,6 +527,7 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
         wave_sync();   // the next tile rewrites the pair arrays over the value tile
     }
     if (__any(corrupt) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_CORRUPT);
+    if (__any(bad_page) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_PAGE);
 
     // ---- merge the wavefronts of the workgroup
     float l_tot[GP], o_tot[GP];
@@ -966,7 +969,7 @@ static int launch_hg(AttnArgs& a, dim3 grid, hipStream_t stream) {
     }
 }
 
-int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
+int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pages& pg, const uint16_t* q,
                              int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
                              const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                              const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
@@ -1001,6 +1004,7 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uin
     a.ws_m = a.ws_acc + plan.slots_max * kD;
     a.ws_l = a.ws_m + plan.slots_max;
     a.status = status;
+    a.pg = pg;
     dim3 grid(a.nchunks, Hkv, B);
     if (a.shared_lut) return G <= 4 ? launch_hg<1, 0>(a, grid, stream) : launch_hg<2, 0>(a, grid, stream);
     return G <= 4 ? launch_hg<1, kLutVOffset>(a, grid, stream) : launch_hg<2, kLutVOffset>(a, grid, stream);

@@ -233,7 +233,7 @@ __device__ __forceinline__ uint16_t f64_to_half_bits(double v) {
 template <int VPL>
 __global__ __launch_bounds__(kWave) void key_mean_kernel(const uint16_t* __restrict__ kv,
                                                          int64_t sb, int64_t st, int64_t sh, int H,
-                                                         int t0, int t_cap,
+                                                         int t0, int t_cap, Pages pg,
                                                          int8_t* __restrict__ mean_q,
                                                          uint16_t* __restrict__ mean_scale,
                                                          uint32_t* status) {
@@ -263,16 +263,20 @@ __global__ __launch_bounds__(kWave) void key_mean_kernel(const uint16_t* __restr
     amax = wave_max(amax);
     const uint16_t sbits = f64_to_half_bits(amax / 127.0);
     const double sc = (double)__half2float(__ushort_as_half(sbits));
-    const int win = t0 / DQ_MEAN_WINDOW + w;
-    const int nwin = t_cap / DQ_MEAN_WINDOW;
-    int8_t* dst = mean_q + ((int64_t)(b * H + h) * nwin + win) * n;
+    bool bad_page = false;
+    const int64_t widx = window_index(pg, H, t_cap, b, h, t0 / DQ_MEAN_WINDOW + w, bad_page);
+    if (bad_page) {             // nothing is written through a block-table entry outside the pool
+        if (lane == 0 && status) atomicOr(status, DQ_STATUS_PAGE);
+        return;
+    }
+    int8_t* dst = mean_q + widx * n;
 #pragma unroll
     for (int k = 0; k < VPL; ++k) {
         double qv = 0.0;
         if (sc > 0.0) qv = fmin(127.0, fmax(-127.0, rint(mu[k] / sc)));
         dst[lane + kWave * k] = (int8_t)qv;
     }
-    if (lane == 0) mean_scale[(int64_t)(b * H + h) * nwin + win] = sbits;
+    if (lane == 0) mean_scale[widx] = sbits;
     const bool bad = __any(!finite) || !isfinite(sc);
     if (bad && lane == 0 && status) atomicOr(status, DQ_STATUS_RANGE);
 }
@@ -282,6 +286,7 @@ struct EncArgs {
     const uint16_t* kv;
     int64_t sb, st, sh;
     int H, t0, n_new, t_cap;
+    Pages pg;                    // records and key means: contiguous or paged
     uint8_t* records;
     const int8_t* mean_q;        // NULL for values
     const uint16_t* mean_scale;
@@ -296,8 +301,8 @@ __device__ __forceinline__ void stream_values(const EncArgs& a, int b, int h, in
     load_rotated<VPL>(a.kv + (int64_t)b * a.sb + ti * a.st + (int64_t)h * a.sh, x, lane);
     if (a.mean_q) {
         constexpr int n = kWave * VPL;
-        const int nwin = a.t_cap / DQ_MEAN_WINDOW;
-        const int64_t wi = (int64_t)(b * a.H + h) * nwin + t / DQ_MEAN_WINDOW;
+        bool bad = false;          // (a bad entry reads page 0; the record write then skips it)
+        const int64_t wi = window_index(a.pg, a.H, a.t_cap, b, h, t / DQ_MEAN_WINDOW, bad);
         const double sc = (double)__half2float(__ushort_as_half(a.mean_scale[wi]));
         const int8_t* mq = a.mean_q + wi * n;
 #pragma unroll
@@ -475,21 +480,37 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     }
     if (range_bad && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_RANGE);
 
-    // Write the records of the active streams: one contiguous span.
-    uint8_t* dst = a.records + ((int64_t)(b * a.H + h) * a.t_cap + first) * C;
-    const int total = active * C;
-    if ((((uintptr_t)dst) & 3) == 0 && (total & 3) == 0) {
-        uint32_t* d32 = reinterpret_cast<uint32_t*>(dst);
-        const uint32_t* s32 = reinterpret_cast<const uint32_t*>(s_rec);
-        for (int k = tid; k < total / 4; k += kEncThreads) d32[k] = s32[k];
+    // Write the records of the active streams: one contiguous span, or one
+    // record at a time through the block table.
+    if (!a.pg.bt) {
+        uint8_t* dst = a.records + ((int64_t)(b * a.H + h) * a.t_cap + first) * C;
+        const int total = active * C;
+        if ((((uintptr_t)dst) & 3) == 0 && (total & 3) == 0) {
+            uint32_t* d32 = reinterpret_cast<uint32_t*>(dst);
+            const uint32_t* s32 = reinterpret_cast<const uint32_t*>(s_rec);
+            for (int k = tid; k < total / 4; k += kEncThreads) d32[k] = s32[k];
+        } else {
+            for (int k = tid; k < total; k += kEncThreads) dst[k] = s_rec[k];
+        }
     } else {
-        for (int k = tid; k < total; k += kEncThreads) dst[k] = s_rec[k];
+        bool bad_page = false;
+        for (int i = wave; i < active; i += kEncWaves) {
+            bool bad = false;
+            const int64_t row = record_row(a.pg, a.H, a.t_cap, b, h, first + i, bad);
+            if (bad) {
+                bad_page = true;
+                continue;
+            }
+            uint8_t* dst = a.records + row * C;
+            for (int k = lane; k < C; k += kWave) dst[k] = s_rec[i * C + k];
+        }
+        if (bad_page && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_PAGE);
     }
 }
 
 }  // namespace
 
-int launch_encode(const dq_tables* tab, const uint16_t* kv, int64_t sb, int64_t st, int64_t sh,
+int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int64_t sb, int64_t st, int64_t sh,
                   int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
                   uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status,
                   hipStream_t stream) {
@@ -498,9 +519,9 @@ int launch_encode(const dq_tables* tab, const uint16_t* kv, int64_t sb, int64_t 
     if (mean_q) {
         dim3 grid(n_new / DQ_MEAN_WINDOW, H, B);
         switch (vpl) {
-            case 1: key_mean_kernel<1><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, mean_q, mean_scale, status); break;
-            case 2: key_mean_kernel<2><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, mean_q, mean_scale, status); break;
-            case 4: key_mean_kernel<4><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, mean_q, mean_scale, status); break;
+            case 1: key_mean_kernel<1><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
+            case 2: key_mean_kernel<2><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
+            case 4: key_mean_kernel<4><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
             default: return DQ_ERR_INVALID_ARG;
         }
         if (int rc = hip_check("key_mean launch", hipGetLastError())) return rc;
@@ -515,6 +536,7 @@ int launch_encode(const dq_tables* tab, const uint16_t* kv, int64_t sb, int64_t 
     a.t0 = t0;
     a.n_new = n_new;
     a.t_cap = t_cap;
+    a.pg = pg;
     a.records = records;
     a.mean_q = mean_q;
     a.mean_scale = mean_scale;

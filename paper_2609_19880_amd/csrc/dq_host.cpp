@@ -293,10 +293,9 @@ void dq_free_tables(dq_tables* t) {
     delete t;
 }
 
-int dq_encode_kv(const dq_tables* t, const uint16_t* kv, int64_t sb, int64_t st, int64_t sh,
-                 int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
-                 uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status,
-                 void* stream) {
+static int encode_kv(const dq_tables* t, const dq::Pages& pg, const uint16_t* kv, int64_t sb, int64_t st,
+                     int64_t sh, int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
+                     uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status, void* stream) {
     if (!table_args_ok(t) || !kv || !records) return DQ_ERR_INVALID_ARG;
     if (t->cfg.head_dim > 256) return DQ_ERR_INVALID_ARG;
     if (B < 0 || H <= 0 || t0 < 0 || n_new < 0 || t_cap <= 0 || t0 + n_new > t_cap)
@@ -308,8 +307,44 @@ int dq_encode_kv(const dq_tables* t, const uint16_t* kv, int64_t sb, int64_t st,
     if (keys && ((t0 % DQ_MEAN_WINDOW) || (n_new % DQ_MEAN_WINDOW) || (t_cap % DQ_MEAN_WINDOW)))
         return DQ_ERR_INVALID_ARG;
     if (B == 0 || n_new == 0) return DQ_OK;
-    return dq::launch_encode(t, kv, sb, st, sh, B, H, t0, n_new, t_cap, records, mean_q,
+    return dq::launch_encode(t, pg, kv, sb, st, sh, B, H, t0, n_new, t_cap, records, mean_q,
                              mean_scale, status, static_cast<hipStream_t>(stream));
+}
+
+static const dq::Pages kContiguous{nullptr, 0, 0, 0};
+
+// A paged layout: page length a power of two in [128, 2^20], a logical
+// capacity max_pages * page_tokens within int32.
+static int paging(const int32_t* bt, int32_t max_pages, int32_t page_tokens, int32_t num_pages,
+                  dq::Pages* pg, int32_t* t_cap) {
+    if (!bt || max_pages <= 0 || num_pages <= 0) return DQ_ERR_INVALID_ARG;
+    if (page_tokens < DQ_MEAN_WINDOW || page_tokens > (1 << 20) || (page_tokens & (page_tokens - 1)))
+        return DQ_ERR_INVALID_ARG;
+    if ((int64_t)max_pages * page_tokens > 0x7FFFFFFF) return DQ_ERR_INVALID_ARG;
+    int shift = 0;
+    while ((1 << shift) < page_tokens) ++shift;
+    *pg = dq::Pages{bt, max_pages, shift, num_pages};
+    *t_cap = max_pages * page_tokens;
+    return DQ_OK;
+}
+
+int dq_encode_kv(const dq_tables* t, const uint16_t* kv, int64_t sb, int64_t st, int64_t sh,
+                 int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
+                 uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status,
+                 void* stream) {
+    return encode_kv(t, kContiguous, kv, sb, st, sh, B, H, t0, n_new, t_cap, records, mean_q, mean_scale,
+                     status, stream);
+}
+
+int dq_encode_kv_paged(const dq_tables* t, const uint16_t* kv, int64_t sb, int64_t st, int64_t sh,
+                       int32_t B, int32_t H, int32_t t0, int32_t n_new, const int32_t* block_table,
+                       int32_t max_pages, int32_t page_tokens, int32_t num_pages, uint8_t* record_pool,
+                       int8_t* mean_q_pool, uint16_t* mean_scale_pool, uint32_t* status, void* stream) {
+    dq::Pages pg;
+    int32_t t_cap = 0;
+    if (int rc = paging(block_table, max_pages, page_tokens, num_pages, &pg, &t_cap)) return rc;
+    return encode_kv(t, pg, kv, sb, st, sh, B, H, t0, n_new, t_cap, record_pool, mean_q_pool, mean_scale_pool,
+                     status, stream);
 }
 
 size_t dq_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d) {
@@ -327,20 +362,41 @@ static int check_attention(const dq_tables* tk, const dq_tables* tv, int32_t B, 
     return DQ_OK;
 }
 
-int dq_decode_attention_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
-                                int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
-                                const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
-                                const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
-                                size_t ws_bytes, uint32_t* status, void* stream) {
+static int attention_partial(const dq_tables* tk, const dq_tables* tv, const dq::Pages& pg, const uint16_t* q,
+                             int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec, const int8_t* kmq,
+                             const uint16_t* kms, const uint8_t* vrec, const int32_t* seq_lens, int32_t t_cap,
+                             float scale, void* ws, size_t ws_bytes, uint32_t* status, void* stream) {
     int rc = check_attention(tk, tv, B, Hq, Hkv, t_cap);
     if (rc != DQ_OK) return rc;
     if (!q || !krec || !kmq || !kms || !vrec || !seq_lens) return DQ_ERR_INVALID_ARG;
     if (!std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
     if (!ws || ws_bytes < dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128))
         return DQ_ERR_WORKSPACE;
-    return dq::launch_attention_partial(tk, tv, q, B, Hq, Hkv, krec, kmq, kms, vrec, seq_lens,
+    return dq::launch_attention_partial(tk, tv, pg, q, B, Hq, Hkv, krec, kmq, kms, vrec, seq_lens,
                                         t_cap, scale, ws, status,
                                         static_cast<hipStream_t>(stream));
+}
+
+int dq_decode_attention_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
+                                int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
+                                const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
+                                const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
+                                size_t ws_bytes, uint32_t* status, void* stream) {
+    return attention_partial(tk, tv, kContiguous, q, B, Hq, Hkv, krec, kmq, kms, vrec, seq_lens, t_cap, scale,
+                             ws, ws_bytes, status, stream);
+}
+
+int dq_decode_attention_paged_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
+                                      int32_t Hq, int32_t Hkv, const uint8_t* k_pool, const int8_t* mean_q_pool,
+                                      const uint16_t* mean_scale_pool, const uint8_t* v_pool,
+                                      const int32_t* block_table, int32_t max_pages, int32_t page_tokens,
+                                      int32_t num_pages, const int32_t* seq_lens, float scale, void* ws,
+                                      size_t ws_bytes, uint32_t* status, void* stream) {
+    dq::Pages pg;
+    int32_t t_cap = 0;
+    if (int rc = paging(block_table, max_pages, page_tokens, num_pages, &pg, &t_cap)) return rc;
+    return attention_partial(tk, tv, pg, q, B, Hq, Hkv, k_pool, mean_q_pool, mean_scale_pool, v_pool, seq_lens,
+                             t_cap, scale, ws, ws_bytes, status, stream);
 }
 
 int dq_decode_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,

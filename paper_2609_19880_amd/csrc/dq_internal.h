@@ -23,6 +23,45 @@ inline int64_t max_chunks(int t_cap) { return (t_cap + kMinChunk - 1) / kMinChun
 inline int64_t ws_slots(int B, int Hq, int t_cap) { return (int64_t)B * Hq * (max_chunks(t_cap) + 1); }
 int cu_count();   // CUs of the current device
 
+// Where the records and key means of (sequence b, KV head h, token t) live.
+//   contiguous (bt == NULL): records [B][H][t_cap][C], means [B][H][t_cap/128][.]
+//   paged: pools [num_pages][H][page][C] and [num_pages][H][page/128][.]; the
+//          logical page i of sequence b is the physical page bt[b * max_pages + i],
+//          page = 2^page_shift >= 128 tokens, t_cap = max_pages * page.
+// A block-table entry outside [0, num_pages) reads page 0 and raises *bad.
+struct Pages {
+    const int32_t* bt;
+    int32_t max_pages;
+    int32_t page_shift;
+    int32_t num_pages;
+};
+
+__device__ __forceinline__ int32_t physical_page(const Pages& pg, int b, int t, bool& bad) {
+    int32_t p = pg.bt[(int64_t)b * pg.max_pages + (t >> pg.page_shift)];
+    if (p < 0 || p >= pg.num_pages) {
+        bad = true;
+        p = 0;
+    }
+    return p;
+}
+
+// Record row (index in units of one record) of token t; rows of the tokens of
+// an aligned 64-token tile are consecutive.
+__device__ __forceinline__ int64_t record_row(const Pages& pg, int H, int t_cap, int b, int h, int t, bool& bad) {
+    if (!pg.bt) return ((int64_t)b * H + h) * t_cap + t;
+    const int64_t p = physical_page(pg, b, t, bad);
+    return ((p * H + h) << pg.page_shift) + (t & ((1 << pg.page_shift) - 1));
+}
+
+// Index of the 128-token mean window w of (b, h).
+__device__ __forceinline__ int64_t window_index(const Pages& pg, int H, int t_cap, int b, int h, int w, bool& bad) {
+    if (!pg.bt) return ((int64_t)b * H + h) * (t_cap / DQ_MEAN_WINDOW) + w;
+    const int t = w * DQ_MEAN_WINDOW;
+    const int64_t p = physical_page(pg, b, t, bad);
+    const int wpp = 1 << (pg.page_shift - 7);
+    return (p * H + h) * wpp + ((t & ((1 << pg.page_shift) - 1)) >> 7);
+}
+
 // Device-resident tables, one allocation.
 //   lut[z], z in [0, 2^p):  bias (z - c_m) in bits 0..11, f_m in bits 12..23,
 //                           m in bits 24..29.
@@ -87,7 +126,7 @@ inline int hip_check(const char* where, hipError_t err) {
 }
 
 // Launchers implemented in the .hip files.  Return DQ_OK or DQ_ERR_HIP.
-int launch_encode(const dq_tables* tab, const uint16_t* kv, int64_t sb, int64_t st,
+int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int64_t sb, int64_t st,
                   int64_t sh, int32_t B, int32_t H, int32_t t0, int32_t n_new,
                   int32_t t_cap, uint8_t* records, int8_t* mean_q,
                   uint16_t* mean_scale, uint32_t* status, hipStream_t stream);
@@ -98,7 +137,7 @@ int launch_decode_symbols(const dq_tables* tab, const uint8_t* records, int64_t 
 
 size_t attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d);
 
-int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
+int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pages& pg, const uint16_t* q,
                              int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
                              const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                              const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,

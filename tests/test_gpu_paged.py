@@ -1,0 +1,133 @@
+"""Paged layout: records and key means in pool pages addressed through a block
+table.  The paged calls must give exactly what the contiguous calls give
+(bit-identical records, means and attention outputs: same arithmetic, only
+the addresses differ), and the contiguous path is the one checked against
+the oracle elsewhere; here it is re-checked against the oracle once more.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import dq_workloads as wlmod
+from oracle import attention, kmean, kv, tables
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+TOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def dq():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_19880_amd as mod
+    return mod
+
+
+def _setup(dq, page=256, max_pages=4, extra=5, seed=41):
+    wl = wlmod.workload("b1_t4k")
+    gtk = dq.Tables(128, wl.k.levels, wl.k.precision, wl.k.record_bytes, wl.k.alpha)
+    gtv = dq.Tables(128, wl.v.levels, wl.v.precision, wl.v.record_bytes, wl.v.alpha)
+    B, Hkv, G = 3, 2, 4
+    t_cap = page * max_pages
+    num_pages = B * max_pages + extra
+    rng = np.random.default_rng(seed)
+    bt = rng.permutation(num_pages)[: B * max_pages].reshape(B, max_pages).astype(np.int32)
+    w2 = wlmod.Workload("paged", B, t_cap, Hkv * G, Hkv, 4, wl.k, wl.v)
+    k = wlmod.make_k(w2, seed).to(DEV)
+    v = wlmod.make_v(w2, seed).to(DEV)
+    q = wlmod.make_q(w2, seed).to(DEV)
+    return wl, gtk, gtv, B, Hkv, G, page, max_pages, t_cap, num_pages, bt, k, v, q
+
+
+def _pools(num_pages, Hkv, page, wl):
+    # one spare page past num_pages: every access through a valid entry stays
+    # inside the first num_pages pages
+    kp = torch.zeros((num_pages + 1, Hkv, page, wl.k.record_bytes), dtype=torch.uint8, device=DEV)
+    vp = torch.zeros((num_pages + 1, Hkv, page, wl.v.record_bytes), dtype=torch.uint8, device=DEV)
+    mq = torch.zeros((num_pages + 1, Hkv, page // 128, 128), dtype=torch.int8, device=DEV)
+    ms = torch.zeros((num_pages + 1, Hkv, page // 128), dtype=torch.int16, device=DEV)
+    return kp, vp, mq, ms
+
+
+def test_paged_encode_and_attention_equal_contiguous(dq):
+    wl, gtk, gtv, B, Hkv, G, page, max_pages, t_cap, num_pages, bt, k, v, q = _setup(dq)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    # contiguous reference
+    cache = dq.KVCache(B, Hkv, Hkv * G, t_cap, gtk, gtv, device=DEV)
+    dq.dq_encode_kv(gtk, k[:, :512], 0, t_cap, cache.k_records, cache.k_mean_q, cache.k_mean_scale, status)
+    dq.dq_encode_kv(gtk, k[:, 512:], 512, t_cap, cache.k_records, cache.k_mean_q, cache.k_mean_scale, status)
+    dq.dq_encode_kv(gtv, v[:, :300], 0, t_cap, cache.v_records, None, None, status)
+    dq.dq_encode_kv(gtv, v[:, 300:], 300, t_cap, cache.v_records, None, None, status)
+    # paged, same appends (values start mid-tile and cross pages)
+    kp, vp, mq, ms = _pools(num_pages, Hkv, page, wl)
+    btd = torch.from_numpy(bt).to(DEV)
+    kpool, vpool, mqpool, mspool = kp[:num_pages], vp[:num_pages], mq[:num_pages], ms[:num_pages]
+    dq.dq_encode_kv_paged(gtk, k[:, :512], 0, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_paged(gtk, k[:, 512:], 512, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_paged(gtv, v[:, :300], 0, btd, vpool, None, None, status)
+    dq.dq_encode_kv_paged(gtv, v[:, 300:], 300, btd, vpool, None, None, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for b in range(B):
+        for i in range(max_pages):
+            p, sl = int(bt[b, i]), slice(i * page, (i + 1) * page)
+            assert torch.equal(kpool[p], cache.k_records[b, :, sl])
+            assert torch.equal(vpool[p], cache.v_records[b, :, sl])
+            assert torch.equal(mqpool[p], cache.k_mean_q[b, :, i * page // 128:(i + 1) * page // 128])
+            assert torch.equal(mspool[p], cache.k_mean_scale[b, :, i * page // 128:(i + 1) * page // 128])
+    assert int(kp[num_pages].abs().sum()) == 0       # the spare page is never touched
+    # attention: identical outputs
+    lens = torch.tensor([t_cap, 0, 700], dtype=torch.int32, device=DEV)
+    out_c = torch.empty((B, Hkv * G, 128), dtype=torch.float32, device=DEV)
+    out_p = torch.empty_like(out_c)
+    dq.dq_decode_attention(gtk, gtv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale, cache.v_records,
+                           lens, out_c, cache.workspace, status=status)
+    ws = torch.empty_like(cache.workspace)
+    dq.dq_decode_attention_paged_partial(gtk, gtv, q, kpool, mqpool, mspool, vpool, btd, lens, ws, status=status)
+    dq.dq_decode_attention_merge(B, Hkv * G, Hkv, lens, t_cap, ws, out_p)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert torch.equal(out_c, out_p)
+    # and the oracle on the same tokens
+    otk = tables.build_tables(128, wl.k.levels, wl.k.precision, wl.k.alpha, wl.k.record_bytes)
+    otv = tables.build_tables(128, wl.v.levels, wl.v.precision, wl.v.alpha, wl.v.record_bytes)
+    kb, vb = wlmod.bf16_bits(k.cpu()), wlmod.bf16_bits(v.cpu())
+    krec, m_q, m_s, ksym = kv.encode_keys(kb, otk)
+    vrec, vsym = kv.encode_values(vb, otv)
+    _, ks, ko, _ = kv.decode_records(krec, otk, 128)
+    _, vs, vo, _ = kv.decode_records(vrec, otv, 128)
+    ref = attention.attention_folded(kv.bf16_to_f64(wlmod.bf16_bits(q.cpu())), ksym, ks, ko,
+                                     kmean.dequantize_mean(m_q, m_s), vsym, vs, vo, lens.tolist(), G,
+                                     1 / np.sqrt(128))
+    got = out_p.cpu().numpy().astype(np.float64)
+    live = [0, 2]
+    scale = np.max(np.abs(ref[live]), axis=-1, keepdims=True)
+    assert float(np.max(np.abs(got[live] - ref[live]) / scale)) < TOL
+    assert np.all(got[1] == 0.0)
+
+
+def test_paged_bad_block_table_entry_is_flagged(dq):
+    wl, gtk, gtv, B, Hkv, G, page, max_pages, t_cap, num_pages, bt, k, v, q = _setup(dq, seed=42)
+    kp, vp, mq, ms = _pools(num_pages, Hkv, page, wl)
+    kpool, vpool, mqpool, mspool = kp[:num_pages], vp[:num_pages], mq[:num_pages], ms[:num_pages]
+    bad = bt.copy()
+    bad[1, 2] = num_pages          # one past the pool
+    btd = torch.from_numpy(bad).to(DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    dq.dq_encode_kv_paged(gtk, k, 0, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_paged(gtv, v, 0, btd, vpool, None, None, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) & dq.DQ_STATUS_PAGE
+    assert int(kp[num_pages].abs().sum()) == 0 and int(mq[num_pages].abs().sum()) == 0
+    status.zero_()
+    lens = torch.tensor([t_cap, t_cap, t_cap], dtype=torch.int32, device=DEV)
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, Hkv * G, Hkv, t_cap), dtype=torch.uint8, device=DEV)
+    out = torch.empty((B, Hkv * G, 128), dtype=torch.float32, device=DEV)
+    dq.dq_decode_attention_paged_partial(gtk, gtv, q, kpool, mqpool, mspool, vpool, btd, lens, ws, status=status)
+    dq.dq_decode_attention_merge(B, Hkv * G, Hkv, lens, t_cap, ws, out)
+    torch.cuda.synchronize()
+    assert int(status.item()) & dq.DQ_STATUS_PAGE
+    assert torch.isfinite(out).all()
