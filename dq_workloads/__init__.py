@@ -28,15 +28,16 @@ PRECISION = 12
 
 @dataclass(frozen=True)
 class Coding:
-    """Coding parameters of one tensor (K or V)."""
+    """Coding parameters of one tensor (K or V); n values per stream."""
     levels: int
     record_bytes: int
     alpha: float
     precision: int = PRECISION
+    n: int = HEAD_DIM
 
     @property
     def bits_per_elem(self) -> float:
-        return 8.0 * self.record_bytes / HEAD_DIM
+        return 8.0 * self.record_bytes / self.n
 
 
 @dataclass(frozen=True)
@@ -50,6 +51,7 @@ class Workload:
     k: Coding
     v: Coding
     head_dim: int = HEAD_DIM
+    streams: str = "head"        # "head": one stream per (token, KV head); "token": per token
 
     @property
     def gqa(self) -> int:
@@ -100,10 +102,18 @@ def workload(name: str, variant: str = "paper", bpe: float | None = None) -> Wor
         return Workload(name, 64, 8192, 32, 8, 4, c, c)
     if name == "b32_t32k_g8":
         return Workload(name, 32, 32768, 64, 8, 8, coding(32, 3.0, variant), coding(16, 2.0, variant))
+    if name in TOKEN_WORKLOADS:
+        # the paper's default operating point (Sec. 5.1): one stream of 1024
+        # values per token, 331 B / 231 B containers (+ the 4-byte s, o header)
+        # with 8 / 6 levels at alpha 1.4
+        k, v = Coding(8, 335, 1.4, n=1024), Coding(6, 235, 1.4, n=1024)
+        B, T = {"b1_t4k_tok": (1, 4096), "b16_t32k_tok": (16, 32768)}[name]
+        return Workload(name, B, T, 32, 8, 4, k, v, streams="token")
     raise KeyError(name)
 
 
 WORKLOADS = ("b1_t4k", "b16_t32k", "b1_t128k", "b64_t8k", "b32_t32k_g8")
+TOKEN_WORKLOADS = ("b1_t4k_tok", "b16_t32k_tok")
 
 
 def key_stats(seed: int, heads: int, d: int, outliers: int):

@@ -6,6 +6,15 @@ Pipeline of Fig. 1 / Sec. 4.2, one stream per (token, KV head):
   bf16 -> fp64 -> Hadamard (hadamard.fwht) -> keys: minus the dequantized
   window mean (kmean) -> Alg. 1 (quantize) -> rANS record (rans).
 
+Reading K2 (streams over all KV heads, the paper's default grouping):
+Sec. 4.1 defines a stream as the values of one token's key or value tensor,
+and Sec. 4.5 / Sec. 5.1 make that one group of H_kv d = 1024 values spanning
+every KV head.  The stream takes the heads in order, each in its rotated
+channel order (value j = h d + c), which is the order the decoder consumes
+them one KV head at a time.  Rotation and the key window mean stay per head;
+the affine (s, o) and the record are per token.  The *_tokenwise functions
+build these streams; with H_kv = 1 they are the per-head streams.
+
 Reading K1 (container overflow): the drift guarantees the ideal cost
 sum r <= B; should the rANS bytes still exceed the record (8 + E > C), the
 budget is lowered by 8 bits and the second Drift and the coder are run again,
@@ -83,18 +92,8 @@ def encode_keys(k_bits: np.ndarray, tab: Tables, window: int = 128):
     """Keys [B, T, H, d] (bf16 bits) -> (records [B, H, T, C],
     mean_q int8 [B, H, T/W, d], mean_scale fp16 [B, H, T/W], sym [B, H, T, d])."""
     B, T, H, d = k_bits.shape
-    if T % window:
-        raise ValueError("token count must be a multiple of the mean window")
-    y = rotate(k_bits).transpose(0, 2, 1, 3)                     # [B, H, T, d]
-    nw = T // window
-    yw = y.reshape(B, H, nw, window, d)
-    mu = kmean.window_mean(yw)                                   # [B, H, nw, d]
-    mq, ms = kmean.quantize_mean(mu)
-    if not np.all(np.isfinite(ms.astype(np.float64))):
-        raise EncodeError("key mean scale overflows fp16")
-    mu_hat = kmean.dequantize_mean(mq, ms)                       # [B, H, nw, d]
-    x = (yw - mu_hat[:, :, :, None, :]).reshape(B * H * T, d)
-    recs, syms, _, _, _ = encode_streams(x, tab)
+    x, mq, ms = _key_streams(k_bits, window)
+    recs, syms, _, _, _ = encode_streams(x.reshape(B * H * T, d), tab)
     C = tab.record_bytes
     return (recs.reshape(B, H, T, C), mq, ms, syms.reshape(B, H, T, d))
 
@@ -119,3 +118,57 @@ def decode_records(records: np.ndarray, tab: Tables, n: int):
     s16, o16 = rans.unpack_header(flat)
     ok = (x == rans.RANS_L) & (ptr <= flat.shape[1])
     return (sym.reshape(*lead, n), s16.reshape(lead), o16.reshape(lead), ok.reshape(lead))
+
+
+def _key_streams(k_bits: np.ndarray, window: int):
+    """Rotated keys minus their dequantized window means, [B, H, T, d],
+    with the INT8 means and their fp16 scales."""
+    B, T, H, d = k_bits.shape
+    if T % window:
+        raise ValueError("token count must be a multiple of the mean window")
+    y = rotate(k_bits).transpose(0, 2, 1, 3)                     # [B, H, T, d]
+    nw = T // window
+    yw = y.reshape(B, H, nw, window, d)
+    mu = kmean.window_mean(yw)
+    mq, ms = kmean.quantize_mean(mu)
+    if not np.all(np.isfinite(ms.astype(np.float64))):
+        raise EncodeError("key mean scale overflows fp16")
+    mu_hat = kmean.dequantize_mean(mq, ms)
+    return (yw - mu_hat[:, :, :, None, :]).reshape(B, H, T, d), mq, ms
+
+
+def encode_keys_tokenwise(k_bits: np.ndarray, tab: Tables, window: int = 128):
+    """Keys [B, T, H, d] -> one stream of n = H d values per token (reading K2).
+
+    Returns (records [B, T, C], mean_q int8 [B, H, T/W, d],
+    mean_scale fp16 [B, H, T/W], sym [B, T, H d]).
+    """
+    B, T, H, d = k_bits.shape
+    if tab.n != H * d:
+        raise ValueError("the table's stream length must be H * d")
+    x, mq, ms = _key_streams(k_bits, window)
+    x = x.transpose(0, 2, 1, 3).reshape(B * T, H * d)
+    recs, syms, _, _, _ = encode_streams(x, tab)
+    return recs.reshape(B, T, tab.record_bytes), mq, ms, syms.reshape(B, T, H * d)
+
+
+def encode_values_tokenwise(v_bits: np.ndarray, tab: Tables):
+    """Values [B, T, H, d] -> (records [B, T, C], sym [B, T, H d]) (reading K2)."""
+    B, T, H, d = v_bits.shape
+    if tab.n != H * d:
+        raise ValueError("the table's stream length must be H * d")
+    x = rotate(v_bits).reshape(B * T, H * d)
+    recs, syms, _, _, _ = encode_streams(x, tab)
+    return recs.reshape(B, T, tab.record_bytes), syms.reshape(B, T, H * d)
+
+
+def tokenwise_as_heads(sym: np.ndarray, s16: np.ndarray, o16: np.ndarray, H: int):
+    """Token streams (sym [B, T, H d], s16 / o16 [B, T]) viewed per KV head:
+    (sym [B, H, T, d], s16 [B, H, T], o16 [B, H, T]); every head of a token
+    shares the token's (s, o)."""
+    B, T, n = sym.shape
+    d = n // H
+    sh = sym.reshape(B, T, H, d).transpose(0, 2, 1, 3)
+    s = np.broadcast_to(s16[:, None, :], (B, H, T))
+    o = np.broadcast_to(o16[:, None, :], (B, H, T))
+    return sh, s, o
