@@ -264,6 +264,42 @@ int dq_decode_attention_paged_partial(const dq_tables* k_tables, const dq_tables
                                       void* stream);
 
 /*
+ * Per-token streams (Sec. 4.1, Sec. 4.5 "Decoding", Sec. 5.1): the paper's
+ * default grouping, one stream of n = 128 kv_heads values per token spanning
+ * every KV head (e.g. 1024 values for 8 heads, with 331 + 4 and 231 + 4 byte
+ * records), instead of one stream per (token, KV head).  The stream takes the
+ * heads in order, each head rotated on its own and, for keys, minus its own
+ * window mean (the means are per head exactly as above); one (s, o) header
+ * serves the whole token.  Tables are built with head_dim = n = 128 kv_heads.
+ *
+ * dq_token_record_stride: bytes between consecutive token records, C rounded
+ *   up to a multiple of 16 (the pad bytes are written as zeros); 0 for an
+ *   invalid table.
+ * dq_encode_kv_token: as dq_encode_kv with kv_heads in {1, 2, 4, 8} and
+ *   head_dim 128; records: u8 [batch][t_cap][stride], 16-byte aligned.
+ * dq_decode_attention_token_partial: one decode step over those records
+ *   (rANS-decoded once per token and consumed one KV head at a time), into the
+ *   workspace of dq_decode_workspace_bytes; finish with
+ *   dq_decode_attention_merge (and optionally add a residual window with
+ *   dq_decode_attention_residual before it).  q_heads / kv_heads <= 4;
+ *   k_mean_q / k_mean_scale as for dq_decode_attention.  Corrupt records set
+ *   DQ_STATUS_CORRUPT.
+ * Return DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_WORKSPACE or DQ_ERR_HIP.
+ */
+int32_t dq_token_record_stride(const dq_tables* tables);
+int dq_encode_kv_token(const dq_tables* tables, const uint16_t* kv, int64_t stride_b,
+                       int64_t stride_t, int64_t stride_h, int32_t batch, int32_t kv_heads,
+                       int32_t t0, int32_t n_new, int32_t t_cap, uint8_t* records,
+                       int8_t* mean_q, uint16_t* mean_scale, uint32_t* status, void* stream);
+int dq_decode_attention_token_partial(const dq_tables* k_tables, const dq_tables* v_tables,
+                                      const uint16_t* q, int32_t batch, int32_t q_heads,
+                                      int32_t kv_heads, const uint8_t* k_records,
+                                      const int8_t* k_mean_q, const uint16_t* k_mean_scale,
+                                      const uint8_t* v_records, const int32_t* seq_lens,
+                                      int32_t t_cap, float softmax_scale, void* workspace,
+                                      size_t workspace_bytes, uint32_t* status, void* stream);
+
+/*
  * Comparator: the same decode step over an uncompressed BF16 cache.
  *   k, v: bf16 [batch][kv_heads][t_cap][head_dim], 16-byte aligned, original
  *         basis; the first seq_lens[b] tokens of sequence b are attended.

@@ -87,6 +87,13 @@ def _load():
     lib.dq_decode_attention_paged_partial.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, I32, I32, P,
                                                       ctypes.c_float, P, SZ, P, P]
     lib.dq_decode_attention_paged_partial.restype = ctypes.c_int
+    lib.dq_token_record_stride.argtypes = [P]
+    lib.dq_token_record_stride.restype = I32
+    lib.dq_encode_kv_token.argtypes = [P, P, I64, I64, I64, I32, I32, I32, I32, I32, P, P, P, P, P]
+    lib.dq_encode_kv_token.restype = ctypes.c_int
+    lib.dq_decode_attention_token_partial.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, ctypes.c_float,
+                                                      P, SZ, P, P]
+    lib.dq_decode_attention_token_partial.restype = ctypes.c_int
     lib.dq_bf16_decode_attention_partial.argtypes = [P, I32, I32, I32, P, P, P, I32, ctypes.c_float, P, SZ, P]
     lib.dq_bf16_decode_attention_partial.restype = ctypes.c_int
     lib.dq_residual_append.argtypes = [P, P, I32, I32, I32, P, P, P, P, I32, P, P]
@@ -371,6 +378,62 @@ def dq_decode_attention_paged_partial(k_tables: Tables, v_tables: Tables, q, k_p
                                                 workspace.numel() * workspace.element_size(), _ptr(status),
                                                 _stream(stream))
     _check(rc, "dq_decode_attention_paged_partial")
+
+
+def dq_token_record_stride(tables: Tables) -> int:
+    """Bytes between per-token records (C rounded up to 16)."""
+    return int(_lib.dq_token_record_stride(tables.handle))
+
+
+def dq_encode_kv_token(tables: Tables, kv, t0: int, t_cap: int, records, mean_q=None, mean_scale=None,
+                       status=None, stream=None):
+    """Append kv (bf16 [B, T_new, H, 128] on the GPU) at cache position t0 as
+    one stream per token over the H heads (tables built with head_dim 128 H).
+    records: uint8 [B, t_cap, stride]; keys also pass mean_q int8
+    [B, H, t_cap/128, 128] and mean_scale [B, H, t_cap/128]."""
+    import torch
+    _need(kv.is_cuda and kv.dtype == torch.bfloat16 and kv.dim() == 4 and kv.stride(3) == 1, "kv")
+    B, T, H, d = kv.shape
+    _need(d == 128 and tables.head_dim == 128 * H, "per-token streams need head_dim 128 and n = 128 H")
+    stride = dq_token_record_stride(tables)
+    _need(records.is_cuda and records.dtype == torch.uint8 and records.is_contiguous()
+          and tuple(records.shape) == (B, t_cap, stride), "records shape/dtype")
+    if mean_q is not None:
+        _need(mean_scale is not None, "mean_q and mean_scale go together")
+        _need(mean_q.dtype == torch.int8 and mean_q.is_contiguous()
+              and tuple(mean_q.shape) == (B, H, t_cap // DQ_MEAN_WINDOW, d), "mean_q shape/dtype")
+        _need(mean_scale.element_size() == 2 and mean_scale.is_contiguous()
+              and tuple(mean_scale.shape) == (B, H, t_cap // DQ_MEAN_WINDOW), "mean_scale shape/dtype")
+    rc = _lib.dq_encode_kv_token(tables.handle, _ptr(kv), kv.stride(0), kv.stride(1), kv.stride(2), B, H,
+                                 int(t0), T, int(t_cap), _ptr(records), _ptr(mean_q), _ptr(mean_scale),
+                                 _ptr(status), _stream(stream))
+    _check(rc, "dq_encode_kv_token")
+
+
+def dq_decode_attention_token_partial(k_tables: Tables, v_tables: Tables, q, k_records, mean_q, mean_scale,
+                                      v_records, seq_lens, workspace, softmax_scale=None, status=None,
+                                      stream=None):
+    """Split-K partials of one decode step over per-token records
+    (uint8 [B, t_cap, stride]); finish with dq_decode_attention_merge."""
+    import torch
+    _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3, "q")
+    B, Hq, d = q.shape
+    _need(k_records.dim() == 3 and k_records.shape[0] == B and k_records.is_contiguous()
+          and k_records.shape[2] == dq_token_record_stride(k_tables), "k_records")
+    t_cap = k_records.shape[1]
+    Hkv = k_tables.head_dim // 128
+    _need(tuple(v_records.shape) == (B, t_cap, dq_token_record_stride(v_tables)) and v_records.is_contiguous(),
+          "v_records")
+    _need(tuple(mean_q.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW, 128) and mean_q.is_contiguous(), "mean_q")
+    _need(tuple(mean_scale.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW) and mean_scale.is_contiguous(), "mean_scale")
+    _need(seq_lens.is_cuda and seq_lens.dtype == torch.int32 and seq_lens.numel() == B, "seq_lens")
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    rc = _lib.dq_decode_attention_token_partial(k_tables.handle, v_tables.handle, _ptr(q), B, Hq, Hkv,
+                                                _ptr(k_records), _ptr(mean_q), _ptr(mean_scale), _ptr(v_records),
+                                                _ptr(seq_lens), t_cap, ctypes.c_float(scale), _ptr(workspace),
+                                                workspace.numel() * workspace.element_size(), _ptr(status),
+                                                _stream(stream))
+    _check(rc, "dq_decode_attention_token_partial")
 
 
 def dq_bf16_decode_attention_partial(q, k, v, seq_lens, workspace, softmax_scale=None, stream=None):

@@ -29,10 +29,12 @@ namespace {
 constexpr int kEncStreams = 64;   // streams per workgroup
 constexpr int kEncWaves = 4;
 constexpr int kEncThreads = kEncWaves * kWave;
+constexpr int kD = 128;           // head_dim of the heads in a per-token stream
 
-// Unnormalized FWHT of n = 64 * VPL values; lane l holds elements
-// l + 64 k.  Stages run h = 1, 2, ..., n/2 as in the definition.
-template <int VPL>
+// Unnormalized FWHT of each group of 64 * SPAN values (a whole stream, or one
+// attention head of a per-token stream); lane l holds elements l + 64 k, group
+// k / SPAN.  Stages run h = 1, 2, ..., 32 SPAN as in the definition.
+template <int VPL, int SPAN = VPL>
 __device__ __forceinline__ void fwht_wave(double (&v)[VPL], int lane) {
 #pragma unroll
     for (int h = 1; h < kWave; h <<= 1) {
@@ -43,7 +45,7 @@ __device__ __forceinline__ void fwht_wave(double (&v)[VPL], int lane) {
         }
     }
 #pragma unroll
-    for (int s = 1; s < VPL; s <<= 1) {
+    for (int s = 1; s < SPAN; s <<= 1) {
 #pragma unroll
         for (int k = 0; k < VPL; ++k) {
             if (!(k & s)) {
@@ -78,6 +80,15 @@ __device__ __forceinline__ void load_rotated(const uint16_t* src, double (&v)[VP
 #pragma unroll
     for (int k = 0; k < VPL; ++k) v[k] = (double)bf16_to_f32(src[lane + kWave * k]);
     fwht_wave<VPL>(v, lane);
+}
+
+// Per-token stream (head_dim 128): head g's channels c = lane + 64 i are
+// elements k = 2 g + i, each head rotated on its own.
+template <int VPL>
+__device__ __forceinline__ void load_token_rotated(const uint16_t* src, int64_t sh, double (&v)[VPL], int lane) {
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) v[k] = (double)bf16_to_f32(src[(int64_t)(k / 2) * sh + lane + kWave * (k % 2)]);
+    fwht_wave<VPL, 2>(v, lane);
 }
 
 struct DriftCtx {
@@ -287,6 +298,7 @@ struct EncArgs {
     int64_t sb, st, sh;
     int H, t0, n_new, t_cap;
     Pages pg;                    // records and key means: contiguous or paged
+    int rec_stride;              // per-token records: bytes from one token to the next
     uint8_t* records;
     const int8_t* mean_q;        // NULL for values
     const uint16_t* mean_scale;
@@ -294,10 +306,26 @@ struct EncArgs {
 };
 
 // x = rotated stream of cache token t minus the dequantized window mean (keys).
-template <int VPL>
+// TOK: the stream spans every KV head (head g in elements 2 g, 2 g + 1).
+template <int VPL, bool TOK>
 __device__ __forceinline__ void stream_values(const EncArgs& a, int b, int h, int t,
                                               double (&x)[VPL], int lane) {
     const int64_t ti = t - a.t0;   // position in the input
+    if (TOK) {
+        load_token_rotated<VPL>(a.kv + (int64_t)b * a.sb + ti * a.st, a.sh, x, lane);
+        if (a.mean_q) {
+            const int nwin = a.t_cap / DQ_MEAN_WINDOW;
+#pragma unroll
+            for (int g = 0; g < VPL / 2; ++g) {
+                const int64_t wi = ((int64_t)b * a.H + g) * nwin + t / DQ_MEAN_WINDOW;
+                const double sc = (double)__half2float(__ushort_as_half(a.mean_scale[wi]));
+                const int8_t* mq = a.mean_q + wi * kD;
+                x[2 * g] = x[2 * g] - sc * (double)mq[lane];
+                x[2 * g + 1] = x[2 * g + 1] - sc * (double)mq[lane + kWave];
+            }
+        }
+        return;
+    }
     load_rotated<VPL>(a.kv + (int64_t)b * a.sb + ti * a.st + (int64_t)h * a.sh, x, lane);
     if (a.mean_q) {
         constexpr int n = kWave * VPL;
@@ -310,7 +338,7 @@ __device__ __forceinline__ void stream_values(const EncArgs& a, int b, int h, in
     }
 }
 
-template <int VPL, int MB>
+template <int VPL, int MB, bool TOK>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     constexpr int n = kWave * VPL;
     extern __shared__ __align__(16) uint8_t smem[];
@@ -359,7 +387,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
         for (int i = wave; i < active; i += kEncWaves) {
             if (pass > 0 && !s_flag[i]) continue;
             double x[VPL];
-            stream_values<VPL>(a, b, h, first + i, x, lane);
+            stream_values<VPL, TOK>(a, b, h, first + i, x, lane);
             uint16_t sb16, ob16;
             if (pass == 0) {
                 double mn = x[0], mx = x[0];
@@ -480,9 +508,15 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     }
     if (range_bad && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_RANGE);
 
-    // Write the records of the active streams: one contiguous span, or one
-    // record at a time through the block table.
-    if (!a.pg.bt) {
+    // Write the records of the active streams: one contiguous span, one record
+    // at a time through the block table, or per-token records at their stride
+    // (zero-padded).
+    if (TOK) {
+        for (int i = wave; i < active; i += kEncWaves) {
+            uint8_t* dst = a.records + ((int64_t)b * a.t_cap + first + i) * a.rec_stride;
+            for (int k = lane; k < a.rec_stride; k += kWave) dst[k] = k < C ? s_rec[i * C + k] : (uint8_t)0;
+        }
+    } else if (!a.pg.bt) {
         uint8_t* dst = a.records + ((int64_t)(b * a.H + h) * a.t_cap + first) * C;
         const int total = active * C;
         if ((((uintptr_t)dst) & 3) == 0 && (total & 3) == 0) {
@@ -513,12 +547,13 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
 int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int64_t sb, int64_t st, int64_t sh,
                   int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
                   uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status,
-                  hipStream_t stream) {
+                  hipStream_t stream, int token_stride) {
+    const bool tok = token_stride > 0;
     const int n = tab->cfg.head_dim;
     const int vpl = n / kWave;
     if (mean_q) {
         dim3 grid(n_new / DQ_MEAN_WINDOW, H, B);
-        switch (vpl) {
+        switch (tok ? kD / kWave : vpl) {
             case 1: key_mean_kernel<1><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
             case 2: key_mean_kernel<2><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
             case 4: key_mean_kernel<4><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
@@ -537,6 +572,7 @@ int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int
     a.n_new = n_new;
     a.t_cap = t_cap;
     a.pg = pg;
+    a.rec_stride = token_stride;
     a.records = records;
     a.mean_q = mean_q;
     a.mean_scale = mean_scale;
@@ -546,20 +582,37 @@ int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int
                         2 * sizeof(uint16_t) * kEncStreams + sizeof(int32_t) * kEncStreams +
                         2 * sizeof(uint32_t) * DQ_MAX_LEVELS +
                         (size_t)kEncStreams * n + (size_t)kEncStreams * a.ta.C;
-    dim3 grid((n_new + kEncStreams - 1) / kEncStreams, H, B);
-    // distortions held in registers for up to 8 levels (16 with two values per lane)
+    dim3 grid((n_new + kEncStreams - 1) / kEncStreams, tok ? 1 : H, B);
+    // distortions held in registers for up to 8 levels (16 with two values per
+    // lane); longer streams recompute them
     const int M = tab->cfg.levels;
-    const int mb = M <= 8 ? 8 : (M <= 16 && vpl <= 2) ? 16 : 0;
-#define DQ_ENC(V, MB) encode_kernel<V, MB><<<grid, kEncThreads, smem, stream>>>(a)
-    switch (vpl * 100 + mb) {
-        case 108: DQ_ENC(1, 8); break;
-        case 116: DQ_ENC(1, 16); break;
-        case 100: DQ_ENC(1, 0); break;
-        case 208: DQ_ENC(2, 8); break;
-        case 216: DQ_ENC(2, 16); break;
-        case 200: DQ_ENC(2, 0); break;
-        case 408: DQ_ENC(4, 8); break;
-        case 400: DQ_ENC(4, 0); break;
+    const int mb = vpl > 4 ? 0 : M <= 8 ? 8 : (M <= 16 && vpl <= 2) ? 16 : 0;
+    const void* fn = nullptr;
+#define DQ_ENC(V, MB, T)                                                                         \
+    do {                                                                                         \
+        fn = reinterpret_cast<const void*>(&encode_kernel<V, MB, T>);                            \
+        if (int rc = hip_check("hipFuncSetAttribute",                                            \
+                               hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, \
+                                                   (int)smem)))                                  \
+            return rc;                                                                           \
+        encode_kernel<V, MB, T><<<grid, kEncThreads, smem, stream>>>(a);                         \
+    } while (0)
+    switch ((tok ? 10000 : 0) + vpl * 100 + mb) {
+        case 108: DQ_ENC(1, 8, false); break;
+        case 116: DQ_ENC(1, 16, false); break;
+        case 100: DQ_ENC(1, 0, false); break;
+        case 208: DQ_ENC(2, 8, false); break;
+        case 216: DQ_ENC(2, 16, false); break;
+        case 200: DQ_ENC(2, 0, false); break;
+        case 408: DQ_ENC(4, 8, false); break;
+        case 400: DQ_ENC(4, 0, false); break;
+        case 10208: DQ_ENC(2, 8, true); break;
+        case 10216: DQ_ENC(2, 16, true); break;
+        case 10200: DQ_ENC(2, 0, true); break;
+        case 10408: DQ_ENC(4, 8, true); break;
+        case 10400: DQ_ENC(4, 0, true); break;
+        case 10800: DQ_ENC(8, 0, true); break;
+        case 11600: DQ_ENC(16, 0, true); break;
         default: return DQ_ERR_INVALID_ARG;
     }
 #undef DQ_ENC

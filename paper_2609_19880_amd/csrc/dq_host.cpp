@@ -293,11 +293,18 @@ void dq_free_tables(dq_tables* t) {
     delete t;
 }
 
+// token_stride > 0: per-token streams over the H heads (the table's n must be
+// 128 H), records at that stride; 0: per (token, head) streams.
 static int encode_kv(const dq_tables* t, const dq::Pages& pg, const uint16_t* kv, int64_t sb, int64_t st,
                      int64_t sh, int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
-                     uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status, void* stream) {
+                     uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status, void* stream,
+                     int32_t token_stride = 0) {
     if (!table_args_ok(t) || !kv || !records) return DQ_ERR_INVALID_ARG;
-    if (t->cfg.head_dim > 256) return DQ_ERR_INVALID_ARG;
+    if (token_stride > 0) {
+        if ((H != 1 && H != 2 && H != 4 && H != 8) || t->cfg.head_dim != 128 * H) return DQ_ERR_INVALID_ARG;
+    } else if (t->cfg.head_dim > 256) {
+        return DQ_ERR_INVALID_ARG;
+    }
     if (B < 0 || H <= 0 || t0 < 0 || n_new < 0 || t_cap <= 0 || t0 + n_new > t_cap)
         return DQ_ERR_INVALID_ARG;
     if (B > 65535 || H > 65535) return DQ_ERR_INVALID_ARG;   // grid dimensions
@@ -308,7 +315,7 @@ static int encode_kv(const dq_tables* t, const dq::Pages& pg, const uint16_t* kv
         return DQ_ERR_INVALID_ARG;
     if (B == 0 || n_new == 0) return DQ_OK;
     return dq::launch_encode(t, pg, kv, sb, st, sh, B, H, t0, n_new, t_cap, records, mean_q,
-                             mean_scale, status, static_cast<hipStream_t>(stream));
+                             mean_scale, status, static_cast<hipStream_t>(stream), token_stride);
 }
 
 static const dq::Pages kContiguous{nullptr, 0, 0, 0};
@@ -345,6 +352,21 @@ int dq_encode_kv_paged(const dq_tables* t, const uint16_t* kv, int64_t sb, int64
     if (int rc = paging(block_table, max_pages, page_tokens, num_pages, &pg, &t_cap)) return rc;
     return encode_kv(t, pg, kv, sb, st, sh, B, H, t0, n_new, t_cap, record_pool, mean_q_pool, mean_scale_pool,
                      status, stream);
+}
+
+int32_t dq_token_record_stride(const dq_tables* t) {
+    if (!table_args_ok(t)) return 0;
+    return (t->cfg.record_bytes + 15) & ~15;
+}
+
+int dq_encode_kv_token(const dq_tables* t, const uint16_t* kv, int64_t sb, int64_t st, int64_t sh,
+                       int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
+                       uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status,
+                       void* stream) {
+    const int32_t stride = dq_token_record_stride(t);
+    if (stride <= 0) return DQ_ERR_INVALID_ARG;
+    return encode_kv(t, kContiguous, kv, sb, st, sh, B, H, t0, n_new, t_cap, records, mean_q, mean_scale,
+                     status, stream, stride);
 }
 
 size_t dq_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d) {
@@ -384,6 +406,24 @@ int dq_decode_attention_partial(const dq_tables* tk, const dq_tables* tv, const 
                                 size_t ws_bytes, uint32_t* status, void* stream) {
     return attention_partial(tk, tv, kContiguous, q, B, Hq, Hkv, krec, kmq, kms, vrec, seq_lens, t_cap, scale,
                              ws, ws_bytes, status, stream);
+}
+
+int dq_decode_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
+                                      int32_t Hq, int32_t Hkv, const uint8_t* k_records, const int8_t* k_mean_q,
+                                      const uint16_t* k_mean_scale, const uint8_t* v_records,
+                                      const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
+                                      size_t ws_bytes, uint32_t* status, void* stream) {
+    if (!table_args_ok(tk) || !table_args_ok(tv)) return DQ_ERR_INVALID_ARG;
+    if (Hkv != 1 && Hkv != 2 && Hkv != 4 && Hkv != 8) return DQ_ERR_INVALID_ARG;
+    if (tk->cfg.head_dim != 128 * Hkv || tv->cfg.head_dim != 128 * Hkv) return DQ_ERR_INVALID_ARG;
+    if (B <= 0 || B > 65535 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 4) return DQ_ERR_INVALID_ARG;
+    if (t_cap <= 0 || t_cap % DQ_MEAN_WINDOW) return DQ_ERR_INVALID_ARG;
+    if (!q || !k_records || !k_mean_q || !k_mean_scale || !v_records || !seq_lens) return DQ_ERR_INVALID_ARG;
+    if (!std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128)) return DQ_ERR_WORKSPACE;
+    return dq::launch_attention_token_partial(tk, tv, q, B, Hq, Hkv, k_records, dq_token_record_stride(tk),
+                                              k_mean_q, k_mean_scale, v_records, dq_token_record_stride(tv),
+                                              seq_lens, t_cap, scale, ws, status, static_cast<hipStream_t>(stream));
 }
 
 int dq_decode_attention_paged_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,

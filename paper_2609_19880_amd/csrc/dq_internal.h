@@ -126,10 +126,12 @@ inline int hip_check(const char* where, hipError_t err) {
 }
 
 // Launchers implemented in the .hip files.  Return DQ_OK or DQ_ERR_HIP.
+// token_stride > 0: one stream per token over the H heads (head_dim 128, the
+// table's n = 128 H), records [B][t_cap][token_stride]; 0: per (token, head).
 int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int64_t sb, int64_t st,
                   int64_t sh, int32_t B, int32_t H, int32_t t0, int32_t n_new,
                   int32_t t_cap, uint8_t* records, int8_t* mean_q,
-                  uint16_t* mean_scale, uint32_t* status, hipStream_t stream);
+                  uint16_t* mean_scale, uint32_t* status, hipStream_t stream, int token_stride = 0);
 
 int launch_decode_symbols(const dq_tables* tab, const uint8_t* records, int64_t n_streams,
                           uint8_t* sym, uint16_t* header, uint32_t* status,
@@ -142,6 +144,15 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pag
                              const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                              const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
                              uint32_t* status, hipStream_t stream);
+
+// Per-token streams over Hkv heads (table n = 128 Hkv, G = Hq / Hkv <= 4),
+// records [B][t_cap][stride]; same workspace as launch_attention_partial.
+int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
+                                   int32_t Hq, int32_t Hkv, const uint8_t* krec, int32_t k_stride,
+                                   const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
+                                   int32_t v_stride, const int32_t* seq_lens, int32_t t_cap, float scale,
+                                   void* ws, uint32_t* status, hipStream_t stream);
+int32_t token_chunk(int32_t B, int32_t t_cap);
 
 int launch_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
                               const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,

@@ -1,0 +1,526 @@
+// Decode attention over per-token streams: one rANS stream of n = 128 H_kv
+// values per token spanning every KV head (the paper's default grouping,
+// Sec. 4.1 and Sec. 5.1), decoded once and consumed one KV head at a time as
+// Sec. 4.5 ("Decoding") describes.
+//
+// Work split.  One workgroup per (context chunk, sequence); each wavefront
+// takes 64-token tiles, one token per lane, and runs the token's key and
+// value streams as two interleaved rANS chains (Alg. 2).  After every 128
+// steps (one KV head) the head's G query heads get their q . k products
+// (Eq. fold-key, on the matrix cores as the levels appear), the online
+// softmax update and P . v (Eq. fold-value); the chains then continue into
+// the next head with their state.  All query heads' accumulators live in the
+// wavefront: two channels per lane per query head.
+//
+// Record bytes.  A record (C bytes at a 16-byte-aligned stride) is read in
+// 16-byte chunks into a per-lane ring of 16 dwords in LDS, laid out
+// [dword row][lane] so that every lane stays in its own bank; a seventeenth
+// row repeats row 0 so that two consecutive dwords are always rows r, r + 1.
+// A decode step reads the two dwords holding its byte position and takes the
+// next 16 bits with a funnel shift and a byte permute.  Every 8 steps a lane
+// whose ring would run short writes its next chunk (held in registers since
+// the previous refill) and loads the one after: 8 steps read at most 16
+// bytes, so one chunk per check keeps the ring ahead of the pointer, and four
+// chunks are never overwritten while still needed.  Ring rows are masked, so
+// a corrupt stream reads garbage inside its ring, never outside; it is
+// flagged at the end (state != L or pointer past the record).
+#include <math.h>
+
+#include <algorithm>
+
+#include "dq_attn.h"
+
+namespace dq {
+namespace {
+
+constexpr int kD = 128;
+constexpr int kTile = 64;
+constexpr int kVSlice = 64;
+constexpr int kVRow = 68;
+constexpr int kMaxLds = 160 * 1024;
+constexpr int kTokWaves = 8;              // wavefronts per workgroup at most
+constexpr int kTokMaxHeads = 8;           // KV heads per stream (n <= 1024)
+constexpr int kTokMaxChunk = 2048;        // bounds the per-window q . mu table
+constexpr int kRingRow = 4 * kTile;       // bytes per ring row: one dword per lane
+constexpr int kRingBytes = 17 * kRingRow; // 16 rows + the copy of row 0
+constexpr int kGroups = kD / 4;           // 4-step groups per head
+
+struct TokLayout {
+    int nw;
+    int lut_k, lut_v;   // 8-byte tables (the same offset when K and V share one)
+    int qlimb;          // [H_kv][32 groups][4 heads] x 16 B (three digit words)
+    int qscale, qsum;   // float [H_q]
+    int qmu;            // float [windows][H_q]
+    int waves;          // first wavefront region
+    int wave_stride;
+    int ring_k, ring_v; // per wavefront
+    int vtile;          // [64 channels][kVRow] bytes
+    int plimb;          // [4 heads][16 token quads] x 16 B
+    int total;
+};
+
+struct TokArgs {
+    TabArgs tk, tv;
+    const uint16_t* q;
+    int Hq, Hkv, G, t_cap, chunk, nchunks;
+    const uint8_t* krec;
+    const int8_t* kmq;
+    const uint16_t* kms;
+    const uint8_t* vrec;
+    int k_stride, v_stride;       // bytes per token record (multiples of 16)
+    const int32_t* seq_lens;
+    float scale_log2;             // softmax_scale * log2(e) / d
+    int32_t* ws_hdr;
+    float* ws_m;
+    float* ws_l;
+    float* ws_acc;
+    uint32_t* status;
+    TokLayout L;
+};
+
+// One step of Alg. 2, state X = 8 x as in the per-head kernel; pb is the
+// lane's bit position in its record (8 x byte position).
+//   dwords j = pb >> 5 and j + 1 come from ring rows j mod 16 and the next
+//   w = bytes (pos, pos + 1, ...) little-endian = (hi:lo) >> (pb mod 32)
+//   r = b_pos << 24 | b_pos+1 << 16
+template <uint32_t LUT_OFF>
+__device__ __forceinline__ uint32_t tstep(uint32_t& X, uint32_t& pb, uint32_t ring_lane, uint32_t mask8,
+                                          int p3) {
+    const uint64_t e = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
+    const uint32_t ex = (uint32_t)e, ey = (uint32_t)(e >> 32);
+    const uint32_t addr = (((pb >> 5) & 15u) << 8) + ring_lane;
+    const uint32_t lo = *LDS_PTR(const uint32_t, addr);
+    const uint32_t hi = *LDS_PTR(const uint32_t, addr + kRingRow);
+    const uint32_t w = __builtin_amdgcn_alignbit(hi, lo, pb);
+    const uint32_t r = __builtin_amdgcn_perm(w, w, 0x00010c0cu);
+    const uint32_t y = __umul24(ex, X >> p3) + ey;
+    const uint32_t sh = (uint32_t)__builtin_clz(y) & 24u;
+    const uint32_t q = r >> (sh ^ 29u);
+    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(y), "v"(sh), "v"(q));
+    pb += sh;
+    return ex;
+}
+
+__device__ __forceinline__ uint4 load_chunk(const uint8_t* rec, uint32_t c, uint32_t last) {
+    return *reinterpret_cast<const uint4*>(rec + 16u * min(c, last));
+}
+
+// Chunk c of the record into ring rows 4 (c mod 4) .. + 3 (and row 16 for c
+// mod 4 = 0).
+__device__ __forceinline__ void put_chunk(uint32_t ring_lane, uint32_t c, const uint4& v) {
+    const uint32_t a = ring_lane + (c & 3u) * 4u * kRingRow;
+    *LDS_PTR(uint32_t, a) = v.x;
+    *LDS_PTR(uint32_t, a + kRingRow) = v.y;
+    *LDS_PTR(uint32_t, a + 2 * kRingRow) = v.z;
+    *LDS_PTR(uint32_t, a + 3 * kRingRow) = v.w;
+    if ((c & 3u) == 0) *LDS_PTR(uint32_t, ring_lane + 16 * kRingRow) = v.x;
+}
+
+// Keeps 16 nc >= pos + 22: the next 8 steps read at most bytes < pos + 22.
+__device__ __forceinline__ void refill(uint32_t pb, uint32_t& nc, uint4& next, uint32_t ring_lane,
+                                       const uint8_t* rec, uint32_t last) {
+    if ((nc << 7) < pb + 176u) {
+        put_chunk(ring_lane, nc, next);
+        ++nc;
+        next = load_chunk(rec, nc, last);
+    }
+}
+
+// Accumulators of query-head slot r of KV head h, channel slice s: element h
+// of the vector acc[s][r], addressed with the wavefront-uniform h (indirect
+// register access; plain arrays would go to scratch memory).
+typedef float v8f __attribute__((ext_vector_type(kTokMaxHeads)));
+
+__device__ __forceinline__ float lane_get(float v, int i) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
+}
+__device__ __forceinline__ float lane_set(float v, int i, float x, int lane) { return lane == i ? x : v; }
+
+template <uint32_t LUTV>
+__global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a) {
+    extern __shared__ __align__(16) uint8_t smem[];
+    const TokLayout& L = a.L;
+    const int G = a.G, Hkv = a.Hkv, Hq = a.Hq;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int nthr = L.nw * kWave;
+    const int c = blockIdx.x, b = blockIdx.z;
+    if ((c | b) == 0 && tid == 0) {
+        a.ws_hdr[0] = a.chunk;
+        a.ws_hdr[1] = a.nchunks;
+        a.ws_hdr[2] = 0;          // set by the residual kernel when it runs
+    }
+    const int T = min(a.seq_lens[b], a.t_cap);
+    const int start = c * a.chunk;
+    if (start >= T) return;   // the merge ignores chunks past the length
+
+    // ---- prologue: tables, rotated queries, their digits, q . mu per window
+    {
+        const int Pk = 1 << a.tk.p, Pv = 1 << a.tv.p;
+        uint2* lk = reinterpret_cast<uint2*>(smem + L.lut_k);
+        for (int i = tid; i < Pk; i += nthr) lk[i] = a.tk.t.lut64[i];
+        if (LUTV != 0) {
+            uint2* lv = reinterpret_cast<uint2*>(smem + LUTV);
+            for (int i = tid; i < Pv; i += nthr) lv[i] = a.tv.t.lut64[i];
+        }
+    }
+    float* qt = reinterpret_cast<float*>(smem + L.waves);          // [H_q][d] scratch
+    float* qscale = reinterpret_cast<float*>(smem + L.qscale);
+    float* qsum = reinterpret_cast<float*>(smem + L.qsum);
+    float* qmu = reinterpret_cast<float*>(smem + L.qmu);
+    uint8_t* qlimb = smem + L.qlimb;
+    for (int i = tid; i < Hq * kD; i += nthr) qt[i] = bf16_to_f32(a.q[(int64_t)b * Hq * kD + i]);
+    __syncthreads();
+    for (int hh = 1; hh < kD; hh <<= 1) {
+        for (int i = tid; i < Hq * (kD / 2); i += nthr) {
+            const int g = i / (kD / 2), r = i % (kD / 2);
+            const int lo = (r / hh) * 2 * hh + (r % hh);
+            const float x0 = qt[g * kD + lo], x1 = qt[g * kD + lo + hh];
+            qt[g * kD + lo] = x0 + x1;
+            qt[g * kD + lo + hh] = x0 - x1;
+        }
+        __syncthreads();
+    }
+    for (int g = tid; g < Hq; g += nthr) {
+        float mx = 0.f, sm = 0.f;
+        for (int j = 0; j < kD; ++j) {
+            mx = fmaxf(mx, fabsf(qt[g * kD + j]));
+            sm += qt[g * kD + j];
+        }
+        qscale[g] = mx * (1.0f / 4194304.0f);
+        qsum[g] = sm;
+    }
+    __syncthreads();
+    // digits of head slot r of KV head h at ((h * 32 + j / 4) * 4 + r) * 16 + j % 4 (+4, +8)
+    for (int i = tid; i < Hkv * 4 * kD; i += nthr) {
+        const int h = i / (4 * kD), r = (i / kD) % 4, j = i % kD;
+        const int g = h * G + r;
+        int v = 0;
+        if (r < G && qscale[g] > 0.f) {
+            v = (int)rintf(qt[g * kD + j] / qscale[g]);
+            v = max(-4194304, min(4194304, v));
+        }
+        int d0, d1, d2;
+        digits3(v, d0, d1, d2);
+        uint8_t* dst = qlimb + ((h * kGroups + j / 4) * 4 + r) * 16 + (j % 4);
+        dst[0] = (uint8_t)d0;
+        dst[4] = (uint8_t)d1;
+        dst[8] = (uint8_t)d2;
+        dst[12] = 0;
+    }
+    const int nwin_total = a.t_cap / DQ_MEAN_WINDOW;
+    const int w0 = start / DQ_MEAN_WINDOW;
+    const int nwin = (a.chunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1;
+    for (int i = tid; i < nwin * Hq; i += nthr) {
+        const int wi = i / Hq, g = i % Hq;
+        float s = 0.f;
+        if (w0 + wi < nwin_total) {
+            const int64_t widx = ((int64_t)b * Hkv + g / G) * nwin_total + w0 + wi;
+            const float sc = half_bits_to_f32(a.kms[widx]);
+            const int8_t* mq = a.kmq + widx * kD;
+            for (int j = 0; j < kD; ++j) s += qt[g * kD + j] * (sc * (float)mq[j]);
+        }
+        qmu[i] = s;
+    }
+    __syncthreads();
+
+    // ---- per-wavefront state
+    uint8_t* wreg = smem + L.waves + wave * L.wave_stride;
+    const uint32_t ring_k = (uint32_t)(L.waves + wave * L.wave_stride + L.ring_k) + 4u * lane;
+    const uint32_t ring_v = (uint32_t)(L.waves + wave * L.wave_stride + L.ring_v) + 4u * lane;
+    uint8_t* vtile = wreg + L.vtile;
+    uint8_t* plimb = wreg + L.plimb;
+    const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
+    const uint32_t sel2 = (lane & 2) ? 0x03020706u : 0x05040100u;
+    const int pk3 = a.tk.p + 3, pv3 = a.tv.p + 3;
+    const uint32_t mask8k = ((1u << a.tk.p) - 1u) << 3, mask8v = ((1u << a.tv.p) - 1u) << 3;
+    const uint32_t last_k = (uint32_t)(a.k_stride / 16 - 1), last_v = (uint32_t)(a.v_stride / 16 - 1);
+    const uint32_t endk = 8u * (uint32_t)a.tk.C, endv = 8u * (uint32_t)a.tv.C;
+
+    // running softmax state of query-head slot 4 h + r in lane 4 h + r
+    float m_vec = -INFINITY, l_vec = 0.f, o_vec = 0.f;
+    v8f acc[2][4];
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[s][r] = v8f{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    bool corrupt = false;
+    const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
+
+    for (int tile = wave; tile < ntiles; tile += L.nw) {
+        const int t_base = start + tile * kTile;
+        const int t = t_base + lane;               // < t_cap: tiles lie inside the capacity
+        const bool valid = t < T;
+        const uint8_t* kr = a.krec + ((int64_t)b * a.t_cap + t) * a.k_stride;
+        const uint8_t* vr = a.vrec + ((int64_t)b * a.t_cap + t) * a.v_stride;
+        const uint4 k0 = load_chunk(kr, 0, last_k), k1 = load_chunk(kr, 1, last_k);
+        const uint4 v0 = load_chunk(vr, 0, last_v), v1 = load_chunk(vr, 1, last_v);
+        uint4 nk = load_chunk(kr, 2, last_k), nv = load_chunk(vr, 2, last_v);
+        wave_sync();   // the previous tile is done with the rings
+        put_chunk(ring_k, 0, k0);
+        put_chunk(ring_k, 1, k1);
+        put_chunk(ring_v, 0, v0);
+        put_chunk(ring_v, 1, v1);
+        uint32_t nck = 2, ncv = 2;
+        uint32_t xk = k0.y << 3, xv = v0.y << 3;
+        uint32_t pbk = 64, pbv = 64;                // payload starts at byte 8
+        const float sk = half_lo(k0.x), ok = half_hi(k0.x);
+        const float sv = half_lo(v0.x), ov = half_hi(v0.x);
+        const float* qm = qmu + ((t / DQ_MEAN_WINDOW) - w0) * Hq;
+        // the rings are read back by this lane only: order the reads after
+        // the writes (LDS keeps a wavefront's accesses in order)
+        asm volatile("" ::: "memory");
+
+        for (int h = 0; h < Hkv; ++h) {
+            v4i dk[3] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
+            uint32_t vlev[kGroups];
+            const uint8_t* qh = qlimb + (h * kGroups * 4 + (lane & 3)) * 16;
+#pragma unroll
+            for (int grp = 0; grp < kGroups; ++grp) {
+                const uint32_t k0s = tstep<0>(xk, pbk, ring_k, mask8k, pk3);
+                const uint32_t v0s = tstep<LUTV>(xv, pbv, ring_v, mask8v, pv3);
+                const uint32_t k1s = tstep<0>(xk, pbk, ring_k, mask8k, pk3);
+                const uint32_t v1s = tstep<LUTV>(xv, pbv, ring_v, mask8v, pv3);
+                const uint32_t k2s = tstep<0>(xk, pbk, ring_k, mask8k, pk3);
+                const uint32_t v2s = tstep<LUTV>(xv, pbv, ring_v, mask8v, pv3);
+                const uint32_t k3s = tstep<0>(xk, pbk, ring_k, mask8k, pk3);
+                const uint32_t v3s = tstep<LUTV>(xv, pbv, ring_v, mask8v, pv3);
+                const uint32_t lk = pack4(k0s, k1s, k2s, k3s);
+                vlev[grp] = pack4(v0s, v1s, v2s, v3s);
+                asm volatile("" : "+v"(vlev[grp]));
+                const uint4 ql = *reinterpret_cast<const uint4*>(qh + grp * 4 * 16);
+                dk[0] = mfma(ql.x, lk, dk[0]);
+                dk[1] = mfma(ql.y, lk, dk[1]);
+                dk[2] = mfma(ql.z, lk, dk[2]);
+                if (grp & 1) {
+                    refill(pbk, nck, nk, ring_k, kr, last_k);
+                    refill(pbv, ncv, nv, ring_v, vr, last_v);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+
+            // ---- scores of the head's query heads and the online softmax
+            float corr[4], pscale[4];
+            int pint[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bool live = r < G;
+                const int g = live ? h * G + r : 0;       // slots past G take no query head
+                const int slot = h * 4 + r;
+                const float dot = combine(dk[0], dk[1], dk[2], r) * qscale[g];
+                const float score = (valid && live) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
+                const float tmax = wave_max(score);
+                const float m_old = lane_get(m_vec, slot);
+                const float mn = fmaxf(m_old, tmax);
+                corr[r] = (m_old == -INFINITY || mn == -INFINITY) ? (m_old == mn ? 1.f : 0.f)
+                                                                  : __builtin_amdgcn_exp2f(m_old - mn);
+                const float p = (score == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(score - mn);
+                const float lt = wave_sum_f32(p);
+                const float ot = wave_sum_f32(p * ov);
+                m_vec = lane_set(m_vec, slot, mn, lane);
+                l_vec = lane_set(l_vec, slot, lane_get(l_vec, slot) * corr[r] + lt, lane);
+                o_vec = lane_set(o_vec, slot, lane_get(o_vec, slot) * corr[r] + ot, lane);
+                const float pw = p * sv;                 // >= 0: scales are non-negative
+                const float smax = wave_max(pw);
+                pscale[r] = smax * (1.0f / 4194304.0f);
+                const float inv = smax > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax) : 0.f;
+                pint[r] = min(4194304, (int)rintf(pw * inv));
+            }
+            {
+                int dd[4][3];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) digits3(pint[r], dd[r][0], dd[r][1], dd[r][2]);
+                uint32_t wt[3];
+#pragma unroll
+                for (int d = 0; d < 3; ++d) {
+                    const uint32_t w = ((uint32_t)dd[0][d] & 0xFFu) | (((uint32_t)dd[1][d] & 0xFFu) << 8) |
+                                       (((uint32_t)dd[2][d] & 0xFFu) << 16) | ((uint32_t)dd[3][d] << 24);
+                    wt[d] = quad_transpose(w, sel1, sel2);
+                }
+                *reinterpret_cast<uint4*>(plimb + ((lane & 3) * (kTile / 4) + (lane >> 2)) * 16) =
+                    uint4{wt[0], wt[1], wt[2], 0u};
+            }
+
+            // ---- P . v over two slices of 64 channels
+            float pv[2][4];
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+                wave_sync();   // the previous slice / head is no longer read
+#pragma unroll
+                for (int grp = 0; grp < kVSlice / 4; ++grp) {
+                    const uint32_t wt = quad_transpose(vlev[s * (kVSlice / 4) + grp], sel1, sel2);
+                    *reinterpret_cast<uint32_t*>(vtile + (grp * 4 + (lane & 3)) * kVRow + (lane >> 2) * 4) = wt;
+                }
+                wave_sync();
+                v4i dv[3] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
+#pragma unroll 4
+                for (int qd = 0; qd < kTile / 4; ++qd) {
+                    const uint32_t bv = *reinterpret_cast<const uint32_t*>(vtile + lane * kVRow + qd * 4);
+                    const uint4 pl = *reinterpret_cast<const uint4*>(plimb + ((lane & 3) * (kTile / 4) + qd) * 16);
+                    dv[0] = mfma(pl.x, bv, dv[0]);
+                    dv[1] = mfma(pl.y, bv, dv[1]);
+                    dv[2] = mfma(pl.z, bv, dv[2]);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) pv[s][r] = combine(dv[0], dv[1], dv[2], r) * pscale[r];
+            }
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc[s][r][h] = acc[s][r][h] * corr[r] + pv[s][r];
+        }
+        // every stream ends at x = L having read no byte past its record
+        corrupt |= valid && ((xk >> 3) != kRansL || pbk > endk);
+        corrupt |= valid && ((xv >> 3) != kRansL || pbv > endv);
+    }
+    if (__any(corrupt) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_CORRUPT);
+
+    // ---- merge the wavefronts of the workgroup, one KV head at a time
+    const int NC = a.nchunks;
+    float* mw = reinterpret_cast<float*>(smem);        // [nw][4]
+    float* lw = mw + L.nw * 4;                         // [nw][4]
+    float* aw = lw + L.nw * 4;                         // [nw][4][d]
+    for (int h = 0; h < Hkv; ++h) {
+        float av[2][4];
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) av[s][r] = acc[s][r][h];
+        __syncthreads();   // LDS free (first head) / previous head merged
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int slot = h * 4 + r;
+            const float mv = lane_get(m_vec, slot), lv = lane_get(l_vec, slot), ovt = lane_get(o_vec, slot);
+            if (lane == 0) {
+                mw[wave * 4 + r] = mv;
+                lw[wave * 4 + r] = lv;
+            }
+            aw[(wave * 4 + r) * kD + lane] = av[0][r] + ovt;
+            aw[(wave * 4 + r) * kD + kVSlice + lane] = av[1][r] + ovt;
+        }
+        __syncthreads();
+        for (int i = tid; i < G * kD; i += nthr) {
+            const int r = i / kD, j = i % kD;
+            float M = -INFINITY;
+            for (int w = 0; w < L.nw; ++w) M = fmaxf(M, mw[w * 4 + r]);
+            float acc = 0.f, l = 0.f;
+            for (int w = 0; w < L.nw; ++w) {
+                const float mv = mw[w * 4 + r];
+                if (mv == -INFINITY) continue;
+                const float e = exp2f(mv - M);
+                acc += aw[(w * 4 + r) * kD + j] * e;
+                l += lw[w * 4 + r] * e;
+            }
+            const int64_t slot = ((int64_t)b * Hq + h * G + r) * (NC + 1) + c;
+            a.ws_acc[slot * kD + j] = acc;
+            if (j == 0) {
+                a.ws_m[slot] = M;
+                a.ws_l[slot] = l;
+            }
+        }
+    }
+}
+
+TokLayout tok_layout(int pk, int pv, bool shared_lut, int Hq, int Hkv, int chunk, int nw) {
+    TokLayout L;
+    int off = 0;
+    L.lut_k = off;
+    off += 8 << pk;
+    L.lut_v = shared_lut ? L.lut_k : off;
+    if (!shared_lut) off += 8 << pv;
+    L.qlimb = off;
+    off += Hkv * kGroups * 4 * 16;
+    L.qscale = off;
+    off += 4 * Hq;
+    L.qsum = off;
+    off += 4 * Hq;
+    L.qmu = off;
+    off += 4 * Hq * ((chunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1);
+    off = (off + 15) & ~15;
+    L.waves = off;
+    L.ring_k = 0;
+    L.ring_v = kRingBytes;
+    L.vtile = 2 * kRingBytes;
+    L.plimb = L.vtile + kVSlice * kVRow;
+    L.wave_stride = (L.plimb + 4 * (kTile / 4) * 16 + 15) & ~15;
+    L.nw = nw;
+    // the prologue's query scratch and the epilogue's merge buffers use the
+    // wavefront regions
+    const int scratch = std::max(Hq * kD * 4, nw * 4 * (kD + 2) * 4);
+    L.total = L.waves + std::max(nw * L.wave_stride, scratch);
+    return L;
+}
+
+}  // namespace
+
+int32_t token_chunk(int32_t B, int32_t t_cap) {
+    const int64_t nc = std::max<int64_t>((t_cap + kTokMaxChunk - 1) / kTokMaxChunk, (cu_count() + B - 1) / B);
+    int chunk = (int)((t_cap + nc - 1) / nc);
+    chunk = ((chunk + kTile - 1) / kTile) * kTile;
+    chunk = std::max(chunk, kMinChunk);
+    return std::min(chunk, kTokMaxChunk);
+}
+
+int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
+                                   int32_t Hq, int32_t Hkv, const uint8_t* krec, int32_t k_stride,
+                                   const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
+                                   int32_t v_stride, const int32_t* seq_lens, int32_t t_cap, float scale,
+                                   void* ws, uint32_t* status, hipStream_t stream) {
+    TokArgs a;
+    a.tk = tab_args(tk);
+    a.tv = tab_args(tv);
+    const bool shared = tk == tv;
+    a.q = q;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.G = Hq / Hkv;
+    a.t_cap = t_cap;
+    a.chunk = token_chunk(B, t_cap);
+    a.nchunks = (t_cap + a.chunk - 1) / a.chunk;
+    a.krec = krec;
+    a.kmq = kmq;
+    a.kms = kms;
+    a.vrec = vrec;
+    a.k_stride = k_stride;
+    a.v_stride = v_stride;
+    a.seq_lens = seq_lens;
+    a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
+    const int64_t slots = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
+    a.ws_hdr = static_cast<int32_t*>(ws);
+    a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
+    a.ws_m = a.ws_acc + slots * kD;
+    a.ws_l = a.ws_m + slots;
+    a.status = status;
+    int nw = kTokWaves;
+    for (; nw > 0; --nw) {
+        a.L = tok_layout(a.tk.p, a.tv.p, shared, Hq, Hkv, a.chunk, nw);
+        if (a.L.total <= kMaxLds) break;
+    }
+    if (nw == 0) return DQ_ERR_INVALID_ARG;
+    const dim3 grid(a.nchunks, 1, B);
+    const void* fn;
+    const uint32_t lutv = shared ? 0u : (uint32_t)a.L.lut_v;
+    switch (lutv) {
+        case 0: fn = reinterpret_cast<const void*>(&attn_token_kernel<0>); break;
+        case 8u << 8: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 8>); break;
+        case 8u << 9: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 9>); break;
+        case 8u << 10: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 10>); break;
+        case 8u << 11: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 11>); break;
+        case 8u << 12: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 12>); break;
+        default: return DQ_ERR_INVALID_ARG;
+    }
+    if (int rc = hip_check("hipFuncSetAttribute",
+                           hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
+        return rc;
+    const size_t smem = (size_t)a.L.total;
+    switch (lutv) {
+        case 0: attn_token_kernel<0><<<grid, nw * kWave, smem, stream>>>(a); break;
+        case 8u << 8: attn_token_kernel<8u << 8><<<grid, nw * kWave, smem, stream>>>(a); break;
+        case 8u << 9: attn_token_kernel<8u << 9><<<grid, nw * kWave, smem, stream>>>(a); break;
+        case 8u << 10: attn_token_kernel<8u << 10><<<grid, nw * kWave, smem, stream>>>(a); break;
+        case 8u << 11: attn_token_kernel<8u << 11><<<grid, nw * kWave, smem, stream>>>(a); break;
+        default: attn_token_kernel<8u << 12><<<grid, nw * kWave, smem, stream>>>(a); break;
+    }
+    return hip_check("attn_token launch", hipGetLastError());
+}
+
+}  // namespace dq

@@ -1,0 +1,220 @@
+"""Per-token streams (one stream of 128 H values per token over all KV heads,
+the paper's default grouping) on the GPU against the oracle, through the C ABI.
+
+Bars as in test_gpu_parity.py: records (first C bytes, then zero padding to
+the 16-byte stride) and key means bit-exact with the oracle's
+encode_*_tokenwise; attention within 2e-3 (row-normalized) of the oracle's
+fp64 folded attention over the oracle's own records, which are uploaded for
+the attention checks.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import dq_workloads as wlmod
+from oracle import attention, kmean, kv, tables
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module")
+def dq():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_19880_amd as mod
+    return mod
+
+
+def _tabs(dq, n, levels, C, p=12, alpha=1.4):
+    return dq.Tables(n, levels, p, C, alpha), tables.build_tables(n, levels, p, alpha, C)
+
+
+def _rel_err(got, ref):
+    scale = np.max(np.abs(ref), axis=-1, keepdims=True)
+    return float(np.max(np.abs(got - ref) / np.maximum(scale, 1e-30)))
+
+
+def _strided(rec, stride):
+    B, T, C = rec.shape
+    out = np.zeros((B, T, stride), dtype=np.uint8)
+    out[:, :, :C] = rec
+    return out
+
+
+def _oracle_attention(q_bits, krec, mq, ms, vrec, otk, otv, lens, H, G):
+    n = 128 * H
+    ksym, ks, ko, okk = kv.decode_records(krec, otk, n)
+    vsym, vs, vo, okv = kv.decode_records(vrec, otv, n)
+    assert okk.all() and okv.all()
+    kh, ksh, koh = kv.tokenwise_as_heads(ksym, ks, ko, H)
+    vh, vsh, voh = kv.tokenwise_as_heads(vsym, vs, vo, H)
+    return attention.attention_folded(kv.bf16_to_f64(q_bits), kh, ksh, koh, kmean.dequantize_mean(mq, ms),
+                                      vh, vsh, voh, lens, G, 1 / np.sqrt(128))
+
+
+def _inputs(H, G, B, T, seed):
+    wl = wlmod.workload("b1_t4k_tok")
+    w2 = wlmod.Workload("tok", B, T, H * G, H, 4, wl.k, wl.v, streams="token")
+    return wlmod.make_k(w2, seed), wlmod.make_v(w2, seed), wlmod.make_q(w2, seed)
+
+
+@pytest.mark.parametrize("p", [12, 8])
+def test_token_encode_bit_exact(dq, p):
+    H, B, T = 8, 2, 256
+    gtk, otk = _tabs(dq, 1024, 8, 335, p)
+    gtv, otv = _tabs(dq, 1024, 6, 235, p)
+    k, v, _ = _inputs(H, 4, B, T, 31)
+    krec, mq, ms, _ = kv.encode_keys_tokenwise(wlmod.bf16_bits(k), otk)
+    vrec, _ = kv.encode_values_tokenwise(wlmod.bf16_bits(v), otv)
+    Sk, Sv = dq.dq_token_record_stride(gtk), dq.dq_token_record_stride(gtv)
+    assert (Sk, Sv) == (336, 240)
+    grk = torch.full((B, T, Sk), 0xAB, dtype=torch.uint8, device=DEV)     # pad bytes must be rewritten
+    grv = torch.full((B, T, Sv), 0xAB, dtype=torch.uint8, device=DEV)
+    gmq = torch.zeros((B, H, T // 128, 128), dtype=torch.int8, device=DEV)
+    gms = torch.zeros((B, H, T // 128), dtype=torch.int16, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    kd, vd = k.to(DEV), v.to(DEV)
+    # appends: keys in whole windows, values at a ragged offset
+    dq.dq_encode_kv_token(gtk, kd[:, :128], 0, T, grk, gmq, gms, status)
+    dq.dq_encode_kv_token(gtk, kd[:, 128:], 128, T, grk, gmq, gms, status)
+    dq.dq_encode_kv_token(gtv, vd[:, :100], 0, T, grv, None, None, status)
+    dq.dq_encode_kv_token(gtv, vd[:, 100:], 100, T, grv, None, None, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert np.array_equal(grk.cpu().numpy(), _strided(krec, Sk))
+    assert np.array_equal(grv.cpu().numpy(), _strided(vrec, Sv))
+    assert np.array_equal(gmq.cpu().numpy(), mq)
+    assert np.array_equal(gms.cpu().numpy().view(np.uint16), ms.view(np.uint16))
+
+
+@pytest.mark.parametrize("p", [12, 8])
+def test_token_attention_matches_oracle(dq, p):
+    H, G, B, T = 8, 4, 4, 384
+    gtk, otk = _tabs(dq, 1024, 8, 335, p)
+    gtv, otv = _tabs(dq, 1024, 6, 235, p)
+    k, v, q = _inputs(H, G, B, T, 32)
+    krec, mq, ms, _ = kv.encode_keys_tokenwise(wlmod.bf16_bits(k), otk)
+    vrec, _ = kv.encode_values_tokenwise(wlmod.bf16_bits(v), otv)
+    Sk, Sv = dq.dq_token_record_stride(gtk), dq.dq_token_record_stride(gtv)
+    lens = [T, 0, 65, 300]
+    grk = torch.from_numpy(_strided(krec, Sk)).to(DEV)
+    grv = torch.from_numpy(_strided(vrec, Sv)).to(DEV)
+    gmq = torch.from_numpy(mq).to(DEV)
+    gms = torch.from_numpy(ms.view(np.int16)).to(DEV)
+    seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, T), dtype=torch.uint8, device=DEV)
+    out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    qd = q.to(DEV)
+    dq.dq_decode_attention_token_partial(gtk, gtv, qd, grk, gmq, gms, grv, seq, ws, status=status)
+    dq.dq_decode_attention_merge(B, H * G, H, seq, T, ws, out)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    got = out.cpu().numpy().astype(np.float64)
+    ref = _oracle_attention(wlmod.bf16_bits(q), krec, mq, ms, vrec, otk, otv, lens, H, G)
+    assert np.all(got[1] == 0.0)
+    live = [0, 2, 3]
+    assert _rel_err(got[live], ref[live]) < TOL
+
+
+@pytest.mark.parametrize("H,G,Ck,Cv", [(8, 1, 335, 235), (4, 2, 170, 120), (2, 4, 88, 62), (1, 4, 44, 32)])
+def test_token_attention_heads_and_groups(dq, H, G, Ck, Cv):
+    """Streams of 128 H values for H = 8, 4, 2, 1 KV heads and 1, 2 or 4 query
+    heads per KV head; the GPU encoder fills the cache."""
+    B, T = 2, 256
+    n = 128 * H
+    gtk, otk = _tabs(dq, n, 8, Ck)
+    gtv, otv = _tabs(dq, n, 6, Cv)
+    assert otk.feasible and otv.feasible
+    k, v, q = _inputs(H, G, B, T, 33 + H)
+    krec, mq, ms, _ = kv.encode_keys_tokenwise(wlmod.bf16_bits(k), otk)
+    vrec, _ = kv.encode_values_tokenwise(wlmod.bf16_bits(v), otv)
+    Sk, Sv = dq.dq_token_record_stride(gtk), dq.dq_token_record_stride(gtv)
+    grk = torch.empty((B, T, Sk), dtype=torch.uint8, device=DEV)
+    grv = torch.empty((B, T, Sv), dtype=torch.uint8, device=DEV)
+    gmq = torch.empty((B, H, T // 128, 128), dtype=torch.int8, device=DEV)
+    gms = torch.empty((B, H, T // 128), dtype=torch.int16, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    dq.dq_encode_kv_token(gtk, k.to(DEV), 0, T, grk, gmq, gms, status)
+    dq.dq_encode_kv_token(gtv, v.to(DEV), 0, T, grv, None, None, status)
+    lens = [T, 129]
+    seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, T), dtype=torch.uint8, device=DEV)
+    out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
+    dq.dq_decode_attention_token_partial(gtk, gtv, q.to(DEV), grk, gmq, gms, grv, seq, ws, status=status)
+    dq.dq_decode_attention_merge(B, H * G, H, seq, T, ws, out)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert np.array_equal(grk.cpu().numpy(), _strided(krec, Sk))
+    assert np.array_equal(grv.cpu().numpy(), _strided(vrec, Sv))
+    ref = _oracle_attention(wlmod.bf16_bits(q), krec, mq, ms, vrec, otk, otv, lens, H, G)
+    assert _rel_err(out.cpu().numpy().astype(np.float64), ref) < TOL
+
+
+def test_token_attention_flags_corrupt_record_and_is_deterministic(dq):
+    H, G, B, T = 8, 4, 2, 256
+    gtk, otk = _tabs(dq, 1024, 8, 335)
+    gtv, otv = _tabs(dq, 1024, 6, 235)
+    k, v, q = _inputs(H, G, B, T, 34)
+    krec, mq, ms, _ = kv.encode_keys_tokenwise(wlmod.bf16_bits(k), otk)
+    vrec, _ = kv.encode_values_tokenwise(wlmod.bf16_bits(v), otv)
+    Sk, Sv = dq.dq_token_record_stride(gtk), dq.dq_token_record_stride(gtv)
+    grk = torch.from_numpy(_strided(krec, Sk)).to(DEV)
+    grv = torch.from_numpy(_strided(vrec, Sv)).to(DEV)
+    gmq = torch.from_numpy(mq).to(DEV)
+    gms = torch.from_numpy(ms.view(np.int16)).to(DEV)
+    seq = torch.tensor([T, 200], dtype=torch.int32, device=DEV)
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, T), dtype=torch.uint8, device=DEV)
+    outs = []
+    for _ in range(2):
+        out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
+        status = torch.zeros(1, dtype=torch.int32, device=DEV)
+        dq.dq_decode_attention_token_partial(gtk, gtv, q.to(DEV), grk, gmq, gms, grv, seq, ws, status=status)
+        dq.dq_decode_attention_merge(B, H * G, H, seq, T, ws, out)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        outs.append(out.cpu())
+    assert torch.equal(outs[0], outs[1])
+    # a record past the length is never read as a token: still clean
+    bad = grv.clone()
+    bad[1, 230, 4:8] = 0
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    dq.dq_decode_attention_token_partial(gtk, gtv, q.to(DEV), grk, gmq, gms, bad, seq, ws, status=status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    # a stream state that is not a valid end state inside the length: flagged,
+    # outputs still finite
+    bad[0, 17, 4:8] = 0
+    out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
+    dq.dq_decode_attention_token_partial(gtk, gtv, q.to(DEV), grk, gmq, gms, bad, seq, ws, status=status)
+    dq.dq_decode_attention_merge(B, H * G, H, seq, T, ws, out)
+    torch.cuda.synchronize()
+    assert int(status.item()) & dq.DQ_STATUS_CORRUPT
+    assert torch.isfinite(out).all()
+
+
+def test_token_entry_points_reject_bad_arguments(dq):
+    H, G, B, T = 8, 4, 1, 256
+    gtk, _ = _tabs(dq, 1024, 8, 335)
+    gtv, _ = _tabs(dq, 1024, 6, 235)
+    g128 = dq.Tables(128, 6, 12, 36, 1.4)
+    lib = dq._lib._lib
+    big = torch.zeros(1 << 22, dtype=torch.uint8, device=DEV)
+    p = big.data_ptr()
+
+    def attn(tk, tv, Hq=H * G, Hkv=H, t_cap=T, ws_bytes=1 << 22):
+        return lib.dq_decode_attention_token_partial(tk.handle, tv.handle, p, B, Hq, Hkv, p, p, p, p, p, t_cap,
+                                                     0.088, p, ws_bytes, p, None)
+
+    assert attn(g128, gtv) == dq.DQ_ERR_INVALID_ARG             # n must be 128 H
+    assert attn(gtk, gtv, Hq=64) == dq.DQ_ERR_INVALID_ARG       # G = 8 is not supported here
+    assert attn(gtk, gtv, Hq=30) == dq.DQ_ERR_INVALID_ARG       # not a multiple of H
+    assert attn(gtk, gtv, t_cap=200) == dq.DQ_ERR_INVALID_ARG
+    assert attn(gtk, gtv, ws_bytes=16) == dq.DQ_ERR_WORKSPACE
+    rc = lib.dq_encode_kv_token(gtk.handle, p, 0, 128 * H, 128, B, 4, 0, 128, T, p, p, p, p, None)
+    assert rc == dq.DQ_ERR_INVALID_ARG                          # 4 heads do not make n = 1024
+    assert lib.dq_token_record_stride(None) == 0
