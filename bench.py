@@ -1,7 +1,7 @@
 """Decode-attention throughput of the D-Quant hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps 100] [--warmup 10] [--workload b16_t32k]
-                    [--variant paper|literal] [--bpe 2.26] [--no-cpu-baseline]
+                    [--variant paper|literal] [--bpe 2.26] [--precision 12] [--no-cpu-baseline]
 
 A step is one decode-attention pass over the whole compressed cache of the
 workload: batch 16 x 32768 tokens x 8 KV heads (32 query heads, head_dim 128)
@@ -9,6 +9,10 @@ with 36-byte key and value records (2.25 bits per element).  The cache is
 filled once by the encoder (timed separately and reported), the raw K/V are
 freed, and the timed region holds only the decode-attention steps with the
 compressed cache resident in HBM.  Prints one JSON line.
+
+--workload b16_t32k_tok runs the paper's default grouping instead: one stream
+of 1024 values per token over the 8 KV heads (331 + 4 and 231 + 4 byte
+records, 8 / 6 levels), decoded by the per-token kernel.
 
 Other modes (for the profiles under profiles/):
     --copy-calibration BYTES   time a plain device copy of BYTES bytes
@@ -45,6 +49,7 @@ def _args():
     ap.add_argument("--workload", default="b16_t32k")
     ap.add_argument("--variant", default="paper", choices=["paper", "literal"])
     ap.add_argument("--bpe", type=float, default=None)
+    ap.add_argument("--precision", type=int, default=None, help="rANS precision p of both tables (default 12)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0)
@@ -112,6 +117,8 @@ def cpu_baseline(wl, seed: int):
     from oracle import attention, kmean, kv, tables
 
     T = wl.context
+    if wl.streams == "token":
+        return cpu_baseline_token(wl, seed)
     otk = tables.build_tables(wl.head_dim, wl.k.levels, wl.k.precision, wl.k.alpha, wl.k.record_bytes)
     otv = tables.build_tables(wl.head_dim, wl.v.levels, wl.v.precision, wl.v.alpha, wl.v.record_bytes)
     one = wl.with_context(T, batch=1)
@@ -141,6 +148,47 @@ def cpu_baseline(wl, seed: int):
                       f"step; single-threaded numpy on {_cpu_model()} ({os.cpu_count()} host cores)"}
 
 
+def cpu_baseline_token(wl, seed: int):
+    """The CPU oracle's decode attention over per-token streams, timed on the
+    first 4096 tokens of one sequence (all heads) and scaled to a whole step."""
+    import numpy as np
+    import dq_workloads as wlmod
+    from oracle import attention, kmean, kv, tables
+
+    n = wl.k.n
+    otk = tables.build_tables(n, wl.k.levels, wl.k.precision, wl.k.alpha, wl.k.record_bytes)
+    otv = tables.build_tables(n, wl.v.levels, wl.v.precision, wl.v.alpha, wl.v.record_bytes)
+    Ts = min(4096, wl.context)
+    one = wl.with_context(Ts, batch=1)
+    k = wlmod.bf16_bits(wlmod.make_k(one, seed + 100))
+    v = wlmod.bf16_bits(wlmod.make_v(one, seed + 100))
+    q = wlmod.bf16_bits(wlmod.make_q(one, seed + 100))
+    krec, mq, ms, _ = kv.encode_keys_tokenwise(k, otk)
+    vrec, _ = kv.encode_values_tokenwise(v, otv)
+    H = wl.kv_heads
+    from threadpoolctl import threadpool_limits
+    reps, t0 = 0, time.perf_counter()
+    with threadpool_limits(limits=1):
+        while True:
+            ksym, ks, ko, _ = kv.decode_records(krec, otk, n)
+            vsym, vs, vo, _ = kv.decode_records(vrec, otv, n)
+            kh, ksh, koh = kv.tokenwise_as_heads(ksym, ks, ko, H)
+            vh, vsh, voh = kv.tokenwise_as_heads(vsym, vs, vo, H)
+            attention.attention_folded(kv.bf16_to_f64(q), kh, ksh, koh, kmean.dequantize_mean(mq, ms),
+                                       vh, vsh, voh, [Ts], wl.gqa, 1 / np.sqrt(wl.head_dim))
+            reps += 1
+            if time.perf_counter() - t0 > 10.0:
+                break
+    per_sample = (time.perf_counter() - t0) / reps
+    scale = wl.batch * wl.context / Ts
+    return {"value": wl.batch * wl.context / (per_sample * scale), "unit": "tokens/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"oracle rANS decode of the per-token K and V records plus fp64 folded attention for "
+                      f"{Ts} tokens of one sequence (all {H} KV heads, {wl.q_heads} query heads); {reps} "
+                      f"repetitions, {per_sample:.3f} s each, scaled x{scale:.0f} to a step; single-threaded "
+                      f"numpy on {_cpu_model()} ({os.cpu_count()} host cores)"}
+
+
 def fill_cache(wl, seed: int, dev):
     """Tables and a compressed cache holding the whole workload, encoded one
     sequence at a time from the seeded generators (sequence b uses seed
@@ -150,18 +198,20 @@ def fill_cache(wl, seed: int, dev):
     import paper_2609_19880_amd as dq
 
     B, T, Hq, Hkv, d = wl.batch, wl.context, wl.q_heads, wl.kv_heads, wl.head_dim
-    tk = dq.Tables(d, wl.k.levels, wl.k.precision, wl.k.record_bytes, wl.k.alpha)
-    tv = dq.Tables(d, wl.v.levels, wl.v.precision, wl.v.record_bytes, wl.v.alpha)
-    cache = dq.KVCache(B, Hkv, Hq, T, tk, tv, device=dev)
+    tok = wl.streams == "token"
+    tk = dq.Tables(wl.k.n, wl.k.levels, wl.k.precision, wl.k.record_bytes, wl.k.alpha)
+    tv = dq.Tables(wl.v.n, wl.v.levels, wl.v.precision, wl.v.record_bytes, wl.v.alpha)
+    cache = (dq.TokenKVCache if tok else dq.KVCache)(B, Hkv, Hq, T, tk, tv, device=dev)
+    enc = dq.dq_encode_kv_token if tok else dq.dq_encode_kv
     enc_ms = 0.0
     for b in range(B):
         k = wlmod.make_k(wl, seed * 1000 + b, device=dev, batch=1)
         v = wlmod.make_v(wl, seed * 1000 + b, device=dev, batch=1)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        dq.dq_encode_kv(tk, k, 0, T, cache.k_records[b:b + 1], cache.k_mean_q[b:b + 1],
-                        cache.k_mean_scale[b:b + 1], cache.status)
-        dq.dq_encode_kv(tv, v, 0, T, cache.v_records[b:b + 1], None, None, cache.status)
+        enc(tk, k, 0, T, cache.k_records[b:b + 1], cache.k_mean_q[b:b + 1], cache.k_mean_scale[b:b + 1],
+            cache.status)
+        enc(tv, v, 0, T, cache.v_records[b:b + 1], None, None, cache.status)
         e1.record()
         torch.cuda.synchronize()
         enc_ms += e0.elapsed_time(e1)
@@ -183,15 +233,13 @@ def decode_step(tk, tv, cache, q, seq, out, ring=None):
     """One step: split-K partials over the whole cache (and the residual
     window's partial, if a ring is given), then the merge."""
     import paper_2609_19880_amd as dq
-    dq.dq_decode_attention_partial(tk, tv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
-                                   cache.v_records, seq, cache.workspace, status=cache.status)
+    cache.partial(q, seq)
     if ring is not None:
         dq.dq_decode_attention_residual(q, ring[0], ring[1], seq, ring[2], cache.t_cap, cache.workspace)
-    dq.dq_decode_attention_merge(cache.batch, cache.q_heads, cache.kv_heads, seq, cache.t_cap,
-                                 cache.workspace, out)
+    cache.merge(seq, out)
 
 
-def bf16_comparator(wl, a, q, seq, out, ws):
+def bf16_comparator(wl, a, q, seq, out, ws, alg_bytes):
     """The same decode step over an uncompressed BF16 cache of the same shape
     (random contents), timed like the compressed one."""
     import torch
@@ -221,7 +269,7 @@ def bf16_comparator(wl, a, q, seq, out, ws):
     return {"ms_per_step": sms, "tokens_per_s": B * T / (sms * 1e-3), "partial_ms": pms,
             "bytes_per_step": nbytes, "gbs": nbytes / (pms * 1e-3) / 1e9,
             "hbm_frac": nbytes / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-            "kv_bytes_ratio": nbytes / (B * T * Hkv * (wl.k.record_bytes + wl.v.record_bytes + (d + 2) / 128))}
+            "kv_bytes_ratio": nbytes / alg_bytes}
 
 
 def main():
@@ -241,6 +289,10 @@ def main():
 
     wl = wlmod.workload(a.workload, a.variant, a.bpe) if a.workload == "b1_t128k" else \
         wlmod.workload(a.workload, a.variant)
+    if a.precision is not None:
+        from dataclasses import replace
+        wl = replace(wl, k=replace(wl.k, precision=a.precision), v=replace(wl.v, precision=a.precision))
+    tok = wl.streams == "token"
     dev = torch.device("cuda")
     B, T, Hq, Hkv, d = wl.batch, wl.context, wl.q_heads, wl.kv_heads, wl.head_dim
     tk, tv, cache, enc_ms = fill_cache(wl, a.seed, dev)
@@ -274,13 +326,12 @@ def main():
     w0 = time.perf_counter()
     for i in range(a.steps):
         ev[4 * i].record()
-        dq.dq_decode_attention_partial(tk, tv, q, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
-                                       cache.v_records, seq, cache.workspace, status=cache.status)
+        cache.partial(q, seq)
         ev[4 * i + 1].record()
         if ring is not None:
             dq.dq_decode_attention_residual(q, ring[0], ring[1], seq, ring[2], T, cache.workspace)
         ev[4 * i + 2].record()
-        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, cache.workspace, out)
+        cache.merge(seq, out)
         ev[4 * i + 3].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -292,13 +343,19 @@ def main():
     step_ms = ev[0].elapsed_time(ev[-1]) / a.steps
 
     # algorithmic bytes of one partial launch: per (token, KV head) the two
-    # records plus the amortized INT8 key mean and its fp16 scale
-    per_unit = wl.k.record_bytes + wl.v.record_bytes + (d + 2) / 128.0
-    units = B * T * Hkv
+    # records plus the amortized INT8 key mean and its fp16 scale (per token
+    # for per-token streams: the two records plus the means of every head)
+    if tok:
+        per_unit = wl.k.record_bytes + wl.v.record_bytes + Hkv * (d + 2) / 128.0
+        units = B * T
+    else:
+        per_unit = wl.k.record_bytes + wl.v.record_bytes + (d + 2) / 128.0
+        units = B * T * Hkv
     alg_bytes = per_unit * units
+    n_symbols = 2 * B * T * Hkv * d
     achieved = alg_bytes / (partial_ms * 1e-3) / 1e9
     tokens_s = B * (T + a.residual) / (step_ms * 1e-3)
-    counters = counter_figures(wl.name, a.variant)
+    counters = None if a.precision not in (None, 12) else counter_figures(wl.name, a.variant)
     traffic = counters[0] if counters else None
 
     rec = {
@@ -315,34 +372,39 @@ def main():
         "dtype": "u8",
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: batch {B} x context {T}, {Hq} query / {Hkv} KV heads, "
-                               f"head_dim {d}, K {wl.k.record_bytes} B / V {wl.v.record_bytes} B records "
-                               f"({8 * wl.k.record_bytes / d:.2f}/{8 * wl.v.record_bytes / d:.2f} bits/elem), "
-                               f"{wl.k.levels}/{wl.v.levels} levels, alpha {wl.k.alpha}/{wl.v.alpha}, p 12",
+                               f"head_dim {d}, "
+                               + (f"one stream of {wl.k.n} values per token, " if tok else "")
+                               + f"K {wl.k.record_bytes} B / V {wl.v.record_bytes} B records "
+                               f"({wl.k.bits_per_elem:.2f}/{wl.v.bits_per_elem:.2f} bits/elem), "
+                               f"{wl.k.levels}/{wl.v.levels} levels, alpha {wl.k.alpha}/{wl.v.alpha}, "
+                               f"p {wl.k.precision}",
+                   "streams": "per token" if tok else "per (token, KV head)",
                    "variant": a.variant, "batch": B, "context": T, "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": d, "k_record_bytes": wl.k.record_bytes, "v_record_bytes": wl.v.record_bytes,
                    "k_levels": wl.k.levels, "v_levels": wl.v.levels, "residual_tokens": a.residual},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                     "kernel": "attn_partial_kernel", "alg_bytes_per_launch": alg_bytes,
+                     "kernel": "attn_token_kernel" if tok else "attn_partial_kernel",
+                     "alg_bytes_per_launch": alg_bytes,
                      "kernel_ms": partial_ms},
         "valu_issue": None if counters is None else {
             "bound": "alu", "achieved": counters[1] / (partial_ms * 1e-3) / 1e9,
             "peak": VALU_PEAK_GINST, "unit": "G wave64 VALU instructions/s",
             "frac": counters[1] / (partial_ms * 1e-3) / 1e9 / VALU_PEAK_GINST,
             "valu_insts_per_launch": counters[1],
-            "valu_lane_ops_per_symbol": counters[1] * 64 / (2 * units * d)},
+            "valu_lane_ops_per_symbol": counters[1] * 64 / n_symbols},
         "merge_ms": merge_ms,
         "residual": None if ring is None else {
             "tokens_per_sequence": a.residual, "ms": residual_ms,
             "gbs": B * Hkv * a.residual * d * 2 * 2 / (residual_ms * 1e-3) / 1e9},
         "wall_ms_per_step": wall * 1e3 / a.steps,
-        "symbols_per_s": 2 * units * d / (step_ms * 1e-3),
+        "symbols_per_s": n_symbols / (step_ms * 1e-3),
         "encode": {"ms": enc_ms, "tokens_per_s": B * T / (enc_ms * 1e-3),
                    "input_gbs": 2 * B * T * Hkv * d * 2 / (enc_ms * 1e-3) / 1e9},
     }
     if a.compare_bf16:
-        rec["bf16_decode"] = bf16_comparator(wl, a, q, seq, out, cache.workspace)
+        rec["bf16_decode"] = bf16_comparator(wl, a, q, seq, out, cache.workspace, alg_bytes)
     if not a.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, a.seed)
     print(json.dumps(rec))

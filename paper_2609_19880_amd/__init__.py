@@ -25,4 +25,4 @@ from ._lib import (  # noqa: F401
     dq_token_record_stride, dq_encode_kv_token, dq_decode_attention_token_partial,
     dq_decode_symbols, dq_strerror, dq_last_error, smallest_feasible_alpha,
 )
-from .cache import KVCache, StreamingKVCache  # noqa: F401
+from .cache import KVCache, StreamingKVCache, TokenKVCache  # noqa: F401

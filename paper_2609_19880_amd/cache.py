@@ -43,11 +43,68 @@ class KVCache:
                                  softmax_scale=softmax_scale, status=self.status)
         return out
 
+    def partial(self, q, seq_lens, softmax_scale=None):
+        """Split-K partials of one decode step into the workspace (finish with merge)."""
+        _lib.dq_decode_attention_partial(self.k_tables, self.v_tables, q, self.k_records, self.k_mean_q,
+                                         self.k_mean_scale, self.v_records, seq_lens, self.workspace,
+                                         softmax_scale=softmax_scale, status=self.status)
+
+    def merge(self, seq_lens, out):
+        _lib.dq_decode_attention_merge(self.batch, self.q_heads, self.kv_heads, seq_lens, self.t_cap,
+                                       self.workspace, out)
+
     def compressed_bytes(self, tokens: int) -> int:
         """Bytes of records and key means that cover `tokens` tokens of every sequence."""
         per_tok = self.k_tables.record_bytes + self.v_tables.record_bytes
         mean = (self.head_dim + 2) * ((tokens + _lib.DQ_MEAN_WINDOW - 1) // _lib.DQ_MEAN_WINDOW)
         return self.batch * self.kv_heads * (per_tok * tokens + mean)
+
+
+class TokenKVCache:
+    """Compressed cache with one stream per token over all KV heads (tables
+    built with head_dim 128 kv_heads): records [B, t_cap, stride] per tensor,
+    key means per head as in KVCache."""
+
+    def __init__(self, batch: int, kv_heads: int, q_heads: int, t_cap: int, k_tables, v_tables,
+                 device="cuda"):
+        if t_cap % _lib.DQ_MEAN_WINDOW:
+            raise ValueError("t_cap must be a multiple of 128")
+        if k_tables.head_dim != 128 * kv_heads or v_tables.head_dim != 128 * kv_heads:
+            raise ValueError("per-token tables need head_dim = 128 kv_heads")
+        d = 128
+        self.batch, self.kv_heads, self.q_heads, self.t_cap, self.head_dim = batch, kv_heads, q_heads, t_cap, d
+        self.k_tables, self.v_tables = k_tables, v_tables
+        nw = t_cap // _lib.DQ_MEAN_WINDOW
+        sk, sv = _lib.dq_token_record_stride(k_tables), _lib.dq_token_record_stride(v_tables)
+        self.k_records = torch.zeros((batch, t_cap, sk), dtype=torch.uint8, device=device)
+        self.v_records = torch.zeros((batch, t_cap, sv), dtype=torch.uint8, device=device)
+        self.k_mean_q = torch.zeros((batch, kv_heads, nw, d), dtype=torch.int8, device=device)
+        self.k_mean_scale = torch.zeros((batch, kv_heads, nw), dtype=torch.int16, device=device)
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+        self.workspace = torch.empty(
+            _lib.dq_decode_workspace_bytes(batch, q_heads, kv_heads, t_cap, d), dtype=torch.uint8, device=device)
+
+    def append(self, k, v, t0: int):
+        """Encode bf16 k, v [B, T_new, H, 128] as cache tokens [t0, t0 + T_new)."""
+        _lib.dq_encode_kv_token(self.k_tables, k, t0, self.t_cap, self.k_records, self.k_mean_q,
+                                self.k_mean_scale, self.status)
+        _lib.dq_encode_kv_token(self.v_tables, v, t0, self.t_cap, self.v_records, None, None, self.status)
+
+    def partial(self, q, seq_lens, softmax_scale=None):
+        _lib.dq_decode_attention_token_partial(self.k_tables, self.v_tables, q, self.k_records, self.k_mean_q,
+                                               self.k_mean_scale, self.v_records, seq_lens, self.workspace,
+                                               softmax_scale=softmax_scale, status=self.status)
+
+    def merge(self, seq_lens, out):
+        _lib.dq_decode_attention_merge(self.batch, self.q_heads, self.kv_heads, seq_lens, self.t_cap,
+                                       self.workspace, out)
+
+    def attend(self, q, seq_lens, out=None, softmax_scale=None):
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        self.partial(q, seq_lens, softmax_scale)
+        self.merge(seq_lens, out)
+        return out
 
 
 class StreamingKVCache:

@@ -13,17 +13,17 @@
 // wavefront: two channels per lane per query head.
 //
 // Record bytes.  A record (C bytes at a 16-byte-aligned stride) is read in
-// 16-byte chunks into a per-lane ring of 16 dwords in LDS, laid out
-// [dword row][lane] so that every lane stays in its own bank; a seventeenth
-// row repeats row 0 so that two consecutive dwords are always rows r, r + 1.
-// A decode step reads the two dwords holding its byte position and takes the
-// next 16 bits with a funnel shift and a byte permute.  Every 8 steps a lane
+// 8-byte chunks into a per-lane ring of 8 dwords in LDS, laid out
+// [dword row][lane] so that every lane stays in its own bank; a ninth row
+// repeats row 0 so that two consecutive dwords are always rows r, r + 1.  A
+// decode step reads the two dwords holding its byte position and takes the
+// next 16 bits with a funnel shift and a byte permute.  Every 4 steps a lane
 // whose ring would run short writes its next chunk (held in registers since
-// the previous refill) and loads the one after: 8 steps read at most 16
-// bytes, so one chunk per check keeps the ring ahead of the pointer, and four
-// chunks are never overwritten while still needed.  Ring rows are masked, so
-// a corrupt stream reads garbage inside its ring, never outside; it is
-// flagged at the end (state != L or pointer past the record).
+// the previous refill) and loads the one after: 4 steps read at most 8 bytes,
+// so one chunk per check keeps the ring 14 bytes ahead of the pointer, and
+// four chunks are never overwritten while still needed.  Ring rows are
+// masked, so a corrupt stream reads garbage inside its ring, never outside;
+// it is flagged at the end (state != L or pointer past the record).
 #include <math.h>
 
 #include <algorithm>
@@ -38,11 +38,12 @@ constexpr int kTile = 64;
 constexpr int kVSlice = 64;
 constexpr int kVRow = 68;
 constexpr int kMaxLds = 160 * 1024;
-constexpr int kTokWaves = 8;              // wavefronts per workgroup at most
+constexpr int kTokWaves = 12;             // wavefronts per workgroup at most
 constexpr int kTokMaxHeads = 8;           // KV heads per stream (n <= 1024)
 constexpr int kTokMaxChunk = 2048;        // bounds the per-window q . mu table
 constexpr int kRingRow = 4 * kTile;       // bytes per ring row: one dword per lane
-constexpr int kRingBytes = 17 * kRingRow; // 16 rows + the copy of row 0
+constexpr int kRingRows = 8;              // dwords of record bytes per lane
+constexpr int kRingBytes = (kRingRows + 1) * kRingRow;   // + the copy of row 0
 constexpr int kGroups = kD / 4;           // 4-step groups per head
 
 struct TokLayout {
@@ -78,58 +79,70 @@ struct TokArgs {
     TokLayout L;
 };
 
-// One step of Alg. 2, state X = 8 x as in the per-head kernel; pb is the
-// lane's bit position in its record (8 x byte position).
-//   dwords j = pb >> 5 and j + 1 come from ring rows j mod 16 and the next
-//   w = bytes (pos, pos + 1, ...) little-endian = (hi:lo) >> (pb mod 32)
-//   r = b_pos << 24 | b_pos+1 << 16
+// Two steps of Alg. 2 on one ring read, state X = 8 x as in the per-head
+// kernel; pb is the lane's bit position in its record (8 x byte position).
+//   dwords j = pb >> 5 and j + 1 come from ring rows j mod 8 and the next
+//   w = bytes pos .. pos + 3, little-endian = (hi:lo) >> (pb mod 32)
+//   r = b_pos << 24 | b_pos+1 << 16 (one byte permute)
+// Each step reads at most 2 bytes, so the second step's bytes are w >> sh of
+// the first.  Returns the two table words (levels in their top bytes).
 template <uint32_t LUT_OFF>
-__device__ __forceinline__ uint32_t tstep(uint32_t& X, uint32_t& pb, uint32_t ring_lane, uint32_t mask8,
-                                          int p3) {
-    const uint64_t e = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
-    const uint32_t ex = (uint32_t)e, ey = (uint32_t)(e >> 32);
-    const uint32_t addr = (((pb >> 5) & 15u) << 8) + ring_lane;
+__device__ __forceinline__ void tstep2(uint32_t& X, uint32_t& pb, uint32_t ring_lane, uint32_t mask8, int p3,
+                                       uint32_t& e0, uint32_t& e1) {
+    uint32_t addr;
+    asm("v_lshl_add_u32 %0, %1, 8, %2" : "=v"(addr) : "v"(__builtin_amdgcn_ubfe(pb, 5, 3)), "v"(ring_lane));
     const uint32_t lo = *LDS_PTR(const uint32_t, addr);
     const uint32_t hi = *LDS_PTR(const uint32_t, addr + kRingRow);
     const uint32_t w = __builtin_amdgcn_alignbit(hi, lo, pb);
-    const uint32_t r = __builtin_amdgcn_perm(w, w, 0x00010c0cu);
-    const uint32_t y = __umul24(ex, X >> p3) + ey;
-    const uint32_t sh = (uint32_t)__builtin_clz(y) & 24u;
-    const uint32_t q = r >> (sh ^ 29u);
-    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(y), "v"(sh), "v"(q));
-    pb += sh;
-    return ex;
+
+    const uint64_t ea = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
+    const uint32_t ya = __umul24((uint32_t)ea, X >> p3) + (uint32_t)(ea >> 32);
+    const uint32_t sha = (uint32_t)__builtin_clz(ya) & 24u;
+    const uint32_t qa = __builtin_amdgcn_perm(w, w, 0x00010c0cu) >> (sha ^ 29u);
+    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(ya), "v"(sha), "v"(qa));
+
+    const uint32_t wb = w >> sha;
+    const uint64_t eb = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
+    const uint32_t yb = __umul24((uint32_t)eb, X >> p3) + (uint32_t)(eb >> 32);
+    const uint32_t shb = (uint32_t)__builtin_clz(yb) & 24u;
+    const uint32_t qb = __builtin_amdgcn_perm(wb, wb, 0x00010c0cu) >> (shb ^ 29u);
+    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(yb), "v"(shb), "v"(qb));
+    asm("v_add3_u32 %0, %1, %2, %3" : "=v"(pb) : "v"(pb), "v"(sha), "v"(shb));
+    e0 = (uint32_t)ea;
+    e1 = (uint32_t)eb;
 }
 
-__device__ __forceinline__ uint4 load_chunk(const uint8_t* rec, uint32_t c, uint32_t last) {
-    return *reinterpret_cast<const uint4*>(rec + 16u * min(c, last));
+__device__ __forceinline__ uint2 load_chunk(const uint8_t* rec, uint32_t c, uint32_t last) {
+    return *reinterpret_cast<const uint2*>(rec + 8u * min(c, last));
 }
 
-// Chunk c of the record into ring rows 4 (c mod 4) .. + 3 (and row 16 for c
+// Chunk c of the record into ring rows 2 (c mod 4), + 1 (and row 8 for c
 // mod 4 = 0).
-__device__ __forceinline__ void put_chunk(uint32_t ring_lane, uint32_t c, const uint4& v) {
-    const uint32_t a = ring_lane + (c & 3u) * 4u * kRingRow;
+__device__ __forceinline__ void put_chunk(uint32_t ring_lane, uint32_t c, const uint2& v) {
+    const uint32_t a = ring_lane + (c & 3u) * 2u * kRingRow;
     *LDS_PTR(uint32_t, a) = v.x;
     *LDS_PTR(uint32_t, a + kRingRow) = v.y;
-    *LDS_PTR(uint32_t, a + 2 * kRingRow) = v.z;
-    *LDS_PTR(uint32_t, a + 3 * kRingRow) = v.w;
-    if ((c & 3u) == 0) *LDS_PTR(uint32_t, ring_lane + 16 * kRingRow) = v.x;
+    if ((c & 3u) == 0) *LDS_PTR(uint32_t, ring_lane + kRingRows * kRingRow) = v.x;
 }
 
-// Keeps 16 nc >= pos + 22: the next 8 steps read at most bytes < pos + 22.
-__device__ __forceinline__ void refill(uint32_t pb, uint32_t& nc, uint4& next, uint32_t ring_lane,
+// Keeps 8 nc >= pos + 14: the next 4 steps read bytes below pos + 14.  thr is
+// 8 (8 nc - 14) - 1 in bits, so the test is one compare.
+__device__ __forceinline__ void refill(uint32_t pb, uint32_t& nc, uint32_t& thr, uint2& next, uint32_t ring_lane,
                                        const uint8_t* rec, uint32_t last) {
-    if ((nc << 7) < pb + 176u) {
+    if (pb > thr) {
         put_chunk(ring_lane, nc, next);
         ++nc;
+        thr += 64u;
         next = load_chunk(rec, nc, last);
     }
 }
 
-// Accumulators of query-head slot r of KV head h, channel slice s: element h
-// of the vector acc[s][r], addressed with the wavefront-uniform h (indirect
-// register access; plain arrays would go to scratch memory).
+// Accumulators of query-head slot r, channel slice s: one vector acc[s][r]
+// over the KV heads.  The head loop is not unrolled, so the vectors are
+// rotated by one element per head and the current head is always element 0.
 typedef float v8f __attribute__((ext_vector_type(kTokMaxHeads)));
+
+__device__ __forceinline__ v8f rot1(const v8f& v) { return v8f{v[1], v[2], v[3], v[4], v[5], v[6], v[7], v[0]}; }
 
 __device__ __forceinline__ float lane_get(float v, int i) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
@@ -233,7 +246,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
     const uint32_t sel2 = (lane & 2) ? 0x03020706u : 0x05040100u;
     const int pk3 = a.tk.p + 3, pv3 = a.tv.p + 3;
     const uint32_t mask8k = ((1u << a.tk.p) - 1u) << 3, mask8v = ((1u << a.tv.p) - 1u) << 3;
-    const uint32_t last_k = (uint32_t)(a.k_stride / 16 - 1), last_v = (uint32_t)(a.v_stride / 16 - 1);
+    const uint32_t last_k = (uint32_t)(a.k_stride / 8 - 1), last_v = (uint32_t)(a.v_stride / 8 - 1);
     const uint32_t endk = 8u * (uint32_t)a.tk.C, endv = 8u * (uint32_t)a.tv.C;
 
     // running softmax state of query-head slot 4 h + r in lane 4 h + r
@@ -252,15 +265,19 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
         const bool valid = t < T;
         const uint8_t* kr = a.krec + ((int64_t)b * a.t_cap + t) * a.k_stride;
         const uint8_t* vr = a.vrec + ((int64_t)b * a.t_cap + t) * a.v_stride;
-        const uint4 k0 = load_chunk(kr, 0, last_k), k1 = load_chunk(kr, 1, last_k);
-        const uint4 v0 = load_chunk(vr, 0, last_v), v1 = load_chunk(vr, 1, last_v);
-        uint4 nk = load_chunk(kr, 2, last_k), nv = load_chunk(vr, 2, last_v);
+        // chunks 0..2 (bytes 0..23) cover the first 4 steps from byte 8
+        const uint2 k0 = load_chunk(kr, 0, last_k), k1 = load_chunk(kr, 1, last_k), k2 = load_chunk(kr, 2, last_k);
+        const uint2 v0 = load_chunk(vr, 0, last_v), v1 = load_chunk(vr, 1, last_v), v2 = load_chunk(vr, 2, last_v);
+        uint2 nk = load_chunk(kr, 3, last_k), nv = load_chunk(vr, 3, last_v);
         wave_sync();   // the previous tile is done with the rings
         put_chunk(ring_k, 0, k0);
         put_chunk(ring_k, 1, k1);
+        put_chunk(ring_k, 2, k2);
         put_chunk(ring_v, 0, v0);
         put_chunk(ring_v, 1, v1);
-        uint32_t nck = 2, ncv = 2;
+        put_chunk(ring_v, 2, v2);
+        uint32_t nck = 3, ncv = 3;
+        uint32_t thrk = 8u * (8u * 3u - 14u) - 1u, thrv = thrk;
         uint32_t xk = k0.y << 3, xv = v0.y << 3;
         uint32_t pbk = 64, pbv = 64;                // payload starts at byte 8
         const float sk = half_lo(k0.x), ok = half_hi(k0.x);
@@ -276,14 +293,11 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
             const uint8_t* qh = qlimb + (h * kGroups * 4 + (lane & 3)) * 16;
 #pragma unroll
             for (int grp = 0; grp < kGroups; ++grp) {
-                const uint32_t k0s = tstep<0>(xk, pbk, ring_k, mask8k, pk3);
-                const uint32_t v0s = tstep<LUTV>(xv, pbv, ring_v, mask8v, pv3);
-                const uint32_t k1s = tstep<0>(xk, pbk, ring_k, mask8k, pk3);
-                const uint32_t v1s = tstep<LUTV>(xv, pbv, ring_v, mask8v, pv3);
-                const uint32_t k2s = tstep<0>(xk, pbk, ring_k, mask8k, pk3);
-                const uint32_t v2s = tstep<LUTV>(xv, pbv, ring_v, mask8v, pv3);
-                const uint32_t k3s = tstep<0>(xk, pbk, ring_k, mask8k, pk3);
-                const uint32_t v3s = tstep<LUTV>(xv, pbv, ring_v, mask8v, pv3);
+                uint32_t k0s, k1s, k2s, k3s, v0s, v1s, v2s, v3s;
+                tstep2<0>(xk, pbk, ring_k, mask8k, pk3, k0s, k1s);
+                tstep2<LUTV>(xv, pbv, ring_v, mask8v, pv3, v0s, v1s);
+                tstep2<0>(xk, pbk, ring_k, mask8k, pk3, k2s, k3s);
+                tstep2<LUTV>(xv, pbv, ring_v, mask8v, pv3, v2s, v3s);
                 const uint32_t lk = pack4(k0s, k1s, k2s, k3s);
                 vlev[grp] = pack4(v0s, v1s, v2s, v3s);
                 asm volatile("" : "+v"(vlev[grp]));
@@ -291,10 +305,8 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
                 dk[0] = mfma(ql.x, lk, dk[0]);
                 dk[1] = mfma(ql.y, lk, dk[1]);
                 dk[2] = mfma(ql.z, lk, dk[2]);
-                if (grp & 1) {
-                    refill(pbk, nck, nk, ring_k, kr, last_k);
-                    refill(pbv, ncv, nv, ring_v, vr, last_v);
-                }
+                refill(pbk, nck, thrk, nk, ring_k, kr, last_k);
+                refill(pbv, ncv, thrv, nv, ring_v, vr, last_v);
                 __builtin_amdgcn_sched_barrier(0);
             }
 
@@ -366,8 +378,17 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) acc[s][r][h] = acc[s][r][h] * corr[r] + pv[s][r];
+                for (int r = 0; r < 4; ++r) {
+                    v8f t = acc[s][r];
+                    t[0] = t[0] * corr[r] + pv[s][r];
+                    acc[s][r] = rot1(t);
+                }
         }
+        for (int h = Hkv; h < kTokMaxHeads; ++h)
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc[s][r] = rot1(acc[s][r]);
         // every stream ends at x = L having read no byte past its record
         corrupt |= valid && ((xk >> 3) != kRansL || pbk > endk);
         corrupt |= valid && ((xv >> 3) != kRansL || pbv > endv);
@@ -384,7 +405,10 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
 #pragma unroll
         for (int s = 0; s < 2; ++s)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) av[s][r] = acc[s][r][h];
+            for (int r = 0; r < 4; ++r) {
+                av[s][r] = acc[s][r][0];
+                acc[s][r] = rot1(acc[s][r]);
+            }
         __syncthreads();   // LDS free (first head) / previous head merged
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
