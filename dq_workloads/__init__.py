@@ -105,8 +105,8 @@ def workload(name: str, variant: str = "paper", bpe: float | None = None) -> Wor
     if name in TOKEN_WORKLOADS:
         # the paper's default operating point (Sec. 5.1): one stream of 1024
         # values per token, 331 B / 231 B containers (+ the 4-byte s, o header)
-        # with 8 / 6 levels at alpha 1.4
-        k, v = Coding(8, 335, 1.4, n=1024), Coding(6, 235, 1.4, n=1024)
+        # with 8 / 6 levels at alpha 1.4, and the 2^8-entry table of Sec. 3
+        k, v = Coding(8, 335, 1.4, precision=8, n=1024), Coding(6, 235, 1.4, precision=8, n=1024)
         B, T = {"b1_t4k_tok": (1, 4096), "b16_t32k_tok": (16, 32768)}[name]
         return Workload(name, B, T, 32, 8, 4, k, v, streams="token")
     raise KeyError(name)

@@ -21,8 +21,8 @@ from oracle import attention, hadamard, kmean, kv, tables
 
 def _tabs():
     wl = wlmod.workload("b1_t4k_tok")
-    tk = tables.build_tables(1024, wl.k.levels, 12, wl.k.alpha, wl.k.record_bytes)
-    tv = tables.build_tables(1024, wl.v.levels, 12, wl.v.alpha, wl.v.record_bytes)
+    tk = tables.build_tables(1024, wl.k.levels, wl.k.precision, wl.k.alpha, wl.k.record_bytes)
+    tv = tables.build_tables(1024, wl.v.levels, wl.v.precision, wl.v.alpha, wl.v.record_bytes)
     return wl, tk, tv
 
 
@@ -70,11 +70,13 @@ def test_token_streams_reconstruct_every_head():
         assert e > 1.0
 
 
-def test_default_operating_point_matches_table2():
+@pytest.mark.parametrize("p", [8, 12])
+def test_default_operating_point_matches_table2(p):
     """N(0,1) tokens of 8 heads x 128 (rotation keeps them N(0,1)): key
     NMSE at M = 8 / 335 B and value NMSE at M = 6 / 235 B within 15 % of
-    Tab. 2 (5.9 % and 14.1 %)."""
-    _, tk, tv = _tabs()
+    Tab. 2 (5.9 % and 14.1 %), with 8- and 12-bit tables."""
+    tk = tables.build_tables(1024, 8, p, 1.4, 335)
+    tv = tables.build_tables(1024, 6, p, 1.4, 235)
     rng = np.random.default_rng(7)
     x = rng.normal(size=(1, 96, 8, 128)).astype(np.float32)
     bits = (x.view(np.uint32) >> 16).astype(np.uint16)          # bf16 by truncation: still ~N(0, 1)
