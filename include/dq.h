@@ -272,11 +272,15 @@ int dq_decode_attention_paged_partial(const dq_tables* k_tables, const dq_tables
  * window mean (the means are per head exactly as above); one (s, o) header
  * serves the whole token.  Tables are built with head_dim = n = 128 kv_heads.
  *
- * dq_token_record_stride: bytes between consecutive token records, C rounded
- *   up to a multiple of 16 (the pad bytes are written as zeros); 0 for an
- *   invalid table.
+ * dq_token_record_stride: bytes of one token's record slot S, C rounded up to
+ *   a multiple of 16 (the pad bytes are written as zeros); 0 for an invalid
+ *   table.
+ * Record buffer: u8 [batch][t_cap / 64][S / 8][64][8], 16-byte aligned: per
+ *   64-token tile, the 8-byte chunks of the 64 records with the chunk index
+ *   outermost (byte k of token t in tile t / 64 at ((k / 8) 64 + t % 64) 8 +
+ *   k % 8), so that the 64 tokens' chunk k / 8 are 512 contiguous bytes.
  * dq_encode_kv_token: as dq_encode_kv with kv_heads in {1, 2, 4, 8} and
- *   head_dim 128; records: u8 [batch][t_cap][stride], 16-byte aligned.
+ *   head_dim 128; writes the record buffer above.
  * dq_decode_attention_token_partial: one decode step over those records
  *   (rANS-decoded once per token and consumed one KV head at a time), into the
  *   workspace of dq_decode_workspace_bytes; finish with

@@ -381,23 +381,30 @@ def dq_decode_attention_paged_partial(k_tables: Tables, v_tables: Tables, q, k_p
 
 
 def dq_token_record_stride(tables: Tables) -> int:
-    """Bytes between per-token records (C rounded up to 16)."""
+    """Bytes of a per-token record slot (C rounded up to 16)."""
     return int(_lib.dq_token_record_stride(tables.handle))
+
+
+def token_records_shape(tables: Tables, batch: int, t_cap: int):
+    """Shape of a per-token record buffer: [B, t_cap / 64, S / 8, 64, 8] --
+    64-token tiles, 8-byte chunks outermost; token t's record is
+    records[b, t // 64, :, t % 64, :] flattened (its first C bytes)."""
+    S = dq_token_record_stride(tables)
+    return (batch, t_cap // 64, S // 8, 64, 8)
 
 
 def dq_encode_kv_token(tables: Tables, kv, t0: int, t_cap: int, records, mean_q=None, mean_scale=None,
                        status=None, stream=None):
     """Append kv (bf16 [B, T_new, H, 128] on the GPU) at cache position t0 as
     one stream per token over the H heads (tables built with head_dim 128 H).
-    records: uint8 [B, t_cap, stride]; keys also pass mean_q int8
-    [B, H, t_cap/128, 128] and mean_scale [B, H, t_cap/128]."""
+    records: uint8 of token_records_shape(tables, B, t_cap); keys also pass
+    mean_q int8 [B, H, t_cap/128, 128] and mean_scale [B, H, t_cap/128]."""
     import torch
     _need(kv.is_cuda and kv.dtype == torch.bfloat16 and kv.dim() == 4 and kv.stride(3) == 1, "kv")
     B, T, H, d = kv.shape
     _need(d == 128 and tables.head_dim == 128 * H, "per-token streams need head_dim 128 and n = 128 H")
-    stride = dq_token_record_stride(tables)
     _need(records.is_cuda and records.dtype == torch.uint8 and records.is_contiguous()
-          and tuple(records.shape) == (B, t_cap, stride), "records shape/dtype")
+          and tuple(records.shape) == token_records_shape(tables, B, t_cap), "records shape/dtype")
     if mean_q is not None:
         _need(mean_scale is not None, "mean_q and mean_scale go together")
         _need(mean_q.dtype == torch.int8 and mean_q.is_contiguous()
@@ -413,16 +420,16 @@ def dq_encode_kv_token(tables: Tables, kv, t0: int, t_cap: int, records, mean_q=
 def dq_decode_attention_token_partial(k_tables: Tables, v_tables: Tables, q, k_records, mean_q, mean_scale,
                                       v_records, seq_lens, workspace, softmax_scale=None, status=None,
                                       stream=None):
-    """Split-K partials of one decode step over per-token records
-    (uint8 [B, t_cap, stride]); finish with dq_decode_attention_merge."""
+    """Split-K partials of one decode step over per-token records (shape
+    token_records_shape); finish with dq_decode_attention_merge."""
     import torch
     _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3, "q")
     B, Hq, d = q.shape
-    _need(k_records.dim() == 3 and k_records.shape[0] == B and k_records.is_contiguous()
-          and k_records.shape[2] == dq_token_record_stride(k_tables), "k_records")
-    t_cap = k_records.shape[1]
+    _need(k_records.dim() == 5 and k_records.shape[0] == B and k_records.is_contiguous(), "k_records")
+    t_cap = k_records.shape[1] * 64
+    _need(tuple(k_records.shape) == token_records_shape(k_tables, B, t_cap), "k_records shape")
     Hkv = k_tables.head_dim // 128
-    _need(tuple(v_records.shape) == (B, t_cap, dq_token_record_stride(v_tables)) and v_records.is_contiguous(),
+    _need(tuple(v_records.shape) == token_records_shape(v_tables, B, t_cap) and v_records.is_contiguous(),
           "v_records")
     _need(tuple(mean_q.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW, 128) and mean_q.is_contiguous(), "mean_q")
     _need(tuple(mean_scale.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW) and mean_scale.is_contiguous(), "mean_scale")

@@ -62,8 +62,9 @@ class KVCache:
 
 class TokenKVCache:
     """Compressed cache with one stream per token over all KV heads (tables
-    built with head_dim 128 kv_heads): records [B, t_cap, stride] per tensor,
-    key means per head as in KVCache."""
+    built with head_dim 128 kv_heads): records of token_records_shape per
+    tensor (64-token tiles, 8-byte chunks outermost), key means per head as in
+    KVCache."""
 
     def __init__(self, batch: int, kv_heads: int, q_heads: int, t_cap: int, k_tables, v_tables,
                  device="cuda"):
@@ -75,9 +76,10 @@ class TokenKVCache:
         self.batch, self.kv_heads, self.q_heads, self.t_cap, self.head_dim = batch, kv_heads, q_heads, t_cap, d
         self.k_tables, self.v_tables = k_tables, v_tables
         nw = t_cap // _lib.DQ_MEAN_WINDOW
-        sk, sv = _lib.dq_token_record_stride(k_tables), _lib.dq_token_record_stride(v_tables)
-        self.k_records = torch.zeros((batch, t_cap, sk), dtype=torch.uint8, device=device)
-        self.v_records = torch.zeros((batch, t_cap, sv), dtype=torch.uint8, device=device)
+        self.k_records = torch.zeros(_lib.token_records_shape(k_tables, batch, t_cap), dtype=torch.uint8,
+                                     device=device)
+        self.v_records = torch.zeros(_lib.token_records_shape(v_tables, batch, t_cap), dtype=torch.uint8,
+                                     device=device)
         self.k_mean_q = torch.zeros((batch, kv_heads, nw, d), dtype=torch.int8, device=device)
         self.k_mean_scale = torch.zeros((batch, kv_heads, nw), dtype=torch.int16, device=device)
         self.status = torch.zeros(1, dtype=torch.int32, device=device)

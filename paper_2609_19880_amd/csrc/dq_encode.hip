@@ -298,7 +298,7 @@ struct EncArgs {
     int64_t sb, st, sh;
     int H, t0, n_new, t_cap;
     Pages pg;                    // records and key means: contiguous or paged
-    int rec_stride;              // per-token records: bytes from one token to the next
+    int rec_stride;              // per-token records: bytes per record slot (multiple of 16)
     uint8_t* records;
     const int8_t* mean_q;        // NULL for values
     const uint16_t* mean_scale;
@@ -512,9 +512,13 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     // at a time through the block table, or per-token records at their stride
     // (zero-padded).
     if (TOK) {
+        // 64-token tiles, 8-byte chunk major: byte k of token t at
+        // ((t / 64) S / 8 + k / 8) 512 + (t % 64) 8 + k % 8
         for (int i = wave; i < active; i += kEncWaves) {
-            uint8_t* dst = a.records + ((int64_t)b * a.t_cap + first + i) * a.rec_stride;
-            for (int k = lane; k < a.rec_stride; k += kWave) dst[k] = k < C ? s_rec[i * C + k] : (uint8_t)0;
+            const int t = first + i;
+            uint8_t* tile = a.records + ((int64_t)b * a.t_cap + (t & ~63)) * a.rec_stride + (t & 63) * 8;
+            for (int k = lane; k < a.rec_stride; k += kWave)
+                tile[(k >> 3) * 512 + (k & 7)] = k < C ? s_rec[i * C + k] : (uint8_t)0;
         }
     } else if (!a.pg.bt) {
         uint8_t* dst = a.records + ((int64_t)(b * a.H + h) * a.t_cap + first) * C;

@@ -12,8 +12,11 @@
 // the next head with their state.  All query heads' accumulators live in the
 // wavefront: two channels per lane per query head.
 //
-// Record bytes.  A record (C bytes at a 16-byte-aligned stride) is read in
-// 8-byte chunks into a per-lane ring of 8 dwords in LDS, laid out
+// Record bytes.  Records (C bytes in S-byte slots, S a multiple of 16) are
+// stored per 64-token tile with 8-byte chunks outermost: chunk c of the tile's
+// token l at c * 512 + l * 8 from the tile, so the 64 lanes of a wavefront
+// loading the same chunk read 512 contiguous bytes.  They are read in 8-byte
+// chunks into a per-lane ring of 8 dwords in LDS, laid out
 // [dword row][lane] so that every lane stays in its own bank; a ninth row
 // repeats row 0 so that two consecutive dwords are always rows r, r + 1.  A
 // decode step reads the two dwords holding its byte position and takes the
@@ -112,8 +115,9 @@ __device__ __forceinline__ void tstep2(uint32_t& X, uint32_t& pb, uint32_t ring_
     e1 = (uint32_t)eb;
 }
 
+// rec: the lane's first chunk (tile + 8 lane); chunks are 512 bytes apart.
 __device__ __forceinline__ uint2 load_chunk(const uint8_t* rec, uint32_t c, uint32_t last) {
-    return *reinterpret_cast<const uint2*>(rec + 8u * min(c, last));
+    return *reinterpret_cast<const uint2*>(rec + 512u * min(c, last));
 }
 
 // Chunk c of the record into ring rows 2 (c mod 4), + 1 (and row 8 for c
@@ -263,8 +267,8 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
         const int t_base = start + tile * kTile;
         const int t = t_base + lane;               // < t_cap: tiles lie inside the capacity
         const bool valid = t < T;
-        const uint8_t* kr = a.krec + ((int64_t)b * a.t_cap + t) * a.k_stride;
-        const uint8_t* vr = a.vrec + ((int64_t)b * a.t_cap + t) * a.v_stride;
+        const uint8_t* kr = a.krec + ((int64_t)b * a.t_cap + t_base) * a.k_stride + 8 * lane;
+        const uint8_t* vr = a.vrec + ((int64_t)b * a.t_cap + t_base) * a.v_stride + 8 * lane;
         // chunks 0..2 (bytes 0..23) cover the first 4 steps from byte 8
         const uint2 k0 = load_chunk(kr, 0, last_k), k1 = load_chunk(kr, 1, last_k), k2 = load_chunk(kr, 2, last_k);
         const uint2 v0 = load_chunk(vr, 0, last_v), v1 = load_chunk(vr, 1, last_v), v2 = load_chunk(vr, 2, last_v);

@@ -1,7 +1,7 @@
 """Per-token streams at the full b16_t32k_tok size, in the launch configuration
 bench.py times (--workload b16_t32k_tok): batch 16 x 32768 tokens, one
-1024-value stream per token and tensor (335 / 235-byte records at 336 / 240
-byte strides, 8 / 6 levels, p 8), one encode call per sequence, then the same
+1024-value stream per token and tensor (335 / 235-byte records in 336 / 240
+byte slots, 8 / 6 levels, p 8), one encode call per sequence, then the same
 partial + merge calls.
 
 The oracle cannot re-encode 524,288 tokens in seconds, so it checks what it
@@ -24,6 +24,7 @@ import torch
 import bench
 import dq_workloads as wlmod
 from oracle import attention, kmean, kv, tables
+from tokrec import from_tiles
 
 pytestmark = pytest.mark.gpu
 
@@ -66,8 +67,8 @@ def test_full_size_token_windows_bit_exact(full, b, w):
     k, v = _inputs(wl, b, t0, t0 + W)
     krec, mq, ms, _ = kv.encode_keys_tokenwise(k, otk)
     vrec, _ = kv.encode_values_tokenwise(v, otv)
-    gk = cache.k_records[b, t0:t0 + W].cpu().numpy()
-    gv = cache.v_records[b, t0:t0 + W].cpu().numpy()
+    gk = from_tiles(cache.k_records[b:b + 1, t0 // 64:(t0 + W) // 64].cpu().numpy())[0]
+    gv = from_tiles(cache.v_records[b:b + 1, t0 // 64:(t0 + W) // 64].cpu().numpy())[0]
     assert np.array_equal(gk[:, :otk.record_bytes], krec[0]) and not gk[:, otk.record_bytes:].any()
     assert np.array_equal(gv[:, :otv.record_bytes], vrec[0]) and not gv[:, otv.record_bytes:].any()
     assert np.array_equal(cache.k_mean_q[b, :, w].cpu().numpy(), mq[0, :, 0])

@@ -2,7 +2,8 @@
 the paper's default grouping) on the GPU against the oracle, through the C ABI.
 
 Bars as in test_gpu_parity.py: records (first C bytes, then zero padding to
-the 16-byte stride) and key means bit-exact with the oracle's
+the 16-byte slot; buffers in 64-token tiles with 8-byte chunks outermost) and
+key means bit-exact with the oracle's
 encode_*_tokenwise; attention within 2e-3 (row-normalized) of the oracle's
 fp64 folded attention over the oracle's own records, which are uploaded for
 the attention checks.
@@ -14,6 +15,7 @@ import torch
 
 import dq_workloads as wlmod
 from oracle import attention, kmean, kv, tables
+from tokrec import to_tiles
 
 pytestmark = pytest.mark.gpu
 
@@ -36,13 +38,6 @@ def _tabs(dq, n, levels, C, p=12, alpha=1.4):
 def _rel_err(got, ref):
     scale = np.max(np.abs(ref), axis=-1, keepdims=True)
     return float(np.max(np.abs(got - ref) / np.maximum(scale, 1e-30)))
-
-
-def _strided(rec, stride):
-    B, T, C = rec.shape
-    out = np.zeros((B, T, stride), dtype=np.uint8)
-    out[:, :, :C] = rec
-    return out
 
 
 def _oracle_attention(q_bits, krec, mq, ms, vrec, otk, otv, lens, H, G):
@@ -72,8 +67,9 @@ def test_token_encode_bit_exact(dq, p):
     vrec, _ = kv.encode_values_tokenwise(wlmod.bf16_bits(v), otv)
     Sk, Sv = dq.dq_token_record_stride(gtk), dq.dq_token_record_stride(gtv)
     assert (Sk, Sv) == (336, 240)
-    grk = torch.full((B, T, Sk), 0xAB, dtype=torch.uint8, device=DEV)     # pad bytes must be rewritten
-    grv = torch.full((B, T, Sv), 0xAB, dtype=torch.uint8, device=DEV)
+    # pad bytes must be rewritten
+    grk = torch.full(dq.token_records_shape(gtk, B, T), 0xAB, dtype=torch.uint8, device=DEV)
+    grv = torch.full(dq.token_records_shape(gtv, B, T), 0xAB, dtype=torch.uint8, device=DEV)
     gmq = torch.zeros((B, H, T // 128, 128), dtype=torch.int8, device=DEV)
     gms = torch.zeros((B, H, T // 128), dtype=torch.int16, device=DEV)
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
@@ -85,8 +81,8 @@ def test_token_encode_bit_exact(dq, p):
     dq.dq_encode_kv_token(gtv, vd[:, 100:], 100, T, grv, None, None, status)
     torch.cuda.synchronize()
     assert int(status.item()) == 0
-    assert np.array_equal(grk.cpu().numpy(), _strided(krec, Sk))
-    assert np.array_equal(grv.cpu().numpy(), _strided(vrec, Sv))
+    assert np.array_equal(grk.cpu().numpy(), to_tiles(krec, Sk))
+    assert np.array_equal(grv.cpu().numpy(), to_tiles(vrec, Sv))
     assert np.array_equal(gmq.cpu().numpy(), mq)
     assert np.array_equal(gms.cpu().numpy().view(np.uint16), ms.view(np.uint16))
 
@@ -101,8 +97,8 @@ def test_token_attention_matches_oracle(dq, p):
     vrec, _ = kv.encode_values_tokenwise(wlmod.bf16_bits(v), otv)
     Sk, Sv = dq.dq_token_record_stride(gtk), dq.dq_token_record_stride(gtv)
     lens = [T, 0, 65, 300]
-    grk = torch.from_numpy(_strided(krec, Sk)).to(DEV)
-    grv = torch.from_numpy(_strided(vrec, Sv)).to(DEV)
+    grk = torch.from_numpy(to_tiles(krec, Sk)).to(DEV)
+    grv = torch.from_numpy(to_tiles(vrec, Sv)).to(DEV)
     gmq = torch.from_numpy(mq).to(DEV)
     gms = torch.from_numpy(ms.view(np.int16)).to(DEV)
     seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
@@ -134,8 +130,8 @@ def test_token_attention_heads_and_groups(dq, H, G, Ck, Cv):
     krec, mq, ms, _ = kv.encode_keys_tokenwise(wlmod.bf16_bits(k), otk)
     vrec, _ = kv.encode_values_tokenwise(wlmod.bf16_bits(v), otv)
     Sk, Sv = dq.dq_token_record_stride(gtk), dq.dq_token_record_stride(gtv)
-    grk = torch.empty((B, T, Sk), dtype=torch.uint8, device=DEV)
-    grv = torch.empty((B, T, Sv), dtype=torch.uint8, device=DEV)
+    grk = torch.empty(dq.token_records_shape(gtk, B, T), dtype=torch.uint8, device=DEV)
+    grv = torch.empty(dq.token_records_shape(gtv, B, T), dtype=torch.uint8, device=DEV)
     gmq = torch.empty((B, H, T // 128, 128), dtype=torch.int8, device=DEV)
     gms = torch.empty((B, H, T // 128), dtype=torch.int16, device=DEV)
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
@@ -149,8 +145,8 @@ def test_token_attention_heads_and_groups(dq, H, G, Ck, Cv):
     dq.dq_decode_attention_merge(B, H * G, H, seq, T, ws, out)
     torch.cuda.synchronize()
     assert int(status.item()) == 0
-    assert np.array_equal(grk.cpu().numpy(), _strided(krec, Sk))
-    assert np.array_equal(grv.cpu().numpy(), _strided(vrec, Sv))
+    assert np.array_equal(grk.cpu().numpy(), to_tiles(krec, Sk))
+    assert np.array_equal(grv.cpu().numpy(), to_tiles(vrec, Sv))
     ref = _oracle_attention(wlmod.bf16_bits(q), krec, mq, ms, vrec, otk, otv, lens, H, G)
     assert _rel_err(out.cpu().numpy().astype(np.float64), ref) < TOL
 
@@ -163,8 +159,8 @@ def test_token_attention_flags_corrupt_record_and_is_deterministic(dq):
     krec, mq, ms, _ = kv.encode_keys_tokenwise(wlmod.bf16_bits(k), otk)
     vrec, _ = kv.encode_values_tokenwise(wlmod.bf16_bits(v), otv)
     Sk, Sv = dq.dq_token_record_stride(gtk), dq.dq_token_record_stride(gtv)
-    grk = torch.from_numpy(_strided(krec, Sk)).to(DEV)
-    grv = torch.from_numpy(_strided(vrec, Sv)).to(DEV)
+    grk = torch.from_numpy(to_tiles(krec, Sk)).to(DEV)
+    grv = torch.from_numpy(to_tiles(vrec, Sv)).to(DEV)
     gmq = torch.from_numpy(mq).to(DEV)
     gms = torch.from_numpy(ms.view(np.int16)).to(DEV)
     seq = torch.tensor([T, 200], dtype=torch.int32, device=DEV)
@@ -181,14 +177,14 @@ def test_token_attention_flags_corrupt_record_and_is_deterministic(dq):
     assert torch.equal(outs[0], outs[1])
     # a record past the length is never read as a token: still clean
     bad = grv.clone()
-    bad[1, 230, 4:8] = 0
+    bad[1, 230 // 64, 0, 230 % 64, 4:8] = 0          # the state word of token 230
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
     dq.dq_decode_attention_token_partial(gtk, gtv, q.to(DEV), grk, gmq, gms, bad, seq, ws, status=status)
     torch.cuda.synchronize()
     assert int(status.item()) == 0
     # a stream state that is not a valid end state inside the length: flagged,
     # outputs still finite
-    bad[0, 17, 4:8] = 0
+    bad[0, 0, 0, 17, 4:8] = 0
     out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
     dq.dq_decode_attention_token_partial(gtk, gtv, q.to(DEV), grk, gmq, gms, bad, seq, ws, status=status)
     dq.dq_decode_attention_merge(B, H * G, H, seq, T, ws, out)
