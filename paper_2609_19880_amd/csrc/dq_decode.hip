@@ -139,11 +139,18 @@ struct AttnArgs {
 //   Y = 8 f (X >> (p + 3)) + 8 (z - c) = 8 x'   (one 24-bit multiply-add)
 //   sh = clz(Y) & 24: 0, 8 or 16 bits to shift in (x' >= 2^9 for p <= 12)
 //   X = (Y << sh) | ((pair << 16) >> (29 - sh)),  29 - sh = sh ^ 29
+//
+// The pair goes straight into the high half of r (ds_read_u16_d16_hi; the low
+// half is never read).  The compiler does not emit that load, so it is
+// written out; it is issued before the table read, which is made to depend on
+// it, and LDS returns in order, so the compiler's wait for the table word
+// also covers the pair (whose only use comes after the table word's).
 template <uint32_t LUT_OFF>
 __device__ __forceinline__ uint32_t dstep(uint32_t& X, uint32_t& pq, uint32_t mask8, int p3) {
-    const uint64_t e = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
+    uint32_t laddr = X & mask8, r;
+    asm volatile("ds_read_u16_d16_hi %0, %2" : "=v"(r), "+v"(laddr) : "v"(pq));
+    const uint64_t e = *LDS_PTR(const uint64_t, laddr + LUT_OFF);
     const uint32_t ex = (uint32_t)e, ey = (uint32_t)(e >> 32);
-    const uint32_t r = (uint32_t)*LDS_PTR(const uint16_t, pq) << 16;
     const uint32_t y = __umul24(ex, X >> p3) + ey;
     const uint32_t sh = (uint32_t)__builtin_clz(y) & 24u;
     const uint32_t q = r >> (sh ^ 29u);
