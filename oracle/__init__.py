@@ -21,8 +21,11 @@ Modules, in pipeline order:
 * ``attention`` -- fp64 decode attention over the dequantized cache, both the
                    direct form and the folded form of Eq. (fold-key) /
                    Eq. (fold-value).
+* ``fixed``     -- the fixed-width comparator at matched storage (App. B):
+                   the same preprocessing, nearest-level rounding, b-bit
+                   symbols in the same record size.
 
 Readings of the paper where it is silent are listed in each module header.
 """
 
-from . import tables, hadamard, kmean, quantize, rans, kv, attention  # noqa: F401
+from . import tables, hadamard, kmean, quantize, rans, kv, attention, fixed  # noqa: F401
