@@ -55,6 +55,8 @@ def _args():
     ap.add_argument("--copy-calibration", type=int, default=0)
     ap.add_argument("--compare-bf16", action="store_true",
                     help="also time the BF16 comparator (uncompressed cache of the same shape)")
+    ap.add_argument("--compare-fixed", action="store_true",
+                    help="also time the fixed-width comparator (App. B: 36-byte INT2 records of the same workload)")
     ap.add_argument("--residual", type=int, default=0,
                     help="also attend over this many raw BF16 tokens per sequence (residual window, <= 255)")
     return ap.parse_args()
@@ -272,6 +274,51 @@ def bf16_comparator(wl, a, q, seq, out, ws, alg_bytes):
             "kv_bytes_ratio": nbytes / alg_bytes}
 
 
+def fixed_comparator(wl, a, q, seq, out, ws):
+    """The same decode step over fixed-width records of the same size (App. B
+    comparator: 36-byte records of 2-bit levels), encoded from the same seeded
+    inputs and timed like the compressed path."""
+    import torch
+    import dq_workloads as wlmod
+    import paper_2609_19880_amd as dq
+    B, T, Hq, Hkv, d = wl.batch, wl.context, wl.q_heads, wl.kv_heads, wl.head_dim
+    C = 36
+    kr = torch.empty((B, Hkv, T, C), dtype=torch.uint8, device="cuda")
+    vr = torch.empty_like(kr)
+    mq = torch.empty((B, Hkv, T // 128, d), dtype=torch.int8, device="cuda")
+    ms = torch.empty((B, Hkv, T // 128), dtype=torch.int16, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for b in range(B):
+        k = wlmod.make_k(wl, a.seed * 1000 + b, device="cuda", batch=1)
+        v = wlmod.make_v(wl, a.seed * 1000 + b, device="cuda", batch=1)
+        dq.dq_encode_kv_fixed(d, C, k, 0, T, kr[b:b + 1], mq[b:b + 1], ms[b:b + 1], status)
+        dq.dq_encode_kv_fixed(d, C, v, 0, T, vr[b:b + 1], None, None, status)
+        del k, v
+    torch.cuda.synchronize()
+    if int(status.item()):
+        raise RuntimeError(f"fixed-width encoder status {int(status.item())}")
+    for _ in range(a.warmup):
+        dq.dq_decode_attention_fixed_partial(q, kr, mq, ms, vr, seq, ws)
+        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 * a.steps)]
+    for i in range(a.steps):
+        ev[3 * i].record()
+        dq.dq_decode_attention_fixed_partial(q, kr, mq, ms, vr, seq, ws)
+        ev[3 * i + 1].record()
+        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
+        ev[3 * i + 2].record()
+    torch.cuda.synchronize()
+    pms = sum(ev[3 * i].elapsed_time(ev[3 * i + 1]) for i in range(a.steps)) / a.steps
+    sms = ev[0].elapsed_time(ev[-1]) / a.steps
+    nbytes = B * Hkv * T * (2 * C + (d + 2) / 128)
+    del kr, vr, mq, ms
+    torch.cuda.empty_cache()
+    return {"record_bytes": C, "bits_per_symbol": 2, "ms_per_step": sms, "tokens_per_s": B * T / (sms * 1e-3),
+            "partial_ms": pms, "bytes_per_step": nbytes, "gbs": nbytes / (pms * 1e-3) / 1e9,
+            "hbm_frac": nbytes / (pms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+
+
 def main():
     a = _args()
     if a.gpus != 1:
@@ -403,6 +450,10 @@ def main():
         "encode": {"ms": enc_ms, "tokens_per_s": B * T / (enc_ms * 1e-3),
                    "input_gbs": 2 * B * T * Hkv * d * 2 / (enc_ms * 1e-3) / 1e9},
     }
+    if a.compare_fixed:
+        if tok or d != 128 or wl.gqa > 4:
+            raise SystemExit("--compare-fixed runs on the per-(token, KV head) workloads with head_dim 128, G <= 4")
+        rec["fixed_width_decode"] = fixed_comparator(wl, a, q, seq, out, cache.workspace)
     if a.compare_bf16:
         rec["bf16_decode"] = bf16_comparator(wl, a, q, seq, out, cache.workspace, alg_bytes)
     if not a.no_cpu_baseline:

@@ -304,6 +304,35 @@ int dq_decode_attention_token_partial(const dq_tables* k_tables, const dq_tables
                                       size_t workspace_bytes, uint32_t* status, void* stream);
 
 /*
+ * Comparator: fixed-width coding at matched storage (App. B).  The same
+ * preprocessing as the D-Quant encoder (rotation, key window means, min-max
+ * grid, least-squares refit, fp16 s and o), symbols by nearest-level rounding,
+ * b = floor(8 (record_bytes - 4) / head_dim) bits each (M = 2^b levels),
+ * packed least-significant bit first after the 4-byte header of a record of
+ * the same size.  With 36-byte records and head_dim 128 that is INT2 with an
+ * fp16 scale and zero point per 128 values (2.25 bits per value, Sec. 3).
+ *
+ * dq_fixed_bits: b for (head_dim, record_bytes), 0 if no whole bit fits or
+ *   more than 8 would.
+ * dq_encode_kv_fixed: as dq_encode_kv without tables; head_dim 64, 128 or 256.
+ * dq_decode_attention_fixed_partial: one decode step over 36-byte fixed-width
+ *   records (head_dim 128, b = 2), same layouts, workspace and merge as
+ *   dq_decode_attention_partial; q_heads / kv_heads <= 4.
+ * Return DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_WORKSPACE or DQ_ERR_HIP.
+ */
+int32_t dq_fixed_bits(int32_t head_dim, int32_t record_bytes);
+int dq_encode_kv_fixed(int32_t head_dim, int32_t record_bytes, const uint16_t* kv, int64_t stride_b,
+                       int64_t stride_t, int64_t stride_h, int32_t batch, int32_t kv_heads, int32_t t0,
+                       int32_t n_new, int32_t t_cap, uint8_t* records, int8_t* mean_q,
+                       uint16_t* mean_scale, uint32_t* status, void* stream);
+int dq_decode_attention_fixed_partial(const uint16_t* q, int32_t batch, int32_t q_heads, int32_t kv_heads,
+                                      const uint8_t* k_records, const int8_t* k_mean_q,
+                                      const uint16_t* k_mean_scale, const uint8_t* v_records,
+                                      const int32_t* seq_lens, int32_t t_cap, float softmax_scale,
+                                      void* workspace, size_t workspace_bytes, uint32_t* status,
+                                      void* stream);
+
+/*
  * Comparator: the same decode step over an uncompressed BF16 cache.
  *   k, v: bf16 [batch][kv_heads][t_cap][head_dim], 16-byte aligned, original
  *         basis; the first seq_lens[b] tokens of sequence b are attended.

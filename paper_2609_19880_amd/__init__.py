@@ -11,7 +11,8 @@ Entry points (same names as the C ABI in ``include/dq.h``):
     dq_decode_attention_merge, dq_decode_attention_residual, dq_residual_append,
     dq_residual_commit, dq_bf16_decode_attention_partial, dq_encode_kv_paged,
     dq_decode_attention_paged_partial, dq_token_record_stride, dq_encode_kv_token,
-    dq_decode_attention_token_partial, dq_decode_symbols, dq_strerror, dq_last_error
+    dq_decode_attention_token_partial, dq_fixed_bits, dq_encode_kv_fixed,
+    dq_decode_attention_fixed_partial, dq_decode_symbols, dq_strerror, dq_last_error
 """
 
 from ._lib import (  # noqa: F401
@@ -23,6 +24,7 @@ from ._lib import (  # noqa: F401
     dq_decode_attention_residual, dq_residual_append, dq_residual_commit,
     dq_bf16_decode_attention_partial, dq_encode_kv_paged, dq_decode_attention_paged_partial,
     dq_token_record_stride, token_records_shape, dq_encode_kv_token, dq_decode_attention_token_partial,
+    dq_fixed_bits, dq_encode_kv_fixed, dq_decode_attention_fixed_partial,
     dq_decode_symbols, dq_strerror, dq_last_error, smallest_feasible_alpha,
 )
 from .cache import KVCache, StreamingKVCache, TokenKVCache  # noqa: F401

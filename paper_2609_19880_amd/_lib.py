@@ -94,6 +94,13 @@ def _load():
     lib.dq_decode_attention_token_partial.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, ctypes.c_float,
                                                       P, SZ, P, P]
     lib.dq_decode_attention_token_partial.restype = ctypes.c_int
+    lib.dq_fixed_bits.argtypes = [I32, I32]
+    lib.dq_fixed_bits.restype = I32
+    lib.dq_encode_kv_fixed.argtypes = [I32, I32, P, I64, I64, I64, I32, I32, I32, I32, I32, P, P, P, P, P]
+    lib.dq_encode_kv_fixed.restype = ctypes.c_int
+    lib.dq_decode_attention_fixed_partial.argtypes = [P, I32, I32, I32, P, P, P, P, P, I32, ctypes.c_float,
+                                                      P, SZ, P, P]
+    lib.dq_decode_attention_fixed_partial.restype = ctypes.c_int
     lib.dq_bf16_decode_attention_partial.argtypes = [P, I32, I32, I32, P, P, P, I32, ctypes.c_float, P, SZ, P]
     lib.dq_bf16_decode_attention_partial.restype = ctypes.c_int
     lib.dq_residual_append.argtypes = [P, P, I32, I32, I32, P, P, P, P, I32, P, P]
@@ -441,6 +448,53 @@ def dq_decode_attention_token_partial(k_tables: Tables, v_tables: Tables, q, k_r
                                                 workspace.numel() * workspace.element_size(), _ptr(status),
                                                 _stream(stream))
     _check(rc, "dq_decode_attention_token_partial")
+
+
+def dq_fixed_bits(head_dim: int, record_bytes: int) -> int:
+    """Bits per symbol of the fixed-width comparator (0: no valid width)."""
+    return int(_lib.dq_fixed_bits(int(head_dim), int(record_bytes)))
+
+
+def dq_encode_kv_fixed(head_dim: int, record_bytes: int, kv, t0: int, t_cap: int, records, mean_q=None,
+                       mean_scale=None, status=None, stream=None):
+    """Fixed-width comparator encoder (App. B): kv bf16 [B, T_new, H, d] at cache
+    position t0 into records uint8 [B, H, t_cap, C]; keys also pass the means."""
+    import torch
+    _need(kv.is_cuda and kv.dtype == torch.bfloat16 and kv.dim() == 4 and kv.stride(3) == 1, "kv")
+    B, T, H, d = kv.shape
+    _need(d == head_dim, "kv head_dim")
+    _need(records.is_cuda and records.dtype == torch.uint8 and records.is_contiguous()
+          and tuple(records.shape) == (B, H, t_cap, record_bytes), "records shape/dtype")
+    if mean_q is not None:
+        _need(mean_scale is not None and tuple(mean_q.shape) == (B, H, t_cap // DQ_MEAN_WINDOW, d)
+              and mean_q.is_contiguous() and mean_scale.is_contiguous(), "mean buffers")
+    rc = _lib.dq_encode_kv_fixed(int(head_dim), int(record_bytes), _ptr(kv), kv.stride(0), kv.stride(1),
+                                 kv.stride(2), B, H, int(t0), T, int(t_cap), _ptr(records), _ptr(mean_q),
+                                 _ptr(mean_scale), _ptr(status), _stream(stream))
+    _check(rc, "dq_encode_kv_fixed")
+
+
+def dq_decode_attention_fixed_partial(q, k_records, mean_q, mean_scale, v_records, seq_lens, workspace,
+                                      softmax_scale=None, status=None, stream=None):
+    """Split-K partials of one decode step over 36-byte fixed-width records
+    [B, H_kv, t_cap, 36]; finish with dq_decode_attention_merge."""
+    import torch
+    _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3, "q")
+    B, Hq, d = q.shape
+    _need(k_records.dim() == 4 and k_records.shape[0] == B and k_records.shape[3] == 36
+          and k_records.is_contiguous() and tuple(v_records.shape) == tuple(k_records.shape)
+          and v_records.is_contiguous(), "records")
+    Hkv, t_cap = k_records.shape[1], k_records.shape[2]
+    _need(tuple(mean_q.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW, 128) and mean_q.is_contiguous()
+          and tuple(mean_scale.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW) and mean_scale.is_contiguous(), "means")
+    _need(seq_lens.is_cuda and seq_lens.dtype == torch.int32 and seq_lens.numel() == B, "seq_lens")
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    rc = _lib.dq_decode_attention_fixed_partial(_ptr(q), B, Hq, Hkv, _ptr(k_records), _ptr(mean_q),
+                                                _ptr(mean_scale), _ptr(v_records), _ptr(seq_lens), t_cap,
+                                                ctypes.c_float(scale), _ptr(workspace),
+                                                workspace.numel() * workspace.element_size(), _ptr(status),
+                                                _stream(stream))
+    _check(rc, "dq_decode_attention_fixed_partial")
 
 
 def dq_bf16_decode_attention_partial(q, k, v, seq_lens, workspace, softmax_scale=None, stream=None):

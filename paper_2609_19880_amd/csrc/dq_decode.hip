@@ -208,7 +208,20 @@ constexpr uint32_t kLutVOffset = 8u << 12;   // value table when it differs from
 
 // RWP: compile-time key and value record lengths (rw_pair), 0 for run-time
 // lengths.
-template <int HG, uint32_t LUTV, int RWP>
+// Fixed-width comparator records (App. B): [fp16 s][fp16 o] then 2-bit levels,
+// symbol j in bits 2 (j mod 4) of payload byte j / 4.  The four levels of
+// payload byte x, one per byte: x | (x >> 4) << 16 puts the two nibbles in
+// the two halves, | << 6 brings bits 2-3 of each half up to its second byte.
+__device__ __forceinline__ uint32_t spread2(uint32_t x) {
+    uint32_t t, u;
+    asm("v_lshl_or_b32 %0, %1, 16, %2" : "=v"(t) : "v"(x >> 4), "v"(x));
+    asm("v_lshl_or_b32 %0, %1, 6, %1" : "=v"(u) : "v"(t));
+    return u & 0x03030303u;
+}
+
+// FIXED: the fixed-width comparator at matched storage; levels come straight
+// from the record words (no tables, no byte pairs, no rANS state).
+template <int HG, uint32_t LUTV, int RWP, bool FIXED = false>
 __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kernel(AttnArgs a) {
     constexpr int RWK = RWP >> 8, RWV = RWP & 0xFF;
     constexpr int GP = 4 * HG;
@@ -228,7 +241,7 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
     if (start >= T) return;   // the merge ignores chunks past the length
 
     // ---- prologue: tables, rotated query, its digits, q . mu per window
-    {
+    if (!FIXED) {
         const int Pk = 1 << a.tk.p, Pv = 1 << a.tv.p;
         uint2* lk = reinterpret_cast<uint2*>(smem + L.lut_k);
         for (int i = tid; i < Pk; i += nthr) lk[i] = a.tk.t.lut64[i];
@@ -349,8 +362,17 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
         // ---- both records of the lane's token -> headers + byte-pair arrays
         const uint32_t hk0 = rk[0], xk0 = rk[1] << 3;
         const uint32_t hv0 = rv[0], xv0 = rv[1] << 3;
-        build_pairs(rk, CWk, smem + pk_lane);
-        build_pairs(rv, CWv, smem + pv_lane);
+        uint32_t ck[FIXED ? 9 : 1], cv[FIXED ? 9 : 1];   // this tile's fixed-width records
+        if (FIXED) {
+#pragma unroll
+            for (int k = 0; k < (FIXED ? 9 : 1); ++k) {
+                ck[k] = rk[k];
+                cv[k] = rv[k];
+            }
+        } else {
+            build_pairs(rk, CWk, smem + pk_lane);
+            build_pairs(rv, CWv, smem + pv_lane);
+        }
         if (kPrefetch && tile + L.nw < ntiles) {
             const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, t_base + L.nw * kTile, bad_page) + lane;
             load_record(rk, a.krec, tok, CWk);
@@ -376,16 +398,23 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
         uint32_t vlev[kD / 4];
 #pragma unroll
         for (int grp = 0; grp < kD / 4; ++grp) {
-            const uint32_t k0 = dstep<0>(xk, pq, mask8k, pk3);
-            const uint32_t v0 = dstep<LUTV>(xv, pv, mask8v, pv3);
-            const uint32_t k1 = dstep<0>(xk, pq, mask8k, pk3);
-            const uint32_t v1 = dstep<LUTV>(xv, pv, mask8v, pv3);
-            const uint32_t k2 = dstep<0>(xk, pq, mask8k, pk3);
-            const uint32_t v2 = dstep<LUTV>(xv, pv, mask8v, pv3);
-            const uint32_t k3 = dstep<0>(xk, pq, mask8k, pk3);
-            const uint32_t v3 = dstep<LUTV>(xv, pv, mask8v, pv3);
-            const uint32_t lk = pack4(k0, k1, k2, k3);
-            vlev[grp] = pack4(v0, v1, v2, v3);
+            uint32_t lk;
+            if (FIXED) {
+                const int w = 1 + (FIXED ? grp / 4 : 0), sh = 8 * (grp % 4);
+                lk = spread2(__builtin_amdgcn_ubfe(ck[w], sh, 8));
+                vlev[grp] = spread2(__builtin_amdgcn_ubfe(cv[w], sh, 8));
+            } else {
+                const uint32_t k0 = dstep<0>(xk, pq, mask8k, pk3);
+                const uint32_t v0 = dstep<LUTV>(xv, pv, mask8v, pv3);
+                const uint32_t k1 = dstep<0>(xk, pq, mask8k, pk3);
+                const uint32_t v1 = dstep<LUTV>(xv, pv, mask8v, pv3);
+                const uint32_t k2 = dstep<0>(xk, pq, mask8k, pk3);
+                const uint32_t v2 = dstep<LUTV>(xv, pv, mask8v, pv3);
+                const uint32_t k3 = dstep<0>(xk, pq, mask8k, pk3);
+                const uint32_t v3 = dstep<LUTV>(xv, pv, mask8v, pv3);
+                lk = pack4(k0, k1, k2, k3);
+                vlev[grp] = pack4(v0, v1, v2, v3);
+            }
             // pack now: left alone, the packing sinks to the value pass and the
             // four table words stay live until then
             asm volatile("" : "+v"(vlev[grp]));
@@ -398,7 +427,7 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
             }
             // a corrupt stream may run past its array: clamp often enough that
             // it cannot leave the workgroup's LDS (kPairSlack above the arrays)
-            if ((grp % kClampGroups) == kClampGroups - 1) {
+            if (!FIXED && (grp % kClampGroups) == kClampGroups - 1) {
                 pq = min(pq, pk_end);
                 pv = min(pv, pv_end);
             }
@@ -406,8 +435,10 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
             __builtin_amdgcn_sched_barrier(0);
         }
         // every stream ends at x = L having read at most its C - 8 payload bytes
-        corrupt |= valid && ((xk >> 3) != kRansL || pq > pk_end);
-        corrupt |= valid && ((xv >> 3) != kRansL || pv > pv_end);
+        if (!FIXED) {
+            corrupt |= valid && ((xk >> 3) != kRansL || pq > pk_end);
+            corrupt |= valid && ((xv >> 3) != kRansL || pv > pv_end);
+        }
 
         // ---- scores (Eq. fold-key) and online softmax; the value scale is
         //      folded into the weight (Eq. fold-value)
@@ -912,13 +943,13 @@ bool attention_supports(const dq_tables* tk, const dq_tables* tv) {
     return true;
 }
 
-template <int HG, uint32_t LUTV, int RWP>
+template <int HG, uint32_t LUTV, int RWP, bool FIXED = false>
 static int launch_rw(AttnArgs& a, dim3 grid, hipStream_t stream) {
     if (int rc = hip_check("hipFuncSetAttribute",
-                           hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_partial_kernel<HG, LUTV, RWP>),
+                           hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_partial_kernel<HG, LUTV, RWP, FIXED>),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
         return rc;
-    attn_partial_kernel<HG, LUTV, RWP><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
+    attn_partial_kernel<HG, LUTV, RWP, FIXED><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
     return hip_check("attn_partial launch", hipGetLastError());
 }
 
@@ -976,6 +1007,45 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pag
     dim3 grid(a.nchunks, Hkv, B);
     if (a.shared_lut) return G <= 4 ? launch_hg<1, 0>(a, grid, stream) : launch_hg<2, 0>(a, grid, stream);
     return G <= 4 ? launch_hg<1, kLutVOffset>(a, grid, stream) : launch_hg<2, kLutVOffset>(a, grid, stream);
+}
+
+int launch_attention_fixed_partial(const Pages& pg, const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                                   const uint8_t* krec, const int8_t* kmq, const uint16_t* kms,
+                                   const uint8_t* vrec, const int32_t* seq_lens, int32_t t_cap, float scale,
+                                   void* ws, uint32_t* status, hipStream_t stream) {
+    const int G = Hq / Hkv;
+    if (G > 4) return DQ_ERR_INVALID_ARG;
+    AttnArgs a{};
+    // no tables: the layout keeps a minimal (unused) table region
+    a.tk.n = a.tv.n = kD;
+    a.tk.M = a.tv.M = 4;
+    a.tk.p = a.tv.p = 8;
+    a.tk.C = a.tv.C = kFixedRecordBytes;
+    a.shared_lut = 1;
+    a.L = attn_layout(8, 8, kFixedRecordBytes, kFixedRecordBytes, G, true, rw_pair(9, 9));
+    if (a.L.nw < 1) return DQ_ERR_INVALID_ARG;
+    const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap, cu_count());
+    a.q = q;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.G = G;
+    a.t_cap = t_cap;
+    a.chunk = plan.chunk;
+    a.nchunks = plan.nchunks;
+    a.krec = krec;
+    a.kmq = kmq;
+    a.kms = kms;
+    a.vrec = vrec;
+    a.seq_lens = seq_lens;
+    a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
+    a.ws_hdr = static_cast<int32_t*>(ws);
+    a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
+    a.ws_m = a.ws_acc + plan.slots_max * kD;
+    a.ws_l = a.ws_m + plan.slots_max;
+    a.status = status;
+    a.pg = pg;
+    dim3 grid(a.nchunks, Hkv, B);
+    return launch_rw<1, 0, rw_pair(9, 9), true>(a, grid, stream);
 }
 
 int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,

@@ -338,7 +338,36 @@ __device__ __forceinline__ void stream_values(const EncArgs& a, int b, int h, in
     }
 }
 
-template <int VPL, int MB, bool TOK>
+// Nearest level on the grid (o, s): argmin_m (x - (o + s m))^2, the same
+// arithmetic as the distortions of a drift, ties to the smallest m.
+template <int VPL>
+__device__ __forceinline__ void nearest(const double (&x)[VPL], double s, double o, int M, int (&m)[VPL]) {
+    double best[VPL];
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) {
+        best[k] = DBL_MAX;
+        m[k] = 0;
+    }
+    for (int mm = 0; mm < M; ++mm) {
+        const double t = s * (double)mm;
+        const double u = o + t;
+#pragma unroll
+        for (int k = 0; k < VPL; ++k) {
+            const double e = x[k] - u;
+            const double D = e * e;
+            if (D < best[k] || mm == 0) {
+                best[k] = D;
+                m[k] = mm;
+            }
+        }
+    }
+}
+
+// FIXED: the fixed-width comparator of App. B -- the same preprocessing and
+// refit with nearest-level rounding in place of both drifts, and b-bit
+// symbols (M = 2^b, b = 8 (C - 4) / n rounded down) packed after the 4-byte
+// header, least significant bit first, instead of the rANS payload.
+template <int VPL, int MB, bool TOK, bool FIXED = false>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     constexpr int n = kWave * VPL;
     extern __shared__ __align__(16) uint8_t smem[];
@@ -363,7 +392,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     const int active = min(kEncStreams, a.t0 + a.n_new - first);
     const int C = ta.C;
 
-    for (int i = tid; i < ta.M; i += kEncThreads) {
+    for (int i = tid; i < (FIXED ? 0 : ta.M); i += kEncThreads) {
         s_cost[i] = ta.t.cost[i];
         s_rate[i] = (double)ta.t.cost[i] * (1.0 / 65536.0);
         // floor(x / f) = mulhi(x, rcp) >> (sh - 1) for x < 2^31, where
@@ -373,7 +402,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
         s_rcp[i] = f > 1 ? (uint32_t)(((1ull << (31 + sh)) + f - 1) / f) : 0u;
         s_rsh[i] = f > 1 ? sh - 1u : 0u;
     }
-    for (int i = tid; i < kLambdaSteps; i += kEncThreads) s_lam[i] = ta.t.lam[i];
+    for (int i = tid; i < (FIXED ? 0 : kLambdaSteps); i += kEncThreads) s_lam[i] = ta.t.lam[i];
     for (int i = tid; i < kEncStreams; i += kEncThreads) {
         s_budget[i] = ta.budget;
         s_flag[i] = 0;
@@ -403,7 +432,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
                 const double s0 = (mx - mn) / (double)(ta.M - 1);
                 const double o0 = mn;
                 int m1[VPL];
-                drift<VPL, MB>(x, s0, o0, ta.budget, dc, m1);
+                if (FIXED)
+                    nearest<VPL>(x, s0, o0, ta.M, m1);
+                else
+                    drift<VPL, MB>(x, s0, o0, ta.budget, dc, m1);
                 // least-squares refit
                 int sm = 0, smm = 0;
                 double mx_[VPL];
@@ -445,12 +477,38 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
             const double s16 = (double)__half2float(__ushort_as_half(sb16));
             const double o16 = (double)__half2float(__ushort_as_half(ob16));
             int m2[VPL];
-            drift<VPL, MB>(x, s16, o16, s_budget[i], dc, m2);
+            if (FIXED)
+                nearest<VPL>(x, s16, o16, ta.M, m2);
+            else
+                drift<VPL, MB>(x, s16, o16, s_budget[i], dc, m2);
 #pragma unroll
             for (int k = 0; k < VPL; ++k) s_sym[i * n + lane + kWave * k] = (uint8_t)m2[k];
         }
         __syncthreads();
 
+        if (FIXED) {
+            // b-bit symbols after the header, lane per stream
+            if (tid < active) {
+                const int i = tid;
+                uint8_t* rec = s_rec + i * C;
+                const int bb = 31 - __builtin_clz(ta.M);
+                for (int k = 0; k < C - 4; ++k) {
+                    uint32_t v = 0;
+                    for (int t = 0; t < 8; ++t) {
+                        const int g = 8 * k + t, j = g / bb;
+                        if (j < n) v |= (uint32_t)((s_sym[i * n + j] >> (g - j * bb)) & 1) << t;
+                    }
+                    rec[4 + k] = (uint8_t)v;
+                }
+                const uint16_t sb = s_s16[i], ob = s_o16[i];
+                rec[0] = (uint8_t)(sb & 0xFF);
+                rec[1] = (uint8_t)(sb >> 8);
+                rec[2] = (uint8_t)(ob & 0xFF);
+                rec[3] = (uint8_t)(ob >> 8);
+            }
+            __syncthreads();
+            break;
+        }
         // Backward rANS, lane per stream (Eq. rans, encoded in reverse).
         if (tid < active && (pass == 0 || s_flag[tid])) {
             const int i = tid;
@@ -621,6 +679,54 @@ int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int
     }
 #undef DQ_ENC
     return hip_check("kernel launch", hipGetLastError());
+}
+
+int launch_encode_fixed(int32_t n, int32_t record_bytes, const Pages& pg, const uint16_t* kv, int64_t sb,
+                        int64_t st, int64_t sh, int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
+                        uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status,
+                        hipStream_t stream) {
+    const int vpl = n / kWave;
+    const int bits = 8 * (record_bytes - 4) / n;
+    if (vpl < 1 || vpl > 4 || bits < 1 || bits > 8) return DQ_ERR_INVALID_ARG;
+    if (mean_q) {
+        dim3 grid(n_new / DQ_MEAN_WINDOW, H, B);
+        switch (vpl) {
+            case 1: key_mean_kernel<1><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
+            case 2: key_mean_kernel<2><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
+            default: key_mean_kernel<4><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
+        }
+        if (int rc = hip_check("key_mean launch", hipGetLastError())) return rc;
+    }
+    EncArgs a{};
+    a.ta.n = n;
+    a.ta.M = 1 << bits;
+    a.ta.C = record_bytes;
+    a.kv = kv;
+    a.sb = sb;
+    a.st = st;
+    a.sh = sh;
+    a.H = H;
+    a.t0 = t0;
+    a.n_new = n_new;
+    a.t_cap = t_cap;
+    a.pg = pg;
+    a.rec_stride = 0;
+    a.records = records;
+    a.mean_q = mean_q;
+    a.mean_scale = mean_scale;
+    a.status = status;
+    const size_t smem = sizeof(double) * DQ_MAX_LEVELS + sizeof(int32_t) * DQ_MAX_LEVELS +
+                        sizeof(float) * kLambdaSteps + sizeof(int64_t) * kEncStreams +
+                        2 * sizeof(uint16_t) * kEncStreams + sizeof(int32_t) * kEncStreams +
+                        2 * sizeof(uint32_t) * DQ_MAX_LEVELS +
+                        (size_t)kEncStreams * n + (size_t)kEncStreams * record_bytes;
+    dim3 grid((n_new + kEncStreams - 1) / kEncStreams, H, B);
+    switch (vpl) {
+        case 1: encode_kernel<1, 0, false, true><<<grid, kEncThreads, smem, stream>>>(a); break;
+        case 2: encode_kernel<2, 0, false, true><<<grid, kEncThreads, smem, stream>>>(a); break;
+        default: encode_kernel<4, 0, false, true><<<grid, kEncThreads, smem, stream>>>(a); break;
+    }
+    return hip_check("encode_fixed launch", hipGetLastError());
 }
 
 }  // namespace dq

@@ -369,6 +369,46 @@ int dq_encode_kv_token(const dq_tables* t, const uint16_t* kv, int64_t sb, int64
                      status, stream, stride);
 }
 
+int32_t dq_fixed_bits(int32_t head_dim, int32_t record_bytes) {
+    if (head_dim <= 0 || record_bytes <= 4) return 0;
+    const int64_t b = 8 * (int64_t)(record_bytes - 4) / head_dim;
+    return b >= 1 && b <= 8 ? (int32_t)b : 0;
+}
+
+int dq_encode_kv_fixed(int32_t head_dim, int32_t record_bytes, const uint16_t* kv, int64_t sb, int64_t st,
+                       int64_t sh, int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
+                       uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status, void* stream) {
+    if (!kv || !records) return DQ_ERR_INVALID_ARG;
+    if (head_dim != 64 && head_dim != 128 && head_dim != 256) return DQ_ERR_INVALID_ARG;
+    if (dq_fixed_bits(head_dim, record_bytes) == 0 || record_bytes > 2 * head_dim + 8) return DQ_ERR_INVALID_ARG;
+    if (B < 0 || H <= 0 || t0 < 0 || n_new < 0 || t_cap <= 0 || t0 + n_new > t_cap) return DQ_ERR_INVALID_ARG;
+    if (B > 65535 || H > 65535) return DQ_ERR_INVALID_ARG;
+    if (sb < 0 || st < 0 || sh < 0) return DQ_ERR_INVALID_ARG;
+    const bool keys = mean_q != nullptr;
+    if (keys != (mean_scale != nullptr)) return DQ_ERR_INVALID_ARG;
+    if (keys && ((t0 % DQ_MEAN_WINDOW) || (n_new % DQ_MEAN_WINDOW) || (t_cap % DQ_MEAN_WINDOW)))
+        return DQ_ERR_INVALID_ARG;
+    if (B == 0 || n_new == 0) return DQ_OK;
+    return dq::launch_encode_fixed(head_dim, record_bytes, kContiguous, kv, sb, st, sh, B, H, t0, n_new, t_cap,
+                                   records, mean_q, mean_scale, status, static_cast<hipStream_t>(stream));
+}
+
+int dq_decode_attention_fixed_partial(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                                      const uint8_t* k_records, const int8_t* k_mean_q,
+                                      const uint16_t* k_mean_scale, const uint8_t* v_records,
+                                      const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
+                                      size_t ws_bytes, uint32_t* status, void* stream) {
+    if (B <= 0 || B > 65535 || Hkv <= 0 || Hkv > 65535 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 4)
+        return DQ_ERR_INVALID_ARG;
+    if (t_cap <= 0 || t_cap % DQ_MEAN_WINDOW) return DQ_ERR_INVALID_ARG;
+    if (!q || !k_records || !k_mean_q || !k_mean_scale || !v_records || !seq_lens) return DQ_ERR_INVALID_ARG;
+    if (!std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128)) return DQ_ERR_WORKSPACE;
+    return dq::launch_attention_fixed_partial(kContiguous, q, B, Hq, Hkv, k_records, k_mean_q, k_mean_scale,
+                                              v_records, seq_lens, t_cap, scale, ws, status,
+                                              static_cast<hipStream_t>(stream));
+}
+
 size_t dq_decode_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d) {
     if (B <= 0 || Hq <= 0 || Hkv <= 0 || t_cap <= 0 || d <= 0) return 0;
     return dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, d);

@@ -154,6 +154,20 @@ int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, con
                                    void* ws, uint32_t* status, hipStream_t stream);
 int32_t token_chunk(int32_t B, int32_t t_cap);
 
+// Fixed-width comparator (App. B): 36-byte records of 128 2-bit levels
+// ([fp16 s][fp16 o][32 payload bytes]), head_dim 128, G <= 4; same workspace.
+constexpr int kFixedRecordBytes = 36;
+int launch_attention_fixed_partial(const Pages& pg, const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                                   const uint8_t* krec, const int8_t* kmq, const uint16_t* kms,
+                                   const uint8_t* vrec, const int32_t* seq_lens, int32_t t_cap, float scale,
+                                   void* ws, uint32_t* status, hipStream_t stream);
+// Fixed-width encoder: same preprocessing, nearest-level rounding, b-bit
+// symbols packed after the 4-byte header of a C-byte record.
+int launch_encode_fixed(int32_t n, int32_t record_bytes, const Pages& pg, const uint16_t* kv, int64_t sb,
+                        int64_t st, int64_t sh, int32_t B, int32_t H, int32_t t0, int32_t n_new, int32_t t_cap,
+                        uint8_t* records, int8_t* mean_q, uint16_t* mean_scale, uint32_t* status,
+                        hipStream_t stream);
+
 int launch_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
                               const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
                               const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
