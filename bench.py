@@ -36,9 +36,15 @@ HBM_PEAK_GBS = 8000.0
 # VALU issue peak: 256 CUs x 4 SIMDs, a wave64 instruction occupies a 16-lane
 # SIMD for 4 cycles, 2.4 GHz
 VALU_PEAK_GINST = 256 * 4 / 4 * 2.4
-COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "attn_partial_b16_t32k_pmc.md")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2609_19880_amd", "csrc", f)
-                  for f in ("dq_decode.hip", "dq_common.h", "dq_internal.h")]
+# committed counter summaries: (workload, variant) -> (summary, kernel sources it was taken from)
+_CSRC = os.path.join(ROOT, "paper_2609_19880_amd", "csrc")
+COUNTER_SUMMARIES = {
+    ("b16_t32k", "paper"): (os.path.join(ROOT, "profiles", "attn_partial_b16_t32k_pmc.md"),
+                            [os.path.join(_CSRC, f) for f in ("dq_decode.hip", "dq_common.h", "dq_internal.h")]),
+    ("b16_t32k_tok", "paper"): (os.path.join(ROOT, "profiles", "attn_token_b16_t32k_tok_pmc.md"),
+                                [os.path.join(_CSRC, f)
+                                 for f in ("dq_token.hip", "dq_attn.h", "dq_common.h", "dq_internal.h")]),
+}
 
 
 def _args():
@@ -97,11 +103,14 @@ def counter_figures(workload: str, variant: str):
     kernel sources as they are now (else None)."""
     import hashlib
     import re
-    if (workload, variant) != ("b16_t32k", "paper") or not os.path.exists(COUNTER_SUMMARY):
+    if (workload, variant) not in COUNTER_SUMMARIES:
         return None
-    text = open(COUNTER_SUMMARY).read()
+    summary, sources = COUNTER_SUMMARIES[(workload, variant)]
+    if not os.path.exists(summary):
+        return None
+    text = open(summary).read()
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in sources:
         h.update(open(f, "rb").read())
     m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
     m_tr = re.search(r"traffic_bytes_per_launch:\s*(\d+)", text)
