@@ -372,7 +372,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     constexpr int n = kWave * VPL;
     extern __shared__ __align__(16) uint8_t smem[];
     // layout: rate[64] f64 | cost[64] | lam[512] | budget[64] i64 | s16[64] | o16[64]
-    //         | flag[64] | rcp[64] | rsh[64] | sym[64][n] | rec[64][C]
+    //         | flag[64] | (f, c, rcp, rsh)[64] | sym[64][n] | rec[64][C]
     double* s_rate = reinterpret_cast<double*>(smem);
     int32_t* s_cost = reinterpret_cast<int32_t*>(s_rate + DQ_MAX_LEVELS);
     float* s_lam = reinterpret_cast<float*>(s_cost + DQ_MAX_LEVELS);
@@ -380,9 +380,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     uint16_t* s_s16 = reinterpret_cast<uint16_t*>(s_budget + kEncStreams);
     uint16_t* s_o16 = s_s16 + kEncStreams;
     int32_t* s_flag = reinterpret_cast<int32_t*>(s_o16 + kEncStreams);
-    uint32_t* s_rcp = reinterpret_cast<uint32_t*>(s_flag + kEncStreams);
-    uint32_t* s_rsh = s_rcp + DQ_MAX_LEVELS;
-    uint8_t* s_sym = reinterpret_cast<uint8_t*>(s_rsh + DQ_MAX_LEVELS);
+    uint4* s_ent = reinterpret_cast<uint4*>(s_flag + kEncStreams);     // coder entry per symbol
+    uint8_t* s_sym = reinterpret_cast<uint8_t*>(s_ent + DQ_MAX_LEVELS);
     uint8_t* s_rec = s_sym + kEncStreams * n;
 
     const TabArgs& ta = a.ta;
@@ -399,8 +398,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
         // sh = ceil(log2 f) and rcp = ceil(2^(31 + sh) / f) (f = 1: x itself)
         const uint32_t f = (uint32_t)ta.t.freq[i];
         const uint32_t sh = f > 1 ? 32u - (uint32_t)__builtin_clz(f - 1u) : 0u;
-        s_rcp[i] = f > 1 ? (uint32_t)(((1ull << (31 + sh)) + f - 1) / f) : 0u;
-        s_rsh[i] = f > 1 ? sh - 1u : 0u;
+        s_ent[i] = uint4{f, (uint32_t)ta.t.cum[i], f > 1 ? (uint32_t)(((1ull << (31 + sh)) + f - 1) / f) : 0u,
+                         f > 1 ? sh - 1u : 0u};
     }
     for (int i = tid; i < (FIXED ? 0 : kLambdaSteps); i += kEncThreads) s_lam[i] = ta.t.lam[i];
     for (int i = tid; i < kEncStreams; i += kEncThreads) {
@@ -520,9 +519,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
             const uint32_t P = 1u << ta.p;
             for (int j = n - 1; j >= 0; --j) {
                 const int m = s_sym[i * n + j];
-                const uint32_t f = (uint32_t)ta.t.freq[m];
-                const uint32_t c = (uint32_t)ta.t.cum[m];
-                const uint32_t rcp = s_rcp[m], rsh = s_rsh[m];
+                const uint4 ent = s_ent[m];
+                const uint32_t f = ent.x, c = ent.y, rcp = ent.z, rsh = ent.w;
                 const uint32_t xmax = xmax_unit * f;
 #pragma unroll
                 for (int r = 0; r < 2; ++r) {
@@ -642,7 +640,7 @@ int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int
     const size_t smem = sizeof(double) * DQ_MAX_LEVELS + sizeof(int32_t) * DQ_MAX_LEVELS +
                         sizeof(float) * kLambdaSteps + sizeof(int64_t) * kEncStreams +
                         2 * sizeof(uint16_t) * kEncStreams + sizeof(int32_t) * kEncStreams +
-                        2 * sizeof(uint32_t) * DQ_MAX_LEVELS +
+                        sizeof(uint4) * DQ_MAX_LEVELS +
                         (size_t)kEncStreams * n + (size_t)kEncStreams * a.ta.C;
     dim3 grid((n_new + kEncStreams - 1) / kEncStreams, tok ? 1 : H, B);
     // distortions held in registers for up to 8 levels (16 with two values per
@@ -718,7 +716,7 @@ int launch_encode_fixed(int32_t n, int32_t record_bytes, const Pages& pg, const 
     const size_t smem = sizeof(double) * DQ_MAX_LEVELS + sizeof(int32_t) * DQ_MAX_LEVELS +
                         sizeof(float) * kLambdaSteps + sizeof(int64_t) * kEncStreams +
                         2 * sizeof(uint16_t) * kEncStreams + sizeof(int32_t) * kEncStreams +
-                        2 * sizeof(uint32_t) * DQ_MAX_LEVELS +
+                        sizeof(uint4) * DQ_MAX_LEVELS +
                         (size_t)kEncStreams * n + (size_t)kEncStreams * record_bytes;
     dim3 grid((n_new + kEncStreams - 1) / kEncStreams, H, B);
     switch (vpl) {
