@@ -214,3 +214,67 @@ def test_token_entry_points_reject_bad_arguments(dq):
     rc = lib.dq_encode_kv_token(gtk.handle, p, 0, 128 * H, 128, B, 4, 0, 128, T, p, p, p, p, None)
     assert rc == dq.DQ_ERR_INVALID_ARG                          # 4 heads do not make n = 1024
     assert lib.dq_token_record_stride(None) == 0
+
+
+def test_token_streams_with_residual_window(dq):
+    """The paper's serving configuration (Sec. 5.1): per-token streams for the
+    compressed tokens plus the newest tokens raw in BF16.  Per-token partial +
+    residual partial + merge against the oracle's attention over the token-wise
+    reconstructions and the raw tokens (reading A3)."""
+    H, G, B, t_cap, r_cap = 8, 4, 3, 384, 256
+    gtk, otk = _tabs(dq, 1024, 8, 335, 8)
+    gtv, otv = _tabs(dq, 1024, 6, 235, 8)
+    comp = [256, 0, 128]                      # compressed tokens (whole windows)
+    res = [128, 40, 0]                        # raw tokens after them
+    T = max(c + r for c, r in zip(comp, res))
+    k, v, q = _inputs(H, G, B, T, 36)
+    kb, vb = wlmod.bf16_bits(k), wlmod.bf16_bits(v)
+    grk = torch.zeros(dq.token_records_shape(gtk, B, t_cap), dtype=torch.uint8, device=DEV)
+    grv = torch.zeros(dq.token_records_shape(gtv, B, t_cap), dtype=torch.uint8, device=DEV)
+    gmq = torch.zeros((B, H, t_cap // 128, 128), dtype=torch.int8, device=DEV)
+    gms = torch.zeros((B, H, t_cap // 128), dtype=torch.int16, device=DEV)
+    rk = torch.zeros((B, H, r_cap, 128), dtype=torch.bfloat16, device=DEV)
+    rv = torch.zeros_like(rk)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    kd, vd = k.to(DEV), v.to(DEV)
+    for b in range(B):
+        n = comp[b]
+        if n:
+            dq.dq_encode_kv_token(gtk, kd[b:b + 1, :n], 0, t_cap, grk[b:b + 1], gmq[b:b + 1], gms[b:b + 1], status)
+            dq.dq_encode_kv_token(gtv, vd[b:b + 1, :n], 0, t_cap, grv[b:b + 1], None, None, status)
+        for i in range(res[b]):
+            rk[b, :, (n + i) % r_cap] = kd[b, n + i]
+            rv[b, :, (n + i) % r_cap] = vd[b, n + i]
+    seq = torch.tensor(comp, dtype=torch.int32, device=DEV)
+    rl = torch.tensor(res, dtype=torch.int32, device=DEV)
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, t_cap), dtype=torch.uint8, device=DEV)
+    out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
+    qd = q.to(DEV)
+    dq.dq_decode_attention_token_partial(gtk, gtv, qd, grk, gmq, gms, grv, seq, ws, status=status)
+    dq.dq_decode_attention_residual(qd, rk, rv, seq, rl, t_cap, ws)
+    dq.dq_decode_attention_merge(B, H * G, H, seq, t_cap, ws, out)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    # oracle: token-wise reconstruction of the compressed tokens, raw residual tokens
+    Tc = max(comp)
+    k_rot = np.zeros((B, H, Tc, 128))
+    v_rot = np.zeros((B, H, Tc, 128))
+    res_k = np.zeros((B, H, max(res), 128))
+    res_v = np.zeros((B, H, max(res), 128))
+    for b in range(B):
+        n = comp[b]
+        if n:
+            krec, mq, ms, ksym = kv.encode_keys_tokenwise(kb[b:b + 1, :n], otk)
+            vrec, vsym = kv.encode_values_tokenwise(vb[b:b + 1, :n], otv)
+            _, ks, ko, _ = kv.decode_records(krec, otk, 1024)
+            _, vs, vo, _ = kv.decode_records(vrec, otv, 1024)
+            kh, ksh, koh = kv.tokenwise_as_heads(ksym, ks, ko, H)
+            vh, vsh, voh = kv.tokenwise_as_heads(vsym, vs, vo, H)
+            k_rot[b, :, :n] = attention.dequantize(kh, ksh, koh, kmean.dequantize_mean(mq, ms))[0]
+            v_rot[b, :, :n] = attention.dequantize(vh, vsh, voh)[0]
+        r = res[b]
+        res_k[b, :, :r] = np.moveaxis(kv.bf16_to_f64(kb[b, n:n + r]), 0, 1)
+        res_v[b, :, :r] = np.moveaxis(kv.bf16_to_f64(vb[b, n:n + r]), 0, 1)
+    ref = attention.attention_with_residual(kv.bf16_to_f64(wlmod.bf16_bits(q)), k_rot, v_rot, comp, res_k, res_v,
+                                            res, G, 1 / np.sqrt(128))
+    assert _rel_err(out.cpu().numpy().astype(np.float64), ref) < TOL
