@@ -69,6 +69,41 @@ def _args():
     return ap.parse_args()
 
 
+def time_steps(calls, steps: int, warmup: int):
+    """Time `steps` decode steps, each the launches in `calls` in order on the
+    current stream.  The timed region holds only the steps, bracketed by a
+    synchronize and one HIP event on each side (no events between kernels).
+    A second pass with an event pair around every launch gives each launch's
+    mean duration.  Returns (ms per step, [mean ms per call], wall seconds of
+    the timed region)."""
+    import torch
+    for _ in range(warmup):
+        for c in calls:
+            c()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        for c in calls:
+            c()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    step_ms = e0.elapsed_time(e1) / steps
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in calls]
+          for _ in range(steps)]
+    for i in range(steps):
+        for j, c in enumerate(calls):
+            ev[i][j][0].record()
+            c()
+            ev[i][j][1].record()
+    torch.cuda.synchronize()
+    per_call = [sum(ev[i][j][0].elapsed_time(ev[i][j][1]) for i in range(steps)) / steps
+                for j in range(len(calls))]
+    return step_ms, per_call, wall
+
+
 def _cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -260,20 +295,9 @@ def bf16_comparator(wl, a, q, seq, out, ws, alg_bytes):
     g.manual_seed(a.seed * 7 + 11)
     k = torch.randn((B, Hkv, T, d), generator=g, device="cuda").to(torch.bfloat16)
     v = torch.randn((B, Hkv, T, d), generator=g, device="cuda").to(torch.bfloat16)
-    for _ in range(a.warmup):
-        dq.dq_bf16_decode_attention_partial(q, k, v, seq, ws)
-        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
-    torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 * a.steps)]
-    for i in range(a.steps):
-        ev[3 * i].record()
-        dq.dq_bf16_decode_attention_partial(q, k, v, seq, ws)
-        ev[3 * i + 1].record()
-        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
-        ev[3 * i + 2].record()
-    torch.cuda.synchronize()
-    pms = sum(ev[3 * i].elapsed_time(ev[3 * i + 1]) for i in range(a.steps)) / a.steps
-    sms = ev[0].elapsed_time(ev[-1]) / a.steps
+    sms, (pms, _), _ = time_steps([lambda: dq.dq_bf16_decode_attention_partial(q, k, v, seq, ws),
+                                   lambda: dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)],
+                                  a.steps, a.warmup)
     nbytes = 2 * B * Hkv * T * d * 2
     del k, v
     torch.cuda.empty_cache()
@@ -306,20 +330,9 @@ def fixed_comparator(wl, a, q, seq, out, ws):
     torch.cuda.synchronize()
     if int(status.item()):
         raise RuntimeError(f"fixed-width encoder status {int(status.item())}")
-    for _ in range(a.warmup):
-        dq.dq_decode_attention_fixed_partial(q, kr, mq, ms, vr, seq, ws)
-        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
-    torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 * a.steps)]
-    for i in range(a.steps):
-        ev[3 * i].record()
-        dq.dq_decode_attention_fixed_partial(q, kr, mq, ms, vr, seq, ws)
-        ev[3 * i + 1].record()
-        dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)
-        ev[3 * i + 2].record()
-    torch.cuda.synchronize()
-    pms = sum(ev[3 * i].elapsed_time(ev[3 * i + 1]) for i in range(a.steps)) / a.steps
-    sms = ev[0].elapsed_time(ev[-1]) / a.steps
+    sms, (pms, _), _ = time_steps([lambda: dq.dq_decode_attention_fixed_partial(q, kr, mq, ms, vr, seq, ws),
+                                   lambda: dq.dq_decode_attention_merge(B, Hq, Hkv, seq, T, ws, out)],
+                                  a.steps, a.warmup)
     nbytes = B * Hkv * T * (2 * C + (d + 2) / 128)
     del kr, vr, mq, ms
     torch.cuda.empty_cache()
@@ -371,32 +384,15 @@ def main():
         rl = torch.full((B,), a.residual, dtype=torch.int32, device=dev)
         ring = (rk, rv, rl)
 
-    def step():
-        decode_step(tk, tv, cache, q, seq, out, ring)
-
-    for _ in range(a.warmup):
-        step()
-    torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4 * a.steps)]
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    for i in range(a.steps):
-        ev[4 * i].record()
-        cache.partial(q, seq)
-        ev[4 * i + 1].record()
-        if ring is not None:
-            dq.dq_decode_attention_residual(q, ring[0], ring[1], seq, ring[2], T, cache.workspace)
-        ev[4 * i + 2].record()
-        cache.merge(seq, out)
-        ev[4 * i + 3].record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
+    calls = [lambda: cache.partial(q, seq)]
+    if ring is not None:
+        calls.append(lambda: dq.dq_decode_attention_residual(q, ring[0], ring[1], seq, ring[2], T, cache.workspace))
+    calls.append(lambda: cache.merge(seq, out))
+    step_ms, per_call, wall = time_steps(calls, a.steps, a.warmup)
     if int(cache.status.item()):
         raise RuntimeError(f"decode status {int(cache.status.item())}")
-    partial_ms = sum(ev[4 * i].elapsed_time(ev[4 * i + 1]) for i in range(a.steps)) / a.steps
-    residual_ms = sum(ev[4 * i + 1].elapsed_time(ev[4 * i + 2]) for i in range(a.steps)) / a.steps
-    merge_ms = sum(ev[4 * i + 2].elapsed_time(ev[4 * i + 3]) for i in range(a.steps)) / a.steps
-    step_ms = ev[0].elapsed_time(ev[-1]) / a.steps
+    partial_ms, merge_ms = per_call[0], per_call[-1]
+    residual_ms = per_call[1] if ring is not None else 0.0
 
     # algorithmic bytes of one partial launch: per (token, KV head) the two
     # records plus the amortized INT8 key mean and its fp16 scale (per token
