@@ -103,7 +103,7 @@ __global__ __launch_bounds__(kThreads) void bf16_partial_kernel(B16Args a) {
 #pragma unroll
         for (int g = 0; g < GP; ++g) {
             const float s = (valid && g < G) ? dot[g] * a.scale_log2 : -INFINITY;
-            const float mn = fmaxf(m_run[g], wave_max(s));
+            const float mn = fmaxf(m_run[g], wave_max_f32(s));
             const float corr = (m_run[g] == -INFINITY || mn == -INFINITY) ? (m_run[g] == mn ? 1.f : 0.f)
                                                                            : __builtin_amdgcn_exp2f(m_run[g] - mn);
             const float p = s == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(s - mn);

@@ -82,12 +82,54 @@ __device__ __forceinline__ T wave_min(T v) {
     return wave_reduce(v, [](T a, T b) { return a < b ? a : b; });
 }
 
-__device__ __forceinline__ int wave_sum_i32(int v) {
-    return wave_reduce(v, [](int a, int b) { return a + b; });
+// Sums: the lanes a row mask leaves out take 0 instead of their own value,
+// which lets each step be one add with a DPP source.  The lanes read at the
+// end (lane 63's row) see the same additions in the same order either way.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp0_u32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROW_MASK, 0xF, false);
 }
 
-__device__ __forceinline__ float wave_sum_f32(float v) {
-    return wave_reduce(v, [](float a, float b) { return a + b; });
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp0(int v) { return (int)dpp0_u32<CTRL, ROW_MASK>((uint32_t)v); }
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp0(float v) { return __uint_as_float(dpp0_u32<CTRL, ROW_MASK>(__float_as_uint(v))); }
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+    v += dpp0<0xB1, 0xF>(v);
+    v += dpp0<0x4E, 0xF>(v);
+    v += dpp0<0x141, 0xF>(v);
+    v += dpp0<0x140, 0xF>(v);
+    v += dpp0<0x142, 0xA>(v);
+    v += dpp0<0x143, 0xC>(v);
+    return lane63(v);
+}
+
+__device__ __forceinline__ int wave_sum_i32(int v) { return wave_sum(v); }
+
+__device__ __forceinline__ float wave_sum_f32(float v) { return wave_sum(v); }
+
+// Maximum of non-NaN floats (the sign of a zero result is unspecified), one
+// v_max_f32 with a DPP source per step.  The DPP operand's wait states after a
+// VALU write (and after a VALU write of EXEC) are issued here, since the
+// compiler does not look inside the statements.
+__device__ __forceinline__ float wave_max_f32(float v) {
+    asm("s_nop 4\n\t"
+        "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_f32_dpp %0, %0, %0 row_half_mirror row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_f32_dpp %0, %0, %0 row_mirror row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+        "s_nop 1"
+        : "+v"(v));
+    return lane63(v);
 }
 
 }  // namespace dq

@@ -196,7 +196,9 @@ __device__ __forceinline__ void build_pairs(const uint32_t (&r)[kMaxRecDwords], 
 // for longer or run-time-length records, whose prefetched record words need
 // more registers.  Up to 8 query heads: 12 (at most 168 VGPRs), without the
 // record prefetch, whose registers the larger accumulators need; 8 for
-// run-time record lengths.
+// run-time record lengths.  When LDS holds no more than 8 wavefronts anyway
+// (two 4096-entry tables), the 8-wavefront instantiation (256 VGPRs) keeps
+// the prefetch.
 // RWP packs the compile-time record lengths in dwords, keys << 8 | values
 // (0: run-time lengths).
 __host__ __device__ constexpr int rw_pair(int rwk, int rwv) { return (rwk << 8) | rwv; }
@@ -221,8 +223,9 @@ __device__ __forceinline__ uint32_t spread2(uint32_t x) {
 
 // FIXED: the fixed-width comparator at matched storage; levels come straight
 // from the record words (no tables, no byte pairs, no rANS state).
-template <int HG, uint32_t LUTV, int RWP, bool FIXED = false>
-__global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kernel(AttnArgs a) {
+// WMAX: the wavefront bound of the instantiation (max_waves, or 8).
+template <int HG, uint32_t LUTV, int RWP, bool FIXED, int WMAX>
+__global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) {
     constexpr int RWK = RWP >> 8, RWV = RWP & 0xFF;
     constexpr int GP = 4 * HG;
     extern __shared__ __align__(16) uint8_t smem[];
@@ -341,8 +344,9 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
     const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
 
     // records of the wavefront's next tile are loaded while it decodes this one
-    // (up to 4 query heads per KV head; with 8 the registers go to accumulators)
-    constexpr bool kPrefetch = HG == 1;
+    // (up to 4 query heads per KV head; with 8 the registers go to accumulators
+    // unless the workgroup has at most 8 wavefronts)
+    constexpr bool kPrefetch = HG == 1 || WMAX <= 8;
     uint32_t rk[kMaxRecDwords], rv[kMaxRecDwords];
     if (kPrefetch && wave < ntiles) {
         const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, start + wave * kTile, bad_page) + lane;
@@ -454,7 +458,7 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
                 const int g = 4 * hg + r;
                 const float dot = combine(dk[hg][0], dk[hg][1], dk[hg][2], r) * qscale[g];
                 const float score = (valid && g < G) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
-                const float tmax = wave_max(score);
+                const float tmax = wave_max_f32(score);
                 const float mn = fmaxf(m_run[g], tmax);
                 // v_exp_f32 directly: arguments are <= 0 and results that would
                 // be denormal may flush to zero
@@ -467,7 +471,7 @@ __global__ __launch_bounds__(max_waves(HG, RWP) * kWave) void attn_partial_kerne
                 accf[1][g] *= corr;
                 m_run[g] = mn;
                 const float pw = p * sv;                 // >= 0: scales are non-negative
-                const float smax = wave_max(pw);
+                const float smax = wave_max_f32(pw);
                 pscale[g] = smax * (1.0f / 4194304.0f);
                 // 22-bit fixed point of pw relative to the tile maximum
                 const float inv = smax > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax) : 0.f;
@@ -943,14 +947,26 @@ bool attention_supports(const dq_tables* tk, const dq_tables* tv) {
     return true;
 }
 
+template <int HG, uint32_t LUTV, int RWP, bool FIXED, int WMAX>
+static int launch_w(AttnArgs& a, dim3 grid, hipStream_t stream) {
+    if (a.L.nw > WMAX) return DQ_ERR_INVALID_ARG;
+    if (int rc = hip_check("hipFuncSetAttribute",
+                           hipFuncSetAttribute(
+                               reinterpret_cast<const void*>(&attn_partial_kernel<HG, LUTV, RWP, FIXED, WMAX>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
+        return rc;
+    attn_partial_kernel<HG, LUTV, RWP, FIXED, WMAX><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
+    return hip_check("attn_partial launch", hipGetLastError());
+}
+
+// Eight query heads per KV head with at most 8 wavefronts (LDS-bound): the
+// 8-wavefront instantiation, which prefetches records.
 template <int HG, uint32_t LUTV, int RWP, bool FIXED = false>
 static int launch_rw(AttnArgs& a, dim3 grid, hipStream_t stream) {
-    if (int rc = hip_check("hipFuncSetAttribute",
-                           hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_partial_kernel<HG, LUTV, RWP, FIXED>),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
-        return rc;
-    attn_partial_kernel<HG, LUTV, RWP, FIXED><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
-    return hip_check("attn_partial launch", hipGetLastError());
+    constexpr int W = max_waves(HG, RWP);
+    if constexpr (HG == 2 && W > 8)
+        if (a.L.nw <= 8) return launch_w<HG, LUTV, RWP, FIXED, 8>(a, grid, stream);
+    return launch_w<HG, LUTV, RWP, FIXED, W>(a, grid, stream);
 }
 
 // Record lengths of the 2.0 / 2.25 / 3.0 / 4.0 bits-per-element budgets at

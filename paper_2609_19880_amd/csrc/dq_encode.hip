@@ -20,6 +20,7 @@
 // (this file is built with -ffp-contract=off), so the records are
 // bit-identical to the reference definition of the format.
 #include <float.h>
+#include <limits.h>
 
 #include "dq_common.h"
 
@@ -100,17 +101,26 @@ struct DriftCtx {
     int rmin;
 };
 
+// min of two non-negative, non-NaN doubles as one v_min_f64 (fmin would first
+// quiet possible signalling NaNs, one more instruction per operand).
+__device__ __forceinline__ double min_nonneg(double a, double b) {
+    double r;
+    asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
 // Assignment at one lambda: each value takes argmin_m D_im + lambda r_m (ties to
 // the smallest m); returns the wavefront's total Q16 cost.  MB > 0: the
 // distortions D[k][m] of the M <= MB levels were computed once per drift;
 // MB = 0: they are recomputed here (t = s m, u = o + t, e = x - u, D = e e).
+// rt: the rates R_m / 2^16 of the MB levels in registers (MB > 0).
 template <int VPL, int MB>
 __device__ __forceinline__ int assign_cost(const double (&x)[VPL], const double (&D)[VPL][MB > 0 ? MB : 1],
-                                           double s, double o, double lam, const DriftCtx& c,
-                                           int (&m)[VPL]) {
+                                           const double (&rt)[MB > 0 ? MB : 1], double s, double o,
+                                           double lam, const DriftCtx& c, int (&m)[VPL]) {
     double best[VPL];
     if (MB > 0) {
-        const double pen0 = lam * c.rate[0];
+        const double pen0 = lam * rt[0];
 #pragma unroll
         for (int k = 0; k < VPL; ++k) {
             best[k] = D[k][0] + pen0;
@@ -119,12 +129,12 @@ __device__ __forceinline__ int assign_cost(const double (&x)[VPL], const double 
 #pragma unroll
         for (int mm = 1; mm < (MB > 0 ? MB : 1); ++mm) {
             if (mm < c.M) {
-                const double pen = lam * c.rate[mm];
+                const double pen = lam * rt[mm];
 #pragma unroll
                 for (int k = 0; k < VPL; ++k) {
                     const double J = D[k][mm] + pen;
                     m[k] = J < best[k] ? mm : m[k];
-                    best[k] = fmin(best[k], J);
+                    best[k] = min_nonneg(best[k], J);
                 }
             }
         }
@@ -162,11 +172,12 @@ __device__ __forceinline__ int assign_cost(const double (&x)[VPL], const double 
 template <int VPL, int MB>
 __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget,
                       const DriftCtx& c, int (&m)[VPL]) {
-    double D[VPL][MB > 0 ? MB : 1];
+    double D[VPL][MB > 0 ? MB : 1], rt[MB > 0 ? MB : 1];
     double dmax = -DBL_MAX, dmin = DBL_MAX;
     if (MB > 0) {
 #pragma unroll
         for (int mm = 0; mm < (MB > 0 ? MB : 1); ++mm) {
+            rt[mm] = mm < c.M ? c.rate[mm] : 0.0;
             const double t = s * (double)mm;
             const double u = o + t;
 #pragma unroll
@@ -204,19 +215,22 @@ __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget
     const int hi = (mant == 0.5) ? ex - 1 : ex;
     int u_hi = hi * kLambdaSteps;
     int u_lo = u_hi - kBracketUnits;
+    // the code length is an int: comparing it with the budget clamped to
+    // INT_MAX decides the same and stays a scalar compare
+    const int budget32 = (int)(budget < INT_MAX ? budget : INT_MAX);
     for (int it = 0; it < kBisectSteps; ++it) {
         const int u_mid = (u_lo + u_hi) >> 1;
         const double lam = ldexp((double)c.lam[u_mid & (kLambdaSteps - 1)], u_mid >> 9);
         int tmp[VPL];
-        const int cst = assign_cost<VPL, MB>(x, D, s, o, lam, c, tmp);
-        if ((int64_t)cst <= budget)
+        const int cst = assign_cost<VPL, MB>(x, D, rt, s, o, lam, c, tmp);
+        if (cst <= budget32)
             u_hi = u_mid;
         else
             u_lo = u_mid;
     }
     const double lam = ldexp((double)c.lam[u_hi & (kLambdaSteps - 1)], u_hi >> 9);
-    const int cst = assign_cost<VPL, MB>(x, D, s, o, lam, c, m);
-    if ((int64_t)cst > budget) {
+    const int cst = assign_cost<VPL, MB>(x, D, rt, s, o, lam, c, m);
+    if (cst > budget32) {
         double best[VPL];
 #pragma unroll
         for (int k = 0; k < VPL; ++k) best[k] = DBL_MAX;

@@ -324,7 +324,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
                 const int slot = h * 4 + r;
                 const float dot = combine(dk[0], dk[1], dk[2], r) * qscale[g];
                 const float score = (valid && live) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
-                const float tmax = wave_max(score);
+                const float tmax = wave_max_f32(score);
                 const float m_old = lane_get(m_vec, slot);
                 const float mn = fmaxf(m_old, tmax);
                 corr[r] = (m_old == -INFINITY || mn == -INFINITY) ? (m_old == mn ? 1.f : 0.f)
@@ -336,7 +336,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
                 l_vec = lane_set(l_vec, slot, lane_get(l_vec, slot) * corr[r] + lt, lane);
                 o_vec = lane_set(o_vec, slot, lane_get(o_vec, slot) * corr[r] + ot, lane);
                 const float pw = p * sv;                 // >= 0: scales are non-negative
-                const float smax = wave_max(pw);
+                const float smax = wave_max_f32(pw);
                 pscale[r] = smax * (1.0f / 4194304.0f);
                 const float inv = smax > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax) : 0.f;
                 pint[r] = min(4194304, (int)rintf(pw * inv));
