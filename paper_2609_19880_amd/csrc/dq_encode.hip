@@ -101,12 +101,42 @@ struct DriftCtx {
     int rmin;
 };
 
-// min of two non-negative, non-NaN doubles as one v_min_f64 (fmin would first
-// quiet possible signalling NaNs, one more instruction per operand).
-__device__ __forceinline__ double min_nonneg(double a, double b) {
+// max / min of two non-NaN doubles as one v_max_f64 / v_min_f64 (fmax and
+// fmin would first quiet possible signalling NaNs, one more instruction per
+// operand).  Distortions and penalties are >= +0, so which of two equal zeros
+// comes out never matters.
+__device__ __forceinline__ double max_nn(double a, double b) {
+    double r;
+    asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ double min_nn(double a, double b) {
     double r;
     asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
     return r;
+}
+
+// DPP copy of a double; lanes that a row mask leaves out are undefined, which
+// a reduction read back from lane 63 never sees.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_copy(double v) {
+    const uint64_t u = (uint64_t)__double_as_longlong(v);
+    const uint64_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)u, CTRL, ROW_MASK, 0xF, false);
+    const uint64_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), CTRL, ROW_MASK, 0xF, false);
+    return __longlong_as_double((long long)(lo | (hi << 32)));
+}
+
+// Wavefront max / min of non-NaN doubles with no -0 (the distortions).
+template <bool MAX>
+__device__ __forceinline__ double wave_ext_nn(double v) {
+    auto op = [](double a, double b) { return MAX ? max_nn(a, b) : min_nn(a, b); };
+    v = op(v, dpp_copy<0xB1, 0xF>(v));
+    v = op(v, dpp_copy<0x4E, 0xF>(v));
+    v = op(v, dpp_copy<0x141, 0xF>(v));
+    v = op(v, dpp_copy<0x140, 0xF>(v));
+    v = op(v, dpp_copy<0x142, 0xA>(v));
+    v = op(v, dpp_copy<0x143, 0xC>(v));
+    return lane63(v);
 }
 
 // Assignment at one lambda: each value takes argmin_m D_im + lambda r_m (ties to
@@ -134,17 +164,23 @@ __device__ __forceinline__ int assign_cost(const double (&x)[VPL], const double 
                 for (int k = 0; k < VPL; ++k) {
                     const double J = D[k][mm] + pen;
                     m[k] = J < best[k] ? mm : m[k];
-                    best[k] = min_nonneg(best[k], J);
+                    best[k] = min_nn(best[k], J);
                 }
             }
         }
     } else {
+        {
+            const double t = s * 0.0;
+            const double u = o + t;
+            const double pen = lam * c.rate[0];
 #pragma unroll
-        for (int k = 0; k < VPL; ++k) {
-            best[k] = DBL_MAX;
-            m[k] = 0;
+            for (int k = 0; k < VPL; ++k) {
+                const double e = x[k] - u;
+                best[k] = e * e + pen;
+                m[k] = 0;
+            }
         }
-        for (int mm = 0; mm < c.M; ++mm) {
+        for (int mm = 1; mm < c.M; ++mm) {
             const double t = s * (double)mm;
             const double u = o + t;
             const double pen = lam * c.rate[mm];
@@ -152,10 +188,8 @@ __device__ __forceinline__ int assign_cost(const double (&x)[VPL], const double 
             for (int k = 0; k < VPL; ++k) {
                 const double e = x[k] - u;
                 const double J = e * e + pen;
-                if (J < best[k] || mm == 0) {
-                    best[k] = J;
-                    m[k] = mm;
-                }
+                m[k] = J < best[k] ? mm : m[k];
+                best[k] = min_nn(best[k], J);
             }
         }
     }
@@ -185,8 +219,8 @@ __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget
                 const double e = x[k] - u;
                 D[k][mm] = e * e;
                 if (mm < c.M) {
-                    dmax = fmax(dmax, D[k][mm]);
-                    dmin = fmin(dmin, D[k][mm]);
+                    dmax = max_nn(dmax, D[k][mm]);
+                    dmin = min_nn(dmin, D[k][mm]);
                 }
             }
         }
@@ -198,13 +232,13 @@ __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget
             for (int k = 0; k < VPL; ++k) {
                 const double e = x[k] - u;
                 const double Dv = e * e;
-                dmax = fmax(dmax, Dv);
-                dmin = fmin(dmin, Dv);
+                dmax = max_nn(dmax, Dv);
+                dmin = min_nn(dmin, Dv);
             }
         }
     }
-    dmax = wave_max(dmax);
-    dmin = wave_min(dmin);
+    dmax = wave_ext_nn<true>(dmax);
+    dmin = wave_ext_nn<false>(dmin);
     if (dmax == dmin) {
 #pragma unroll
         for (int k = 0; k < VPL; ++k) m[k] = c.cheapest;
@@ -218,16 +252,24 @@ __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget
     // the code length is an int: comparing it with the budget clamped to
     // INT_MAX decides the same and stays a scalar compare
     const int budget32 = (int)(budget < INT_MAX ? budget : INT_MAX);
+    // m holds the assignment at u_hi once a step has moved u_hi: the final
+    // assignment at u_hi is then that step's, and within the budget
+    bool at_hi = false;
     for (int it = 0; it < kBisectSteps; ++it) {
         const int u_mid = (u_lo + u_hi) >> 1;
         const double lam = ldexp((double)c.lam[u_mid & (kLambdaSteps - 1)], u_mid >> 9);
         int tmp[VPL];
         const int cst = assign_cost<VPL, MB>(x, D, rt, s, o, lam, c, tmp);
-        if (cst <= budget32)
+        if (cst <= budget32) {
             u_hi = u_mid;
-        else
+            at_hi = true;
+#pragma unroll
+            for (int k = 0; k < VPL; ++k) m[k] = tmp[k];
+        } else {
             u_lo = u_mid;
+        }
     }
+    if (at_hi) return;
     const double lam = ldexp((double)c.lam[u_hi & (kLambdaSteps - 1)], u_hi >> 9);
     const int cst = assign_cost<VPL, MB>(x, D, rt, s, o, lam, c, m);
     if (cst > budget32) {
