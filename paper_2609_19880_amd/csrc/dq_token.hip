@@ -86,9 +86,11 @@ struct TokArgs {
 // kernel; pb is the lane's bit position in its record (8 x byte position).
 //   dwords j = pb >> 5 and j + 1 come from ring rows j mod 8 and the next
 //   w = bytes pos .. pos + 3, little-endian = (hi:lo) >> (pb mod 32)
-//   r = b_pos << 24 | b_pos+1 << 16 (one byte permute)
-// Each step reads at most 2 bytes, so the second step's bytes are w >> sh of
-// the first.  Returns the two table words (levels in their top bytes).
+//   r = b_pos << 24 | b_pos+1 << 16 | b_pos+2 << 8 | b_pos+3 (byte reverse)
+// r >> (29 - sh) puts the sh bits to shift in at bits 3 and up; what lands in
+// the low three bits of X is never read.  Each step reads at most 2 bytes, so
+// the second step's bytes are r << sh of the first.  Returns the two table
+// words (levels in their top bytes).
 template <uint32_t LUT_OFF>
 __device__ __forceinline__ void tstep2(uint32_t& X, uint32_t& pb, uint32_t ring_lane, uint32_t mask8, int p3,
                                        uint32_t& e0, uint32_t& e1) {
@@ -96,19 +98,19 @@ __device__ __forceinline__ void tstep2(uint32_t& X, uint32_t& pb, uint32_t ring_
     asm("v_lshl_add_u32 %0, %1, 8, %2" : "=v"(addr) : "v"(__builtin_amdgcn_ubfe(pb, 5, 3)), "v"(ring_lane));
     const uint32_t lo = *LDS_PTR(const uint32_t, addr);
     const uint32_t hi = *LDS_PTR(const uint32_t, addr + kRingRow);
-    const uint32_t w = __builtin_amdgcn_alignbit(hi, lo, pb);
+    const uint32_t w = __builtin_amdgcn_perm(0u, __builtin_amdgcn_alignbit(hi, lo, pb), 0x00010203u);
 
     const uint64_t ea = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
     const uint32_t ya = __umul24((uint32_t)ea, X >> p3) + (uint32_t)(ea >> 32);
     const uint32_t sha = (uint32_t)__builtin_clz(ya) & 24u;
-    const uint32_t qa = __builtin_amdgcn_perm(w, w, 0x00010c0cu) >> (sha ^ 29u);
+    const uint32_t qa = w >> (sha ^ 29u);
     asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(ya), "v"(sha), "v"(qa));
 
-    const uint32_t wb = w >> sha;
+    const uint32_t wb = w << sha;
     const uint64_t eb = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
     const uint32_t yb = __umul24((uint32_t)eb, X >> p3) + (uint32_t)(eb >> 32);
     const uint32_t shb = (uint32_t)__builtin_clz(yb) & 24u;
-    const uint32_t qb = __builtin_amdgcn_perm(wb, wb, 0x00010c0cu) >> (shb ^ 29u);
+    const uint32_t qb = wb >> (shb ^ 29u);
     asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(yb), "v"(shb), "v"(qb));
     asm("v_add3_u32 %0, %1, %2, %3" : "=v"(pb) : "v"(pb), "v"(sha), "v"(shb));
     e0 = (uint32_t)ea;
