@@ -20,6 +20,13 @@ Readings
   payload bits [b j, b j + b), least significant bit first, bit k of the
   payload being bit k mod 8 of byte 4 + k // 8; the rest is zero.  At the
   measured 36-byte, 128-value records b = 2: the paper's INT2 example.
+* F3 App. B's own charge: each fixed-width symbol costs the ideal log2 M bits,
+  so the comparator takes the largest M with M**n <= 2**(8 (C - 4)) (the
+  record less its fp16 scale and offset).  At the per-token operating point
+  (n = 1024, 335 / 235-byte records) that is 6 key and 3 value levels, the
+  counts App. B states; at 128-value, 36-byte records it is 4, the same as F1.
+  Such symbols are an accounting device (6**1024 fills 331 bytes to the
+  bit), used for reconstruction error only; F1 is the stored format.
 * F2 quantizer: Alg. 1 with each Drift replaced by nearest-level rounding,
   i.e. FitMinMax -> nearest -> Refit -> fp16 -> nearest; "nearest" is
   argmin_m D_im of reading Q1 with ties to the smallest m (Drift's assignment
@@ -36,6 +43,15 @@ from . import kv, quantize, rans
 def bits_per_symbol(n: int, record_bytes: int) -> int:
     """Reading F1: b = floor(8 (C - 4) / n)."""
     return (8 * (record_bytes - 4)) // n
+
+
+def ideal_levels(n: int, record_bytes: int) -> int:
+    """Reading F3: the largest M with M**n <= 2**(8 (C - 4)) (exact integers)."""
+    budget = 1 << (8 * (record_bytes - 4))
+    M = 1
+    while (M + 1) ** n <= budget:
+        M += 1
+    return M
 
 
 def nearest(x: np.ndarray, s: np.ndarray, o: np.ndarray, M: int) -> np.ndarray:

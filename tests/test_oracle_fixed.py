@@ -7,6 +7,9 @@
   from ties, and reconstructs values on the grid exactly.
 * App. B's direction: at matched storage D-Quant's reconstruction error is
   below the fixed-width one (N(0,1) streams, 36-byte records).
+* App. B's level counts at the per-token operating point: charged the ideal
+  log2 M bits, 335 / 235-byte records of 1024 values allow 6 key and 3 value
+  levels; D-Quant's 8 / 6 levels reconstruct N(0,1) tokens with less error.
 """
 
 import numpy as np
@@ -68,3 +71,27 @@ def test_entropy_coding_beats_fixed_width_at_matched_storage():
     m0 = fixed.nearest(x, s0, o0, 4)
     e0 = ((x - (s0[:, None] * m0 + o0[:, None])) ** 2).sum() / (x ** 2).sum()
     assert e_fixed < e0
+
+
+def test_ideal_levels_at_the_paper_operating_points():
+    assert fixed.ideal_levels(1024, 335) == 6          # App. B: 6 key levels
+    assert fixed.ideal_levels(1024, 235) == 3          # App. B: 3 value levels
+    assert fixed.ideal_levels(128, 36) == 4            # INT2, the stored format at 36 bytes
+    assert fixed.ideal_levels(128, 36) == 1 << fixed.bits_per_symbol(128, 36)
+    assert 1024 * np.log2(6) <= 8 * 331 < 1024 * np.log2(7)
+    assert 1024 * np.log2(3) <= 8 * 231 < 1024 * np.log2(4)
+
+
+def test_entropy_coding_beats_fixed_width_at_the_per_token_point():
+    rng = np.random.default_rng(3)
+    x = rng.normal(size=(200, 1024))
+    for C, M_dq in ((335, 8), (235, 6)):
+        M_fx = fixed.ideal_levels(1024, C)
+        m, s16, o16 = fixed.quantize_streams(x, M_fx)
+        xf = s16.astype(np.float64)[:, None] * m + o16.astype(np.float64)[:, None]
+        t = tables.build_tables(1024, M_dq, 8, 1.4, C)
+        _, sym, ds, do, _ = kv.encode_streams(x, t)
+        xd = ds.astype(np.float64)[:, None] * sym + do.astype(np.float64)[:, None]
+        e_fixed = ((x - xf) ** 2).sum() / (x ** 2).sum()
+        e_dq = ((x - xd) ** 2).sum() / (x ** 2).sum()
+        assert e_dq < 0.75 * e_fixed, (C, e_dq, e_fixed)
