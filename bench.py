@@ -47,6 +47,11 @@ COUNTER_SUMMARIES = {
                                  for f in ("dq_token.hip", "dq_attn.h", "dq_common.h", "dq_internal.h")]),
 }
 
+# encoder counters: summary, sources, streams per dispatch they were taken over
+ENCODE_SUMMARY = (os.path.join(ROOT, "profiles", "encode_kernel_b16_t32k_pmc.md"),
+                  [os.path.join(_CSRC, f) for f in ("dq_encode.hip", "dq_common.h", "dq_internal.h")],
+                  16 * 32768 * 8)
+
 
 def _args():
     ap = argparse.ArgumentParser()
@@ -133,15 +138,11 @@ def copy_calibration(nbytes: int, steps: int):
                       "gbs_read_plus_write": 2 * nbytes / ms / 1e6}))
 
 
-def counter_figures(workload: str, variant: str):
-    """HBM bytes and VALU instructions per partial launch from the committed
-    rocprofv3 counter summary, if it was taken on this workload from the
-    kernel sources as they are now (else None)."""
+def _summary_text(summary: str, sources):
+    """The text of a committed rocprofv3 counter summary if the kernel sources
+    still hash to the value it records (else None)."""
     import hashlib
     import re
-    if (workload, variant) not in COUNTER_SUMMARIES:
-        return None
-    summary, sources = COUNTER_SUMMARIES[(workload, variant)]
     if not os.path.exists(summary):
         return None
     text = open(summary).read()
@@ -149,11 +150,39 @@ def counter_figures(workload: str, variant: str):
     for f in sources:
         h.update(open(f, "rb").read())
     m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    return text if m_sha and m_sha.group(1) == h.hexdigest() else None
+
+
+def counter_figures(workload: str, variant: str):
+    """HBM bytes and VALU instructions per partial launch from the committed
+    rocprofv3 counter summary, if it was taken on this workload from the
+    kernel sources as they are now (else None)."""
+    import re
+    if (workload, variant) not in COUNTER_SUMMARIES:
+        return None
+    text = _summary_text(*COUNTER_SUMMARIES[(workload, variant)])
+    if text is None:
+        return None
     m_tr = re.search(r"traffic_bytes_per_launch:\s*(\d+)", text)
     m_valu = re.search(r"\|\s*SQ_INSTS_VALU\s*\|\s*([\d,]+)", text)
-    if not (m_sha and m_tr and m_valu) or m_sha.group(1) != h.hexdigest():
+    if not (m_tr and m_valu):
         return None
     return int(m_tr.group(1)), int(m_valu.group(1).replace(",", ""))
+
+
+def encode_valu_per_stream(wl, variant: str):
+    """VALU instructions per encoded stream from the committed encoder counter
+    summary (taken on 36-byte, 6-level, p 12 per-(token, KV head) records),
+    for workloads that encode with that coding (else None)."""
+    import re
+    summary, sources, streams = ENCODE_SUMMARY
+    c = wl.k
+    if (wl.streams != "head" or variant != "paper" or wl.v != c or wl.head_dim != 128
+            or (c.record_bytes, c.levels, c.precision, c.alpha) != (36, 6, 12, 1.4)):
+        return None
+    text = _summary_text(summary, sources)
+    m = None if text is None else re.search(r"\|\s*SQ_INSTS_VALU\s*\|\s*([\d,]+)\s*\|", text)
+    return None if m is None else int(m.group(1).replace(",", "")) / streams
 
 
 def cpu_baseline(wl, seed: int):
@@ -409,6 +438,8 @@ def main():
     tokens_s = B * (T + a.residual) / (step_ms * 1e-3)
     counters = None if a.precision not in (None, 12) else counter_figures(wl.name, a.variant)
     traffic = counters[0] if counters else None
+    n_streams = 2 * B * T if tok else 2 * B * T * Hkv
+    enc_vps = None if a.precision not in (None, 12) else encode_valu_per_stream(wl, a.variant)
 
     rec = {
         "metric": METRIC,
@@ -454,8 +485,14 @@ def main():
         "symbols_per_s": n_symbols / (step_ms * 1e-3),
         "encode": {"what": f"prefill append of {B} x {T} tokens, K and V, one encode call per tensor",
                    "ms": enc_ms, "tokens_per_s": B * T / (enc_ms * 1e-3),
-                   "streams_per_s": (2 * B * T if tok else 2 * B * T * Hkv) / (enc_ms * 1e-3),
-                   "input_gbs": 2 * B * T * Hkv * d * 2 / (enc_ms * 1e-3) / 1e9},
+                   "streams_per_s": n_streams / (enc_ms * 1e-3),
+                   "input_gbs": 2 * B * T * Hkv * d * 2 / (enc_ms * 1e-3) / 1e9,
+                   "valu_issue": None if enc_vps is None else {
+                       "bound": "alu", "valu_insts_per_stream": enc_vps,
+                       "achieved": enc_vps * n_streams / (enc_ms * 1e-3) / 1e9,
+                       "peak": VALU_PEAK_GINST, "unit": "G wave64 VALU instructions/s",
+                       "frac": enc_vps * n_streams / (enc_ms * 1e-3) / 1e9 / VALU_PEAK_GINST,
+                       "note": "encode_kernel instructions over the whole append time (key means included)"}},
     }
     if a.compare_fixed:
         if tok or d != 128 or wl.gqa > 4:
