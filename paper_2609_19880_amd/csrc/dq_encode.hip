@@ -5,16 +5,17 @@
 //    each token (Hadamard, Sec. 4.2), sums the window left to right in fp64,
 //    and stores the channel mean as INT8 with one fp16 scale (App. B,
 //    "windowed INT8 channel-mean removal").
-//  * encode: one workgroup per (batch, head, 64 consecutive tokens).  Each
-//    wavefront takes a stream at a time with its n values spread over the
-//    lanes and keeps them in registers through Alg. 1 (FitMinMax -> Drift ->
-//    Refit -> fp16 -> Drift); no n x M distortion matrix goes to memory (the
-//    distortions of up to 8 or 16 levels stay in registers for the 13
-//    assignments of a drift, more levels are recomputed on the fly) and the
-//    code length is reduced across the wavefront, as Sec. 4.5 describes for
-//    the encoder.  The symbols of the 64 streams then go through LDS to
-//    lane-per-stream backward rANS (divisions by f as exact multiply-high
-//    reciprocals), and the 64 records are written as one contiguous span.
+//  * encode: one workgroup per (batch, head, 64 consecutive tokens; 32 for
+//    per-token streams).  Each wavefront takes a stream at a time with its n
+//    values spread over the lanes and keeps them in registers through Alg. 1
+//    (FitMinMax -> Drift -> Refit -> fp16 -> Drift); no n x M distortion
+//    matrix goes to memory (the distortions of up to 8 or 16 levels stay in
+//    registers for the assignments of a drift, more levels are recomputed on
+//    the fly) and the code length is reduced across the wavefront, as
+//    Sec. 4.5 describes for the encoder.  The symbols of the workgroup's
+//    streams then go through LDS to lane-per-stream backward rANS (divisions
+//    by f as exact multiply-high reciprocals), and the records are written as
+//    one contiguous span.
 //
 // Every floating-point step is fp64 in a fixed order without contraction
 // (this file is built with -ffp-contract=off), so the records are
@@ -28,6 +29,11 @@ namespace dq {
 namespace {
 
 constexpr int kEncStreams = 64;   // streams per workgroup
+// Per-token streams (n = 1024) stage 32: their symbols and records then take
+// about 48 KB of LDS, so that two workgroups share a CU (64 streams would
+// leave one wavefront per SIMD).
+constexpr int kEncStreamsTok = 32;
+__host__ __device__ constexpr int enc_streams(bool tok) { return tok ? kEncStreamsTok : kEncStreams; }
 constexpr int kEncWaves = 4;
 constexpr int kEncThreads = kEncWaves * kWave;
 constexpr int kD = 128;           // head_dim of the heads in a per-token stream
@@ -426,6 +432,7 @@ __device__ __forceinline__ void nearest(const double (&x)[VPL], double s, double
 template <int VPL, int MB, bool TOK, bool FIXED = false>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     constexpr int n = kWave * VPL;
+    constexpr int NS = enc_streams(TOK);
     extern __shared__ __align__(16) uint8_t smem[];
     // layout: rate[64] f64 | cost[64] | lam[512] | budget[64] i64 | s16[64] | o16[64]
     //         | flag[64] | (f, c, rcp, rsh)[64] | sym[64][n] | rec[64][C]
@@ -433,18 +440,18 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
     int32_t* s_cost = reinterpret_cast<int32_t*>(s_rate + DQ_MAX_LEVELS);
     float* s_lam = reinterpret_cast<float*>(s_cost + DQ_MAX_LEVELS);
     int64_t* s_budget = reinterpret_cast<int64_t*>(s_lam + kLambdaSteps);
-    uint16_t* s_s16 = reinterpret_cast<uint16_t*>(s_budget + kEncStreams);
-    uint16_t* s_o16 = s_s16 + kEncStreams;
-    int32_t* s_flag = reinterpret_cast<int32_t*>(s_o16 + kEncStreams);
-    uint4* s_ent = reinterpret_cast<uint4*>(s_flag + kEncStreams);     // coder entry per symbol
+    uint16_t* s_s16 = reinterpret_cast<uint16_t*>(s_budget + NS);
+    uint16_t* s_o16 = s_s16 + NS;
+    int32_t* s_flag = reinterpret_cast<int32_t*>(s_o16 + NS);
+    uint4* s_ent = reinterpret_cast<uint4*>(s_flag + NS);     // coder entry per symbol
     uint8_t* s_sym = reinterpret_cast<uint8_t*>(s_ent + DQ_MAX_LEVELS);
-    uint8_t* s_rec = s_sym + kEncStreams * n;
+    uint8_t* s_rec = s_sym + NS * n;
 
     const TabArgs& ta = a.ta;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int b = blockIdx.z, h = blockIdx.y;
-    const int first = a.t0 + blockIdx.x * kEncStreams;
-    const int active = min(kEncStreams, a.t0 + a.n_new - first);
+    const int first = a.t0 + blockIdx.x * NS;
+    const int active = min(NS, a.t0 + a.n_new - first);
     const int C = ta.C;
 
     for (int i = tid; i < (FIXED ? 0 : ta.M); i += kEncThreads) {
@@ -458,7 +465,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
                          f > 1 ? sh - 1u : 0u};
     }
     for (int i = tid; i < (FIXED ? 0 : kLambdaSteps); i += kEncThreads) s_lam[i] = ta.t.lam[i];
-    for (int i = tid; i < kEncStreams; i += kEncThreads) {
+    for (int i = tid; i < NS; i += kEncThreads) {
         s_budget[i] = ta.budget;
         s_flag[i] = 0;
     }
@@ -693,12 +700,13 @@ int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int
     a.mean_q = mean_q;
     a.mean_scale = mean_scale;
     a.status = status;
+    const int ns = enc_streams(tok);
     const size_t smem = sizeof(double) * DQ_MAX_LEVELS + sizeof(int32_t) * DQ_MAX_LEVELS +
-                        sizeof(float) * kLambdaSteps + sizeof(int64_t) * kEncStreams +
-                        2 * sizeof(uint16_t) * kEncStreams + sizeof(int32_t) * kEncStreams +
+                        sizeof(float) * kLambdaSteps + sizeof(int64_t) * ns +
+                        2 * sizeof(uint16_t) * ns + sizeof(int32_t) * ns +
                         sizeof(uint4) * DQ_MAX_LEVELS +
-                        (size_t)kEncStreams * n + (size_t)kEncStreams * a.ta.C;
-    dim3 grid((n_new + kEncStreams - 1) / kEncStreams, tok ? 1 : H, B);
+                        (size_t)ns * n + (size_t)ns * a.ta.C;
+    dim3 grid((n_new + ns - 1) / ns, tok ? 1 : H, B);
     // distortions held in registers for up to 8 levels (16 with two values per
     // lane); longer streams recompute them
     const int M = tab->cfg.levels;
