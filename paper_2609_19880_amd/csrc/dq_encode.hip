@@ -259,7 +259,10 @@ __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget
     // INT_MAX decides the same and stays a scalar compare
     const int budget32 = (int)(budget < INT_MAX ? budget : INT_MAX);
     // m holds the assignment at u_hi once a step has moved u_hi: the final
-    // assignment at u_hi is then that step's, and within the budget
+    // assignment at u_hi is then that step's, and within the budget.  With 16
+    // values per lane the copy's registers cost more occupancy than the
+    // final assignment it saves, which is then recomputed.
+    constexpr bool kKeepHi = VPL <= 4;
     bool at_hi = false;
     for (int it = 0; it < kBisectSteps; ++it) {
         const int u_mid = (u_lo + u_hi) >> 1;
@@ -268,9 +271,11 @@ __device__ void drift(const double (&x)[VPL], double s, double o, int64_t budget
         const int cst = assign_cost<VPL, MB>(x, D, rt, s, o, lam, c, tmp);
         if (cst <= budget32) {
             u_hi = u_mid;
-            at_hi = true;
+            if (kKeepHi) {
+                at_hi = true;
 #pragma unroll
-            for (int k = 0; k < VPL; ++k) m[k] = tmp[k];
+                for (int k = 0; k < VPL; ++k) m[k] = tmp[k];
+            }
         } else {
             u_lo = u_mid;
         }
@@ -429,8 +434,10 @@ __device__ __forceinline__ void nearest(const double (&x)[VPL], double s, double
 // refit with nearest-level rounding in place of both drifts, and b-bit
 // symbols (M = 2^b, b = 8 (C - 4) / n rounded down) packed after the 4-byte
 // header, least significant bit first, instead of the rANS payload.
+// Per-token streams and 16 levels in registers: three workgroups per CU (at
+// most 168 VGPRs; the per-token LDS staging, about 48 KB, fits three).
 template <int VPL, int MB, bool TOK, bool FIXED = false>
-__global__ __launch_bounds__(kEncThreads) void encode_kernel(EncArgs a) {
+__global__ __launch_bounds__(kEncThreads, (TOK || MB == 16) ? 3 : 1) void encode_kernel(EncArgs a) {
     constexpr int n = kWave * VPL;
     constexpr int NS = enc_streams(TOK);
     extern __shared__ __align__(16) uint8_t smem[];
