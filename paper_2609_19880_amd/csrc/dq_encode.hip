@@ -30,7 +30,7 @@ namespace {
 
 constexpr int kEncStreams = 64;   // streams per workgroup
 // Per-token streams (n = 1024) stage 32: their symbols and records then take
-// about 48 KB of LDS, so that two workgroups share a CU (64 streams would
+// about 48 KB of LDS, so that three workgroups share a CU (64 streams would
 // leave one wavefront per SIMD).
 constexpr int kEncStreamsTok = 32;
 __host__ __device__ constexpr int enc_streams(bool tok) { return tok ? kEncStreamsTok : kEncStreams; }
