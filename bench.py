@@ -64,6 +64,8 @@ def _args():
     ap.add_argument("--precision", type=int, default=None, help="rANS precision p of both tables (default 12)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of a HIP graph captured from one step instead of eager launches")
     ap.add_argument("--copy-calibration", type=int, default=0)
     ap.add_argument("--compare-bf16", action="store_true",
                     help="also time the BF16 comparator (uncompressed cache of the same shape)")
@@ -74,24 +76,41 @@ def _args():
     return ap.parse_args()
 
 
-def time_steps(calls, steps: int, warmup: int):
+def time_steps(calls, steps: int, warmup: int, graph: bool = False):
     """Time `steps` decode steps, each the launches in `calls` in order on the
-    current stream.  The timed region holds only the steps, bracketed by a
-    synchronize and one HIP event on each side (no events between kernels).
-    A second pass with an event pair around every launch gives each launch's
-    mean duration.  Returns (ms per step, [mean ms per call], wall seconds of
-    the timed region)."""
+    current stream (graph: one replay of a HIP graph captured from them).  The
+    timed region holds only the steps, bracketed by a synchronize and one HIP
+    event on each side (no events between kernels).  A second pass, eager,
+    with an event pair around every launch gives each launch's mean duration.
+    Returns (ms per step, [mean ms per call], wall seconds of the timed
+    region)."""
     import torch
-    for _ in range(warmup):
+
+    def step():
         for c in calls:
             c()
+
+    for _ in range(warmup):
+        step()
     torch.cuda.synchronize()
+    if graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for _ in range(warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        step = g.replay
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     w0 = time.perf_counter()
     e0.record()
     for _ in range(steps):
-        for c in calls:
-            c()
+        step()
     e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -417,7 +436,7 @@ def main():
     if ring is not None:
         calls.append(lambda: dq.dq_decode_attention_residual(q, ring[0], ring[1], seq, ring[2], T, cache.workspace))
     calls.append(lambda: cache.merge(seq, out))
-    step_ms, per_call, wall = time_steps(calls, a.steps, a.warmup)
+    step_ms, per_call, wall = time_steps(calls, a.steps, a.warmup, graph=a.graph)
     if int(cache.status.item()):
         raise RuntimeError(f"decode status {int(cache.status.item())}")
     partial_ms, merge_ms = per_call[0], per_call[-1]
@@ -482,6 +501,7 @@ def main():
             "tokens_per_sequence": a.residual, "ms": residual_ms,
             "gbs": B * Hkv * a.residual * d * 2 * 2 / (residual_ms * 1e-3) / 1e9},
         "wall_ms_per_step": wall * 1e3 / a.steps,
+        "step_launch": "graph replay" if a.graph else "eager",
         "symbols_per_s": n_symbols / (step_ms * 1e-3),
         "encode": {"what": f"prefill append of {B} x {T} tokens, K and V, one encode call per tensor",
                    "ms": enc_ms, "tokens_per_s": B * T / (enc_ms * 1e-3),
