@@ -106,6 +106,17 @@ __device__ __forceinline__ T wave_sum(T v) {
     return lane63(v);
 }
 
+// Sum over each half-wavefront: lanes 16-31 end with the sum of lanes 0-31,
+// lanes 48-63 with that of lanes 32-63.
+__device__ __forceinline__ float half_sum_f32(float v) {
+    v += dpp0<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
+    v += dpp0<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
+    v += dpp0<0x141, 0xF>(v);   // row_half_mirror
+    v += dpp0<0x140, 0xF>(v);   // row_mirror: every lane holds its row's sum
+    v += dpp0<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3
+    return v;
+}
+
 __device__ __forceinline__ int wave_sum_i32(int v) { return wave_sum(v); }
 
 __device__ __forceinline__ float wave_sum_f32(float v) { return wave_sum(v); }

@@ -242,6 +242,10 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     const int T = min(a.seq_lens[b], a.t_cap);
     const int start = c * a.chunk;
     if (start >= T) return;   // the merge ignores chunks past the length
+    const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
+    const int Ck = RWK ? 4 * RWK : a.tk.C, Cv = RWV ? 4 * RWV : a.tv.C, CWk = Ck / 4, CWv = Cv / 4;
+    bool bad_page = false;
+
 
     // ---- prologue: tables, rotated query, its digits, q . mu per window
     if (!FIXED) {
@@ -301,17 +305,30 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     const int nwin_total = a.t_cap / DQ_MEAN_WINDOW;
     const int w0 = start / DQ_MEAN_WINDOW;
     const int nwin = (a.chunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1;
-    bool bad_page = false;
-    for (int i = tid; i < nwin * GP; i += nthr) {
-        const int wi = i / GP, g = i % GP;
-        float s = 0.f;
-        if (g < G && w0 + wi < nwin_total) {
-            const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + wi, bad_page);
-            const float sc = half_bits_to_f32(a.kms[widx]);
-            const int8_t* mq = a.kmq + widx * kD;
-            for (int j = 0; j < kD; ++j) s += qt[g * kD + j] * (sc * (float)mq[j]);
+    // half a wavefront per window, two windows per pass: lane l takes
+    // channels 4 (l % 32) .. 4 (l % 32) + 3 of window 2 pass + l / 32
+    {
+        const int r = lane >> 5, c4 = 4 * (lane & 31);
+        for (int wi = 2 * wave + r; wi - r < nwin; wi += 2 * L.nw) {
+            float f[4] = {0.f, 0.f, 0.f, 0.f};
+            if (wi < nwin && w0 + wi < nwin_total) {
+                const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + wi, bad_page);
+                const float sc = half_bits_to_f32(a.kms[widx]);
+                const uint32_t mv = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + c4);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) f[k] = sc * (float)(int8_t)((mv >> (8 * k)) & 0xFF);
+            }
+#pragma unroll
+            for (int g = 0; g < GP; ++g) {
+                float s = 0.f;
+                if (g < G) {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) s = s + qt[g * kD + c4 + k] * f[k];
+                    s = half_sum_f32(s);
+                }
+                if ((lane & 31) == 31 && wi < nwin) qmu[wi * GP + g] = s;
+            }
         }
-        qmu[i] = s;
     }
     __syncthreads();
 
@@ -326,7 +343,6 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     uint8_t* plimb = wreg + L.plimb;
     const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
     const uint32_t sel2 = (lane & 2) ? 0x03020706u : 0x05040100u;
-    const int Ck = RWK ? 4 * RWK : a.tk.C, Cv = RWV ? 4 * RWV : a.tv.C, CWk = Ck / 4, CWv = Cv / 4;
     const int pk3 = a.tk.p + 3, pv3 = a.tv.p + 3;
     const uint32_t mask8k = ((1u << a.tk.p) - 1u) << 3, mask8v = ((1u << a.tv.p) - 1u) << 3;
     const int64_t bh = (int64_t)b * a.Hkv + h;
@@ -341,7 +357,6 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
         accf[1][g] = 0.f;
     }
     bool corrupt = false;
-    const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
 
     // records of the wavefront's next tile are loaded while it decodes this one
     // (up to 4 query heads per KV head; with 8 the registers go to accumulators
