@@ -229,16 +229,29 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
     const int nwin_total = a.t_cap / DQ_MEAN_WINDOW;
     const int w0 = start / DQ_MEAN_WINDOW;
     const int nwin = (a.chunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1;
-    for (int i = tid; i < nwin * Hq; i += nthr) {
-        const int wi = i / Hq, g = i % Hq;
-        float s = 0.f;
-        if (w0 + wi < nwin_total) {
-            const int64_t widx = ((int64_t)b * Hkv + g / G) * nwin_total + w0 + wi;
-            const float sc = half_bits_to_f32(a.kms[widx]);
-            const int8_t* mq = a.kmq + widx * kD;
-            for (int j = 0; j < kD; ++j) s += qt[g * kD + j] * (sc * (float)mq[j]);
+    // half a wavefront per (window, KV head), two per pass: lane l takes
+    // channels 4 (l % 32) .. 4 (l % 32) + 3 and the KV head's G query heads
+    {
+        const int r = lane >> 5, c4 = 4 * (lane & 31);
+        for (int it = 2 * wave + r; it - r < nwin * Hkv; it += 2 * L.nw) {
+            const int wi = it / Hkv, hk = it % Hkv;
+            float f[4] = {0.f, 0.f, 0.f, 0.f};
+            if (it < nwin * Hkv && w0 + wi < nwin_total) {
+                const int64_t widx = ((int64_t)b * Hkv + hk) * nwin_total + w0 + wi;
+                const float sc = half_bits_to_f32(a.kms[widx]);
+                const uint32_t mv = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + c4);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) f[k] = sc * (float)(int8_t)((mv >> (8 * k)) & 0xFF);
+            }
+            for (int q = 0; q < G; ++q) {
+                const int g = hk * G + q;
+                float s = 0.f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) s = s + qt[g * kD + c4 + k] * f[k];
+                s = half_sum_f32(s);
+                if ((lane & 31) == 31 && it < nwin * Hkv) qmu[wi * Hq + g] = s;
+            }
         }
-        qmu[i] = s;
     }
     __syncthreads();
 
