@@ -37,6 +37,38 @@ __device__ __forceinline__ void digits3(int v, int& d0, int& d1, int& d2) {
     d2 = (v1 - d1) >> 8;
 }
 
+// Rotated query heads (unnormalized Hadamard, stages h = 1, 2, ..., 64 in
+// the order of the definition) into qt [nh][128] fp32, a wavefront per head
+// with channels l and l + 64 in lane l; qscale = max |q_rot| / 2^22 and qsum =
+// sum of q_rot per head, 0 for the slots nh .. slots - 1.
+__device__ __forceinline__ void rotate_query_heads(const uint16_t* q, int nh, int slots, int wave, int nw,
+                                                   int lane, float* qt, float* qscale, float* qsum) {
+    for (int g = wave; g < slots; g += nw) {
+        if (g >= nh) {
+            if (lane == 0) {
+                qscale[g] = 0.f;
+                qsum[g] = 0.f;
+            }
+            continue;
+        }
+        float v0 = bf16_to_f32(q[g * 128 + lane]), v1 = bf16_to_f32(q[g * 128 + lane + 64]);
+        for (int hh = 1; hh < 64; hh <<= 1) {
+            const float p0 = __shfl_xor(v0, hh), p1 = __shfl_xor(v1, hh);
+            v0 = (lane & hh) ? p0 - v0 : v0 + p0;
+            v1 = (lane & hh) ? p1 - v1 : v1 + p1;
+        }
+        const float r0 = v0 + v1, r1 = v0 - v1;
+        qt[g * 128 + lane] = r0;
+        qt[g * 128 + lane + 64] = r1;
+        const float mx = wave_max_f32(fmaxf(fabsf(r0), fabsf(r1)));
+        const float sm = wave_sum_f32(r0 + r1);
+        if (lane == 0) {
+            qscale[g] = mx * (1.0f / 4194304.0f);
+            qsum[g] = sm;
+        }
+    }
+}
+
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ v4i mfma(uint32_t a, uint32_t b, v4i c) {

@@ -263,29 +263,7 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     float* qmu = reinterpret_cast<float*>(smem + L.qmu);
     uint8_t* qlimb = smem + L.qlimb;
     const int hq0 = h * G;
-    for (int i = tid; i < G * kD; i += nthr) qt[i] = bf16_to_f32(a.q[((int64_t)b * a.Hq + hq0) * kD + i]);
-    __syncthreads();
-    for (int hh = 1; hh < kD; hh <<= 1) {
-        for (int i = tid; i < G * (kD / 2); i += nthr) {
-            const int g = i / (kD / 2), r = i % (kD / 2);
-            const int lo = (r / hh) * 2 * hh + (r % hh);
-            const float x0 = qt[g * kD + lo], x1 = qt[g * kD + lo + hh];
-            qt[g * kD + lo] = x0 + x1;
-            qt[g * kD + lo + hh] = x0 - x1;
-        }
-        __syncthreads();
-    }
-    if (tid < GP) {
-        float mx = 0.f, sm = 0.f;
-        if (tid < G) {
-            for (int j = 0; j < kD; ++j) {
-                mx = fmaxf(mx, fabsf(qt[tid * kD + j]));
-                sm += qt[tid * kD + j];
-            }
-        }
-        qscale[tid] = mx * (1.0f / 4194304.0f);
-        qsum[tid] = sm;
-    }
+    rotate_query_heads(a.q + ((int64_t)b * a.Hq + hq0) * kD, G, GP, wave, L.nw, lane, qt, qscale, qsum);
     __syncthreads();
     for (int i = tid; i < GP * kD; i += nthr) {
         const int g = i / kD, j = i % kD;

@@ -187,27 +187,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
     float* qsum = reinterpret_cast<float*>(smem + L.qsum);
     float* qmu = reinterpret_cast<float*>(smem + L.qmu);
     uint8_t* qlimb = smem + L.qlimb;
-    for (int i = tid; i < Hq * kD; i += nthr) qt[i] = bf16_to_f32(a.q[(int64_t)b * Hq * kD + i]);
-    __syncthreads();
-    for (int hh = 1; hh < kD; hh <<= 1) {
-        for (int i = tid; i < Hq * (kD / 2); i += nthr) {
-            const int g = i / (kD / 2), r = i % (kD / 2);
-            const int lo = (r / hh) * 2 * hh + (r % hh);
-            const float x0 = qt[g * kD + lo], x1 = qt[g * kD + lo + hh];
-            qt[g * kD + lo] = x0 + x1;
-            qt[g * kD + lo + hh] = x0 - x1;
-        }
-        __syncthreads();
-    }
-    for (int g = tid; g < Hq; g += nthr) {
-        float mx = 0.f, sm = 0.f;
-        for (int j = 0; j < kD; ++j) {
-            mx = fmaxf(mx, fabsf(qt[g * kD + j]));
-            sm += qt[g * kD + j];
-        }
-        qscale[g] = mx * (1.0f / 4194304.0f);
-        qsum[g] = sm;
-    }
+    rotate_query_heads(a.q + (int64_t)b * Hq * kD, Hq, Hq, wave, L.nw, lane, qt, qscale, qsum);
     __syncthreads();
     // digits of head slot r of KV head h at ((h * 32 + j / 4) * 4 + r) * 16 + j % 4 (+4, +8)
     for (int i = tid; i < Hkv * 4 * kD; i += nthr) {
