@@ -41,7 +41,7 @@ VALU_PEAK_GINST = 256 * 4 / 4 * 2.4
 _CSRC = os.path.join(ROOT, "paper_2609_19880_amd", "csrc")
 COUNTER_SUMMARIES = {
     ("b16_t32k", "paper"): (os.path.join(ROOT, "profiles", "attn_partial_b16_t32k_pmc.md"),
-                            [os.path.join(_CSRC, f) for f in ("dq_decode.hip", "dq_common.h", "dq_internal.h")]),
+                            [os.path.join(_CSRC, f) for f in ("dq_decode.hip", "dq_attn.h", "dq_common.h", "dq_internal.h")]),
     ("b16_t32k_tok", "paper"): (os.path.join(ROOT, "profiles", "attn_token_b16_t32k_tok_pmc.md"),
                                 [os.path.join(_CSRC, f)
                                  for f in ("dq_token.hip", "dq_attn.h", "dq_common.h", "dq_internal.h")]),

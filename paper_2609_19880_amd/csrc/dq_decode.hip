@@ -393,6 +393,16 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
 #pragma unroll
             for (int d = 0; d < 3; ++d) dk[hg][d] = v4i{0, 0, 0, 0};
         uint32_t vlev[kD / 4];
+        // query digits: with two head groups (8 wavefronts per CU) they are
+        // read one group ahead, so that the products do not wait for the read;
+        // with 16 wavefronts the others cover that wait, and reading in place
+        // keeps the registers of the one-group case free
+        constexpr bool kAhead = HG > 1;
+        uint4 qla[HG];
+        if constexpr (kAhead) {
+#pragma unroll
+            for (int hg = 0; hg < HG; ++hg) qla[hg] = *reinterpret_cast<const uint4*>(qlimb + (hg * 4 + (lane & 3)) * 16);
+        }
 #pragma unroll
         for (int grp = 0; grp < kD / 4; ++grp) {
             uint32_t lk;
@@ -417,10 +427,18 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
             asm volatile("" : "+v"(vlev[grp]));
 #pragma unroll
             for (int hg = 0; hg < HG; ++hg) {
-                const uint4 ql = *reinterpret_cast<const uint4*>(qlimb + ((grp * GP) + hg * 4 + (lane & 3)) * 16);
-                dk[hg][0] = mfma(ql.x, lk, dk[hg][0]);
-                dk[hg][1] = mfma(ql.y, lk, dk[hg][1]);
-                dk[hg][2] = mfma(ql.z, lk, dk[hg][2]);
+                if constexpr (kAhead) {
+                    dk[hg][0] = mfma(qla[hg].x, lk, dk[hg][0]);
+                    dk[hg][1] = mfma(qla[hg].y, lk, dk[hg][1]);
+                    dk[hg][2] = mfma(qla[hg].z, lk, dk[hg][2]);
+                    if (grp + 1 < kD / 4)
+                        qla[hg] = *reinterpret_cast<const uint4*>(qlimb + (((grp + 1) * GP) + hg * 4 + (lane & 3)) * 16);
+                } else {
+                    const uint4 ql = *reinterpret_cast<const uint4*>(qlimb + ((grp * GP) + hg * 4 + (lane & 3)) * 16);
+                    dk[hg][0] = mfma(ql.x, lk, dk[hg][0]);
+                    dk[hg][1] = mfma(ql.y, lk, dk[hg][1]);
+                    dk[hg][2] = mfma(ql.z, lk, dk[hg][2]);
+                }
             }
             // a corrupt stream may run past its array: clamp often enough that
             // it cannot leave the workgroup's LDS (kPairSlack above the arrays)

@@ -39,7 +39,7 @@ namespace {
 constexpr int kD = 128;
 constexpr int kTile = 64;
 constexpr int kVSlice = 64;
-constexpr int kVRow = 68;
+constexpr int kVRow = 80;                // bytes per row of the value and weight tiles (64 + pad)
 constexpr int kMaxLds = 160 * 1024;
 constexpr int kTokWaves = 12;             // wavefronts per workgroup at most
 constexpr int kTokMaxHeads = 8;           // KV heads per stream (n <= 1024)
@@ -58,8 +58,8 @@ struct TokLayout {
     int waves;          // first wavefront region
     int wave_stride;
     int ring_k, ring_v; // per wavefront
-    int vtile;          // [64 channels][kVRow] bytes
-    int plimb;          // [4 heads][16 token quads] x 16 B
+    int vtile;          // [64 channels][kVRow]: levels of 64 tokens
+    int plimb;          // [4 heads][4 rows][kVRow]: weight digits 0..2 of 64 tokens, row 3 zero
     int total;
 };
 
@@ -132,19 +132,41 @@ __device__ __forceinline__ void put_chunk(uint32_t ring_lane, uint32_t c, const 
 }
 
 // Keeps 8 nc >= pos + 14: the next 4 steps read bytes below pos + 14.  thr is
-// 8 (8 nc - 14) - 1 in bits, so the test is one compare.
-__device__ __forceinline__ void refill(uint32_t pb, uint32_t& nc, uint32_t& thr, uint2& next, uint32_t ring_lane,
-                                       const uint8_t* rec, uint32_t last) {
-    if (pb > thr) {
-        put_chunk(ring_lane, nc, next);
-        ++nc;
-        thr += 64u;
-        next = load_chunk(rec, nc, last);
+// 8 (8 nc - 14) - 1 in bits, so the test is one compare.  Both rings are
+// written before either chunk load is issued: the loads complete in order, so
+// the writes wait only for chunks loaded at earlier refills, never for the
+// other ring's load of this group.
+__device__ __forceinline__ void refill2(uint32_t pbk, uint32_t& nck, uint32_t& thrk, uint2& nk, uint32_t ring_k,
+                                        const uint8_t* kr, uint32_t last_k, uint32_t pbv, uint32_t& ncv,
+                                        uint32_t& thrv, uint2& nv, uint32_t ring_v, const uint8_t* vr,
+                                        uint32_t last_v) {
+    const bool rk = pbk > thrk, rv = pbv > thrv;
+    if (rk) put_chunk(ring_k, nck, nk);
+    if (rv) put_chunk(ring_v, ncv, nv);
+    if (rk) {
+        ++nck;
+        thrk += 64u;
+        nk = load_chunk(kr, nck, last_k);
+    }
+    if (rv) {
+        ++ncv;
+        thrv += 64u;
+        nv = load_chunk(vr, ncv, last_v);
     }
 }
 
-// Accumulators of query-head slot r, channel slice s: one vector acc[s][r]
-// over the KV heads.  The head loop is not unrolled, so the vectors are
+// P . v on the 16x16x32 int8 matrix cores: rows are (query-head slot,
+// digit), K is 32 tokens, columns 16 channels.  Lane l gives row l mod 16 and
+// tokens 8 (l / 16) .. + 7 of A, column l mod 16 and the same tokens of B,
+// and receives rows 4 (l / 16) .. + 3 of column l mod 16: one slot's three
+// digit sums (and the zero row) for one channel.
+__device__ __forceinline__ v4i mfma_pv(uint64_t a, uint64_t b, v4i c) {
+    return __builtin_amdgcn_mfma_i32_16x16x32_i8((long)a, (long)b, c, 0, 0, 0);
+}
+
+// Accumulators of channel block cb of slice s: one vector acc[s][cb]
+// over the KV heads, for query-head slot l / 16 and channel 64 s + 16 cb +
+// l mod 16 in lane l.  The head loop is not unrolled, so the vectors are
 // rotated by one element per head and the current head is always element 0.
 typedef float v8f __attribute__((ext_vector_type(kTokMaxHeads)));
 
@@ -240,7 +262,12 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
     const uint32_t ring_k = (uint32_t)(L.waves + wave * L.wave_stride + L.ring_k) + 4u * lane;
     const uint32_t ring_v = (uint32_t)(L.waves + wave * L.wave_stride + L.ring_v) + 4u * lane;
     uint8_t* vtile = wreg + L.vtile;
-    uint8_t* plimb = wreg + L.plimb;
+    uint8_t* plimb = vtile + kVSlice * kVRow;   // the weight tile follows the value tile
+    // row 3 of each slot's weight digits stays zero (the prologue's query
+    // scratch overlapped it)
+    *reinterpret_cast<uint32_t*>(plimb + (4 * (lane >> 4) + 3) * kVRow + 4 * (lane & 15)) = 0u;
+    const int pslot = lane >> 4;                               // query-head slot of this lane's P . v sums
+    const int prow = (lane & 15) * kVRow + 8 * (lane >> 4);    // operand row and token offset of this lane
     const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
     const uint32_t sel2 = (lane & 2) ? 0x03020706u : 0x05040100u;
     const int pk3 = a.tk.p + 3, pv3 = a.tv.p + 3;
@@ -254,7 +281,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[s][r] = v8f{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int cb = 0; cb < 4; ++cb) acc[s][cb] = v8f{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     bool corrupt = false;
     const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
 
@@ -290,6 +317,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
             v4i dk[3] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
             uint32_t vlev[kGroups];
             const uint8_t* qh = qlimb + (h * kGroups * 4 + (lane & 3)) * 16;
+            uint4 ql = *reinterpret_cast<const uint4*>(qh);   // digits of group 0; then one group ahead
 #pragma unroll
             for (int grp = 0; grp < kGroups; ++grp) {
                 uint32_t k0s, k1s, k2s, k3s, v0s, v1s, v2s, v3s;
@@ -300,12 +328,11 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
                 const uint32_t lk = pack4(k0s, k1s, k2s, k3s);
                 vlev[grp] = pack4(v0s, v1s, v2s, v3s);
                 asm volatile("" : "+v"(vlev[grp]));
-                const uint4 ql = *reinterpret_cast<const uint4*>(qh + grp * 4 * 16);
                 dk[0] = mfma(ql.x, lk, dk[0]);
                 dk[1] = mfma(ql.y, lk, dk[1]);
                 dk[2] = mfma(ql.z, lk, dk[2]);
-                refill(pbk, nck, thrk, nk, ring_k, kr, last_k);
-                refill(pbv, ncv, thrv, nv, ring_v, vr, last_v);
+                if (grp + 1 < kGroups) ql = *reinterpret_cast<const uint4*>(qh + (grp + 1) * 4 * 16);
+                refill2(pbk, nck, thrk, nk, ring_k, kr, last_k, pbv, ncv, thrv, nv, ring_v, vr, last_v);
                 __builtin_amdgcn_sched_barrier(0);
             }
 
@@ -347,47 +374,58 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
                                        (((uint32_t)dd[2][d] & 0xFFu) << 16) | ((uint32_t)dd[3][d] << 24);
                     wt[d] = quad_transpose(w, sel1, sel2);
                 }
-                *reinterpret_cast<uint4*>(plimb + ((lane & 3) * (kTile / 4) + (lane >> 2)) * 16) =
-                    uint4{wt[0], wt[1], wt[2], 0u};
+                // lane 4 q + i: slot i, tokens 4 q .. 4 q + 3, rows 4 i + digit
+                uint8_t* pw = plimb + (lane & 3) * 4 * kVRow + (lane >> 2) * 4;
+                *reinterpret_cast<uint32_t*>(pw) = wt[0];
+                *reinterpret_cast<uint32_t*>(pw + kVRow) = wt[1];
+                *reinterpret_cast<uint32_t*>(pw + 2 * kVRow) = wt[2];
             }
+            const float corr_l = pslot == 0 ? corr[0] : pslot == 1 ? corr[1] : pslot == 2 ? corr[2] : corr[3];
+            const float pscale_l =
+                pslot == 0 ? pscale[0] : pslot == 1 ? pscale[1] : pslot == 2 ? pscale[2] : pscale[3];
 
             // ---- P . v over two slices of 64 channels
-            float pv[2][4];
+            uint64_t pa[2];
 #pragma unroll
-            for (int s = 0; s < 2; ++s) {
-                wave_sync();   // the previous slice / head is no longer read
+            for (int sl = 0; sl < 2; ++sl) {
+                wave_sync();   // the previous slice / head is no longer read; the weights are written
 #pragma unroll
                 for (int grp = 0; grp < kVSlice / 4; ++grp) {
-                    const uint32_t wt = quad_transpose(vlev[s * (kVSlice / 4) + grp], sel1, sel2);
+                    const uint32_t wt = quad_transpose(vlev[sl * (kVSlice / 4) + grp], sel1, sel2);
                     *reinterpret_cast<uint32_t*>(vtile + (grp * 4 + (lane & 3)) * kVRow + (lane >> 2) * 4) = wt;
                 }
                 wave_sync();
-                v4i dv[3] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
-#pragma unroll 4
-                for (int qd = 0; qd < kTile / 4; ++qd) {
-                    const uint32_t bv = *reinterpret_cast<const uint32_t*>(vtile + lane * kVRow + qd * 4);
-                    const uint4 pl = *reinterpret_cast<const uint4*>(plimb + ((lane & 3) * (kTile / 4) + qd) * 16);
-                    dv[0] = mfma(pl.x, bv, dv[0]);
-                    dv[1] = mfma(pl.y, bv, dv[1]);
-                    dv[2] = mfma(pl.z, bv, dv[2]);
+                if (sl == 0) {   // from the value tile's address: one base register for both tiles
+                    pa[0] = *reinterpret_cast<const uint64_t*>(vtile + prow + kVSlice * kVRow);
+                    pa[1] = *reinterpret_cast<const uint64_t*>(vtile + prow + kVSlice * kVRow + 32);
                 }
+                // all operands first, then four independent product chains
+                uint64_t vb[kVSlice / 16][2];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) pv[s][r] = combine(dv[0], dv[1], dv[2], r) * pscale[r];
+                for (int cb = 0; cb < kVSlice / 16; ++cb) {
+                    vb[cb][0] = *reinterpret_cast<const uint64_t*>(vtile + cb * 16 * kVRow + prow);
+                    vb[cb][1] = *reinterpret_cast<const uint64_t*>(vtile + cb * 16 * kVRow + prow + 32);
+                }
+                v4i dv[kVSlice / 16];
+#pragma unroll
+                for (int cb = 0; cb < kVSlice / 16; ++cb) dv[cb] = mfma_pv(pa[0], vb[cb][0], v4i{0, 0, 0, 0});
+#pragma unroll
+                for (int cb = 0; cb < kVSlice / 16; ++cb) dv[cb] = mfma_pv(pa[1], vb[cb][1], dv[cb]);
+#pragma unroll
+                for (int cb = 0; cb < kVSlice / 16; ++cb) {
+                    const float pv =
+                        ((float)dv[cb][2] * 65536.0f + (float)dv[cb][1] * 256.0f + (float)dv[cb][0]) * pscale_l;
+                    v8f t = acc[sl][cb];
+                    t[0] = t[0] * corr_l + pv;
+                    acc[sl][cb] = rot1(t);
+                }
             }
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    v8f t = acc[s][r];
-                    t[0] = t[0] * corr[r] + pv[s][r];
-                    acc[s][r] = rot1(t);
-                }
         }
         for (int h = Hkv; h < kTokMaxHeads; ++h)
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) acc[s][r] = rot1(acc[s][r]);
+                for (int cb = 0; cb < 4; ++cb) acc[s][cb] = rot1(acc[s][cb]);
         // every stream ends at x = L having read no byte past its record
         corrupt |= valid && ((xk >> 3) != kRansL || pbk > endk);
         corrupt |= valid && ((xv >> 3) != kRansL || pbv > endv);
@@ -404,21 +442,29 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
 #pragma unroll
         for (int s = 0; s < 2; ++s)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                av[s][r] = acc[s][r][0];
-                acc[s][r] = rot1(acc[s][r]);
+            for (int cb = 0; cb < 4; ++cb) {
+                av[s][cb] = acc[s][cb][0];
+                acc[s][cb] = rot1(acc[s][cb]);
             }
         __syncthreads();   // LDS free (first head) / previous head merged
+        float ov4[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int slot = h * 4 + r;
-            const float mv = lane_get(m_vec, slot), lv = lane_get(l_vec, slot), ovt = lane_get(o_vec, slot);
+            const float mv = lane_get(m_vec, slot), lv = lane_get(l_vec, slot);
+            ov4[r] = lane_get(o_vec, slot);
             if (lane == 0) {
                 mw[wave * 4 + r] = mv;
                 lw[wave * 4 + r] = lv;
             }
-            aw[(wave * 4 + r) * kD + lane] = av[0][r] + ovt;
-            aw[(wave * 4 + r) * kD + kVSlice + lane] = av[1][r] + ovt;
+        }
+        {
+            const float ovt = pslot == 0 ? ov4[0] : pslot == 1 ? ov4[1] : pslot == 2 ? ov4[2] : ov4[3];
+            float* row = aw + (wave * 4 + pslot) * kD + (lane & 15);
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int cb = 0; cb < 4; ++cb) row[s * kVSlice + cb * 16] = av[s][cb] + ovt;
         }
         __syncthreads();
         for (int i = tid; i < G * kD; i += nthr) {
@@ -463,8 +509,8 @@ TokLayout tok_layout(int pk, int pv, bool shared_lut, int Hq, int Hkv, int chunk
     L.ring_k = 0;
     L.ring_v = kRingBytes;
     L.vtile = 2 * kRingBytes;
-    L.plimb = L.vtile + kVSlice * kVRow;
-    L.wave_stride = (L.plimb + 4 * (kTile / 4) * 16 + 15) & ~15;
+    L.plimb = L.vtile + kVSlice * kVRow;   // the kernel relies on this placement
+    L.wave_stride = (L.plimb + 16 * kVRow + 15) & ~15;
     L.nw = nw;
     // the prologue's query scratch and the epilogue's merge buffers use the
     // wavefront regions
