@@ -8,9 +8,10 @@
 // value streams as two interleaved rANS chains (Alg. 2).  After every 128
 // steps (one KV head) the head's G query heads get their q . k products
 // (Eq. fold-key, on the matrix cores as the levels appear), the online
-// softmax update and P . v (Eq. fold-value); the chains then continue into
-// the next head with their state.  All query heads' accumulators live in the
-// wavefront: two channels per lane per query head.
+// softmax update and P . v (Eq. fold-value, on the 16x16x32 matrix cores);
+// the chains then continue into the next head with their state.  All query
+// heads' accumulators live in the wavefront: per KV head, lane l holds query
+// head slot l / 16 for 8 of the 128 channels.
 //
 // Record bytes.  Records (C bytes in S-byte slots, S a multiple of 16) are
 // stored per 64-token tile with 8-byte chunks outermost: chunk c of the tile's
