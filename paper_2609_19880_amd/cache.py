@@ -118,16 +118,28 @@ class StreamingKVCache:
     key-mean window and leave it, so at least the 128 most recent tokens are
     always raw.  Decode attention runs over both parts in one step.  All
     sequences of the batch advance together (same length).
+
+    streams="head" keeps one stream per (token, KV head) (a KVCache);
+    streams="token" the paper's default grouping, one stream per token over
+    all KV heads (a TokenKVCache, tables built with head_dim 128 kv_heads).
+    The ring, its append and commit, and the residual attention are the same
+    for both.
     """
 
     WINDOW = _lib.DQ_MEAN_WINDOW
 
     def __init__(self, batch: int, kv_heads: int, q_heads: int, t_cap: int, k_tables, v_tables,
-                 device="cuda", r_cap: int = 256):
+                 device="cuda", r_cap: int = 256, streams: str = "head"):
         if r_cap % self.WINDOW or not (2 * self.WINDOW <= r_cap <= 256):
             raise ValueError("r_cap must be 256 (two mean windows)")
-        self.cache = KVCache(batch, kv_heads, q_heads, t_cap, k_tables, v_tables, device=device)
-        d = k_tables.head_dim
+        if streams == "head":
+            self.cache = KVCache(batch, kv_heads, q_heads, t_cap, k_tables, v_tables, device=device)
+        elif streams == "token":
+            self.cache = TokenKVCache(batch, kv_heads, q_heads, t_cap, k_tables, v_tables, device=device)
+        else:
+            raise ValueError("streams must be 'head' or 'token'")
+        self.streams = streams
+        d = self.cache.head_dim
         self.r_cap = r_cap
         self.res_k = torch.zeros((batch, kv_heads, r_cap, d), dtype=torch.bfloat16, device=device)
         self.res_v = torch.zeros_like(self.res_k)
@@ -183,9 +195,7 @@ class StreamingKVCache:
         c = self.cache
         if out is None:
             out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
-        _lib.dq_decode_attention_partial(c.k_tables, c.v_tables, q, c.k_records, c.k_mean_q, c.k_mean_scale,
-                                         c.v_records, self.seq_lens, c.workspace, softmax_scale=softmax_scale,
-                                         status=c.status)
+        c.partial(q, self.seq_lens, softmax_scale)
         _lib.dq_decode_attention_residual(q, self.res_k, self.res_v, self.seq_lens, self.res_lens, c.t_cap,
                                           c.workspace, softmax_scale=softmax_scale)
         _lib.dq_decode_attention_merge(c.batch, c.q_heads, c.kv_heads, self.seq_lens, c.t_cap, c.workspace, out)

@@ -15,7 +15,7 @@ import torch
 
 import dq_workloads as wlmod
 from oracle import attention, kmean, kv, tables
-from tokrec import to_tiles
+from tokrec import from_tiles, to_tiles
 
 pytestmark = pytest.mark.gpu
 
@@ -278,3 +278,69 @@ def test_token_streams_with_residual_window(dq):
     ref = attention.attention_with_residual(kv.bf16_to_f64(wlmod.bf16_bits(q)), k_rot, v_rot, comp, res_k, res_v,
                                             res, G, 1 / np.sqrt(128))
     assert _rel_err(out.cpu().numpy().astype(np.float64), ref) < TOL
+
+
+def _oracle_stream(q_bits, kb, vb, comp, res, otk, otv, H, G):
+    """Oracle attention over `comp` encoded tokens (token-wise streams, as the
+    cache flushes them) followed by `res` raw tokens, the same for every
+    sequence."""
+    B = kb.shape[0]
+    k_rot = np.zeros((B, H, max(comp, 1), 128))
+    v_rot = np.zeros((B, H, max(comp, 1), 128))
+    if comp:
+        krec, mq, ms, ksym = kv.encode_keys_tokenwise(kb[:, :comp], otk)
+        vrec, vsym = kv.encode_values_tokenwise(vb[:, :comp], otv)
+        _, ks, ko, _ = kv.decode_records(krec, otk, 128 * H)
+        _, vs, vo, _ = kv.decode_records(vrec, otv, 128 * H)
+        kh, ksh, koh = kv.tokenwise_as_heads(ksym, ks, ko, H)
+        vh, vsh, voh = kv.tokenwise_as_heads(vsym, vs, vo, H)
+        k_rot[:, :, :comp] = attention.dequantize(kh, ksh, koh, kmean.dequantize_mean(mq, ms))
+        v_rot[:, :, :comp] = attention.dequantize(vh, vsh, voh)
+    res_k = np.moveaxis(kv.bf16_to_f64(kb[:, comp:comp + res]), 1, 2)
+    res_v = np.moveaxis(kv.bf16_to_f64(vb[:, comp:comp + res]), 1, 2)
+    return attention.attention_with_residual(kv.bf16_to_f64(q_bits), k_rot, v_rot, [comp] * B, res_k, res_v,
+                                             [res] * B, G, 1 / np.sqrt(128))
+
+
+def test_streaming_cache_over_token_streams(dq):
+    """Serving semantics (Sec. 5.1) with the paper's per-token streams: a
+    prefill, then one decode token at a time through the BF16 ring, each full
+    window flushed into per-token records.  At several lengths the step
+    (per-token partial + residual partial + merge) matches the oracle's
+    attention over the token-wise reconstructions of the flushed tokens and
+    the raw ring tokens; at the end the records and key means are the
+    oracle's, bit for bit."""
+    H, G, B, t_cap = 2, 4, 2, 1024
+    gtk, otk = _tabs(dq, 128 * H, 8, 88, 8)
+    gtv, otv = _tabs(dq, 128 * H, 6, 62, 8)
+    prefill, steps = 300, 300
+    T = prefill + steps
+    k, v, _ = _inputs(H, G, B, T, 41)
+    kb, vb = wlmod.bf16_bits(k), wlmod.bf16_bits(v)
+    kd, vd = k.to(DEV), v.to(DEV)
+    cache = dq.StreamingKVCache(B, H, H * G, t_cap, gtk, gtv, streams="token")
+    cache.prefill(kd[:, :prefill], vd[:, :prefill])
+    checks = {prefill, prefill + 84, prefill + 85, T}
+    for t in range(prefill, T + 1):
+        if t in checks:
+            q = _inputs(H, G, B, 128, 1000 + t)[2]
+            out = cache.attend(q.to(DEV))
+            torch.cuda.synchronize()
+            assert int(cache.status.item()) == 0
+            comp, res = cache.n_comp, cache.n_res
+            assert comp + res == t and comp % 128 == 0 and res >= min(t, 128)
+            assert cache.seq_lens.tolist() == [comp] * B and cache.res_lens.tolist() == [res] * B
+            ref = _oracle_stream(wlmod.bf16_bits(q), kb, vb, comp, res, otk, otv, H, G)
+            assert _rel_err(out.cpu().numpy().astype(np.float64), ref) < TOL, t
+        if t < T:
+            cache.append(kd[:, t].contiguous(), vd[:, t].contiguous())
+    n = cache.n_comp
+    krec, mq, ms, _ = kv.encode_keys_tokenwise(kb[:, :n], otk)
+    vrec, _ = kv.encode_values_tokenwise(vb[:, :n], otv)
+    gk = from_tiles(cache.cache.k_records.cpu().numpy())
+    gv = from_tiles(cache.cache.v_records.cpu().numpy())
+    assert np.array_equal(gk[:, :n, :krec.shape[2]], krec) and not gk[:, :n, krec.shape[2]:].any()
+    assert np.array_equal(gv[:, :n, :vrec.shape[2]], vrec) and not gv[:, :n, vrec.shape[2]:].any()
+    assert np.array_equal(cache.cache.k_mean_q[:, :, :n // 128].cpu().numpy(), mq)
+    assert np.array_equal(cache.cache.k_mean_scale[:, :, :n // 128].cpu().numpy().view(np.uint16),
+                          ms.view(np.uint16))
