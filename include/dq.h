@@ -304,6 +304,33 @@ int dq_decode_attention_token_partial(const dq_tables* k_tables, const dq_tables
                                       size_t workspace_bytes, uint32_t* status, void* stream);
 
 /*
+ * Per-token records in pool pages (the paged layout above, Sec. 4.1's fixed
+ * stride kept within a page): a pool page holds the records of page_tokens
+ * tokens in the tile layout of the record buffer, so the record pool is
+ * u8 [num_pages][page_tokens / 64][S / 8][64][8] and token t of sequence b is
+ * row t mod page_tokens of pool page block_table[b * max_pages + t /
+ * page_tokens].  Key-mean pools, the block table, page_tokens, the logical
+ * capacity and DQ_STATUS_PAGE are as for dq_encode_kv_paged and
+ * dq_decode_attention_paged_partial; otherwise the calls mean what
+ * dq_encode_kv_token and dq_decode_attention_token_partial mean.
+ */
+int dq_encode_kv_token_paged(const dq_tables* tables, const uint16_t* kv, int64_t stride_b,
+                             int64_t stride_t, int64_t stride_h, int32_t batch, int32_t kv_heads,
+                             int32_t t0, int32_t n_new, const int32_t* block_table,
+                             int32_t max_pages, int32_t page_tokens, int32_t num_pages,
+                             uint8_t* record_pool, int8_t* mean_q_pool, uint16_t* mean_scale_pool,
+                             uint32_t* status, void* stream);
+int dq_decode_attention_token_paged_partial(const dq_tables* k_tables, const dq_tables* v_tables,
+                                            const uint16_t* q, int32_t batch, int32_t q_heads,
+                                            int32_t kv_heads, const uint8_t* k_pool,
+                                            const int8_t* mean_q_pool, const uint16_t* mean_scale_pool,
+                                            const uint8_t* v_pool, const int32_t* block_table,
+                                            int32_t max_pages, int32_t page_tokens, int32_t num_pages,
+                                            const int32_t* seq_lens, float softmax_scale,
+                                            void* workspace, size_t workspace_bytes, uint32_t* status,
+                                            void* stream);
+
+/*
  * Comparator: fixed-width coding at matched storage (App. B).  The same
  * preprocessing as the D-Quant encoder (rotation, key window means, min-max
  * grid, least-squares refit, fp16 s and o), symbols by nearest-level rounding,

@@ -24,6 +24,7 @@ from ._lib import (  # noqa: F401
     dq_decode_attention_residual, dq_residual_append, dq_residual_commit,
     dq_bf16_decode_attention_partial, dq_encode_kv_paged, dq_decode_attention_paged_partial,
     dq_token_record_stride, token_records_shape, dq_encode_kv_token, dq_decode_attention_token_partial,
+    token_pool_shape, dq_encode_kv_token_paged, dq_decode_attention_token_paged_partial,
     dq_fixed_bits, dq_encode_kv_fixed, dq_decode_attention_fixed_partial,
     dq_decode_symbols, dq_strerror, dq_last_error, smallest_feasible_alpha,
 )

@@ -94,6 +94,12 @@ def _load():
     lib.dq_decode_attention_token_partial.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, ctypes.c_float,
                                                       P, SZ, P, P]
     lib.dq_decode_attention_token_partial.restype = ctypes.c_int
+    lib.dq_encode_kv_token_paged.argtypes = [P, P, I64, I64, I64, I32, I32, I32, I32, P, I32, I32, I32, P, P, P,
+                                             P, P]
+    lib.dq_encode_kv_token_paged.restype = ctypes.c_int
+    lib.dq_decode_attention_token_paged_partial.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, I32, I32,
+                                                            P, ctypes.c_float, P, SZ, P, P]
+    lib.dq_decode_attention_token_paged_partial.restype = ctypes.c_int
     lib.dq_fixed_bits.argtypes = [I32, I32]
     lib.dq_fixed_bits.restype = I32
     lib.dq_encode_kv_fixed.argtypes = [I32, I32, P, I64, I64, I64, I32, I32, I32, I32, I32, P, P, P, P, P]
@@ -448,6 +454,69 @@ def dq_decode_attention_token_partial(k_tables: Tables, v_tables: Tables, q, k_r
                                                 workspace.numel() * workspace.element_size(), _ptr(status),
                                                 _stream(stream))
     _check(rc, "dq_decode_attention_token_partial")
+
+
+def token_pool_shape(tables: Tables, num_pages: int, page_tokens: int):
+    """Shape of a paged per-token record pool: [num_pages, page / 64, S / 8, 64,
+    8] -- each page holds the 64-token tiles of page_tokens tokens."""
+    S = dq_token_record_stride(tables)
+    return (num_pages, page_tokens // 64, S // 8, 64, 8)
+
+
+def _token_pool_args(tables, record_pool, block_table, kv_heads, mean_q_pool=None, mean_scale_pool=None):
+    import torch
+    _need(record_pool.is_cuda and record_pool.dtype == torch.uint8 and record_pool.is_contiguous()
+          and record_pool.dim() == 5, "record pool must be uint8 [num_pages, page/64, S/8, 64, 8]")
+    num_pages, page = record_pool.shape[0], record_pool.shape[1] * 64
+    _need(tuple(record_pool.shape) == token_pool_shape(tables, num_pages, page), "record pool shape")
+    _need(block_table.is_cuda and block_table.dtype == torch.int32 and block_table.is_contiguous()
+          and block_table.dim() == 2, "block_table must be int32 [batch, max_pages]")
+    if mean_q_pool is not None:
+        _need(mean_q_pool.dtype == torch.int8 and mean_q_pool.is_contiguous()
+              and tuple(mean_q_pool.shape) == (num_pages, kv_heads, page // DQ_MEAN_WINDOW, 128), "mean_q pool")
+        _need(mean_scale_pool is not None and mean_scale_pool.element_size() == 2 and mean_scale_pool.is_contiguous()
+              and tuple(mean_scale_pool.shape) == (num_pages, kv_heads, page // DQ_MEAN_WINDOW), "mean_scale pool")
+    return num_pages, page, block_table.shape[1]
+
+
+def dq_encode_kv_token_paged(tables: Tables, kv, t0: int, block_table, record_pool, mean_q_pool=None,
+                             mean_scale_pool=None, status=None, stream=None):
+    """dq_encode_kv_token into a paged pool of token_pool_shape; block_table
+    int32 [B, max_pages]; keys also pass the mean pools [num_pages, H, page/128, ...]."""
+    import torch
+    _need(kv.is_cuda and kv.dtype == torch.bfloat16 and kv.dim() == 4 and kv.stride(3) == 1, "kv")
+    B, T, H, d = kv.shape
+    _need(d == 128 and tables.head_dim == 128 * H, "per-token streams need head_dim 128 and n = 128 H")
+    num_pages, page, max_pages = _token_pool_args(tables, record_pool, block_table, H, mean_q_pool, mean_scale_pool)
+    _need(block_table.shape[0] == B, "block_table rows")
+    rc = _lib.dq_encode_kv_token_paged(tables.handle, _ptr(kv), kv.stride(0), kv.stride(1), kv.stride(2), B, H,
+                                       int(t0), T, _ptr(block_table), max_pages, page, num_pages, _ptr(record_pool),
+                                       _ptr(mean_q_pool), _ptr(mean_scale_pool), _ptr(status), _stream(stream))
+    _check(rc, "dq_encode_kv_token_paged")
+
+
+def dq_decode_attention_token_paged_partial(k_tables: Tables, v_tables: Tables, q, k_pool, mean_q_pool,
+                                            mean_scale_pool, v_pool, block_table, seq_lens, workspace,
+                                            softmax_scale=None, status=None, stream=None):
+    """dq_decode_attention_token_partial over paged pools; finish with
+    dq_decode_attention_merge(..., t_cap = max_pages * page_tokens, ...)."""
+    import torch
+    _need(mean_q_pool is not None and mean_q_pool.dim() == 4, "mean_q pool")
+    Hkv = mean_q_pool.shape[1]
+    num_pages, page, max_pages = _token_pool_args(k_tables, k_pool, block_table, Hkv, mean_q_pool, mean_scale_pool)
+    _need(v_pool.is_cuda and v_pool.dtype == torch.uint8 and v_pool.is_contiguous()
+          and tuple(v_pool.shape) == token_pool_shape(v_tables, num_pages, page), "v pool")
+    _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3, "q")
+    B, Hq, d = q.shape
+    _need(block_table.shape[0] == B and seq_lens.is_cuda and seq_lens.dtype == torch.int32
+          and seq_lens.numel() == B, "block_table / seq_lens")
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    rc = _lib.dq_decode_attention_token_paged_partial(
+        k_tables.handle, v_tables.handle, _ptr(q), B, Hq, Hkv, _ptr(k_pool), _ptr(mean_q_pool),
+        _ptr(mean_scale_pool), _ptr(v_pool), _ptr(block_table), max_pages, page, num_pages, _ptr(seq_lens),
+        ctypes.c_float(scale), _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(status),
+        _stream(stream))
+    _check(rc, "dq_decode_attention_token_paged_partial")
 
 
 def dq_fixed_bits(head_dim: int, record_bytes: int) -> int:

@@ -381,10 +381,10 @@ __device__ __forceinline__ void stream_values(const EncArgs& a, int b, int h, in
     if (TOK) {
         load_token_rotated<VPL>(a.kv + (int64_t)b * a.sb + ti * a.st, a.sh, x, lane);
         if (a.mean_q) {
-            const int nwin = a.t_cap / DQ_MEAN_WINDOW;
+            bool bad = false;      // (a bad entry reads page 0; the record write then skips it)
 #pragma unroll
             for (int g = 0; g < VPL / 2; ++g) {
-                const int64_t wi = ((int64_t)b * a.H + g) * nwin + t / DQ_MEAN_WINDOW;
+                const int64_t wi = window_index(a.pg, a.H, a.t_cap, b, g, t / DQ_MEAN_WINDOW, bad);
                 const double sc = (double)__half2float(__ushort_as_half(a.mean_scale[wi]));
                 const int8_t* mq = a.mean_q + wi * kD;
                 x[2 * g] = x[2 * g] - sc * (double)mq[lane];
@@ -638,14 +638,23 @@ __global__ __launch_bounds__(kEncThreads, (TOK || MB == 16) ? 3 : 1) void encode
     // at a time through the block table, or per-token records at their stride
     // (zero-padded).
     if (TOK) {
-        // 64-token tiles, 8-byte chunk major: byte k of token t at
-        // ((t / 64) S / 8 + k / 8) 512 + (t % 64) 8 + k % 8
+        // 64-token tiles, 8-byte chunk major: byte k of the token in row r at
+        // ((r / 64) S / 8 + k / 8) 512 + (r % 64) 8 + k % 8, the row of token
+        // t through the block table when there is one
+        bool bad_page = false;
         for (int i = wave; i < active; i += kEncWaves) {
             const int t = first + i;
-            uint8_t* tile = a.records + ((int64_t)b * a.t_cap + (t & ~63)) * a.rec_stride + (t & 63) * 8;
+            bool bad = false;
+            const int64_t row = token_row(a.pg, a.t_cap, b, t, bad);
+            if (bad) {
+                bad_page = true;
+                continue;
+            }
+            uint8_t* tile = a.records + (row & ~(int64_t)63) * a.rec_stride + (row & 63) * 8;
             for (int k = lane; k < a.rec_stride; k += kWave)
                 tile[(k >> 3) * 512 + (k & 7)] = k < C ? s_rec[i * C + k] : (uint8_t)0;
         }
+        if (bad_page && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_PAGE);
     } else if (!a.pg.bt) {
         uint8_t* dst = a.records + ((int64_t)(b * a.H + h) * a.t_cap + first) * C;
         const int total = active * C;

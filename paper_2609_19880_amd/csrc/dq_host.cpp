@@ -369,6 +369,19 @@ int dq_encode_kv_token(const dq_tables* t, const uint16_t* kv, int64_t sb, int64
                      status, stream, stride);
 }
 
+int dq_encode_kv_token_paged(const dq_tables* t, const uint16_t* kv, int64_t sb, int64_t st, int64_t sh,
+                             int32_t B, int32_t H, int32_t t0, int32_t n_new, const int32_t* block_table,
+                             int32_t max_pages, int32_t page_tokens, int32_t num_pages, uint8_t* record_pool,
+                             int8_t* mean_q_pool, uint16_t* mean_scale_pool, uint32_t* status, void* stream) {
+    const int32_t stride = dq_token_record_stride(t);
+    if (stride <= 0) return DQ_ERR_INVALID_ARG;
+    dq::Pages pg;
+    int32_t t_cap = 0;
+    if (int rc = paging(block_table, max_pages, page_tokens, num_pages, &pg, &t_cap)) return rc;
+    return encode_kv(t, pg, kv, sb, st, sh, B, H, t0, n_new, t_cap, record_pool, mean_q_pool, mean_scale_pool,
+                     status, stream, stride);
+}
+
 int32_t dq_fixed_bits(int32_t head_dim, int32_t record_bytes) {
     if (head_dim <= 0 || record_bytes <= 4) return 0;
     const int64_t b = 8 * (int64_t)(record_bytes - 4) / head_dim;
@@ -448,11 +461,10 @@ int dq_decode_attention_partial(const dq_tables* tk, const dq_tables* tv, const 
                              ws, ws_bytes, status, stream);
 }
 
-int dq_decode_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
-                                      int32_t Hq, int32_t Hkv, const uint8_t* k_records, const int8_t* k_mean_q,
-                                      const uint16_t* k_mean_scale, const uint8_t* v_records,
-                                      const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
-                                      size_t ws_bytes, uint32_t* status, void* stream) {
+static int token_partial(const dq_tables* tk, const dq_tables* tv, const dq::Pages& pg, const uint16_t* q,
+                         int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* k_records, const int8_t* k_mean_q,
+                         const uint16_t* k_mean_scale, const uint8_t* v_records, const int32_t* seq_lens,
+                         int32_t t_cap, float scale, void* ws, size_t ws_bytes, uint32_t* status, void* stream) {
     if (!table_args_ok(tk) || !table_args_ok(tv)) return DQ_ERR_INVALID_ARG;
     if (Hkv != 1 && Hkv != 2 && Hkv != 4 && Hkv != 8) return DQ_ERR_INVALID_ARG;
     if (tk->cfg.head_dim != 128 * Hkv || tv->cfg.head_dim != 128 * Hkv) return DQ_ERR_INVALID_ARG;
@@ -461,9 +473,32 @@ int dq_decode_attention_token_partial(const dq_tables* tk, const dq_tables* tv, 
     if (!q || !k_records || !k_mean_q || !k_mean_scale || !v_records || !seq_lens) return DQ_ERR_INVALID_ARG;
     if (!std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
     if (!ws || ws_bytes < dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128)) return DQ_ERR_WORKSPACE;
-    return dq::launch_attention_token_partial(tk, tv, q, B, Hq, Hkv, k_records, dq_token_record_stride(tk),
+    return dq::launch_attention_token_partial(tk, tv, pg, q, B, Hq, Hkv, k_records, dq_token_record_stride(tk),
                                               k_mean_q, k_mean_scale, v_records, dq_token_record_stride(tv),
                                               seq_lens, t_cap, scale, ws, status, static_cast<hipStream_t>(stream));
+}
+
+int dq_decode_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
+                                      int32_t Hq, int32_t Hkv, const uint8_t* k_records, const int8_t* k_mean_q,
+                                      const uint16_t* k_mean_scale, const uint8_t* v_records,
+                                      const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
+                                      size_t ws_bytes, uint32_t* status, void* stream) {
+    return token_partial(tk, tv, kContiguous, q, B, Hq, Hkv, k_records, k_mean_q, k_mean_scale, v_records,
+                         seq_lens, t_cap, scale, ws, ws_bytes, status, stream);
+}
+
+int dq_decode_attention_token_paged_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q,
+                                            int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* k_pool,
+                                            const int8_t* mean_q_pool, const uint16_t* mean_scale_pool,
+                                            const uint8_t* v_pool, const int32_t* block_table, int32_t max_pages,
+                                            int32_t page_tokens, int32_t num_pages, const int32_t* seq_lens,
+                                            float scale, void* ws, size_t ws_bytes, uint32_t* status,
+                                            void* stream) {
+    dq::Pages pg;
+    int32_t t_cap = 0;
+    if (int rc = paging(block_table, max_pages, page_tokens, num_pages, &pg, &t_cap)) return rc;
+    return token_partial(tk, tv, pg, q, B, Hq, Hkv, k_pool, mean_q_pool, mean_scale_pool, v_pool, seq_lens, t_cap,
+                         scale, ws, ws_bytes, status, stream);
 }
 
 int dq_decode_attention_paged_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,

@@ -53,6 +53,16 @@ __device__ __forceinline__ int64_t record_row(const Pages& pg, int H, int t_cap,
     return ((p * H + h) << pg.page_shift) + (t & ((1 << pg.page_shift) - 1));
 }
 
+// Row of token t of sequence b in a per-token record buffer, whose rows hold
+// the records of all heads of one token: b t_cap + t, or row t mod page of
+// pool page p (rows p page .. p page + page - 1).  A page holds whole
+// 64-token tiles.
+__device__ __forceinline__ int64_t token_row(const Pages& pg, int t_cap, int b, int t, bool& bad) {
+    if (!pg.bt) return (int64_t)b * t_cap + t;
+    const int64_t p = physical_page(pg, b, t, bad);
+    return (p << pg.page_shift) + (t & ((1 << pg.page_shift) - 1));
+}
+
 // Index of the 128-token mean window w of (b, h).
 __device__ __forceinline__ int64_t window_index(const Pages& pg, int H, int t_cap, int b, int h, int w, bool& bad) {
     if (!pg.bt) return ((int64_t)b * H + h) * (t_cap / DQ_MEAN_WINDOW) + w;
@@ -146,8 +156,10 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pag
                              uint32_t* status, hipStream_t stream);
 
 // Per-token streams over Hkv heads (table n = 128 Hkv, G = Hq / Hkv <= 4),
-// records [B][t_cap][stride]; same workspace as launch_attention_partial.
-int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
+// records [B][t_cap][stride] in 64-token tiles, or token rows of pool pages
+// through pg; same workspace as launch_attention_partial.
+int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const Pages& pg, const uint16_t* q,
+                                   int32_t B,
                                    int32_t Hq, int32_t Hkv, const uint8_t* krec, int32_t k_stride,
                                    const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                                    int32_t v_stride, const int32_t* seq_lens, int32_t t_cap, float scale,

@@ -73,6 +73,7 @@ struct TokArgs {
     const uint16_t* kms;
     const uint8_t* vrec;
     int k_stride, v_stride;       // bytes per token record (multiples of 16)
+    Pages pg;                     // block table of a paged cache (bt null: contiguous)
     const int32_t* seq_lens;
     float scale_log2;             // softmax_scale * log2(e) / d
     int32_t* ws_hdr;
@@ -178,7 +179,9 @@ __device__ __forceinline__ float lane_get(float v, int i) {
 }
 __device__ __forceinline__ float lane_set(float v, int i, float x, int lane) { return lane == i ? x : v; }
 
-template <uint32_t LUTV>
+// PAGED: records and key means through the block table; a separate
+// instantiation, so that the contiguous kernel carries none of its state.
+template <uint32_t LUTV, bool PAGED>
 __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a) {
     extern __shared__ __align__(16) uint8_t smem[];
     const TokLayout& L = a.L;
@@ -194,6 +197,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
     const int T = min(a.seq_lens[b], a.t_cap);
     const int start = c * a.chunk;
     if (start >= T) return;   // the merge ignores chunks past the length
+    bool bad_page = false;    // a block-table entry outside the pool (read as page 0)
 
     // ---- prologue: tables, rotated queries, their digits, q . mu per window
     {
@@ -240,7 +244,8 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
             const int wi = it / Hkv, hk = it % Hkv;
             float f[4] = {0.f, 0.f, 0.f, 0.f};
             if (it < nwin * Hkv && w0 + wi < nwin_total) {
-                const int64_t widx = ((int64_t)b * Hkv + hk) * nwin_total + w0 + wi;
+                const int64_t widx = PAGED ? window_index(a.pg, Hkv, a.t_cap, b, hk, w0 + wi, bad_page)
+                                           : ((int64_t)b * Hkv + hk) * nwin_total + w0 + wi;
                 const float sc = half_bits_to_f32(a.kms[widx]);
                 const uint32_t mv = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + c4);
 #pragma unroll
@@ -290,8 +295,10 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
         const int t_base = start + tile * kTile;
         const int t = t_base + lane;               // < t_cap: tiles lie inside the capacity
         const bool valid = t < T;
-        const uint8_t* kr = a.krec + ((int64_t)b * a.t_cap + t_base) * a.k_stride + 8 * lane;
-        const uint8_t* vr = a.vrec + ((int64_t)b * a.t_cap + t_base) * a.v_stride + 8 * lane;
+        // a tile never straddles a page
+        const int64_t row0 = PAGED ? token_row(a.pg, a.t_cap, b, t_base, bad_page) : (int64_t)b * a.t_cap + t_base;
+        const uint8_t* kr = a.krec + row0 * a.k_stride + 8 * lane;
+        const uint8_t* vr = a.vrec + row0 * a.v_stride + 8 * lane;
         // chunks 0..2 (bytes 0..23) cover the first 4 steps from byte 8
         const uint2 k0 = load_chunk(kr, 0, last_k), k1 = load_chunk(kr, 1, last_k), k2 = load_chunk(kr, 2, last_k);
         const uint2 v0 = load_chunk(vr, 0, last_v), v1 = load_chunk(vr, 1, last_v), v2 = load_chunk(vr, 2, last_v);
@@ -432,6 +439,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
         corrupt |= valid && ((xv >> 3) != kRansL || pbv > endv);
     }
     if (__any(corrupt) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_CORRUPT);
+    if (PAGED && __any(bad_page) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_PAGE);
 
     // ---- merge the wavefronts of the workgroup, one KV head at a time
     const int NC = a.nchunks;
@@ -530,7 +538,28 @@ int32_t token_chunk(int32_t B, int32_t t_cap) {
     return std::min(chunk, kTokMaxChunk);
 }
 
-int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
+namespace {
+
+template <uint32_t LUTV>
+int launch_token_kernel(const TokArgs& a, dim3 grid, int nw, hipStream_t stream) {
+    const bool paged = a.pg.bt != nullptr;
+    const void* fn = paged ? reinterpret_cast<const void*>(&attn_token_kernel<LUTV, true>)
+                           : reinterpret_cast<const void*>(&attn_token_kernel<LUTV, false>);
+    if (int rc = hip_check("hipFuncSetAttribute",
+                           hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
+        return rc;
+    const size_t smem = (size_t)a.L.total;
+    if (paged)
+        attn_token_kernel<LUTV, true><<<grid, nw * kWave, smem, stream>>>(a);
+    else
+        attn_token_kernel<LUTV, false><<<grid, nw * kWave, smem, stream>>>(a);
+    return hip_check("attn_token launch", hipGetLastError());
+}
+
+}  // namespace
+
+int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const Pages& pg, const uint16_t* q,
+                                   int32_t B,
                                    int32_t Hq, int32_t Hkv, const uint8_t* krec, int32_t k_stride,
                                    const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                                    int32_t v_stride, const int32_t* seq_lens, int32_t t_cap, float scale,
@@ -552,6 +581,7 @@ int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, con
     a.vrec = vrec;
     a.k_stride = k_stride;
     a.v_stride = v_stride;
+    a.pg = pg;
     a.seq_lens = seq_lens;
     a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
     const int64_t slots = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
@@ -567,30 +597,16 @@ int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, con
     }
     if (nw == 0) return DQ_ERR_INVALID_ARG;
     const dim3 grid(a.nchunks, 1, B);
-    const void* fn;
-    const uint32_t lutv = shared ? 0u : (uint32_t)a.L.lut_v;
-    switch (lutv) {
-        case 0: fn = reinterpret_cast<const void*>(&attn_token_kernel<0>); break;
-        case 8u << 8: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 8>); break;
-        case 8u << 9: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 9>); break;
-        case 8u << 10: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 10>); break;
-        case 8u << 11: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 11>); break;
-        case 8u << 12: fn = reinterpret_cast<const void*>(&attn_token_kernel<8u << 12>); break;
+    const hipStream_t st = stream;
+    switch (shared ? 0u : (uint32_t)a.L.lut_v) {
+        case 0: return launch_token_kernel<0>(a, grid, nw, st);
+        case 8u << 8: return launch_token_kernel<8u << 8>(a, grid, nw, st);
+        case 8u << 9: return launch_token_kernel<8u << 9>(a, grid, nw, st);
+        case 8u << 10: return launch_token_kernel<8u << 10>(a, grid, nw, st);
+        case 8u << 11: return launch_token_kernel<8u << 11>(a, grid, nw, st);
+        case 8u << 12: return launch_token_kernel<8u << 12>(a, grid, nw, st);
         default: return DQ_ERR_INVALID_ARG;
     }
-    if (int rc = hip_check("hipFuncSetAttribute",
-                           hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
-        return rc;
-    const size_t smem = (size_t)a.L.total;
-    switch (lutv) {
-        case 0: attn_token_kernel<0><<<grid, nw * kWave, smem, stream>>>(a); break;
-        case 8u << 8: attn_token_kernel<8u << 8><<<grid, nw * kWave, smem, stream>>>(a); break;
-        case 8u << 9: attn_token_kernel<8u << 9><<<grid, nw * kWave, smem, stream>>>(a); break;
-        case 8u << 10: attn_token_kernel<8u << 10><<<grid, nw * kWave, smem, stream>>>(a); break;
-        case 8u << 11: attn_token_kernel<8u << 11><<<grid, nw * kWave, smem, stream>>>(a); break;
-        default: attn_token_kernel<8u << 12><<<grid, nw * kWave, smem, stream>>>(a); break;
-    }
-    return hip_check("attn_token launch", hipGetLastError());
 }
 
 }  // namespace dq

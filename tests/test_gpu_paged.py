@@ -5,6 +5,8 @@ the addresses differ), and the contiguous path is the one checked against
 the oracle elsewhere; here it is re-checked against the oracle once more.
 """
 
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -131,3 +133,144 @@ def test_paged_bad_block_table_entry_is_flagged(dq):
     torch.cuda.synchronize()
     assert int(status.item()) & dq.DQ_STATUS_PAGE
     assert torch.isfinite(out).all()
+
+
+# ---- per-token records (one stream per token over all KV heads) in pages
+
+def _token_setup(dq, page=256, max_pages=4, extra=5, seed=43):
+    H, G, B = 2, 4, 3
+    gtk = dq.Tables(128 * H, 8, 8, 88, 1.4)
+    gtv = dq.Tables(128 * H, 6, 8, 62, 1.4)
+    t_cap = page * max_pages
+    num_pages = B * max_pages + extra
+    rng = np.random.default_rng(seed)
+    bt = rng.permutation(num_pages)[: B * max_pages].reshape(B, max_pages).astype(np.int32)
+    wl = wlmod.workload("b1_t4k_tok")
+    w2 = wlmod.Workload("tok_paged", B, t_cap, H * G, H, 4, wl.k, wl.v, streams="token")
+    k = wlmod.make_k(w2, seed).to(DEV)
+    v = wlmod.make_v(w2, seed).to(DEV)
+    q = wlmod.make_q(w2, seed).to(DEV)
+    return gtk, gtv, B, H, G, page, max_pages, t_cap, num_pages, bt, k, v, q
+
+
+def _token_pools(dq, gtk, gtv, num_pages, H, page):
+    # one spare page past num_pages, as above
+    kp = torch.zeros(dq.token_pool_shape(gtk, num_pages + 1, page), dtype=torch.uint8, device=DEV)
+    vp = torch.zeros(dq.token_pool_shape(gtv, num_pages + 1, page), dtype=torch.uint8, device=DEV)
+    mq = torch.zeros((num_pages + 1, H, page // 128, 128), dtype=torch.int8, device=DEV)
+    ms = torch.zeros((num_pages + 1, H, page // 128), dtype=torch.int16, device=DEV)
+    return kp, vp, mq, ms
+
+
+def test_token_paged_encode_and_attention_equal_contiguous(dq):
+    gtk, gtv, B, H, G, page, max_pages, t_cap, num_pages, bt, k, v, q = _token_setup(dq)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    cache = dq.TokenKVCache(B, H, H * G, t_cap, gtk, gtv, device=DEV)
+    dq.dq_encode_kv_token(gtk, k[:, :512], 0, t_cap, cache.k_records, cache.k_mean_q, cache.k_mean_scale, status)
+    dq.dq_encode_kv_token(gtk, k[:, 512:], 512, t_cap, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
+                          status)
+    dq.dq_encode_kv_token(gtv, v[:, :300], 0, t_cap, cache.v_records, None, None, status)
+    dq.dq_encode_kv_token(gtv, v[:, 300:], 300, t_cap, cache.v_records, None, None, status)
+    kp, vp, mq, ms = _token_pools(dq, gtk, gtv, num_pages, H, page)
+    btd = torch.from_numpy(bt).to(DEV)
+    kpool, vpool, mqpool, mspool = kp[:num_pages], vp[:num_pages], mq[:num_pages], ms[:num_pages]
+    dq.dq_encode_kv_token_paged(gtk, k[:, :512], 0, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_token_paged(gtk, k[:, 512:], 512, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_token_paged(gtv, v[:, :300], 0, btd, vpool, None, None, status)
+    dq.dq_encode_kv_token_paged(gtv, v[:, 300:], 300, btd, vpool, None, None, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    tiles = page // 64
+    for b in range(B):
+        for i in range(max_pages):
+            p = int(bt[b, i])
+            assert torch.equal(kpool[p], cache.k_records[b, i * tiles:(i + 1) * tiles])
+            assert torch.equal(vpool[p], cache.v_records[b, i * tiles:(i + 1) * tiles])
+            assert torch.equal(mqpool[p], cache.k_mean_q[b, :, i * page // 128:(i + 1) * page // 128])
+            assert torch.equal(mspool[p], cache.k_mean_scale[b, :, i * page // 128:(i + 1) * page // 128])
+    assert int(kp[num_pages].abs().sum()) == 0 and int(vp[num_pages].abs().sum()) == 0
+    lens = torch.tensor([t_cap, 0, 700], dtype=torch.int32, device=DEV)
+    out_c = cache.attend(q, lens)
+    ws = torch.empty_like(cache.workspace)
+    out_p = torch.empty_like(out_c)
+    dq.dq_decode_attention_token_paged_partial(gtk, gtv, q, kpool, mqpool, mspool, vpool, btd, lens, ws,
+                                               status=status)
+    dq.dq_decode_attention_merge(B, H * G, H, lens, t_cap, ws, out_p)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert torch.equal(out_c, out_p)
+    # and the oracle on the same tokens
+    otk = tables.build_tables(128 * H, 8, 8, 1.4, 88)
+    otv = tables.build_tables(128 * H, 6, 8, 1.4, 62)
+    kb, vb = wlmod.bf16_bits(k.cpu()), wlmod.bf16_bits(v.cpu())
+    krec, m_q, m_s, _ = kv.encode_keys_tokenwise(kb, otk)
+    vrec, _ = kv.encode_values_tokenwise(vb, otv)
+    ksym, ks, ko, _ = kv.decode_records(krec, otk, 128 * H)
+    vsym, vs, vo, _ = kv.decode_records(vrec, otv, 128 * H)
+    kh, ksh, koh = kv.tokenwise_as_heads(ksym, ks, ko, H)
+    vh, vsh, voh = kv.tokenwise_as_heads(vsym, vs, vo, H)
+    ref = attention.attention_folded(kv.bf16_to_f64(wlmod.bf16_bits(q.cpu())), kh, ksh, koh,
+                                     kmean.dequantize_mean(m_q, m_s), vh, vsh, voh, lens.tolist(), G,
+                                     1 / np.sqrt(128))
+    got = out_p.cpu().numpy().astype(np.float64)
+    live = [0, 2]
+    scale = np.max(np.abs(ref[live]), axis=-1, keepdims=True)
+    assert float(np.max(np.abs(got[live] - ref[live]) / scale)) < TOL
+    assert np.all(got[1] == 0.0)
+
+
+def test_token_paged_bad_block_table_entry_is_flagged(dq):
+    gtk, gtv, B, H, G, page, max_pages, t_cap, num_pages, bt, k, v, q = _token_setup(dq, seed=44)
+    kp, vp, mq, ms = _token_pools(dq, gtk, gtv, num_pages, H, page)
+    kpool, vpool, mqpool, mspool = kp[:num_pages], vp[:num_pages], mq[:num_pages], ms[:num_pages]
+    bad = bt.copy()
+    bad[1, 2] = num_pages          # one past the pool
+    btd = torch.from_numpy(bad).to(DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    dq.dq_encode_kv_token_paged(gtk, k, 0, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_token_paged(gtv, v, 0, btd, vpool, None, None, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) & dq.DQ_STATUS_PAGE
+    assert int(kp[num_pages].abs().sum()) == 0 and int(mq[num_pages].abs().sum()) == 0
+    status.zero_()
+    lens = torch.tensor([t_cap, t_cap, t_cap], dtype=torch.int32, device=DEV)
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, t_cap), dtype=torch.uint8, device=DEV)
+    out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
+    dq.dq_decode_attention_token_paged_partial(gtk, gtv, q, kpool, mqpool, mspool, vpool, btd, lens, ws,
+                                               status=status)
+    dq.dq_decode_attention_merge(B, H * G, H, lens, t_cap, ws, out)
+    torch.cuda.synchronize()
+    assert int(status.item()) & dq.DQ_STATUS_PAGE
+    assert torch.isfinite(out).all()
+
+
+def test_token_paged_arguments_rejected(dq):
+    gtk, gtv, B, H, G, page, max_pages, t_cap, num_pages, bt, k, v, q = _token_setup(dq, seed=45)
+    lib = dq._lib._lib
+    kp, vp, mq, ms = _token_pools(dq, gtk, gtv, num_pages, H, page)
+    btd = torch.from_numpy(bt).to(DEV)
+    p = kp.data_ptr()
+
+    def enc(page_tokens=page, num=num_pages, maxp=max_pages, tab=gtk, n_new=128):
+        return lib.dq_encode_kv_token_paged(tab.handle, k.data_ptr(), k.stride(0), k.stride(1), k.stride(2), B, H,
+                                            0, n_new, btd.data_ptr(), maxp, page_tokens, num, p, None, None, None,
+                                            None)
+    assert enc() == dq.DQ_OK
+    assert enc(page_tokens=192) == dq.DQ_ERR_INVALID_ARG      # not a power of two
+    assert enc(page_tokens=64) == dq.DQ_ERR_INVALID_ARG       # below a mean window
+    assert enc(num=0) == dq.DQ_ERR_INVALID_ARG
+    assert enc(maxp=0) == dq.DQ_ERR_INVALID_ARG
+    assert enc(n_new=t_cap + 128) == dq.DQ_ERR_INVALID_ARG   # past the logical capacity
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, t_cap), dtype=torch.uint8, device=DEV)
+    lens = torch.tensor([t_cap] * B, dtype=torch.int32, device=DEV)
+
+    def attn(Hq=H * G, ws_bytes=ws.numel(), page_tokens=page):
+        return lib.dq_decode_attention_token_paged_partial(gtk.handle, gtv.handle, q.data_ptr(), B, Hq, H, p,
+                                                           mq.data_ptr(), ms.data_ptr(), vp.data_ptr(),
+                                                           btd.data_ptr(), max_pages, page_tokens, num_pages,
+                                                           lens.data_ptr(), ctypes.c_float(1 / 128 ** 0.5),
+                                                           ws.data_ptr(), ws_bytes, None, None)
+    assert attn(Hq=H * 8) == dq.DQ_ERR_INVALID_ARG           # G = 8 is not supported for per-token streams
+    assert attn(ws_bytes=64) == dq.DQ_ERR_WORKSPACE
+    assert attn(page_tokens=100) == dq.DQ_ERR_INVALID_ARG
+    torch.cuda.synchronize()
