@@ -393,11 +393,11 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
 #pragma unroll
             for (int d = 0; d < 3; ++d) dk[hg][d] = v4i{0, 0, 0, 0};
         uint32_t vlev[kD / 4];
-        // query digits: with two head groups (8 wavefronts per CU) they are
-        // read one group ahead, so that the products do not wait for the read;
-        // with 16 wavefronts the others cover that wait, and reading in place
-        // keeps the registers of the one-group case free
-        constexpr bool kAhead = HG > 1;
+        // query digits: with up to 12 wavefronts per CU they are read one
+        // group ahead, so that the products do not wait for the read; with 16
+        // the others cover that wait, and reading in place keeps the
+        // registers of that case free
+        constexpr bool kAhead = HG > 1 || WMAX <= 12;
         uint4 qla[HG];
         if constexpr (kAhead) {
 #pragma unroll

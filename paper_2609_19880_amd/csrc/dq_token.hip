@@ -597,14 +597,13 @@ int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, con
     }
     if (nw == 0) return DQ_ERR_INVALID_ARG;
     const dim3 grid(a.nchunks, 1, B);
-    const hipStream_t st = stream;
     switch (shared ? 0u : (uint32_t)a.L.lut_v) {
-        case 0: return launch_token_kernel<0>(a, grid, nw, st);
-        case 8u << 8: return launch_token_kernel<8u << 8>(a, grid, nw, st);
-        case 8u << 9: return launch_token_kernel<8u << 9>(a, grid, nw, st);
-        case 8u << 10: return launch_token_kernel<8u << 10>(a, grid, nw, st);
-        case 8u << 11: return launch_token_kernel<8u << 11>(a, grid, nw, st);
-        case 8u << 12: return launch_token_kernel<8u << 12>(a, grid, nw, st);
+        case 0: return launch_token_kernel<0>(a, grid, nw, stream);
+        case 8u << 8: return launch_token_kernel<8u << 8>(a, grid, nw, stream);
+        case 8u << 9: return launch_token_kernel<8u << 9>(a, grid, nw, stream);
+        case 8u << 10: return launch_token_kernel<8u << 10>(a, grid, nw, stream);
+        case 8u << 11: return launch_token_kernel<8u << 11>(a, grid, nw, stream);
+        case 8u << 12: return launch_token_kernel<8u << 12>(a, grid, nw, stream);
         default: return DQ_ERR_INVALID_ARG;
     }
 }
