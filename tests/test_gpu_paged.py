@@ -137,10 +137,10 @@ def test_paged_bad_block_table_entry_is_flagged(dq):
 
 # ---- per-token records (one stream per token over all KV heads) in pages
 
-def _token_setup(dq, page=256, max_pages=4, extra=5, seed=43):
-    H, G, B = 2, 4, 3
-    gtk = dq.Tables(128 * H, 8, 8, 88, 1.4)
-    gtv = dq.Tables(128 * H, 6, 8, 62, 1.4)
+def _token_setup(dq, page=256, max_pages=4, extra=5, seed=43, H=2, G=4, Ck=88, Cv=62, p=8):
+    B = 3
+    gtk = dq.Tables(128 * H, 8, p, Ck, 1.4)
+    gtv = dq.Tables(128 * H, 6, p, Cv, 1.4)
     t_cap = page * max_pages
     num_pages = B * max_pages + extra
     rng = np.random.default_rng(seed)
@@ -162,34 +162,42 @@ def _token_pools(dq, gtk, gtv, num_pages, H, page):
     return kp, vp, mq, ms
 
 
-def test_token_paged_encode_and_attention_equal_contiguous(dq):
-    gtk, gtv, B, H, G, page, max_pages, t_cap, num_pages, bt, k, v, q = _token_setup(dq)
+# (KV heads, query heads per KV head, K / V record bytes, p, page tokens, pages per sequence):
+# a small stream, the paper's operating point (8 heads, 331 + 4 / 231 + 4 bytes)
+# and p = 12 with two query heads per KV head
+TOKEN_PAGED = [(2, 4, 88, 62, 8, 256, 4), (8, 4, 335, 235, 8, 128, 2), (4, 2, 170, 120, 12, 128, 4)]
+
+
+@pytest.mark.parametrize("H,G,Ck,Cv,p,page,max_pages", TOKEN_PAGED)
+def test_token_paged_encode_and_attention_equal_contiguous(dq, H, G, Ck, Cv, p, page, max_pages):
+    gtk, gtv, B, H, G, page, max_pages, t_cap, num_pages, bt, k, v, q = _token_setup(
+        dq, page=page, max_pages=max_pages, H=H, G=G, Ck=Ck, Cv=Cv, p=p)
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
     cache = dq.TokenKVCache(B, H, H * G, t_cap, gtk, gtv, device=DEV)
-    dq.dq_encode_kv_token(gtk, k[:, :512], 0, t_cap, cache.k_records, cache.k_mean_q, cache.k_mean_scale, status)
-    dq.dq_encode_kv_token(gtk, k[:, 512:], 512, t_cap, cache.k_records, cache.k_mean_q, cache.k_mean_scale,
-                          status)
-    dq.dq_encode_kv_token(gtv, v[:, :300], 0, t_cap, cache.v_records, None, None, status)
-    dq.dq_encode_kv_token(gtv, v[:, 300:], 300, t_cap, cache.v_records, None, None, status)
+    kh, vs = t_cap // 2, 300 * t_cap // 1024      # keys in whole windows, values mid-tile
+    dq.dq_encode_kv_token(gtk, k[:, :kh], 0, t_cap, cache.k_records, cache.k_mean_q, cache.k_mean_scale, status)
+    dq.dq_encode_kv_token(gtk, k[:, kh:], kh, t_cap, cache.k_records, cache.k_mean_q, cache.k_mean_scale, status)
+    dq.dq_encode_kv_token(gtv, v[:, :vs], 0, t_cap, cache.v_records, None, None, status)
+    dq.dq_encode_kv_token(gtv, v[:, vs:], vs, t_cap, cache.v_records, None, None, status)
     kp, vp, mq, ms = _token_pools(dq, gtk, gtv, num_pages, H, page)
     btd = torch.from_numpy(bt).to(DEV)
     kpool, vpool, mqpool, mspool = kp[:num_pages], vp[:num_pages], mq[:num_pages], ms[:num_pages]
-    dq.dq_encode_kv_token_paged(gtk, k[:, :512], 0, btd, kpool, mqpool, mspool, status)
-    dq.dq_encode_kv_token_paged(gtk, k[:, 512:], 512, btd, kpool, mqpool, mspool, status)
-    dq.dq_encode_kv_token_paged(gtv, v[:, :300], 0, btd, vpool, None, None, status)
-    dq.dq_encode_kv_token_paged(gtv, v[:, 300:], 300, btd, vpool, None, None, status)
+    dq.dq_encode_kv_token_paged(gtk, k[:, :kh], 0, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_token_paged(gtk, k[:, kh:], kh, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_token_paged(gtv, v[:, :vs], 0, btd, vpool, None, None, status)
+    dq.dq_encode_kv_token_paged(gtv, v[:, vs:], vs, btd, vpool, None, None, status)
     torch.cuda.synchronize()
     assert int(status.item()) == 0
     tiles = page // 64
     for b in range(B):
         for i in range(max_pages):
-            p = int(bt[b, i])
-            assert torch.equal(kpool[p], cache.k_records[b, i * tiles:(i + 1) * tiles])
-            assert torch.equal(vpool[p], cache.v_records[b, i * tiles:(i + 1) * tiles])
-            assert torch.equal(mqpool[p], cache.k_mean_q[b, :, i * page // 128:(i + 1) * page // 128])
-            assert torch.equal(mspool[p], cache.k_mean_scale[b, :, i * page // 128:(i + 1) * page // 128])
+            pp = int(bt[b, i])
+            assert torch.equal(kpool[pp], cache.k_records[b, i * tiles:(i + 1) * tiles])
+            assert torch.equal(vpool[pp], cache.v_records[b, i * tiles:(i + 1) * tiles])
+            assert torch.equal(mqpool[pp], cache.k_mean_q[b, :, i * page // 128:(i + 1) * page // 128])
+            assert torch.equal(mspool[pp], cache.k_mean_scale[b, :, i * page // 128:(i + 1) * page // 128])
     assert int(kp[num_pages].abs().sum()) == 0 and int(vp[num_pages].abs().sum()) == 0
-    lens = torch.tensor([t_cap, 0, 700], dtype=torch.int32, device=DEV)
+    lens = torch.tensor([t_cap, 0, 700 * t_cap // 1024], dtype=torch.int32, device=DEV)
     out_c = cache.attend(q, lens)
     ws = torch.empty_like(cache.workspace)
     out_p = torch.empty_like(out_c)
@@ -200,8 +208,8 @@ def test_token_paged_encode_and_attention_equal_contiguous(dq):
     assert int(status.item()) == 0
     assert torch.equal(out_c, out_p)
     # and the oracle on the same tokens
-    otk = tables.build_tables(128 * H, 8, 8, 1.4, 88)
-    otv = tables.build_tables(128 * H, 6, 8, 1.4, 62)
+    otk = tables.build_tables(128 * H, 8, p, 1.4, Ck)
+    otv = tables.build_tables(128 * H, 6, p, 1.4, Cv)
     kb, vb = wlmod.bf16_bits(k.cpu()), wlmod.bf16_bits(v.cpu())
     krec, m_q, m_s, _ = kv.encode_keys_tokenwise(kb, otk)
     vrec, _ = kv.encode_values_tokenwise(vb, otv)
