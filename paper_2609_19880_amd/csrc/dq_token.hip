@@ -21,11 +21,14 @@
 // [dword row][lane] so that every lane stays in its own bank; a ninth row
 // repeats row 0 so that two consecutive dwords are always rows r, r + 1.  A
 // decode step reads the two dwords holding its byte position and takes the
-// next 16 bits with a funnel shift and a byte permute.  Every 4 steps a lane
-// whose ring would run short writes its next chunk (held in registers since
-// the previous refill) and loads the one after: 4 steps read at most 8 bytes,
-// so one chunk per check keeps the ring 14 bytes ahead of the pointer, and
-// four chunks are never overwritten while still needed.  Ring rows are
+// next 16 bits with a funnel shift and a byte permute.  Every 8 steps a lane
+// whose ring holds fewer than 20 bytes from its position writes its next
+// chunk (held in registers since the previous refill) and loads the one
+// after, and does so once more in the rare case that it is still short: 8
+// steps read at most 16 bytes, and their two-dword windows reach at most 19
+// bytes past the position.  A chunk is written only while the ring is short,
+// so the chunk four back that it replaces lies wholly behind the position
+// and is never read again.  Ring rows are
 // masked, so a corrupt stream reads garbage inside its ring, never outside;
 // it is flagged at the end (state != L or pointer past the record).
 #include <math.h>
@@ -133,8 +136,9 @@ __device__ __forceinline__ void put_chunk(uint32_t ring_lane, uint32_t c, const 
     if ((c & 3u) == 0) *LDS_PTR(uint32_t, ring_lane + kRingRows * kRingRow) = v.x;
 }
 
-// Keeps 8 nc >= pos + 14: the next 4 steps read bytes below pos + 14.  thr is
-// 8 (8 nc - 14) - 1 in bits, so the test is one compare.  Both rings are
+// One chunk per ring toward 8 nc >= pos + 20 (the bytes the next 8 steps can
+// read).  thr is 8 (8 nc - 20) - 1 in bits, so the test is one compare.  Both
+// rings are
 // written before either chunk load is issued: the loads complete in order, so
 // the writes wait only for chunks loaded at earlier refills, never for the
 // other ring's load of this group.
@@ -299,19 +303,23 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
         const int64_t row0 = PAGED ? token_row(a.pg, a.t_cap, b, t_base, bad_page) : (int64_t)b * a.t_cap + t_base;
         const uint8_t* kr = a.krec + row0 * a.k_stride + 8 * lane;
         const uint8_t* vr = a.vrec + row0 * a.v_stride + 8 * lane;
-        // chunks 0..2 (bytes 0..23) cover the first 4 steps from byte 8
-        const uint2 k0 = load_chunk(kr, 0, last_k), k1 = load_chunk(kr, 1, last_k), k2 = load_chunk(kr, 2, last_k);
-        const uint2 v0 = load_chunk(vr, 0, last_v), v1 = load_chunk(vr, 1, last_v), v2 = load_chunk(vr, 2, last_v);
-        uint2 nk = load_chunk(kr, 3, last_k), nv = load_chunk(vr, 3, last_v);
+        // chunks 0..3 (bytes 0..31) cover the first 8 steps from byte 8
+        const uint2 k0 = load_chunk(kr, 0, last_k), k1 = load_chunk(kr, 1, last_k), k2 = load_chunk(kr, 2, last_k),
+                    k3 = load_chunk(kr, 3, last_k);
+        const uint2 v0 = load_chunk(vr, 0, last_v), v1 = load_chunk(vr, 1, last_v), v2 = load_chunk(vr, 2, last_v),
+                    v3 = load_chunk(vr, 3, last_v);
+        uint2 nk = load_chunk(kr, 4, last_k), nv = load_chunk(vr, 4, last_v);
         wave_sync();   // the previous tile is done with the rings
         put_chunk(ring_k, 0, k0);
         put_chunk(ring_k, 1, k1);
         put_chunk(ring_k, 2, k2);
+        put_chunk(ring_k, 3, k3);
         put_chunk(ring_v, 0, v0);
         put_chunk(ring_v, 1, v1);
         put_chunk(ring_v, 2, v2);
-        uint32_t nck = 3, ncv = 3;
-        uint32_t thrk = 8u * (8u * 3u - 14u) - 1u, thrv = thrk;
+        put_chunk(ring_v, 3, v3);
+        uint32_t nck = 4, ncv = 4;
+        uint32_t thrk = 8u * (8u * 4u - 20u) - 1u, thrv = thrk;
         uint32_t xk = k0.y << 3, xv = v0.y << 3;
         uint32_t pbk = 64, pbv = 64;                // payload starts at byte 8
         const float sk = half_lo(k0.x), ok = half_hi(k0.x);
@@ -340,7 +348,10 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
                 dk[1] = mfma(ql.y, lk, dk[1]);
                 dk[2] = mfma(ql.z, lk, dk[2]);
                 if (grp + 1 < kGroups) ql = *reinterpret_cast<const uint4*>(qh + (grp + 1) * 4 * 16);
-                refill2(pbk, nck, thrk, nk, ring_k, kr, last_k, pbv, ncv, thrv, nv, ring_v, vr, last_v);
+                if (grp & 1) {
+                    refill2(pbk, nck, thrk, nk, ring_k, kr, last_k, pbv, ncv, thrv, nv, ring_v, vr, last_v);
+                    refill2(pbk, nck, thrk, nk, ring_k, kr, last_k, pbv, ncv, thrv, nv, ring_v, vr, last_v);
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
 
