@@ -28,9 +28,9 @@
 // steps read at most 16 bytes, and their two-dword windows reach at most 19
 // bytes past the position.  A chunk is written only while the ring is short,
 // so the chunk four back that it replaces lies wholly behind the position
-// and is never read again.  Ring rows are
-// masked, so a corrupt stream reads garbage inside its ring, never outside;
-// it is flagged at the end (state != L or pointer past the record).
+// and is never read again.  Ring rows are masked, so a corrupt stream reads
+// garbage inside its ring, never outside; it is flagged at the end (state !=
+// L or pointer past the record).
 #include <math.h>
 
 #include <algorithm>
@@ -138,10 +138,9 @@ __device__ __forceinline__ void put_chunk(uint32_t ring_lane, uint32_t c, const 
 
 // One chunk per ring toward 8 nc >= pos + 20 (the bytes the next 8 steps can
 // read).  thr is 8 (8 nc - 20) - 1 in bits, so the test is one compare.  Both
-// rings are
-// written before either chunk load is issued: the loads complete in order, so
-// the writes wait only for chunks loaded at earlier refills, never for the
-// other ring's load of this group.
+// rings are written before either chunk load is issued: the loads complete in
+// order, so the writes wait only for chunks loaded at earlier refills, never
+// for the other ring's load of this group.
 __device__ __forceinline__ void refill2(uint32_t pbk, uint32_t& nck, uint32_t& thrk, uint2& nk, uint32_t ring_k,
                                         const uint8_t* kr, uint32_t last_k, uint32_t pbv, uint32_t& ncv,
                                         uint32_t& thrv, uint2& nv, uint32_t ring_v, const uint8_t* vr,
