@@ -163,6 +163,33 @@ int dq_decode_attention(const dq_tables* k_tables, const dq_tables* v_tables,
                         uint32_t* status, void* stream);
 
 /*
+ * dq_decode_attention without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops and
+ * harnesses that forbid hipMalloc).  The split-K workspace lives in a static
+ * device array of DQ_NO_ALLOC_SCRATCH_BYTES inside the library, one per
+ * device, held until the process ends; its address is looked up on the first
+ * call on each device (with that device current).  Arguments, layouts,
+ * results and status bits are those of dq_decode_attention, and the same
+ * kernels run.  No call allocates or frees memory.
+ * Every call on a device shares that device's array, which keeps the last
+ * call's contents: calls that overlap on one device (different streams, or
+ * different host threads) race and give undefined results; serialize them.
+ * The workspace this needs is 256 + 520 batch q_heads (chunks + 1) bytes,
+ * chunks being the context split chosen from (batch, kv_heads, t_cap) and the
+ * CU count (2 for 16 x 32768 tokens x 8 KV heads on 256 CUs: 0.8 MB).
+ * Returns DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_WORKSPACE when the sizes need more
+ * than the array holds (dq_last_error says how much), or DQ_ERR_HIP.
+ */
+#define DQ_NO_ALLOC_SCRATCH_BYTES (8u << 20)
+int dq_decode_attention_no_alloc(const dq_tables* k_tables, const dq_tables* v_tables,
+                                 const uint16_t* q, int32_t batch, int32_t q_heads,
+                                 int32_t kv_heads, const uint8_t* k_records,
+                                 const int8_t* k_mean_q, const uint16_t* k_mean_scale,
+                                 const uint8_t* v_records, const int32_t* seq_lens,
+                                 int32_t t_cap, float softmax_scale, float* out,
+                                 uint32_t* status, void* stream);
+
+/*
  * The two halves of dq_decode_attention, for callers that merge partial
  * results themselves (e.g. context split over devices) or time them apart.
  * _partial writes one (max, sum, accumulator) triple per (sequence, query

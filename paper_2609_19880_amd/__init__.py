@@ -7,9 +7,9 @@ raises if the library has not been built (``__graft_entry__.build()``).
 
 Entry points (same names as the C ABI in ``include/dq.h``):
     dq_compute_tables, dq_build_tables, dq_encode_kv,
-    dq_decode_workspace_bytes, dq_decode_attention, dq_decode_attention_partial,
-    dq_decode_attention_merge, dq_decode_attention_residual, dq_residual_append,
-    dq_residual_commit, dq_bf16_decode_attention_partial, dq_encode_kv_paged,
+    dq_decode_workspace_bytes, dq_decode_attention, dq_decode_attention_no_alloc,
+    dq_decode_attention_partial, dq_decode_attention_merge, dq_decode_attention_residual,
+    dq_residual_append, dq_residual_commit, dq_bf16_decode_attention_partial, dq_encode_kv_paged,
     dq_decode_attention_paged_partial, dq_token_record_stride, dq_encode_kv_token,
     dq_decode_attention_token_partial, dq_fixed_bits, dq_encode_kv_fixed,
     dq_decode_attention_fixed_partial, dq_decode_symbols, dq_strerror, dq_last_error
@@ -20,8 +20,9 @@ from ._lib import (  # noqa: F401
     DQ_STATUS_RANGE, DQ_STATUS_OVERFLOW, DQ_STATUS_CORRUPT, DQ_STATUS_WINDOW, DQ_STATUS_PAGE, DQ_MEAN_WINDOW,
     DqError, Tables, TableInfo, library_path,
     dq_compute_tables, dq_build_tables, dq_encode_kv, dq_decode_workspace_bytes,
-    dq_decode_attention, dq_decode_attention_partial, dq_decode_attention_merge,
-    dq_decode_attention_residual, dq_residual_append, dq_residual_commit,
+    dq_decode_attention, dq_decode_attention_no_alloc, DQ_NO_ALLOC_SCRATCH_BYTES,
+    dq_decode_attention_partial, dq_decode_attention_merge, dq_decode_attention_residual,
+    dq_residual_append, dq_residual_commit,
     dq_bf16_decode_attention_partial, dq_encode_kv_paged, dq_decode_attention_paged_partial,
     dq_token_record_stride, token_records_shape, dq_encode_kv_token, dq_decode_attention_token_partial,
     token_pool_shape, dq_encode_kv_token_paged, dq_decode_attention_token_paged_partial,

@@ -74,6 +74,9 @@ def _load():
     lib.dq_decode_attention.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, ctypes.c_float,
                                         P, P, SZ, P, P]
     lib.dq_decode_attention.restype = ctypes.c_int
+    lib.dq_decode_attention_no_alloc.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, ctypes.c_float,
+                                                 P, P, P]
+    lib.dq_decode_attention_no_alloc.restype = ctypes.c_int
     lib.dq_decode_attention_partial.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32,
                                                 ctypes.c_float, P, SZ, P, P]
     lib.dq_decode_attention_partial.restype = ctypes.c_int
@@ -618,6 +621,36 @@ def dq_decode_attention(k_tables: Tables, v_tables: Tables, q, k_records, k_mean
                                   _ptr(seq_lens), t_cap, ctypes.c_float(scale), _ptr(out),
                                   _ptr(workspace), ws_bytes, _ptr(status), _stream(stream))
     _check(rc, "dq_decode_attention")
+
+
+DQ_NO_ALLOC_SCRATCH_BYTES = 8 << 20
+
+
+def dq_decode_attention_no_alloc(k_tables: Tables, v_tables: Tables, q, k_records, k_mean_q, k_mean_scale,
+                                 v_records, seq_lens, out, softmax_scale=None, status=None, stream=None):
+    """dq_decode_attention with the split-K workspace in the library's static
+    per-device scratch array: nothing is allocated.  Calls that overlap on one
+    device race (they share the array)."""
+    import torch
+    _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3, "q")
+    B, Hq, d = q.shape
+    _need(k_records.dim() == 4 and k_records.is_contiguous() and k_records.dtype == torch.uint8, "k_records")
+    _, Hkv, t_cap, Ck = k_records.shape
+    _need(Ck == k_tables.record_bytes and k_records.shape[0] == B, "k_records shape")
+    _need(v_records.is_contiguous() and tuple(v_records.shape) == (B, Hkv, t_cap, v_tables.record_bytes),
+          "v_records shape")
+    _need(k_mean_q.is_contiguous() and tuple(k_mean_q.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW, d), "k_mean_q")
+    _need(k_mean_scale.is_contiguous() and tuple(k_mean_scale.shape) == (B, Hkv, t_cap // DQ_MEAN_WINDOW),
+          "k_mean_scale")
+    _need(seq_lens.is_cuda and seq_lens.dtype == torch.int32 and seq_lens.numel() == B, "seq_lens")
+    _need(out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and tuple(out.shape) == (B, Hq, d),
+          "out")
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    rc = _lib.dq_decode_attention_no_alloc(k_tables.handle, v_tables.handle, _ptr(q), B, Hq, Hkv,
+                                           _ptr(k_records), _ptr(k_mean_q), _ptr(k_mean_scale), _ptr(v_records),
+                                           _ptr(seq_lens), t_cap, ctypes.c_float(scale), _ptr(out), _ptr(status),
+                                           _stream(stream))
+    _check(rc, "dq_decode_attention_no_alloc")
 
 
 def dq_decode_symbols(tables: Tables, records, sym, header=None, status=None, stream=None):

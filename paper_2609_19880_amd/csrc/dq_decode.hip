@@ -17,6 +17,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "dq_attn.h"
 
@@ -999,7 +1000,7 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pag
                              int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
                              const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                              const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
-                             uint32_t* status, hipStream_t stream) {
+                             uint32_t* status, hipStream_t stream, int64_t ws_slots) {
     if (!attention_supports(tk, tv)) return DQ_ERR_INVALID_ARG;
     const int G = Hq / Hkv;
     AttnArgs a;
@@ -1025,10 +1026,11 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pag
     a.vrec = vrec;
     a.seq_lens = seq_lens;
     a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
+    const int64_t slots = ws_slots > 0 ? ws_slots : plan.slots_max;
     a.ws_hdr = static_cast<int32_t*>(ws);
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
-    a.ws_m = a.ws_acc + plan.slots_max * kD;
-    a.ws_l = a.ws_m + plan.slots_max;
+    a.ws_m = a.ws_acc + slots * kD;
+    a.ws_l = a.ws_m + slots;
     a.status = status;
     a.pg = pg;
     dim3 grid(a.nchunks, Hkv, B);
@@ -1076,9 +1078,9 @@ int launch_attention_fixed_partial(const Pages& pg, const uint16_t* q, int32_t B
 }
 
 int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
-                           int32_t t_cap, const void* ws, float* out, hipStream_t stream) {
+                           int32_t t_cap, const void* ws, float* out, hipStream_t stream, int64_t ws_slots) {
     (void)Hkv;
-    const int64_t slots = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
+    const int64_t slots = ws_slots > 0 ? ws_slots : (int64_t)B * Hq * (max_chunks(t_cap) + 1);
     const int32_t* hdr = static_cast<const int32_t*>(ws);
     const float* acc = reinterpret_cast<const float*>(static_cast<const uint8_t*>(ws) + kWsHeader);
     const float* m = acc + slots * kD;
@@ -1125,10 +1127,43 @@ int launch_residual_commit(int32_t* seq_lens, int32_t* res_lens, int32_t B, int3
     return hip_check("residual_commit launch", hipGetLastError());
 }
 
-int cu_count() {
-    static int cached[64] = {0};
+int64_t attention_plan_slots(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap) {
+    const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap, cu_count());
+    return (int64_t)B * Hq * (plan.nchunks + 1);
+}
+
+// ------------------------------------------------ allocation-free workspace
+//
+// dq_decode_attention_no_alloc keeps its split-K workspace in this array
+// instead of caller memory.  Each device that loads the library holds its own
+// copy until the process ends; host code reaches it only through the device
+// address hipGetSymbolAddress returns (the name itself is a host-side
+// stand-in).  Nothing in it has to start at zero: the partial kernel writes
+// the header and every slot the merge reads.
+static __device__ __align__(256) uint8_t scratch[DQ_NO_ALLOC_SCRATCH_BYTES];
+
+int no_alloc_scratch(void** out) {
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (int rc = hip_check("hipGetDevice", hipGetDevice(&dev))) return rc;
+    if (dev < 0 || dev >= kMaxDevices) return DQ_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        if (int rc = hip_check("hipGetSymbolAddress(scratch)", hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))))
+            return rc;
+        if (!p) return hip_fail("hipGetSymbolAddress(scratch)", hipErrorInvalidSymbol);
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return DQ_OK;
+}
+
+int cu_count() {
+    static int cached[kMaxDevices] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
     if (cached[dev] == 0) {
         int n = 0;
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)

@@ -538,6 +538,34 @@ int dq_decode_attention(const dq_tables* tk, const dq_tables* tv, const uint16_t
     return dq_decode_attention_merge(B, Hq, Hkv, seq_lens, t_cap, ws, ws_bytes, out, stream);
 }
 
+int dq_decode_attention_no_alloc(const dq_tables* tk, const dq_tables* tv, const uint16_t* q, int32_t B,
+                                 int32_t Hq, int32_t Hkv, const uint8_t* krec, const int8_t* kmq,
+                                 const uint16_t* kms, const uint8_t* vrec, const int32_t* seq_lens,
+                                 int32_t t_cap, float scale, float* out, uint32_t* status, void* stream) {
+    int rc = check_attention(tk, tv, B, Hq, Hkv, t_cap);
+    if (rc != DQ_OK) return rc;
+    if (!q || !krec || !kmq || !kms || !vrec || !seq_lens || !out) return DQ_ERR_INVALID_ARG;
+    if (!std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
+    // the workspace of this call's own chunk plan, packed: header, then
+    // accumulators, maxima and sums of B Hq (chunks + 1) slots
+    const int64_t slots = dq::attention_plan_slots(B, Hq, Hkv, t_cap);
+    const int64_t need = dq::kWsHeader + slots * (128 + 2) * (int64_t)sizeof(float);
+    if (need > (int64_t)DQ_NO_ALLOC_SCRATCH_BYTES) {
+        std::snprintf(g_last_error, sizeof(g_last_error),
+                      "dq_decode_attention_no_alloc: %lld bytes of split-K workspace needed, the static "
+                      "scratch holds %lld",
+                      (long long)need, (long long)DQ_NO_ALLOC_SCRATCH_BYTES);
+        return DQ_ERR_WORKSPACE;
+    }
+    void* ws = nullptr;
+    if ((rc = dq::no_alloc_scratch(&ws))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = dq::launch_attention_partial(tk, tv, kContiguous, q, B, Hq, Hkv, krec, kmq, kms, vrec, seq_lens, t_cap,
+                                      scale, ws, status, s, slots);
+    if (rc != DQ_OK) return rc;
+    return dq::launch_attention_merge(B, Hq, Hkv, seq_lens, t_cap, ws, out, s, slots);
+}
+
 int dq_decode_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
                                  const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
                                  const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,

@@ -149,11 +149,23 @@ int launch_decode_symbols(const dq_tables* tab, const uint8_t* records, int64_t 
 
 size_t attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d);
 
+// ws_slots: (max, sum, accumulator) slots the workspace holds, which places
+// the max and sum arrays after the accumulators; 0 = the size
+// attention_workspace_bytes allows for (512-token chunks).
 int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pages& pg, const uint16_t* q,
                              int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
                              const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                              const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
-                             uint32_t* status, hipStream_t stream);
+                             uint32_t* status, hipStream_t stream, int64_t ws_slots = 0);
+
+// Slots the chunk plan of these sizes uses on the current device:
+// B Hq (chunks + 1), the last one per query head for the residual window.
+int64_t attention_plan_slots(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap);
+
+// Device address of the current device's copy of the library's static
+// scratch array (DQ_NO_ALLOC_SCRATCH_BYTES), looked up once per device.
+int no_alloc_scratch(void** out);
+constexpr int kMaxDevices = 64;
 
 // Per-token streams over Hkv heads (table n = 128 Hkv, G = Hq / Hkv <= 4),
 // records [B][t_cap][stride] in 64-token tiles, or token rows of pool pages
@@ -193,6 +205,7 @@ int launch_bf16_partial(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, c
                         const uint16_t* v, const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
                         hipStream_t stream);
 int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
-                           int32_t t_cap, const void* ws, float* out, hipStream_t stream);
+                           int32_t t_cap, const void* ws, float* out, hipStream_t stream,
+                           int64_t ws_slots = 0);
 
 }  // namespace dq

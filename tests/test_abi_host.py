@@ -30,6 +30,13 @@ def test_library_exports_every_declared_symbol():
     assert not missing, missing
 
 
+def test_no_alloc_scratch_size_matches_header():
+    src = open(os.path.join(ROOT, "include", "dq.h")).read()
+    m = re.search(r"#define DQ_NO_ALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", src)
+    assert m, "DQ_NO_ALLOC_SCRATCH_BYTES not found"
+    assert dq.DQ_NO_ALLOC_SCRATCH_BYTES == int(m.group(1)) << int(m.group(2))
+
+
 def test_strerror():
     assert dq.dq_strerror(dq.DQ_OK) == "ok"
     assert "infeasible" in dq.dq_strerror(dq.DQ_ERR_INFEASIBLE)
