@@ -167,3 +167,76 @@ def make_v(wl: Workload, seed: int, device="cpu", batch: int | None = None,
 def bf16_bits(t: torch.Tensor) -> np.ndarray:
     """bf16 tensor -> numpy uint16 bit patterns (host copy)."""
     return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+# Degenerate inputs: each (token, KV head) vector takes one of these patterns.
+#   zero       all channels 0 (e.g. a padding token)
+#   onehot0    one non-zero channel, channel 0
+#   const      every channel the same value
+#   onehot     one non-zero channel, a random channel other than 0, random sign
+#   twolevel   a base value, with the next bf16 value up on a random subset
+#   tiny       one non-zero channel of magnitude about 1e-6
+#   normal     N(0, 1) channels
+EDGE_KINDS = ("zero", "onehot0", "const", "onehot", "twolevel", "tiny", "normal")
+
+
+def _edge_vector(kind: str, rng: np.random.Generator, d: int, mag: float) -> np.ndarray:
+    v = np.zeros(d, dtype=np.float32)
+    if kind == "onehot0":
+        v[0] = mag
+    elif kind == "const":
+        v[:] = mag
+    elif kind == "onehot":
+        v[1 + rng.integers(d - 1)] = mag * rng.choice([-1.0, 1.0])
+    elif kind == "twolevel":
+        bits = torch.tensor([mag], dtype=torch.float32).to(torch.bfloat16).view(torch.int16)
+        lo = float(bits.view(torch.bfloat16).float()[0])
+        hi = float((bits + 1).view(torch.bfloat16).float()[0])     # the next bf16 value up
+        v[:] = lo
+        v[rng.random(d) < 0.5] = hi
+    elif kind == "tiny":
+        v[rng.integers(d)] = np.float32(1e-6 * mag)
+    elif kind == "normal":
+        v[:] = rng.normal(size=d)
+    elif kind != "zero":
+        raise ValueError(kind)
+    return v
+
+
+def make_edge(seed: int, batch: int, context: int, kv_heads: int, head_dim: int = HEAD_DIM,
+              kinds=EDGE_KINDS, same_heads: bool = False) -> torch.Tensor:
+    """Degenerate K or V inputs [B, T, H, d] bf16: token t of head h takes
+    kinds[(t + h) % len(kinds)] (kinds[t % len(kinds)] for every head when
+    same_heads, with one magnitude per token, so that the whole token is
+    one pattern), magnitudes drawn from U(0.25, 4)."""
+    rng = np.random.default_rng(seed + 104729)
+    out = np.zeros((batch, context, kv_heads, head_dim), dtype=np.float32)
+    for b in range(batch):
+        for t in range(context):
+            mag = float(rng.uniform(0.25, 4.0))
+            for h in range(kv_heads):
+                kind = kinds[(t if same_heads else t + h) % len(kinds)]
+                out[b, t, h] = _edge_vector(kind, rng, head_dim, mag if same_heads else float(rng.uniform(0.25, 4.0)))
+    return torch.from_numpy(out).to(torch.bfloat16)
+
+
+def make_edge_keys(seed: int, batch: int, context: int, kv_heads: int, head_dim: int = HEAD_DIM) -> torch.Tensor:
+    """Degenerate keys [B, T, H, d] bf16, one pattern per 128-token window
+    (cycling): every token 127 e_0; every token 0; every token the same
+    N(0, 1) vector (a token equal to its window's mean); the mixed patterns of
+    make_edge."""
+    if context % MEAN_WINDOW:
+        raise ValueError("context must be a multiple of the mean window")
+    mixed = make_edge(seed, batch, context, kv_heads, head_dim).float().numpy()
+    rng = np.random.default_rng(seed + 15485863)
+    out = np.zeros((batch, context, kv_heads, head_dim), dtype=np.float32)
+    for w in range(context // MEAN_WINDOW):
+        sl = slice(w * MEAN_WINDOW, (w + 1) * MEAN_WINDOW)
+        kind = w % 4
+        if kind == 0:
+            out[:, sl, :, 0] = 127.0
+        elif kind == 2:
+            out[:, sl] = rng.normal(size=(batch, 1, kv_heads, head_dim)).astype(np.float32)
+        elif kind == 3:
+            out[:, sl] = mixed[:, sl]
+    return torch.from_numpy(out).to(torch.bfloat16)

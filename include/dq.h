@@ -47,7 +47,8 @@ extern "C" {
 
 /* Bits OR-ed into the caller's device status word. */
 #define DQ_STATUS_RANGE 1u    /* encode: non-finite input, or scale/offset/mean overflowed fp16 */
-#define DQ_STATUS_OVERFLOW 2u /* encode: a stream could not be fitted into its record          */
+#define DQ_STATUS_OVERFLOW 2u /* encode: a stream could not be fitted into its record (written as
+                                 zeros); the coded-length bound makes this unreachable for n <= 1024 */
 #define DQ_STATUS_CORRUPT 4u  /* decode: a record did not end in state 2^21 inside its C bytes  */
 #define DQ_STATUS_WINDOW 8u   /* residual window: append to a full ring, or commit more than it holds */
 #define DQ_STATUS_PAGE 16u    /* paged layout: a block-table entry outside the page pool (skipped)     */
@@ -85,9 +86,9 @@ typedef struct dq_tables dq_tables;
 
 /*
  * Builds the entropy model on the host only (no GPU needed):
- * level probabilities from normal CDF mass on the grid [-a_n, a_n] (Sec. 4.2,
- * "Gaussian order statistics"), sharpened p^alpha (Sec. 4.4), apportioned to
- * integers summing to 2^p (Eq. rans), Q16 costs R_m = round(2^16 (p - log2 f_m))
+ * level probabilities from normal CDF mass on the grid [-a_n, a_n] (the
+ * order-statistics model of normal samples, Sec. 4.2), sharpened p^alpha
+ * (Sec. 4.4), apportioned to integers summing to 2^p (Eq. rans), Q16 costs R_m = round(2^16 (p - log2 f_m))
  * (Alg. 1), the lambda grid 2^(k/512) as fp32, and the feasibility test.
  * Output arrays may be NULL; sizes: freq, cum, cost_q16: levels entries;
  * sym_of_z: 2^p entries; lambda512: 512 entries.
@@ -363,8 +364,9 @@ int dq_decode_attention_token_paged_partial(const dq_tables* k_tables, const dq_
  * grid, least-squares refit, fp16 s and o), symbols by nearest-level rounding,
  * b = floor(8 (record_bytes - 4) / head_dim) bits each (M = 2^b levels),
  * packed least-significant bit first after the 4-byte header of a record of
- * the same size.  With 36-byte records and head_dim 128 that is INT2 with an
- * fp16 scale and zero point per 128 values (2.25 bits per value, Sec. 3).
+ * the same size.  With 36-byte records and head_dim 128 that is 128 two-bit
+ * codes sharing one fp16 scale and one fp16 offset: 2.25 bits per value, the
+ * 2-bit example of Sec. 3.
  *
  * dq_fixed_bits: b for (head_dim, record_bytes), 0 if no whole bit fits or
  *   more than 8 would.

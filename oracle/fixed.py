@@ -4,13 +4,13 @@ TEST INFRASTRUCTURE ONLY -- see the package header.
 
 What the paper fixes
 --------------------
-* App. B compares D-Quant's entropy-coded container with a fixed-width
-  representation of the same storage: identical preprocessing (Hadamard
-  rotation, windowed INT8 channel-mean removal for keys, token-wise min-max
-  affine grid, least-squares refitting, FP16 metadata), symbols assigned by
-  nearest-neighbour rounding, each symbol charged log2 M bits.
-* Sec. 3 (Background): a fixed-width b-bit code has exactly 2**b levels; INT2
-  with an fp16 scale and zero point per 128 values costs 2.25 bits per value.
+* App. B sets D-Quant's entropy-coded record against a fixed-width code
+  given the same bytes.  Everything before the coder is shared (rotation, the
+  keys' 8-bit window means, the per-token min-max grid, the least-squares
+  refit, fp16 scale and offset); the fixed-width side rounds every value to its
+  nearest level and is charged log2 M bits per symbol.
+* Sec. 3 (Background): b bits give exactly 2**b levels; 2-bit codes for 128
+  values plus one fp16 scale and one fp16 offset come to 2.25 bits per value.
 
 Readings
 --------

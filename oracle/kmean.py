@@ -4,7 +4,7 @@ TEST INFRASTRUCTURE ONLY -- see the package header.
 
 Sec. 4.2: keys remove a windowed channel-wise mean after rotation (Tab. 1 shows
 why: rotation alone leaves a channel mean that a token-level offset cannot
-absorb).  App. B names it "windowed INT8 channel-mean removal".
+absorb); App. B adds that the mean is kept in INT8.
 
 Readings
 --------

@@ -10,12 +10,12 @@ What the paper fixes
   sum_i r(m_i) <= B, solved through Eq. (lagrangian): for a fixed lambda each
   value independently takes argmin_m D_i(m) + lambda r(m); bisection on lambda.
 * Alg. 1: FitMinMax -> Drift -> Refit -> fp16(s), fp16(o) -> Drift -> rANS.
-  Drift bisects log2 lambda (App. A: "bisect the exponent") for T = 12 steps
+  Drift bisects log2 lambda rather than lambda (App. A) for T = 12 steps
   inside [hi - 40, hi], hi = log2(8 (max D - min D)), keeping hi when the
   candidate fits, and returns the assignment at hi.
-* App. B: the refit is a least-squares refit; App. A: s and o are rounded to
-  FP16 before the final assignment so the encoder optimizes against the grid the
-  decoder uses.
+* App. B: the refit is a least-squares refit.  App. A: s and o become fp16
+  ahead of the second Drift, whose assignment then targets exactly the levels
+  the decoder reconstructs.
 
 Readings (all arithmetic is fp64 with a fixed operation order, no fused
 multiply-add; where floating point decides an integer both sides of a parity
@@ -91,8 +91,13 @@ def assign(D: np.ndarray, lam: np.ndarray, rate: np.ndarray) -> np.ndarray:
 
 
 def drift(x: np.ndarray, s: np.ndarray, o: np.ndarray, tab: Tables,
-          budget_q16: np.ndarray) -> np.ndarray:
-    """Drift(x, s, o, r, B) of Alg. 1 for a batch of streams x[S, n]."""
+          budget_q16: np.ndarray, trace: dict | None = None) -> np.ndarray:
+    """Drift(x, s, o, r, B) of Alg. 1 for a batch of streams x[S, n].
+
+    If `trace` is a dict it receives the bisection bracket per stream, in
+    lambda-grid units: "U_hi0" / "U_lo0" (the initial hi and lo), "U_hi" (the
+    final hi, whose assignment is returned unless reading Q5 or Q4 applies)
+    and "flat" (reading Q4)."""
     S = x.shape[0]
     M = tab.M
     rate = tab.rate
@@ -107,12 +112,16 @@ def drift(x: np.ndarray, s: np.ndarray, o: np.ndarray, tab: Tables,
     hi = np.where(mant == 0.5, ex - 1, ex).astype(np.int64)
     U_hi = hi * LAMBDA_STEPS
     U_lo = U_hi - BRACKET_UNITS
+    if trace is not None:
+        trace.update(U_hi0=U_hi.copy(), U_lo0=U_lo.copy(), flat=flat.copy())
     for _ in range(BISECT_STEPS):
         U_mid = (U_lo + U_hi) >> 1
         m = assign(D, lam_of_units(U_mid, tab.lam), rate)
         fits = cost[m].sum(axis=1) <= budget_q16
         U_hi = np.where(fits, U_mid, U_hi)
         U_lo = np.where(fits, U_lo, U_mid)
+    if trace is not None:
+        trace["U_hi"] = U_hi.copy()
     m = assign(D, lam_of_units(U_hi, tab.lam), rate)
     over = cost[m].sum(axis=1) > budget_q16
     if np.any(over):

@@ -14,8 +14,8 @@ What the paper fixes
 
 Readings (the paper is silent or loose here)
 --------------------------------------------
-* T1 "Gaussian order statistics": the min and max of a stream of n standard
-  normals are replaced by their expectations -a_n and +a_n, with
+* T1 the entropy model from order statistics of normal samples (Sec. 4.2):
+  the min and max of a stream of n standard normals are replaced by their expectations -a_n and +a_n, with
   a_n = E[max of n iid N(0,1)].  Level m then covers the interval between the
   edges e_m = a_n((2m-1)/(M-1) - 1) and e_{m+1} (e_0 = -inf, e_M = +inf), and
   its probability is the normal CDF mass between them.  Only the lower half is

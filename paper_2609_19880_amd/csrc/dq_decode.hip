@@ -290,7 +290,9 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
         const int r = lane >> 5, c4 = 4 * (lane & 31);
         for (int wi = 2 * wave + r; wi - r < nwin; wi += 2 * L.nw) {
             float f[4] = {0.f, 0.f, 0.f, 0.f};
-            if (wi < nwin && w0 + wi < nwin_total) {
+            // windows from the sequence's length on are never used: their
+            // block-table entries may be unmapped
+            if (wi < nwin && w0 + wi < nwin_total && (w0 + wi) * DQ_MEAN_WINDOW < T) {
                 const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + wi, bad_page);
                 const float sc = half_bits_to_f32(a.kms[widx]);
                 const uint32_t mv = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + c4);

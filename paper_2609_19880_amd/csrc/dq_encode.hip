@@ -3,8 +3,8 @@
 // Two kernels:
 //  * key_mean: one wavefront per (batch, head, 128-token window).  Rotates
 //    each token (Hadamard, Sec. 4.2), sums the window left to right in fp64,
-//    and stores the channel mean as INT8 with one fp16 scale (App. B,
-//    "windowed INT8 channel-mean removal").
+//    and stores the channel mean as INT8 with one fp16 scale (Sec. 4.2,
+//    App. B).
 //  * encode: one workgroup per (batch, head, 64 consecutive tokens; 32 for
 //    per-token streams).  Each wavefront takes a stream at a time with its n
 //    values spread over the lanes and keeps them in registers through Alg. 1
@@ -606,10 +606,16 @@ __global__ __launch_bounds__(kEncThreads, (TOK || MB == 16) ? 3 : 1) void encode
                 xs = xs + q * (P - f) + c;
             }
             if (emitted > cap) {
+                // Defensive: with L = 2^21 the coded length is at most
+                // sum r + n (2^-17 + log2(1 + 2^p / L)) bits, under 8 bits
+                // past the budget for n <= 1024, so a drifted stream always
+                // fits.  Should one not, retry 8 bits lower; when the budget
+                // runs out the record is all zeros (decoding flags it corrupt).
                 s_flag[i] = 1;
                 s_budget[i] -= (int64_t)8 * 65536;
                 if (s_budget[i] < (int64_t)n * ta.rmin) {
                     s_flag[i] = 0;
+                    for (int k = 0; k < C; ++k) rec[k] = 0;
                     if (a.status) atomicOr(a.status, DQ_STATUS_OVERFLOW);
                 }
             } else {

@@ -246,7 +246,9 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
         for (int it = 2 * wave + r; it - r < nwin * Hkv; it += 2 * L.nw) {
             const int wi = it / Hkv, hk = it % Hkv;
             float f[4] = {0.f, 0.f, 0.f, 0.f};
-            if (it < nwin * Hkv && w0 + wi < nwin_total) {
+            // windows from the sequence's length on are never used: their
+            // block-table entries may be unmapped
+            if (it < nwin * Hkv && w0 + wi < nwin_total && (w0 + wi) * DQ_MEAN_WINDOW < T) {
                 const int64_t widx = PAGED ? window_index(a.pg, Hkv, a.t_cap, b, hk, w0 + wi, bad_page)
                                            : ((int64_t)b * Hkv + hk) * nwin_total + w0 + wi;
                 const float sc = half_bits_to_f32(a.kms[widx]);

@@ -282,3 +282,63 @@ def test_token_paged_arguments_rejected(dq):
     assert attn(ws_bytes=64) == dq.DQ_ERR_WORKSPACE
     assert attn(page_tokens=100) == dq.DQ_ERR_INVALID_ARG
     torch.cuda.synchronize()
+
+
+# ---- block tables whose entries past a sequence's length are unmapped (-1),
+#      as serving engines leave them: a valid call, no status bit
+
+def _unmap_past_length(bt, lens, page):
+    out = bt.copy()
+    for b, n in enumerate(lens):
+        out[b, (n + page - 1) // page:] = -1
+    return out
+
+
+@pytest.mark.parametrize("lens_frac", [(1.0, 0.0, 0.68), (0.3, 0.55, 0.126)])
+def test_paged_unmapped_tail_entries_are_not_read(dq, lens_frac):
+    wl, gtk, gtv, B, Hkv, G, page, max_pages, t_cap, num_pages, bt, k, v, q = _setup(dq, seed=46)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    cache = dq.KVCache(B, Hkv, Hkv * G, t_cap, gtk, gtv, device=DEV)
+    cache.append(k, v, 0)
+    kp, vp, mq, ms = _pools(num_pages, Hkv, page, wl)
+    kpool, vpool, mqpool, mspool = kp[:num_pages], vp[:num_pages], mq[:num_pages], ms[:num_pages]
+    btd = torch.from_numpy(bt).to(DEV)
+    dq.dq_encode_kv_paged(gtk, k, 0, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_paged(gtv, v, 0, btd, vpool, None, None, status)
+    lens = [int(f * t_cap) for f in lens_frac]
+    seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    out_c = cache.attend(q, seq)
+    btu = torch.from_numpy(_unmap_past_length(bt, lens, page)).to(DEV)
+    ws = torch.empty_like(cache.workspace)
+    out_p = torch.empty_like(out_c)
+    dq.dq_decode_attention_paged_partial(gtk, gtv, q, kpool, mqpool, mspool, vpool, btu, seq, ws, status=status)
+    dq.dq_decode_attention_merge(B, Hkv * G, Hkv, seq, t_cap, ws, out_p)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0 and int(cache.status.item()) == 0
+    assert torch.equal(out_c, out_p)
+
+
+@pytest.mark.parametrize("lens_frac", [(1.0, 0.0, 0.68), (0.3, 0.55, 0.126)])
+def test_token_paged_unmapped_tail_entries_are_not_read(dq, lens_frac):
+    gtk, gtv, B, H, G, page, max_pages, t_cap, num_pages, bt, k, v, q = _token_setup(dq, seed=47)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    cache = dq.TokenKVCache(B, H, H * G, t_cap, gtk, gtv, device=DEV)
+    dq.dq_encode_kv_token(gtk, k, 0, t_cap, cache.k_records, cache.k_mean_q, cache.k_mean_scale, status)
+    dq.dq_encode_kv_token(gtv, v, 0, t_cap, cache.v_records, None, None, status)
+    kp, vp, mq, ms = _token_pools(dq, gtk, gtv, num_pages, H, page)
+    kpool, vpool, mqpool, mspool = kp[:num_pages], vp[:num_pages], mq[:num_pages], ms[:num_pages]
+    btd = torch.from_numpy(bt).to(DEV)
+    dq.dq_encode_kv_token_paged(gtk, k, 0, btd, kpool, mqpool, mspool, status)
+    dq.dq_encode_kv_token_paged(gtv, v, 0, btd, vpool, None, None, status)
+    lens = [int(f * t_cap) for f in lens_frac]
+    seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    out_c = cache.attend(q, seq)
+    btu = torch.from_numpy(_unmap_past_length(bt, lens, page)).to(DEV)
+    ws = torch.empty_like(cache.workspace)
+    out_p = torch.empty_like(out_c)
+    dq.dq_decode_attention_token_paged_partial(gtk, gtv, q, kpool, mqpool, mspool, vpool, btu, seq, ws,
+                                               status=status)
+    dq.dq_decode_attention_merge(B, H * G, H, seq, t_cap, ws, out_p)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert torch.equal(out_c, out_p)

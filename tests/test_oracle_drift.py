@@ -155,3 +155,71 @@ def test_fp16_metadata_is_what_the_record_uses():
     recs, syms, s16, o16, budgets = kv.encode_streams(x, t)
     m2 = quantize.final_drift(x, s16, o16, t, budgets)
     assert np.array_equal(m2, syms)
+
+
+# ---- the bisection schedule of Alg. 1: hi = ceil(log2(8 (max D - min D))),
+#      lo = hi - 40 octaves, T = 12 halvings, answer at the final hi
+
+def _fits(D, U, t, budget):
+    m = quantize.assign(D, quantize.lam_of_units(U, t.lam), t.rate)
+    return t.cost[m].sum(axis=1) <= budget
+
+
+def _schedule_violations(x, s, o, t, budget):
+    """Streams whose Drift bracket contradicts Alg. 1's schedule."""
+    tr = {}
+    m = quantize.drift(x, s, o, t, budget, trace=tr)
+    D = quantize.distortion(x, s, o, t.M)
+    live = ~tr["flat"]
+    delta = 8.0 * (D.max(axis=(1, 2)) - D.min(axis=(1, 2)))
+    U_hi0, U_lo0, U_hi = tr["U_hi0"], tr["U_lo0"], tr["U_hi"]
+    bad = np.zeros(x.shape[0], dtype=bool)
+    # the initial hi is the integer ceiling of log2(8 dD): 2^(hi-1) < 8 dD <= 2^hi
+    hi0 = U_hi0 // 512
+    bad |= live & ((U_hi0 % 512 != 0) | ~(np.ldexp(1.0, hi0 - 1) < delta) | ~(delta <= np.ldexp(1.0, hi0)))
+    # a 40-octave bracket on the 1/512-octave grid
+    bad |= live & (U_hi0 - U_lo0 != 40 * 512)
+    # twelve halvings of 20480 units leave brackets of 5 units: the final hi
+    # lies on that grid, it fits, and one step below it does not (unless that
+    # is the bracket's untested lower end)
+    fits_hi = _fits(D, U_hi, t, budget)
+    fits_below = _fits(D, U_hi - 5, t, budget)
+    bad |= live & ((U_hi0 - U_hi) % 5 != 0)
+    bad |= live & fits_hi & fits_below & (U_hi - 5 != U_lo0)
+    # the result is the assignment at the final hi whenever that fits
+    at_hi = quantize.assign(D, quantize.lam_of_units(U_hi, t.lam), t.rate)
+    bad |= live & fits_hi & np.any(m != at_hi, axis=1)
+    return bad, live & fits_hi
+
+
+def _schedule_inputs():
+    rng = np.random.default_rng(19)
+    x = rng.normal(size=(300, 128)) * rng.uniform(0.05, 20, size=(300, 1)) + rng.normal(size=(300, 1))
+    x[::7, :3] *= 9.0          # outliers, as rotated keys carry
+    return x
+
+
+@pytest.mark.parametrize("M,C", [(6, 36), (5, 32), (9, 48), (17, 64)])
+def test_drift_bisection_schedule(M, C):
+    """Both drifts of Alg. 1 follow its schedule exactly on every stream."""
+    t = _tab(M, C)
+    x = _schedule_inputs()
+    s0, o0 = quantize.fit_minmax(x, M)
+    bad, checked = _schedule_violations(x, s0, o0, t, t.budget_q16)
+    assert not bad.any()
+    assert checked.sum() > 250
+    s16, o16 = quantize.first_pass(x, t)
+    bad, checked = _schedule_violations(x, s16.astype(np.float64), o16.astype(np.float64), t, t.budget_q16)
+    assert not bad.any()
+
+
+@pytest.mark.parametrize("steps,octaves", [(11, 40), (13, 40), (12, 20), (12, 41)])
+def test_drift_schedule_pin_catches_a_wrong_schedule(monkeypatch, steps, octaves):
+    """Plants a wrong T or bracket in the oracle: the schedule pin fails."""
+    monkeypatch.setattr(quantize, "BISECT_STEPS", steps)
+    monkeypatch.setattr(quantize, "BRACKET_UNITS", octaves * 512)
+    t = _tab(6, 36)
+    x = _schedule_inputs()
+    s0, o0 = quantize.fit_minmax(x, 6)
+    bad, _ = _schedule_violations(x, s0, o0, t, t.budget_q16)
+    assert bad.any()

@@ -152,3 +152,44 @@ def test_rotation_spreads_outlier_channels():
     assert np.all(var_rot.max(axis=-1) / var_rot.min(axis=-1) < 1.6)
     assert np.allclose(var_rot.mean(axis=-1), var_raw.sum(axis=-1), rtol=0.1)
     _ = hadamard
+
+
+@pytest.mark.parametrize("n,M,p,C", [(128, 6, 12, 36), (128, 5, 12, 32), (128, 17, 12, 64), (128, 9, 12, 48),
+                                     (1024, 8, 8, 335), (1024, 6, 8, 235), (1024, 8, 12, 335)])
+def test_coded_length_bound(n, M, p, C):
+    """Reading K1's retry is never needed: from a start at L, each coding step
+    of Eq. rans raises log2(x) + bits emitted by at most
+    p - log2 f_m + log2(1 + 2^p / L) (renormalization never raises it), the
+    final state is >= L, and R_m is within 2^-17 bit of p - log2 f_m, so
+    8 E <= sum R / 2^16 + n (2^-17 + log2(1 + 2^p / L)).  The drifted cost is
+    within the budget 8 (C - 8) bits, a multiple of 8, and the slack is under
+    8 bits for n <= 1024, so E <= C - 8: every record fits."""
+    t = tables.build_tables(n, M, p, 1.4, C)
+    rng = np.random.default_rng(n + M + p)
+    x = rng.normal(size=(300, n)) * rng.uniform(0.1, 5, size=(300, 1))
+    x[::5, : n // 64] *= 8.0
+    _, syms, _, _, budgets = kv.encode_streams(x, t)
+    assert np.all(budgets == t.budget_q16)                 # no retry happened
+    _, _, length = rans.encode(syms, t)
+    slack = n * (2.0 ** -17 + np.log2(1.0 + 2.0 ** p / rans.RANS_L))
+    assert slack < 8.0
+    bits = 8.0 * length
+    assert np.all(bits <= t.cost[syms].sum(axis=1) / tables.Q16 + slack)
+    assert np.all(rans.PAYLOAD_OFFSET + length <= C)
+
+
+def test_paper_levels_are_the_level_sweep_best():
+    """The paper-variant level counts and the literal variant's alphas are the
+    ones the committed oracle sweep picked."""
+    from conftest import read_golden
+    rows = read_golden("level_sweep.txt")
+    best = {int(r[1]): int(r[2]) for r in rows if r[0] == "best"}
+    alpha = {(int(r[1]), int(r[2])): float(r[3]) for r in rows if r[0] == "alpha"}
+    assert best == wlmod.PAPER_LEVELS
+    assert alpha == wlmod.LITERAL_ALPHA
+    # and "best" is the argmin of the NMSE rows
+    nmse = {}
+    for r in rows:
+        if r[0] not in ("best", "alpha"):
+            nmse.setdefault(int(r[0]), []).append((float(r[2]), int(r[1])))
+    assert {C: min(v)[1] for C, v in nmse.items()} == best
