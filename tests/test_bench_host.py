@@ -44,3 +44,19 @@ def test_encoder_figure_applies_to_the_summarized_coding_only():
     b = bench.encode_valu_per_stream(wlmod.workload("b64_t8k"), "paper")
     assert a == b                      # same coding: the same per-stream figure, or both None
     assert a is None or 500 < a < 20000
+
+
+def test_cpu_baseline_uses_a_pool_of_host_cores(monkeypatch):
+    monkeypatch.setattr(bench, "CPU_SECONDS", 0.5)
+    for name in ("b1_t4k", "b1_t4k_tok"):
+        r = bench.cpu_baseline(wlmod.workload(name), 0)
+        assert r["kind"] == "oracle" and r["unit"] == "tokens/s" and r["value"] > 0
+        assert r["cores"] == bench._pool_size() and 1 <= r["cores"] <= 16
+        assert f"{r['cores']} single-threaded processes" in r["sample"]
+
+
+def test_paper_context_quotes_the_papers_hardware():
+    c = bench.PAPER_CONTEXT
+    assert "H20" in c["hardware"]
+    assert c["decode_tokens_per_s"]["d_quant"] == 563.6 and c["decode_tokens_per_s"]["bf16"] == 159.5
+    assert c["throughput_gain"] == 3.5 and c["peak_memory_gib"]["d_quant_batch_128_8k_prompt"] == 49.4
