@@ -75,6 +75,28 @@ __device__ __forceinline__ v4i mfma(uint32_t a, uint32_t b, v4i c) {
     return __builtin_amdgcn_mfma_i32_4x4x4i8((int)a, (int)b, c, 0, 0, 0);
 }
 
+// v_mfma_i32_16x16x32_i8: lane l gives row l % 16 and K = 8 (l / 16) .. + 7
+// of A, the same K of column l % 16 of B, and receives rows 4 (l / 16) .. + 3
+// of column l % 16.
+__device__ __forceinline__ v4i mfma16(uint64_t a, uint64_t b, v4i c) {
+    return __builtin_amdgcn_mfma_i32_16x16x32_i8((long)a, (long)b, c, 0, 0, 0);
+}
+
+// ds_read_b64_tr_b8 at LDS byte address off.  Within each group of 16 lanes,
+// lane 8 h + i receives byte i of the 8-byte rows that the group's lanes h,
+// h + 2, ..., h + 14 address (in that order): token-major rows come back
+// K-major, as the 16x16x32 products take them.
+__device__ __forceinline__ uint64_t lds_tr8(uint32_t off) {
+    typedef int v2i __attribute__((ext_vector_type(2)));
+    const v2i r = __builtin_amdgcn_ds_read_tr8_b64_v2i32(LDS_PTR(v2i, off));
+    return (uint64_t)(uint32_t)r.x | ((uint64_t)(uint32_t)r.y << 32);
+}
+
+// v[slot] for slot in 0..3 (v held in registers, slot per lane).
+__device__ __forceinline__ float pick4(const float* v, int slot) {
+    return slot == 0 ? v[0] : slot == 1 ? v[1] : slot == 2 ? v[2] : v[3];
+}
+
 __device__ __forceinline__ float combine(const v4i& d0, const v4i& d1, const v4i& d2, int r) {
     return (float)d2[r] * 65536.0f + (float)d1[r] * 256.0f + (float)d0[r];
 }

@@ -28,7 +28,7 @@ constexpr int kD = 128;          // head_dim of the attention kernels
 constexpr int kTile = 64;        // tokens per wavefront tile (one per lane)
 constexpr int kMaxWaves = 16;    // wavefronts per workgroup (LDS permitting)
 constexpr int kVSlice = 64;      // value channels per PV pass
-constexpr int kVRow = 68;        // bytes per channel row of the value tile (64 + pad)
+constexpr int kVRowT = 80;       // bytes per token row of the value tile (64 channels + pad)
 constexpr int kMaxRecDwords = 16;
 constexpr int kMaxLds = 160 * 1024;
 constexpr int kMaxChunk = 16384;  // bounds the per-window q . mu table in LDS
@@ -70,28 +70,36 @@ __global__ void decode_symbols_kernel(TabArgs ta, const uint8_t* __restrict__ re
 // token's key stream then its value stream (Alg. 2), 128 steps each.
 //
 // Decode step.  The state is kept as X = 8 x (its low three bits are never
-// read), which with 8-byte table entries (8 f_m | m << 24, 8 (z - c_m)) in LDS
+// read), which with 8-byte table entries (f_m | m << 24, z - c_m) in LDS
 // makes the table address one mask of X and the state update
 // x' = f (x >> p) + (z - c) one 24-bit multiply-add.  Renormalization bytes
 // are staged per lane as overlapping big-endian byte pairs
 // P[k] = (b_k << 8) | b_{k+1}: one aligned 16-bit LDS read yields the next
 // 16 bits wherever the lane's byte pointer stands.  Since x' >= 2^9 for
-// p <= 12, the number of bytes Alg. 2 reads (0, 1 or 2) is sh / 8 with
-// sh = clz(8 x') & 24, and
-//     X = (8 x' << sh) | ((P[ptr] << 16) >> (29 - sh)),   ptr += sh / 8.
+// p <= 12, the number of bytes Alg. 2 reads (0, 1 or 2) is n = sh / 8 with
+// sh = (clz(x') - 3) & 24, and with s = 29 - sh (13, 21 or 29)
+//     X = alignbit(x', P[ptr] << 16, s) = (x' << (3 + sh)) | (P[ptr] << 16 >> s),
+// whose first sh bits of the pair land at bit 3 (the low three bits are
+// left-overs of the pair, never read).  The byte pointer advances by n
+// positions of 128 bytes, 464 - 16 s bytes: the register holds the pointer
+// less 464 j at step j of a 16-step window, so that it moves by -16 s and
+// each read carries its 464 j as the instruction's offset.
 //
-// Contractions (Eq. fold-key / fold-value) run on the matrix cores with
-// v_mfma_i32_4x4x4_16b_i8 (16 blocks of 4x4x4; lane l is column l % 4 of
-// block l / 4).  Decoded levels are bytes and enter as they are; the rotated
-// query and the softmax weights (with the value scale folded in) enter as
-// three signed 8-bit digits of a 22-bit fixed-point value, accumulated exactly
-// in int32 and recombined in fp32.
-//   q . k:  block = 4 tokens, K = 4 channels.  A = the query digits of head
-//           l % 4, B = the 4 levels the lane just decoded, D = the lane's own
-//           token's dot products for 4 heads.
-//   P . v:  block = 4 channels, K = 4 tokens.  Levels go through a 4x4 byte
-//           transpose inside each lane quad and a channel-major LDS tile;
-//           D = 4 heads of channel l of the 64-channel slice.
+// Contractions (Eq. fold-key / fold-value) run on the matrix cores.  Decoded
+// levels are bytes and enter as they are; the rotated query and the softmax
+// weights (with the value scale folded in) enter as three signed 8-bit digits
+// of a 22-bit fixed-point value, accumulated exactly in int32 and recombined
+// in fp32.
+//   q . k:  v_mfma_i32_4x4x4_16b_i8 (16 blocks of 4x4x4; lane l is column
+//           l % 4 of block l / 4), block = 4 tokens, K = 4 channels.  A = the
+//           query digits of head l % 4, B = the 4 levels the lane just
+//           decoded, D = the lane's own token's dot products for 4 heads.
+//   P . v:  v_mfma_i32_16x16x32_i8, rows = (query-head slot, digit), K = 32
+//           tokens, columns = 16 channels.  Each lane writes its token's
+//           levels and weight digits to token-major LDS rows as they are, and
+//           ds_read_b64_tr_b8 hands every lane the 8 tokens of one row or
+//           column the product wants; D = one slot's three digit sums (and a
+//           zero row) of channel l % 16.
 
 struct AttnLayout {
     int nw;             // wavefronts per workgroup
@@ -102,8 +110,8 @@ struct AttnLayout {
     int waves;          // first wavefront region
     int wave_stride;
     int pk, pv;             // key / value byte-pair arrays: [position][64 lanes] x 2 B
-    int vtile;              // [64 channels][kVRow] bytes, over the pair arrays
-    int plimb;              // [HG][4 heads][16 token quads] x 16 B (three digit words)
+    int vtile;              // [64 tokens][kVRowT] level bytes of a 64-channel slice, over the pair arrays
+    int plimb;              // [HG][64 tokens][16] weight digits: byte 4 slot + digit (digit 3: zero)
     int total;
 };
 
@@ -112,6 +120,8 @@ __host__ inline int align16(int v) { return (v + 15) & ~15; }
 constexpr int kPairRow = 2 * kTile;     // bytes per payload position: one pair per lane
 constexpr int kPairSlack = 4096;         // LDS above the last array that a corrupt stream may read
 constexpr int kClampGroups = 4;          // pointers are clamped every 4 x 4 decode steps
+constexpr int kWindow = 4 * kClampGroups;            // decode steps per pointer window
+constexpr int kPairStep = 29 * kPairRow / 8;         // 464: read offset per step of a window
 
 struct AttnArgs {
     TabArgs tk, tv;
@@ -137,9 +147,10 @@ struct AttnArgs {
 // One step of Alg. 2 on the state kept as X = 8 x (+ up to 7 in the low bits,
 // which nothing reads).  Returns the table word (level in its top byte).
 //   table address = X & (2^p - 1) << 3          (8-byte entries at lut_off)
-//   Y = 8 f (X >> (p + 3)) + 8 (z - c) = 8 x'   (one 24-bit multiply-add)
-//   sh = clz(Y) & 24: 0, 8 or 16 bits to shift in (x' >= 2^9 for p <= 12)
-//   X = (Y << sh) | ((pair << 16) >> (29 - sh)),  29 - sh = sh ^ 29
+//   y = f (X >> (p + 3)) + (z - c) = x'          (one 24-bit multiply-add)
+//   s = ((clz(y) - 3) & 24) ^ 29 = 29 - 8 n      (n = 0, 1 or 2 bytes to read)
+//   X = alignbit(y, pair << 16, s),  Q -= 16 s   (J: step in the 16-step window,
+//                                                  a constant once unrolled)
 //
 // The pair goes straight into the high half of r (ds_read_u16_d16_hi; the low
 // half is never read).  The compiler does not emit that load, so it is
@@ -147,19 +158,15 @@ struct AttnArgs {
 // it, and LDS returns in order, so the compiler's wait for the table word
 // also covers the pair (whose only use comes after the table word's).
 template <uint32_t LUT_OFF>
-__device__ __forceinline__ uint32_t dstep(uint32_t& X, uint32_t& pq, uint32_t mask8, int p3) {
+__device__ __forceinline__ uint32_t dstep(uint32_t& X, uint32_t& Q, uint32_t mask8, int p3, int J) {
     uint32_t laddr = X & mask8, r;
-    asm volatile("ds_read_u16_d16_hi %0, %2" : "=v"(r), "+v"(laddr) : "v"(pq));
+    asm volatile("ds_read_u16_d16_hi %0, %2 offset:%3" : "=v"(r), "+v"(laddr) : "v"(Q), "i"(kPairStep * J));
     const uint64_t e = *LDS_PTR(const uint64_t, laddr + LUT_OFF);
     const uint32_t ex = (uint32_t)e, ey = (uint32_t)(e >> 32);
     const uint32_t y = __umul24(ex, X >> p3) + ey;
-    const uint32_t sh = (uint32_t)__builtin_clz(y) & 24u;
-    const uint32_t q = r >> (sh ^ 29u);
-    // one v_lshl_or_b32, so that the next table address stays a single mask
-    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(y), "v"(sh), "v"(q));
-    // pq += (sh / 8) positions of kPairRow bytes, as one v_lshl_add_u32 (left
-    // to itself the compiler keeps a running sum and adds it to the base)
-    asm("v_lshl_add_u32 %0, %1, 4, %2" : "=v"(pq) : "v"(sh), "v"(pq));
+    const uint32_t s = (((uint32_t)__builtin_clz(y) - 3u) & 24u) ^ 29u;
+    X = __builtin_amdgcn_alignbit(y, r, s);
+    asm("v_mad_i32_i24 %0, %1, -16, %2" : "=v"(Q) : "v"(s), "v"(Q));
     return ex;
 }
 
@@ -251,11 +258,14 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     // ---- prologue: tables, rotated query, its digits, q . mu per window
     if (!FIXED) {
         const int Pk = 1 << a.tk.p, Pv = 1 << a.tv.p;
+        // the device table holds 8 f | m << 24 and 8 (z - c); the decode step
+        // takes f | m << 24 and z - c
+        auto unscaled = [](uint2 e) { return uint2{(e.x & 0xFF000000u) | ((e.x & 0x00FFFFFFu) >> 3), e.y >> 3}; };
         uint2* lk = reinterpret_cast<uint2*>(smem + L.lut_k);
-        for (int i = tid; i < Pk; i += nthr) lk[i] = a.tk.t.lut64[i];
+        for (int i = tid; i < Pk; i += nthr) lk[i] = unscaled(a.tk.t.lut64[i]);
         if (LUTV != 0) {
             uint2* lv = reinterpret_cast<uint2*>(smem + LUTV);
-            for (int i = tid; i < Pv; i += nthr) lv[i] = a.tv.t.lut64[i];
+            for (int i = tid; i < Pv; i += nthr) lv[i] = unscaled(a.tv.t.lut64[i]);
         }
     }
     float* qt = reinterpret_cast<float*>(smem + L.waves);          // [G][d] scratch
@@ -322,21 +332,30 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     const uint32_t pv_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.pv) + col;
     uint8_t* vtile = wreg + L.vtile;     // overlays the pair arrays once both streams are decoded
     uint8_t* plimb = wreg + L.plimb;
-    const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
-    const uint32_t sel2 = (lane & 2) ? 0x03020706u : 0x05040100u;
+    // P . v: lane l serves query-head slot l / 16 and channel l % 16 of each
+    // 16-channel block; its tr8 reads start at token row 8 (l / 16) +
+    // (l % 16) / 2 of a 32-token block, byte 8 (l % 2) of the row's block
+    const int slot = lane >> 4;
+    const uint32_t trow = (uint32_t)(8 * (lane >> 4) + ((lane & 15) >> 1));
+    const uint32_t a_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.plimb) + trow * 16 + 8 * (lane & 1);
+    const uint32_t b_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.vtile) + trow * kVRowT + 8 * (lane & 1);
     const int pk3 = a.tk.p + 3, pv3 = a.tv.p + 3;
     const uint32_t mask8k = ((1u << a.tk.p) - 1u) << 3, mask8v = ((1u << a.tv.p) - 1u) << 3;
     const int64_t bh = (int64_t)b * a.Hkv + h;
 
-    float m_run[GP], l_part[GP], acco[GP], accf[2][GP];
+    // softmax state per query head (the same in every lane); the P . v sums
+    // of slot l / 16 of group hg, channel 64 s + 16 cb + l % 16 in acc[s][hg][cb]
+    float m_run[GP], l_part[GP], acco[GP], acc[2][HG][4];
 #pragma unroll
     for (int g = 0; g < GP; ++g) {
         m_run[g] = -INFINITY;
         l_part[g] = 0.f;
         acco[g] = 0.f;
-        accf[0][g] = 0.f;
-        accf[1][g] = 0.f;
     }
+#pragma unroll
+    for (int hg = 0; hg < HG; ++hg)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) acc[0][hg][cb] = acc[1][hg][cb] = 0.f;
     bool corrupt = false;
 
     // records of the wavefront's next tile are loaded while it decodes this one
@@ -414,14 +433,15 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
                 lk = spread2(__builtin_amdgcn_ubfe(ck[w], sh, 8));
                 vlev[grp] = spread2(__builtin_amdgcn_ubfe(cv[w], sh, 8));
             } else {
-                const uint32_t k0 = dstep<0>(xk, pq, mask8k, pk3);
-                const uint32_t v0 = dstep<LUTV>(xv, pv, mask8v, pv3);
-                const uint32_t k1 = dstep<0>(xk, pq, mask8k, pk3);
-                const uint32_t v1 = dstep<LUTV>(xv, pv, mask8v, pv3);
-                const uint32_t k2 = dstep<0>(xk, pq, mask8k, pk3);
-                const uint32_t v2 = dstep<LUTV>(xv, pv, mask8v, pv3);
-                const uint32_t k3 = dstep<0>(xk, pq, mask8k, pk3);
-                const uint32_t v3 = dstep<LUTV>(xv, pv, mask8v, pv3);
+                const int j0 = 4 * (grp % kClampGroups);     // step of the pointer window
+                const uint32_t k0 = dstep<0>(xk, pq, mask8k, pk3, j0);
+                const uint32_t v0 = dstep<LUTV>(xv, pv, mask8v, pv3, j0);
+                const uint32_t k1 = dstep<0>(xk, pq, mask8k, pk3, j0 + 1);
+                const uint32_t v1 = dstep<LUTV>(xv, pv, mask8v, pv3, j0 + 1);
+                const uint32_t k2 = dstep<0>(xk, pq, mask8k, pk3, j0 + 2);
+                const uint32_t v2 = dstep<LUTV>(xv, pv, mask8v, pv3, j0 + 2);
+                const uint32_t k3 = dstep<0>(xk, pq, mask8k, pk3, j0 + 3);
+                const uint32_t v3 = dstep<LUTV>(xv, pv, mask8v, pv3, j0 + 3);
                 lk = pack4(k0, k1, k2, k3);
                 vlev[grp] = pack4(v0, v1, v2, v3);
             }
@@ -443,11 +463,17 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
                     dk[hg][2] = mfma(ql.z, lk, dk[hg][2]);
                 }
             }
-            // a corrupt stream may run past its array: clamp often enough that
-            // it cannot leave the workgroup's LDS (kPairSlack above the arrays)
+            // end of a pointer window: the registers become the pointers again;
+            // a corrupt stream may run past its array, so clamp often enough
+            // that it cannot leave the workgroup's LDS (kPairSlack above the
+            // arrays), except after the last window, whose pointer is checked
             if (!FIXED && (grp % kClampGroups) == kClampGroups - 1) {
-                pq = min(pq, pk_end);
-                pv = min(pv, pv_end);
+                pq += kWindow * kPairStep;
+                pv += kWindow * kPairStep;
+                if (grp + 1 < kD / 4) {
+                    pq = min(pq, pk_end);
+                    pv = min(pv, pv_end);
+                }
             }
             // keep the scheduler inside one group: live ranges stay short
             __builtin_amdgcn_sched_barrier(0);
@@ -463,7 +489,7 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
         const float sk = half_lo(hk0), ok = half_hi(hk0);
         const float sv = half_lo(hv0), ov = half_hi(hv0);
         const float* qm = qmu + ((t / DQ_MEAN_WINDOW) - w0) * GP;
-        float pscale[GP];
+        float pscale[GP], corrs[GP];
         int pint[GP];
 #pragma unroll
         for (int hg = 0; hg < HG; ++hg)
@@ -481,8 +507,7 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
                 const float p = (score == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(score - mn);
                 l_part[g] = l_part[g] * corr + p;
                 acco[g] = acco[g] * corr + p * ov;
-                accf[0][g] *= corr;
-                accf[1][g] *= corr;
+                corrs[g] = corr;
                 m_run[g] = mn;
                 const float pw = p * sv;                 // >= 0: scales are non-negative
                 const float smax = wave_max_f32(pw);
@@ -491,55 +516,59 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
                 const float inv = smax > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax) : 0.f;
                 pint[g] = min(4194304, (int)rintf(pw * inv));
             }
-        // weight digits -> LDS [hg][head][token quad] x (d0, d1, d2) words
+        // weight digits -> LDS, one 16-byte token row per slot group: byte
+        // 4 r + d holds digit d of slot r (byte 4 r + 3 stays zero)
 #pragma unroll
         for (int hg = 0; hg < HG; ++hg) {
-            int dd[4][3];
+            uint32_t w[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) digits3(pint[4 * hg + r], dd[r][0], dd[r][1], dd[r][2]);
-            uint32_t wt[3];
-#pragma unroll
-            for (int d = 0; d < 3; ++d) {
-                const uint32_t w = ((uint32_t)dd[0][d] & 0xFFu) | (((uint32_t)dd[1][d] & 0xFFu) << 8) |
-                                   (((uint32_t)dd[2][d] & 0xFFu) << 16) | ((uint32_t)dd[3][d] << 24);
-                wt[d] = quad_transpose(w, sel1, sel2);
+            for (int r = 0; r < 4; ++r) {
+                int d0, d1, d2;
+                digits3(pint[4 * hg + r], d0, d1, d2);
+                w[r] = ((uint32_t)d0 & 0xFFu) | (((uint32_t)d1 & 0xFFu) << 8) | (((uint32_t)d2 & 0xFFu) << 16);
             }
-            *reinterpret_cast<uint4*>(plimb + ((hg * 4 + (lane & 3)) * (kTile / 4) + (lane >> 2)) * 16) =
-                uint4{wt[0], wt[1], wt[2], 0u};
+            *reinterpret_cast<uint4*>(plimb + hg * (kTile * 16) + lane * 16) = uint4{w[0], w[1], w[2], w[3]};
+        }
+        float scale_l[HG];
+#pragma unroll
+        for (int hg = 0; hg < HG; ++hg) {
+            const float corr_l = pick4(corrs + 4 * hg, slot);
+            scale_l[hg] = pick4(pscale + 4 * hg, slot);
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                acc[0][hg][cb] *= corr_l;
+                acc[1][hg][cb] *= corr_l;
+            }
         }
 
         // ---- P . v over two slices of 64 channels
+        wave_sync();   // the weight rows (and, below, the value rows) are read by other lanes
+        uint64_t pa[HG][2];
+#pragma unroll
+        for (int hg = 0; hg < HG; ++hg)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) pa[hg][kb] = lds_tr8(a_lane + hg * (kTile * 16) + kb * 32 * 16);
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
-            wave_sync();   // pair arrays (first slice) or the previous slice are no longer read
+            if (s) wave_sync();   // the first slice's value rows are no longer read
+            // the lane's 64 levels of the slice: 4 x 16 bytes of its token row
 #pragma unroll
-            for (int grp = 0; grp < kVSlice / 4; ++grp) {
-                const uint32_t wt = quad_transpose(vlev[s * (kVSlice / 4) + grp], sel1, sel2);
-                *reinterpret_cast<uint32_t*>(vtile + (grp * 4 + (lane & 3)) * kVRow + (lane >> 2) * 4) = wt;
-            }
+            for (int q = 0; q < 4; ++q)
+                *reinterpret_cast<uint4*>(vtile + lane * kVRowT + 16 * q) =
+                    uint4{vlev[16 * s + 4 * q], vlev[16 * s + 4 * q + 1], vlev[16 * s + 4 * q + 2],
+                          vlev[16 * s + 4 * q + 3]};
             wave_sync();
-            v4i dv[HG][3];
 #pragma unroll
-            for (int hg = 0; hg < HG; ++hg)
-#pragma unroll
-                for (int d = 0; d < 3; ++d) dv[hg][d] = v4i{0, 0, 0, 0};
-#pragma unroll 4
-            for (int qd = 0; qd < kTile / 4; ++qd) {
-                const uint32_t bv = *reinterpret_cast<const uint32_t*>(vtile + lane * kVRow + qd * 4);
+            for (int cb = 0; cb < 4; ++cb) {
+                const uint64_t b0 = lds_tr8(b_lane + 16 * cb);
+                const uint64_t b1 = lds_tr8(b_lane + 32 * kVRowT + 16 * cb);
 #pragma unroll
                 for (int hg = 0; hg < HG; ++hg) {
-                    const uint4 pl = *reinterpret_cast<const uint4*>(
-                        plimb + ((hg * 4 + (lane & 3)) * (kTile / 4) + qd) * 16);
-                    dv[hg][0] = mfma(pl.x, bv, dv[hg][0]);
-                    dv[hg][1] = mfma(pl.y, bv, dv[hg][1]);
-                    dv[hg][2] = mfma(pl.z, bv, dv[hg][2]);
+                    v4i d = mfma16(pa[hg][0], b0, v4i{0, 0, 0, 0});
+                    d = mfma16(pa[hg][1], b1, d);
+                    acc[s][hg][cb] += ((float)d[2] * 65536.0f + (float)d[1] * 256.0f + (float)d[0]) * scale_l[hg];
                 }
             }
-#pragma unroll
-            for (int hg = 0; hg < HG; ++hg)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    accf[s][4 * hg + r] += combine(dv[hg][0], dv[hg][1], dv[hg][2], r) * pscale[4 * hg + r];
         }
         wave_sync();   // the next tile rewrites the pair arrays over the value tile
     }
@@ -563,8 +592,16 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
             mw[wave * GP + g] = m_run[g];
             lw[wave * GP + g] = l_tot[g];
         }
-        aw[(wave * GP + g) * kD + lane] = accf[0][g] + o_tot[g];
-        aw[(wave * GP + g) * kD + kVSlice + lane] = accf[1][g] + o_tot[g];
+    }
+#pragma unroll
+    for (int hg = 0; hg < HG; ++hg) {
+        const float o_l = pick4(o_tot + 4 * hg, slot);
+        float* row = aw + (wave * GP + 4 * hg + slot) * kD + (lane & 15);
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+            row[16 * cb] = acc[0][hg][cb] + o_l;
+            row[kVSlice + 16 * cb] = acc[1][hg][cb] + o_l;
+        }
     }
     __syncthreads();
     const int NC = a.nchunks;
@@ -890,9 +927,9 @@ AttnLayout attn_layout(int pk, int pvb, int Ck, int Cv, int G, bool shared_lut, 
     L.pk = w;                                      // key pairs, then value pairs
     L.pv = w + align16((Ck - kPayloadOffset) * kPairRow);
     L.vtile = w;                                   // reuses the pair arrays
-    L.plimb = w + align16(kVSlice * kVRow);        // so do the weight digits
+    L.plimb = w + align16(kTile * kVRowT);         // so do the weight digits
     w = std::max(L.pv + align16((Cv - kPayloadOffset) * kPairRow),
-                 L.plimb + align16(HG * 4 * (kTile / 4) * 16));
+                 L.plimb + align16(HG * kTile * 16));
     L.wave_stride = w;
     int nw = (kMaxLds - kPairSlack - off) / w;
     if (nw > max_waves(HG, rw)) nw = max_waves(HG, rw);
