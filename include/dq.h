@@ -175,9 +175,9 @@ int dq_decode_attention(const dq_tables* k_tables, const dq_tables* v_tables,
  * Every call on a device shares that device's array, which keeps the last
  * call's contents: calls that overlap on one device (different streams, or
  * different host threads) race and give undefined results; serialize them.
- * The workspace this needs is 256 + 520 batch q_heads (chunks + 1) bytes,
+ * The workspace this needs is 256 + 520 batch q_heads (chunks + 4) bytes,
  * chunks being the context split chosen from (batch, kv_heads, t_cap) and the
- * CU count (2 for 16 x 32768 tokens x 8 KV heads on 256 CUs: 0.8 MB).
+ * CU count (2 for 16 x 32768 tokens x 8 KV heads on 256 CUs: 1.6 MB).
  * Returns DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_WORKSPACE when the sizes need more
  * than the array holds (dq_last_error says how much), or DQ_ERR_HIP.
  */

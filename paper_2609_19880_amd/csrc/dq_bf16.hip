@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kThreads) void bf16_partial_kernel(B16Args a) {
     }
     for (int i = tid; i < G * kD; i += kThreads) {
         const int g = i / kD, j = i % kD;
-        const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * (NC + 1) + c;
+        const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * (NC + kResSlots) + c;
         a.ws_acc[slot * kD + j] = rot[i];
         if (j == 0) {
             a.ws_m[slot] = gm[g];

@@ -133,10 +133,10 @@ struct AttnArgs {
     const uint8_t* vrec;
     const int32_t* seq_lens;
     float scale_log2;            // softmax_scale * log2(e) / d
-    int32_t* ws_hdr;             // [0] chunk, [1] chunk count NC, [2] residual slot written
-    float* ws_m;                 // [B][Hq][NC + 1]   (slot NC: the residual window)
-    float* ws_l;                 // [B][Hq][NC + 1]
-    float* ws_acc;               // [B][Hq][NC + 1][d]
+    int32_t* ws_hdr;             // [0] chunk, [1] chunk count NC, [2] residual slots written
+    float* ws_m;                 // [B][Hq][NC + kResSlots]   (slots NC..: the residual window)
+    float* ws_l;                 // [B][Hq][NC + kResSlots]
+    float* ws_acc;               // [B][Hq][NC + kResSlots][d]
     uint32_t* status;
     int shared_lut;
     Pages pg;                    // records and key means: contiguous or paged
@@ -617,7 +617,7 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
             acc += aw[(w * GP + g) * kD + j] * e;
             l += lw[w * GP + g] * e;
         }
-        const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * (NC + 1) + c;
+        const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * (NC + kResSlots) + c;
         a.ws_acc[slot * kD + j] = acc;
         if (j == 0) {
             a.ws_m[slot] = M;
@@ -635,17 +635,17 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
     __shared__ float o[kD];
     __shared__ float red[kD];
     const int hq = blockIdx.x, b = blockIdx.y, j = threadIdx.x;
-    const int chunk = ws_hdr[0], NC = ws_hdr[1], residual = ws_hdr[2];
+    const int chunk = ws_hdr[0], NC = ws_hdr[1], residual = min(max(ws_hdr[2], 0), kResSlots);
     const int T = max(0, min(seq_lens[b], t_cap));
     float* dst = out + ((int64_t)b * Hq + hq) * kD;
-    // the chunks that hold tokens, then the residual window's slot (an empty
-    // window wrote m = -inf)
+    // the chunks that hold tokens, then the residual window's slots (a part
+    // of the window without tokens wrote m = -inf)
     const int nc = min(NC, (T + chunk - 1) / chunk);
-    const int64_t base = ((int64_t)b * Hq + hq) * (NC + 1);
-    // partials in use: chunks 0..nc-1, then the residual slot NC
-    const int np = nc + (residual ? 1 : 0);
+    const int64_t base = ((int64_t)b * Hq + hq) * (NC + kResSlots);
+    // partials in use: chunks 0..nc-1, then the residual slots NC..
+    const int np = nc + residual;
     float M = -INFINITY;
-    for (int i = j; i < np; i += kD) M = fmaxf(M, ws_m[base + (i < nc ? i : NC)]);
+    for (int i = j; i < np; i += kD) M = fmaxf(M, ws_m[base + (i < nc ? i : NC + i - nc)]);
     red[j] = M;
     __syncthreads();
     for (int s2 = kD / 2; s2 > 0; s2 >>= 1) {
@@ -665,7 +665,7 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int i = min(i0 + u, np - 1);
-            const int c = i < nc ? i : NC;          // same for every thread of the block
+            const int c = i < nc ? i : NC + i - nc;  // same for every thread of the block
             av[u] = ws_acc[(base + c) * kD + j];
             mv[u] = ws_m[base + c];
             lv[u] = ws_l[base + c];
@@ -699,6 +699,7 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
 constexpr int kResThreads = 256;
 constexpr int kMaxResidual = 256;
 constexpr int kMaxGroup = 8;
+constexpr int kResPart = kMaxResidual / kResSlots;   // tokens per workgroup (64)
 
 struct ResArgs {
     const uint16_t* q;
@@ -714,45 +715,82 @@ struct ResArgs {
     float* ws_acc;
 };
 
-// One workgroup per (KV head, sequence): logits of the G query heads against
-// the raw keys, softmax statistics, the weighted sum of the raw values, and
-// the rotation H of that sum so that the merge's inverse rotation H / d
-// returns it (H H = d I).  The result is one more split-K partial, in slot NC.
+// One workgroup per (part, KV head, sequence); the r residual tokens of a
+// sequence are cut into kResSlots parts of ceil(r / kResSlots) <= 64 tokens.
+// Every key and value row of the part is requested at the
+// start (one memory round trip); then the logits of the G query heads, the
+// softmax statistics of the part, the weighted sum of its raw values, and the
+// rotation H of that sum so that the merge's inverse rotation H / d returns it
+// (H H = d I).  The result is one more split-K partial, in slot NC + i; a part
+// without tokens writes m = -inf and zeros.
 __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
     __shared__ __align__(16) float qs[kMaxGroup][kD];
-    __shared__ float sc[kMaxGroup][kMaxResidual];
-    __shared__ float part[1][kMaxGroup][kD];
-    __shared__ float pq[4][kMaxGroup][kD];
+    __shared__ float sc[kMaxGroup][kResPart];
+    __shared__ float pq[kResThreads / 32][kMaxGroup][kD];
     __shared__ float stat[2][kMaxGroup];
-    const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int part = blockIdx.x, h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
     const int lane = tid & (kWave - 1), wave = tid / kWave;
     const int G = a.G, NC = a.ws_hdr[1];
-    if ((h | b) == 0 && tid == 0) a.ws_hdr[2] = 1;
+    if ((part | h | b) == 0 && tid == 0) a.ws_hdr[2] = kResSlots;
     const int r = max(0, min(a.res_lens[b], a.r_cap));
-    const int first = max(0, a.seq_lens[b]) % a.r_cap;
+    const int ps = (r + kResSlots - 1) / kResSlots;
+    const int t0 = part * ps;
+    const int n = max(0, min(ps, r - t0));
     const int hq0 = h * G;
+    const int64_t slot0 = ((int64_t)b * a.Hq + hq0) * (NC + kResSlots) + NC + part;
+    if (n == 0) {
+        for (int i = tid; i < G * kD; i += kResThreads) {
+            const int g = i / kD, j = i % kD;
+            const int64_t slot = slot0 + (int64_t)g * (NC + kResSlots);
+            a.ws_acc[slot * kD + j] = 0.f;
+            if (j == 0) {
+                a.ws_m[slot] = -INFINITY;
+                a.ws_l[slot] = 0.f;
+            }
+        }
+        return;
+    }
+    const int first = max(0, a.seq_lens[b]) % a.r_cap;
+    const int64_t row0 = ((int64_t)b * a.Hkv + h) * a.r_cap;
+    // ring slot of token i < n of the part (first + t0 + i < 2 r_cap)
+    auto ring = [&](int i) {
+        const int s = first + t0 + i;
+        return s < a.r_cap ? s : s - a.r_cap;
+    };
+
+    // ---- every load of the workgroup in flight together: thread tid takes
+    //      channels 32 (tid % 4) .. + 31 of key row tid / 4, and channels
+    //      4 (tid % 32) .. + 3 of value rows 8 (tid / 32) .. + 7 (rows past the
+    //      part read its last token and are given weight 0)
+    const int kt = tid >> 2, kc = 32 * (tid & 3);
+    const int vc = 4 * (tid & 31), vg = tid >> 5;
+    uint4 kr[4];
+    {
+        const uint4* src = reinterpret_cast<const uint4*>(a.rk + (row0 + ring(min(kt, n - 1))) * kD + kc);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) kr[u] = src[u];
+    }
+    uint2 vr[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+        vr[u] = *reinterpret_cast<const uint2*>(a.rv + (row0 + ring(min(8 * vg + u, n - 1))) * kD + vc);
     for (int i = tid; i < G * kD; i += kResThreads)
         qs[i / kD][i % kD] = bf16_to_f32(a.q[((int64_t)b * a.Hq + hq0) * kD + i]);
     __syncthreads();
-    const int64_t row0 = ((int64_t)b * a.Hkv + h) * a.r_cap;
-    if (tid < r) {
-        const int slot = first + tid < a.r_cap ? first + tid : first + tid - a.r_cap;
-        const uint4* kp = reinterpret_cast<const uint4*>(a.rk + (row0 + slot) * kD);
-        // the whole 256-byte key row in flight at once
-        uint4 row[kD / 8];
-#pragma unroll
-        for (int c8 = 0; c8 < kD / 8; ++c8) row[c8] = kp[c8];
+
+    // ---- logits: quarter dot products, summed over the lane quad
+    {
         float dot[kMaxGroup];
 #pragma unroll
         for (int g = 0; g < kMaxGroup; ++g) dot[g] = 0.f;
 #pragma unroll
-        for (int c8 = 0; c8 < kD / 8; ++c8) {
-            const uint32_t ww[4] = {row[c8].x, row[c8].y, row[c8].z, row[c8].w};
+        for (int u = 0; u < 4; ++u) {
+            const uint32_t ww[4] = {kr[u].x, kr[u].y, kr[u].z, kr[u].w};
 #pragma unroll
             for (int g = 0; g < kMaxGroup; ++g) {
                 if (g < G) {
-                    const float4 qa = *reinterpret_cast<const float4*>(&qs[g][c8 * 8]);
-                    const float4 qb = *reinterpret_cast<const float4*>(&qs[g][c8 * 8 + 4]);
+                    const float4 qa = *reinterpret_cast<const float4*>(&qs[g][kc + 8 * u]);
+                    const float4 qb = *reinterpret_cast<const float4*>(&qs[g][kc + 8 * u + 4]);
                     const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
@@ -761,87 +799,74 @@ __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
             }
         }
 #pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g)
-            if (g < G) sc[g][tid] = dot[g] * a.scale_log2;
+        for (int g = 0; g < kMaxGroup; ++g) {
+            if (g < G) {
+                float v = dot[g];
+                v += dpp_step<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
+                v += dpp_step<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
+                if ((tid & 3) == 0) sc[g][kt] = kt < n ? v * a.scale_log2 : -INFINITY;
+            }
+        }
     }
     __syncthreads();
+    // ---- softmax statistics of the part, a wavefront per head
     for (int g = wave; g < G; g += kResThreads / kWave) {
-        float mx = -INFINITY;
-        for (int t = lane; t < r; t += kWave) mx = fmaxf(mx, sc[g][t]);
-        mx = wave_max(mx);
-        float sum = 0.f;
-        for (int t = lane; t < r; t += kWave) {
-            const float p = exp2f(sc[g][t] - mx);
-            sc[g][t] = p;
-            sum += p;
-        }
-        sum = wave_sum_f32(sum);
+        const float v = sc[g][lane];
+        const float mx = wave_max(v);
+        const float p = lane < n ? exp2f(v - mx) : 0.f;
+        sc[g][lane] = p;
+        const float sum = wave_sum_f32(p);
         if (lane == 0) {
             stat[0][g] = mx;
             stat[1][g] = sum;
         }
     }
     __syncthreads();
+    // ---- weighted values: 8 tokens x 4 channels per thread
     {
-        // thread (channel pair jp, quarter): channels 2 jp, 2 jp + 1 of tokens
-        // quarter, quarter + 4, ...; all of its value loads are issued before
-        // any is used (loads on a clamped token; tokens past r are skipped)
-        const int jp = tid % (kD / 2), quarter = tid / (kD / 2);
-        constexpr int kPer = kMaxResidual / 4;
-        uint32_t vw[kPer];
+        float acc[kMaxGroup][4];
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int tc = min(quarter + 4 * u, max(r - 1, 0));
-            const int slot = first + tc < a.r_cap ? first + tc : first + tc - a.r_cap;
-            // every slot of the ring is allocated, so the clamped load is in bounds even for r = 0
-            vw[u] = *reinterpret_cast<const uint32_t*>(a.rv + (row0 + slot) * kD + 2 * jp);
-        }
-        float acc0[kMaxGroup], acc1[kMaxGroup];
+        for (int g = 0; g < kMaxGroup; ++g)
 #pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g) acc0[g] = acc1[g] = 0.f;
+            for (int k = 0; k < 4; ++k) acc[g][k] = 0.f;
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int t = quarter + 4 * u;
-            if (t < r) {
-                const float v0 = __uint_as_float(vw[u] << 16), v1 = __uint_as_float(vw[u] & 0xFFFF0000u);
+        for (int u = 0; u < 8; ++u) {
+            const int t = 8 * vg + u;
+            const float v[4] = {__uint_as_float(vr[u].x << 16), __uint_as_float(vr[u].x & 0xFFFF0000u),
+                                __uint_as_float(vr[u].y << 16), __uint_as_float(vr[u].y & 0xFFFF0000u)};
 #pragma unroll
-                for (int g = 0; g < kMaxGroup; ++g) {
-                    if (g < G) {
-                        acc0[g] += sc[g][t] * v0;
-                        acc1[g] += sc[g][t] * v1;
-                    }
+            for (int g = 0; g < kMaxGroup; ++g) {
+                if (g < G) {
+                    const float w = t < n ? sc[g][t] : 0.f;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) acc[g][k] += w * v[k];
                 }
             }
         }
 #pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g) {
-            if (g < G) {
-                pq[quarter][g][2 * jp] = acc0[g];
-                pq[quarter][g][2 * jp + 1] = acc1[g];
-            }
-        }
+        for (int g = 0; g < kMaxGroup; ++g)
+            if (g < G)
+                *reinterpret_cast<float4*>(&pq[vg][g][vc]) = float4{acc[g][0], acc[g][1], acc[g][2], acc[g][3]};
     }
     __syncthreads();
-    for (int i = tid; i < G * kD; i += kResThreads) {
-        const int g = i / kD, j = i % kD;
-        part[0][g][j] = pq[0][g][j] + pq[1][g][j] + pq[2][g][j] + pq[3][g][j];
-    }
-    __syncthreads();
-    for (int hh = 1; hh < kD; hh <<= 1) {
-        for (int i = tid; i < G * (kD / 2); i += kResThreads) {
-            const int g = i / (kD / 2), x = i % (kD / 2);
-            const int lo = (x / hh) * 2 * hh + (x % hh);
-            const float x0 = part[0][g][lo], x1 = part[0][g][lo + hh];
-            part[0][g][lo] = x0 + x1;
-            part[0][g][lo + hh] = x0 - x1;
+    // ---- sum of the 8 token groups and the rotation H, a wavefront per head
+    //      (channels l and l + 64 in lane l, stages h = 1, 2, ..., 64)
+    for (int g = wave; g < G; g += kResThreads / kWave) {
+        float v0 = 0.f, v1 = 0.f;
+#pragma unroll
+        for (int k = 0; k < kResThreads / 32; ++k) {
+            v0 += pq[k][g][lane];
+            v1 += pq[k][g][lane + 64];
         }
-        __syncthreads();
-    }
-    for (int i = tid; i < G * kD; i += kResThreads) {
-        const int g = i / kD, j = i % kD;
-        const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * (NC + 1) + NC;
-        a.ws_acc[slot * kD + j] = part[0][g][j];
-        if (j == 0) {
+        for (int hh = 1; hh < 64; hh <<= 1) {
+            const float p0 = __shfl_xor(v0, hh), p1 = __shfl_xor(v1, hh);
+            v0 = (lane & hh) ? p0 - v0 : v0 + p0;
+            v1 = (lane & hh) ? p1 - v1 : v1 + p1;
+        }
+        const int64_t slot = slot0 + (int64_t)g * (NC + kResSlots);
+        a.ws_acc[slot * kD + lane] = v0 + v1;
+        a.ws_acc[slot * kD + lane + 64] = v0 - v1;
+        if (lane == 0) {
             a.ws_m[slot] = stat[0][g];
             a.ws_l[slot] = stat[1][g];
         }
@@ -966,7 +991,7 @@ ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap, int num_cus) {
     chunk = std::min(chunk, kMaxChunk);
     p.chunk = chunk;
     p.nchunks = (t_cap + chunk - 1) / chunk;
-    p.slots_max = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
+    p.slots_max = ws_slots(B, Hq, t_cap);
     return p;
 }
 
@@ -986,7 +1011,7 @@ int launch_decode_symbols(const dq_tables* tab, const uint8_t* records, int64_t 
 
 size_t attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d) {
     (void)Hkv;
-    const int64_t slots = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
+    const int64_t slots = ws_slots(B, Hq, t_cap);
     return (size_t)kWsHeader + (size_t)(slots * d + 2 * slots) * sizeof(float);
 }
 
@@ -1039,7 +1064,7 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pag
                              int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
                              const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                              const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
-                             uint32_t* status, hipStream_t stream, int64_t ws_slots) {
+                             uint32_t* status, hipStream_t stream, int64_t ws_slots_used) {
     if (!attention_supports(tk, tv)) return DQ_ERR_INVALID_ARG;
     const int G = Hq / Hkv;
     AttnArgs a;
@@ -1065,7 +1090,7 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pag
     a.vrec = vrec;
     a.seq_lens = seq_lens;
     a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
-    const int64_t slots = ws_slots > 0 ? ws_slots : plan.slots_max;
+    const int64_t slots = ws_slots_used > 0 ? ws_slots_used : plan.slots_max;
     a.ws_hdr = static_cast<int32_t*>(ws);
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
     a.ws_m = a.ws_acc + slots * kD;
@@ -1117,9 +1142,9 @@ int launch_attention_fixed_partial(const Pages& pg, const uint16_t* q, int32_t B
 }
 
 int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
-                           int32_t t_cap, const void* ws, float* out, hipStream_t stream, int64_t ws_slots) {
+                           int32_t t_cap, const void* ws, float* out, hipStream_t stream, int64_t ws_slots_used) {
     (void)Hkv;
-    const int64_t slots = ws_slots > 0 ? ws_slots : (int64_t)B * Hq * (max_chunks(t_cap) + 1);
+    const int64_t slots = ws_slots_used > 0 ? ws_slots_used : ws_slots(B, Hq, t_cap);
     const int32_t* hdr = static_cast<const int32_t*>(ws);
     const float* acc = reinterpret_cast<const float*>(static_cast<const uint8_t*>(ws) + kWsHeader);
     const float* m = acc + slots * kD;
@@ -1132,7 +1157,7 @@ int launch_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t 
                               const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
                               const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
                               void* ws, hipStream_t stream) {
-    const int64_t slots = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
+    const int64_t slots = ws_slots(B, Hq, t_cap);
     ResArgs a;
     a.q = q;
     a.rk = res_k;
@@ -1148,7 +1173,7 @@ int launch_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t 
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
     a.ws_m = a.ws_acc + slots * kD;
     a.ws_l = a.ws_m + slots;
-    attn_residual_kernel<<<dim3(Hkv, B), kResThreads, 0, stream>>>(a);
+    attn_residual_kernel<<<dim3(kResSlots, Hkv, B), kResThreads, 0, stream>>>(a);
     return hip_check("attn_residual launch", hipGetLastError());
 }
 
@@ -1168,7 +1193,7 @@ int launch_residual_commit(int32_t* seq_lens, int32_t* res_lens, int32_t B, int3
 
 int64_t attention_plan_slots(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap) {
     const ChunkPlan plan = chunk_plan(B, Hq, Hkv, t_cap, cu_count());
-    return (int64_t)B * Hq * (plan.nchunks + 1);
+    return (int64_t)B * Hq * (plan.nchunks + kResSlots);
 }
 
 // ------------------------------------------------ allocation-free workspace

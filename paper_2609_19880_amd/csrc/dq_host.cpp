@@ -547,7 +547,7 @@ int dq_decode_attention_no_alloc(const dq_tables* tk, const dq_tables* tv, const
     if (!q || !krec || !kmq || !kms || !vrec || !seq_lens || !out) return DQ_ERR_INVALID_ARG;
     if (!std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
     // the workspace of this call's own chunk plan, packed: header, then
-    // accumulators, maxima and sums of B Hq (chunks + 1) slots
+    // accumulators, maxima and sums of B Hq (chunks + 4) slots
     const int64_t slots = dq::attention_plan_slots(B, Hq, Hkv, t_cap);
     const int64_t need = dq::kWsHeader + slots * (128 + 2) * (int64_t)sizeof(float);
     if (need > (int64_t)DQ_NO_ALLOC_SCRATCH_BYTES) {

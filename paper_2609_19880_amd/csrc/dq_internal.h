@@ -15,12 +15,15 @@ constexpr int kBisectSteps = 12;            // T of Alg. 1
 constexpr int kBracketUnits = 40 * kLambdaSteps;  // hi - lo = 40 octaves
 
 // Split-K attention workspace: a 256-byte header (chunk size, chunk count NC,
-// residual slot written), then fp32 acc [B][Hq][NC + 1][d], m and l
-// [B][Hq][NC + 1], sized for chunks of at least kMinChunk tokens.
+// residual slots written), then fp32 acc [B][Hq][NC + kResSlots][d], m and l
+// [B][Hq][NC + kResSlots], sized for chunks of at least kMinChunk tokens.
+// Slots NC .. NC + kResSlots - 1 of each (sequence, query head) hold the
+// residual window's partials, one per workgroup of its split.
 constexpr int kWsHeader = 256;
 constexpr int kMinChunk = 512;
+constexpr int kResSlots = 4;
 inline int64_t max_chunks(int t_cap) { return (t_cap + kMinChunk - 1) / kMinChunk; }
-inline int64_t ws_slots(int B, int Hq, int t_cap) { return (int64_t)B * Hq * (max_chunks(t_cap) + 1); }
+inline int64_t ws_slots(int B, int Hq, int t_cap) { return (int64_t)B * Hq * (max_chunks(t_cap) + kResSlots); }
 int cu_count();   // CUs of the current device
 
 // Where the records and key means of (sequence b, KV head h, token t) live.
@@ -149,17 +152,18 @@ int launch_decode_symbols(const dq_tables* tab, const uint8_t* records, int64_t 
 
 size_t attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap, int32_t d);
 
-// ws_slots: (max, sum, accumulator) slots the workspace holds, which places
-// the max and sum arrays after the accumulators; 0 = the size
+// ws_slots_used: (max, sum, accumulator) slots the workspace holds, which
+// places the max and sum arrays after the accumulators; 0 = the size
 // attention_workspace_bytes allows for (512-token chunks).
 int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pages& pg, const uint16_t* q,
                              int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
                              const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
                              const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
-                             uint32_t* status, hipStream_t stream, int64_t ws_slots = 0);
+                             uint32_t* status, hipStream_t stream, int64_t ws_slots_used = 0);
 
 // Slots the chunk plan of these sizes uses on the current device:
-// B Hq (chunks + 1), the last one per query head for the residual window.
+// B Hq (chunks + kResSlots), the last ones per query head for the residual
+// window.
 int64_t attention_plan_slots(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap);
 
 // Device address of the current device's copy of the library's static
@@ -206,6 +210,6 @@ int launch_bf16_partial(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, c
                         hipStream_t stream);
 int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* seq_lens,
                            int32_t t_cap, const void* ws, float* out, hipStream_t stream,
-                           int64_t ws_slots = 0);
+                           int64_t ws_slots_used = 0);
 
 }  // namespace dq

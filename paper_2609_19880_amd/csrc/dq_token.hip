@@ -500,7 +500,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
                 acc += aw[(w * 4 + r) * kD + j] * e;
                 l += lw[w * 4 + r] * e;
             }
-            const int64_t slot = ((int64_t)b * Hq + h * G + r) * (NC + 1) + c;
+            const int64_t slot = ((int64_t)b * Hq + h * G + r) * (NC + kResSlots) + c;
             a.ws_acc[slot * kD + j] = acc;
             if (j == 0) {
                 a.ws_m[slot] = M;
@@ -596,7 +596,7 @@ int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, con
     a.pg = pg;
     a.seq_lens = seq_lens;
     a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
-    const int64_t slots = (int64_t)B * Hq * (max_chunks(t_cap) + 1);
+    const int64_t slots = ws_slots(B, Hq, t_cap);
     a.ws_hdr = static_cast<int32_t*>(ws);
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
     a.ws_m = a.ws_acc + slots * kD;
