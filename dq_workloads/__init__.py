@@ -240,3 +240,12 @@ def make_edge_keys(seed: int, batch: int, context: int, kv_heads: int, head_dim:
         elif kind == 3:
             out[:, sl] = mixed[:, sl]
     return torch.from_numpy(out).to(torch.bfloat16)
+
+
+def make_ternary(seed: int, batch: int, context: int, kv_heads: int, head_dim: int = HEAD_DIM) -> torch.Tensor:
+    """K or V inputs [B, T, H, d] bf16 with every channel in {-1, 0, 1}
+    (probabilities 1/4, 1/2, 1/4): the sums and differences of up to 128 such
+    values are integers below 256, which bf16 holds exactly."""
+    rng = np.random.default_rng(seed + 1299709)
+    v = rng.choice(np.array([-1.0, 0.0, 0.0, 1.0], dtype=np.float32), size=(batch, context, kv_heads, head_dim))
+    return torch.from_numpy(v).to(torch.bfloat16)

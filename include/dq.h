@@ -69,6 +69,13 @@ typedef struct dq_config {
     int32_t precision_bits; /* p: rANS precision, 8..12 (Eq. rans)              */
     int32_t record_bytes;   /* C: record size in bytes, 9..2n+8                 */
     double alpha;           /* sharpening exponent, >= 1 (Sec. 4.4; paper 1.4)  */
+    int32_t prerotated;     /* 0: the library rotates every head's vector with
+                               the Hadamard matrix (Sec. 4.2; keys need this,
+                               RoPE does not commute with it).  1: the tensor
+                               arrives already in the rotated basis, as values
+                               do when the rotation is folded into the
+                               projection weights offline (Sec. 4.2): no
+                               online rotation, see dq_decode_attention.     */
 } dq_config;
 
 typedef struct dq_table_info {
@@ -118,8 +125,10 @@ void dq_free_tables(dq_tables* tables);
  *            quantization (Sec. 4.2).  Both NULL for values (no mean removal);
  *            with them, t0 and n_new must be multiples of 128.
  *   status:  device u32, may be NULL; DQ_STATUS_RANGE / DQ_STATUS_OVERFLOW.
- * Every stream is rotated with the unnormalized Sylvester Hadamard matrix.
- * The records are bit-identical to the reference definition of the format.
+ * Every stream is rotated with the unnormalized Sylvester Hadamard matrix,
+ * unless the tables were built with prerotated = 1 (then the input is coded
+ * as it is).  The records are bit-identical to the reference definition of
+ * the format.
  * Requires head_dim <= 256, 1 <= kv_heads <= 65535, 0 <= batch <= 65535,
  * t0 >= 0, n_new >= 0, t0 + n_new <= t_cap and non-negative strides; with the
  * mean buffers also t0, n_new and t_cap multiples of 128.  Returns DQ_OK
@@ -140,7 +149,13 @@ size_t dq_decode_workspace_bytes(int32_t batch, int32_t q_heads, int32_t kv_head
  * One decode step of attention over the compressed cache (Sec. 4.5 decoding,
  * App. A): logits softmax_scale * q . k_hat over the first seq_lens[b] tokens,
  * output sum_t a_t v_hat_t, with query head i reading KV head
- * i / (q_heads / kv_heads).
+ * i / (q_heads / kv_heads).  q and out are in the basis the caller gives keys
+ * and values in: with online rotation (prerotated = 0) that is the original
+ * basis (the query is rotated and the output rotated back inside); with
+ * prerotated keys the query must come in the keys' basis, and with
+ * prerotated values the output stays in the values' basis (the caller's
+ * output projection absorbs the rotation).  The raw tokens of a residual
+ * window are taken in the same bases.
  *   q:        bf16 [batch][q_heads][head_dim]
  *   k_records, v_records: u8 [batch][kv_heads][t_cap][C_k or C_v]
  *   k_mean_q, k_mean_scale: as written by dq_encode_kv for the keys

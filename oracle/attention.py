@@ -24,6 +24,11 @@ Readings
   sequence is then seq_len[b] compressed tokens followed by res_len[b] raw
   tokens (original basis, no rotation, no mean removal), and the softmax runs
   over all of them; a sequence with no tokens at all gives 0.
+* A4 prerotated tensors (reading V0 of kv): keys coded without rotation are
+  in the caller's basis, and so is the query (logit q . k_hat, no 1/d);
+  values coded without rotation give the output in their own basis
+  (sum_t a_t v_hat_t, no inverse rotation), which the caller's output
+  projection absorbs.  Raw residual tokens are taken in the same bases.
 """
 
 from __future__ import annotations
@@ -41,15 +46,16 @@ def dequantize(sym, s16, o16, mean_hat=None, window=128):
     return x
 
 
-def attention_direct(q, k_rot, v_rot, seq_lens, gqa, softmax_scale):
+def attention_direct(q, k_rot, v_rot, seq_lens, gqa, softmax_scale, rotate_k=True, rotate_v=True):
     """Textbook softmax(q K^T * scale) V in the original basis, fp64.
 
-    q [B, Hq, d] fp64; k_rot, v_rot [B, Hkv, T, d] rotated reconstructions.
+    q [B, Hq, d] fp64; k_rot, v_rot [B, Hkv, T, d] rotated reconstructions
+    (in the caller's basis when rotate_k / rotate_v is False, reading A4).
     """
     B, Hq, d = q.shape
     H = hadamard.sylvester(d).astype(np.float64)
-    k = k_rot @ H / d
-    v = v_rot @ H / d
+    k = k_rot @ H / d if rotate_k else k_rot
+    v = v_rot @ H / d if rotate_v else v_rot
     out = np.zeros((B, Hq, d), dtype=np.float64)
     for b in range(B):
         T = int(seq_lens[b])
@@ -66,13 +72,15 @@ def attention_direct(q, k_rot, v_rot, seq_lens, gqa, softmax_scale):
 
 
 def attention_folded(q, k_sym, k_s, k_o, k_mean_hat, v_sym, v_s, v_o, seq_lens,
-                     gqa, softmax_scale, window=128):
+                     gqa, softmax_scale, window=128, rotate_k=True, rotate_v=True):
     """Eq. (fold-key) / Eq. (fold-value) evaluated directly on the symbols, fp64.
 
-    k_mean_hat [B, Hkv, T/W, d] or None.
+    k_mean_hat [B, Hkv, T/W, d] or None.  rotate_k / rotate_v False: the
+    keys / values were coded without rotation (reading A4).
     """
     B, Hq, d = q.shape
-    q_rot = hadamard.fwht(q)
+    q_rot = hadamard.fwht(q) if rotate_k else q
+    scale = softmax_scale / d if rotate_k else softmax_scale
     out = np.zeros((B, Hq, d), dtype=np.float64)
     for b in range(B):
         T = int(seq_lens[b])
@@ -85,28 +93,30 @@ def attention_folded(q, k_sym, k_s, k_o, k_mean_hat, v_sym, v_s, v_o, seq_lens,
             logit = k_s[b, h, :T].astype(np.float64) * dot + k_o[b, h, :T].astype(np.float64) * qr.sum()
             if k_mean_hat is not None:
                 logit = logit + np.repeat(k_mean_hat[b, h] @ qr, window)[:T]
-            s = logit * (softmax_scale / d)
+            s = logit * scale
             s = s - s.max()
             a = np.exp(s)
             a = a / a.sum()
             acc = (a * v_s[b, h, :T].astype(np.float64)) @ v_sym[b, h, :T].astype(np.float64)
             acc = acc + (a * v_o[b, h, :T].astype(np.float64)).sum()
-            out[b, i] = hadamard.fwht(acc) / d
+            out[b, i] = hadamard.fwht(acc) / d if rotate_v else acc
     return out
 
 
-def attention_with_residual(q, k_rot, v_rot, seq_lens, res_k, res_v, res_lens, gqa, softmax_scale):
+def attention_with_residual(q, k_rot, v_rot, seq_lens, res_k, res_v, res_lens, gqa, softmax_scale,
+                            rotate_k=True, rotate_v=True):
     """Decode attention over compressed tokens and a raw residual window, fp64.
 
     q [B, Hq, d]; k_rot, v_rot [B, Hkv, T, d] rotated reconstructions of the
     compressed tokens; res_k, res_v [B, Hkv, R, d] raw residual tokens, of
     which the first res_lens[b] are in use.  Textbook softmax over the union
-    of the two sets in the original basis (reading A3).
+    of the two sets in the original basis (reading A3; the caller's basis
+    for tensors coded without rotation, reading A4).
     """
     B, Hq, d = q.shape
     H = hadamard.sylvester(d).astype(np.float64)
-    k = k_rot @ H / d
-    v = v_rot @ H / d
+    k = k_rot @ H / d if rotate_k else k_rot
+    v = v_rot @ H / d if rotate_v else v_rot
     out = np.zeros((B, Hq, d), dtype=np.float64)
     for b in range(B):
         T, R = int(seq_lens[b]), int(res_lens[b])

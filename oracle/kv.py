@@ -15,6 +15,10 @@ them one KV head at a time.  Rotation and the key window mean stay per head;
 the affine (s, o) and the record are per token.  The *_tokenwise functions
 build these streams; with H_kv = 1 they are the per-head streams.
 
+Reading V0 (prerotated tensors, Sec. 4.2: the value rotation can be folded
+into the projection weights offline): with rotate=False the input already is
+the rotated vector and is coded as it is, with no Hadamard.
+
 Reading K1 (container overflow): the drift guarantees the ideal cost
 sum r <= B; should the rANS bytes still exceed the record (8 + E > C), the
 budget is lowered by 8 bits and the second Drift and the coder are run again,
@@ -83,25 +87,25 @@ def encode_streams(x: np.ndarray, tab: Tables):
     return recs, syms, s16s, o16s, budgets
 
 
-def rotate(bits: np.ndarray) -> np.ndarray:
-    """bf16 [..., d] -> rotated fp64 [..., d]."""
-    return hadamard.fwht(bf16_to_f64(bits))
+def rotate(bits: np.ndarray, on: bool = True) -> np.ndarray:
+    """bf16 [..., d] -> rotated fp64 [..., d] (on=False: fp64 as given, reading V0)."""
+    return hadamard.fwht(bf16_to_f64(bits)) if on else bf16_to_f64(bits)
 
 
-def encode_keys(k_bits: np.ndarray, tab: Tables, window: int = 128):
+def encode_keys(k_bits: np.ndarray, tab: Tables, window: int = 128, rotate_on: bool = True):
     """Keys [B, T, H, d] (bf16 bits) -> (records [B, H, T, C],
     mean_q int8 [B, H, T/W, d], mean_scale fp16 [B, H, T/W], sym [B, H, T, d])."""
     B, T, H, d = k_bits.shape
-    x, mq, ms = _key_streams(k_bits, window)
+    x, mq, ms = _key_streams(k_bits, window, rotate_on)
     recs, syms, _, _, _ = encode_streams(x.reshape(B * H * T, d), tab)
     C = tab.record_bytes
     return (recs.reshape(B, H, T, C), mq, ms, syms.reshape(B, H, T, d))
 
 
-def encode_values(v_bits: np.ndarray, tab: Tables):
+def encode_values(v_bits: np.ndarray, tab: Tables, rotate_on: bool = True):
     """Values [B, T, H, d] (bf16 bits) -> (records [B, H, T, C], sym)."""
     B, T, H, d = v_bits.shape
-    x = rotate(v_bits).transpose(0, 2, 1, 3).reshape(B * H * T, d)
+    x = rotate(v_bits, rotate_on).transpose(0, 2, 1, 3).reshape(B * H * T, d)
     recs, syms, _, _, _ = encode_streams(x, tab)
     return recs.reshape(B, H, T, tab.record_bytes), syms.reshape(B, H, T, d)
 
@@ -120,13 +124,13 @@ def decode_records(records: np.ndarray, tab: Tables, n: int):
     return (sym.reshape(*lead, n), s16.reshape(lead), o16.reshape(lead), ok.reshape(lead))
 
 
-def _key_streams(k_bits: np.ndarray, window: int):
+def _key_streams(k_bits: np.ndarray, window: int, rotate_on: bool = True):
     """Rotated keys minus their dequantized window means, [B, H, T, d],
     with the INT8 means and their fp16 scales."""
     B, T, H, d = k_bits.shape
     if T % window:
         raise ValueError("token count must be a multiple of the mean window")
-    y = rotate(k_bits).transpose(0, 2, 1, 3)                     # [B, H, T, d]
+    y = rotate(k_bits, rotate_on).transpose(0, 2, 1, 3)          # [B, H, T, d]
     nw = T // window
     yw = y.reshape(B, H, nw, window, d)
     mu = kmean.window_mean(yw)
@@ -137,7 +141,7 @@ def _key_streams(k_bits: np.ndarray, window: int):
     return (yw - mu_hat[:, :, :, None, :]).reshape(B, H, T, d), mq, ms
 
 
-def encode_keys_tokenwise(k_bits: np.ndarray, tab: Tables, window: int = 128):
+def encode_keys_tokenwise(k_bits: np.ndarray, tab: Tables, window: int = 128, rotate_on: bool = True):
     """Keys [B, T, H, d] -> one stream of n = H d values per token (reading K2).
 
     Returns (records [B, T, C], mean_q int8 [B, H, T/W, d],
@@ -146,18 +150,18 @@ def encode_keys_tokenwise(k_bits: np.ndarray, tab: Tables, window: int = 128):
     B, T, H, d = k_bits.shape
     if tab.n != H * d:
         raise ValueError("the table's stream length must be H * d")
-    x, mq, ms = _key_streams(k_bits, window)
+    x, mq, ms = _key_streams(k_bits, window, rotate_on)
     x = x.transpose(0, 2, 1, 3).reshape(B * T, H * d)
     recs, syms, _, _, _ = encode_streams(x, tab)
     return recs.reshape(B, T, tab.record_bytes), mq, ms, syms.reshape(B, T, H * d)
 
 
-def encode_values_tokenwise(v_bits: np.ndarray, tab: Tables):
+def encode_values_tokenwise(v_bits: np.ndarray, tab: Tables, rotate_on: bool = True):
     """Values [B, T, H, d] -> (records [B, T, C], sym [B, T, H d]) (reading K2)."""
     B, T, H, d = v_bits.shape
     if tab.n != H * d:
         raise ValueError("the table's stream length must be H * d")
-    x = rotate(v_bits).reshape(B * T, H * d)
+    x = rotate(v_bits, rotate_on).reshape(B * T, H * d)
     recs, syms, _, _, _ = encode_streams(x, tab)
     return recs.reshape(B, T, tab.record_bytes), syms.reshape(B, T, H * d)
 

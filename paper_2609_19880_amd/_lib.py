@@ -45,7 +45,7 @@ class DqError(RuntimeError):
 class _Config(ctypes.Structure):
     _fields_ = [("head_dim", ctypes.c_int32), ("levels", ctypes.c_int32),
                 ("precision_bits", ctypes.c_int32), ("record_bytes", ctypes.c_int32),
-                ("alpha", ctypes.c_double)]
+                ("alpha", ctypes.c_double), ("prerotated", ctypes.c_int32)]
 
 
 class _Info(ctypes.Structure):
@@ -146,8 +146,9 @@ class TableInfo:
     expected_max: float
 
 
-def _cfg(head_dim, levels, precision_bits, record_bytes, alpha) -> _Config:
-    return _Config(int(head_dim), int(levels), int(precision_bits), int(record_bytes), float(alpha))
+def _cfg(head_dim, levels, precision_bits, record_bytes, alpha, prerotated=False) -> _Config:
+    return _Config(int(head_dim), int(levels), int(precision_bits), int(record_bytes), float(alpha),
+                   1 if prerotated else 0)
 
 
 def _info(i: _Info) -> TableInfo:
@@ -177,13 +178,18 @@ class Tables:
     """Owner of a dq_tables handle (host + device copy on the current device)."""
 
     def __init__(self, head_dim: int, levels: int, precision_bits: int, record_bytes: int,
-                 alpha: float):
+                 alpha: float, prerotated: bool = False):
+        """prerotated: the tensor arrives already in the rotated basis (values
+        whose rotation is folded into the projection weights): no online
+        Hadamard in the encoder, and decode attention leaves the query (keys)
+        or the output (values) in that basis."""
         self.head_dim = int(head_dim)
         self.levels = int(levels)
         self.precision_bits = int(precision_bits)
         self.record_bytes = int(record_bytes)
         self.alpha = float(alpha)
-        cfg = _cfg(head_dim, levels, precision_bits, record_bytes, alpha)
+        self.prerotated = bool(prerotated)
+        cfg = _cfg(head_dim, levels, precision_bits, record_bytes, alpha, prerotated)
         handle = ctypes.c_void_p()
         info = _Info()
         self._handle = None
@@ -205,8 +211,8 @@ class Tables:
 
 
 def dq_build_tables(head_dim: int, levels: int, precision_bits: int, record_bytes: int,
-                    alpha: float) -> Tables:
-    return Tables(head_dim, levels, precision_bits, record_bytes, alpha)
+                    alpha: float, prerotated: bool = False) -> Tables:
+    return Tables(head_dim, levels, precision_bits, record_bytes, alpha, prerotated)
 
 
 def smallest_feasible_alpha(head_dim: int, levels: int, precision_bits: int, record_bytes: int,

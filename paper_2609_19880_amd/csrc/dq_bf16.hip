@@ -54,6 +54,7 @@ __global__ __launch_bounds__(kThreads) void bf16_partial_kernel(B16Args a) {
         a.ws_hdr[0] = a.chunk;
         a.ws_hdr[1] = a.nchunks;
         a.ws_hdr[2] = 0;
+        a.ws_hdr[3] = 1;          // partials are stored rotated (H acc)
     }
     const int T = max(0, min(a.seq_lens[b], a.t_cap));
     const int start = c * a.chunk;

@@ -133,7 +133,9 @@ struct AttnArgs {
     const uint8_t* vrec;
     const int32_t* seq_lens;
     float scale_log2;            // softmax_scale * log2(e) / d
-    int32_t* ws_hdr;             // [0] chunk, [1] chunk count NC, [2] residual slots written
+    int32_t* ws_hdr;             // [0] chunk, [1] chunk count NC, [2] residual slots written,
+                                 // [3] 1 if the merge rotates the output back (values rotated online)
+    int rot_q, rot_out;          // keys / values rotated online (tables not prerotated)
     float* ws_m;                 // [B][Hq][NC + kResSlots]   (slots NC..: the residual window)
     float* ws_l;                 // [B][Hq][NC + kResSlots]
     float* ws_acc;               // [B][Hq][NC + kResSlots][d]
@@ -246,6 +248,7 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
         a.ws_hdr[0] = a.chunk;
         a.ws_hdr[1] = a.nchunks;
         a.ws_hdr[2] = 0;          // set by the residual kernel when it runs
+        a.ws_hdr[3] = a.rot_out;
     }
     const int T = min(a.seq_lens[b], a.t_cap);
     const int start = c * a.chunk;
@@ -254,6 +257,19 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     const int Ck = RWK ? 4 * RWK : a.tk.C, Cv = RWV ? 4 * RWV : a.tv.C, CWk = Ck / 4, CWv = Cv / 4;
     bool bad_page = false;
 
+
+    // records of the wavefront's first tile, requested before the prologue so
+    // that their latency overlaps it; each later tile's records are loaded
+    // while the wavefront decodes the one before (up to 4 query heads per KV
+    // head; with 8 the registers go to accumulators unless the workgroup has
+    // at most 8 wavefronts)
+    constexpr bool kPrefetch = HG == 1 || WMAX <= 8;
+    uint32_t rk[kMaxRecDwords], rv[kMaxRecDwords];
+    if (kPrefetch && wave < ntiles) {
+        const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, start + wave * kTile, bad_page) + lane;
+        load_record(rk, a.krec, tok, CWk);
+        load_record(rv, a.vrec, tok, CWv);
+    }
 
     // ---- prologue: tables, rotated query, its digits, q . mu per window
     if (!FIXED) {
@@ -274,7 +290,7 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     float* qmu = reinterpret_cast<float*>(smem + L.qmu);
     uint8_t* qlimb = smem + L.qlimb;
     const int hq0 = h * G;
-    rotate_query_heads(a.q + ((int64_t)b * a.Hq + hq0) * kD, G, GP, wave, L.nw, lane, qt, qscale, qsum);
+    rotate_query_heads(a.q + ((int64_t)b * a.Hq + hq0) * kD, G, GP, wave, L.nw, lane, qt, qscale, qsum, a.rot_q);
     __syncthreads();
     for (int i = tid; i < GP * kD; i += nthr) {
         const int g = i / kD, j = i % kD;
@@ -358,16 +374,6 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
         for (int cb = 0; cb < 4; ++cb) acc[0][hg][cb] = acc[1][hg][cb] = 0.f;
     bool corrupt = false;
 
-    // records of the wavefront's next tile are loaded while it decodes this one
-    // (up to 4 query heads per KV head; with 8 the registers go to accumulators
-    // unless the workgroup has at most 8 wavefronts)
-    constexpr bool kPrefetch = HG == 1 || WMAX <= 8;
-    uint32_t rk[kMaxRecDwords], rv[kMaxRecDwords];
-    if (kPrefetch && wave < ntiles) {
-        const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, start + wave * kTile, bad_page) + lane;
-        load_record(rk, a.krec, tok, CWk);
-        load_record(rv, a.vrec, tok, CWv);
-    }
     for (int tile = wave; tile < ntiles; tile += L.nw) {
         const int t_base = start + tile * kTile;
         const int t = t_base + lane;
@@ -677,6 +683,10 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
             l += lv[u] * e;
         }
     }
+    if (!ws_hdr[3]) {          // values were coded in the caller's basis
+        dst[j] = acc / l;
+        return;
+    }
     o[j] = acc / l;
     __syncthreads();
     // inverse rotation of the value basis: H v / d
@@ -721,8 +731,10 @@ struct ResArgs {
 // start (one memory round trip); then the logits of the G query heads, the
 // softmax statistics of the part, the weighted sum of its raw values, and the
 // rotation H of that sum so that the merge's inverse rotation H / d returns it
-// (H H = d I).  The result is one more split-K partial, in slot NC + i; a part
-// without tokens writes m = -inf and zeros.
+// (H H = d I); without that rotation when the values were coded in the
+// caller's basis (the merge then leaves the output as it is).  The result is
+// one more split-K partial, in slot NC + i; a part without tokens writes
+// m = -inf and zeros.
 __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
     __shared__ __align__(16) float qs[kMaxGroup][kD];
     __shared__ float sc[kMaxGroup][kResPart];
@@ -730,7 +742,7 @@ __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
     __shared__ float stat[2][kMaxGroup];
     const int part = blockIdx.x, h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
     const int lane = tid & (kWave - 1), wave = tid / kWave;
-    const int G = a.G, NC = a.ws_hdr[1];
+    const int G = a.G, NC = a.ws_hdr[1], rotate = a.ws_hdr[3];
     if ((part | h | b) == 0 && tid == 0) a.ws_hdr[2] = kResSlots;
     const int r = max(0, min(a.res_lens[b], a.r_cap));
     const int ps = (r + kResSlots - 1) / kResSlots;
@@ -858,14 +870,19 @@ __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
             v0 += pq[k][g][lane];
             v1 += pq[k][g][lane + 64];
         }
-        for (int hh = 1; hh < 64; hh <<= 1) {
-            const float p0 = __shfl_xor(v0, hh), p1 = __shfl_xor(v1, hh);
-            v0 = (lane & hh) ? p0 - v0 : v0 + p0;
-            v1 = (lane & hh) ? p1 - v1 : v1 + p1;
+        float r0 = v0, r1 = v1;
+        if (rotate) {
+            for (int hh = 1; hh < 64; hh <<= 1) {
+                const float p0 = __shfl_xor(v0, hh), p1 = __shfl_xor(v1, hh);
+                v0 = (lane & hh) ? p0 - v0 : v0 + p0;
+                v1 = (lane & hh) ? p1 - v1 : v1 + p1;
+            }
+            r0 = v0 + v1;
+            r1 = v0 - v1;
         }
         const int64_t slot = slot0 + (int64_t)g * (NC + kResSlots);
-        a.ws_acc[slot * kD + lane] = v0 + v1;
-        a.ws_acc[slot * kD + lane + 64] = v0 - v1;
+        a.ws_acc[slot * kD + lane] = r0;
+        a.ws_acc[slot * kD + lane + 64] = r1;
         if (lane == 0) {
             a.ws_m[slot] = stat[0][g];
             a.ws_l[slot] = stat[1][g];
@@ -1089,7 +1106,10 @@ int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pag
     a.kms = kms;
     a.vrec = vrec;
     a.seq_lens = seq_lens;
-    a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
+    a.rot_q = tk->cfg.prerotated ? 0 : 1;
+    a.rot_out = tv->cfg.prerotated ? 0 : 1;
+    // the rotated query and key meet with a factor d (H H = d I)
+    a.scale_log2 = scale * 1.4426950408889634f / (a.rot_q ? (float)kD : 1.0f);
     const int64_t slots = ws_slots_used > 0 ? ws_slots_used : plan.slots_max;
     a.ws_hdr = static_cast<int32_t*>(ws);
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
@@ -1130,6 +1150,7 @@ int launch_attention_fixed_partial(const Pages& pg, const uint16_t* q, int32_t B
     a.kms = kms;
     a.vrec = vrec;
     a.seq_lens = seq_lens;
+    a.rot_q = a.rot_out = 1;
     a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
     a.ws_hdr = static_cast<int32_t*>(ws);
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);

@@ -82,20 +82,22 @@ __device__ __forceinline__ double fold_sum(const double (&v)[VPL]) {
     return s;
 }
 
+// rotate = 0: the input is already in the rotated basis (prerotated tables).
 template <int VPL>
-__device__ __forceinline__ void load_rotated(const uint16_t* src, double (&v)[VPL], int lane) {
+__device__ __forceinline__ void load_rotated(const uint16_t* src, double (&v)[VPL], int lane, int rotate) {
 #pragma unroll
     for (int k = 0; k < VPL; ++k) v[k] = (double)bf16_to_f32(src[lane + kWave * k]);
-    fwht_wave<VPL>(v, lane);
+    if (rotate) fwht_wave<VPL>(v, lane);
 }
 
 // Per-token stream (head_dim 128): head g's channels c = lane + 64 i are
 // elements k = 2 g + i, each head rotated on its own.
 template <int VPL>
-__device__ __forceinline__ void load_token_rotated(const uint16_t* src, int64_t sh, double (&v)[VPL], int lane) {
+__device__ __forceinline__ void load_token_rotated(const uint16_t* src, int64_t sh, double (&v)[VPL], int lane,
+                                                   int rotate) {
 #pragma unroll
     for (int k = 0; k < VPL; ++k) v[k] = (double)bf16_to_f32(src[(int64_t)(k / 2) * sh + lane + kWave * (k % 2)]);
-    fwht_wave<VPL, 2>(v, lane);
+    if (rotate) fwht_wave<VPL, 2>(v, lane);
 }
 
 struct DriftCtx {
@@ -314,7 +316,7 @@ __global__ __launch_bounds__(kWave) void key_mean_kernel(const uint16_t* __restr
                                                          int t0, int t_cap, Pages pg,
                                                          int8_t* __restrict__ mean_q,
                                                          uint16_t* __restrict__ mean_scale,
-                                                         uint32_t* status) {
+                                                         uint32_t* status, int rotate) {
     constexpr int n = kWave * VPL;
     const int w = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int lane = threadIdx.x;
@@ -325,7 +327,7 @@ __global__ __launch_bounds__(kWave) void key_mean_kernel(const uint16_t* __restr
     const int tw = w * DQ_MEAN_WINDOW;
     for (int t = 0; t < DQ_MEAN_WINDOW; ++t) {
         double v[VPL];
-        load_rotated<VPL>(base + (int64_t)(tw + t) * st, v, lane);
+        load_rotated<VPL>(base + (int64_t)(tw + t) * st, v, lane, rotate);
 #pragma unroll
         for (int k = 0; k < VPL; ++k) acc[k] = acc[k] + v[k];
     }
@@ -370,6 +372,7 @@ struct EncArgs {
     const int8_t* mean_q;        // NULL for values
     const uint16_t* mean_scale;
     uint32_t* status;
+    int rotate;                  // 0: the input is already in the rotated basis
 };
 
 // x = rotated stream of cache token t minus the dequantized window mean (keys).
@@ -379,7 +382,7 @@ __device__ __forceinline__ void stream_values(const EncArgs& a, int b, int h, in
                                               double (&x)[VPL], int lane) {
     const int64_t ti = t - a.t0;   // position in the input
     if (TOK) {
-        load_token_rotated<VPL>(a.kv + (int64_t)b * a.sb + ti * a.st, a.sh, x, lane);
+        load_token_rotated<VPL>(a.kv + (int64_t)b * a.sb + ti * a.st, a.sh, x, lane, a.rotate);
         if (a.mean_q) {
             bool bad = false;      // (a bad entry reads page 0; the record write then skips it)
 #pragma unroll
@@ -393,7 +396,7 @@ __device__ __forceinline__ void stream_values(const EncArgs& a, int b, int h, in
         }
         return;
     }
-    load_rotated<VPL>(a.kv + (int64_t)b * a.sb + ti * a.st + (int64_t)h * a.sh, x, lane);
+    load_rotated<VPL>(a.kv + (int64_t)b * a.sb + ti * a.st + (int64_t)h * a.sh, x, lane, a.rotate);
     if (a.mean_q) {
         constexpr int n = kWave * VPL;
         bool bad = false;          // (a bad entry reads page 0; the record write then skips it)
@@ -696,12 +699,13 @@ int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int
     const bool tok = token_stride > 0;
     const int n = tab->cfg.head_dim;
     const int vpl = n / kWave;
+    const int rotate = tab->cfg.prerotated ? 0 : 1;
     if (mean_q) {
         dim3 grid(n_new / DQ_MEAN_WINDOW, H, B);
         switch (tok ? kD / kWave : vpl) {
-            case 1: key_mean_kernel<1><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
-            case 2: key_mean_kernel<2><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
-            case 4: key_mean_kernel<4><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
+            case 1: key_mean_kernel<1><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status, rotate); break;
+            case 2: key_mean_kernel<2><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status, rotate); break;
+            case 4: key_mean_kernel<4><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status, rotate); break;
             default: return DQ_ERR_INVALID_ARG;
         }
         if (int rc = hip_check("key_mean launch", hipGetLastError())) return rc;
@@ -722,6 +726,7 @@ int launch_encode(const dq_tables* tab, const Pages& pg, const uint16_t* kv, int
     a.mean_q = mean_q;
     a.mean_scale = mean_scale;
     a.status = status;
+    a.rotate = rotate;
     const int ns = enc_streams(tok);
     const size_t smem = sizeof(double) * DQ_MAX_LEVELS + sizeof(int32_t) * DQ_MAX_LEVELS +
                         sizeof(float) * kLambdaSteps + sizeof(int64_t) * ns +
@@ -775,9 +780,9 @@ int launch_encode_fixed(int32_t n, int32_t record_bytes, const Pages& pg, const 
     if (mean_q) {
         dim3 grid(n_new / DQ_MEAN_WINDOW, H, B);
         switch (vpl) {
-            case 1: key_mean_kernel<1><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
-            case 2: key_mean_kernel<2><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
-            default: key_mean_kernel<4><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status); break;
+            case 1: key_mean_kernel<1><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status, 1); break;
+            case 2: key_mean_kernel<2><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status, 1); break;
+            default: key_mean_kernel<4><<<grid, kWave, 0, stream>>>(kv, sb, st, sh, H, t0, t_cap, pg, mean_q, mean_scale, status, 1); break;
         }
         if (int rc = hip_check("key_mean launch", hipGetLastError())) return rc;
     }
@@ -799,6 +804,7 @@ int launch_encode_fixed(int32_t n, int32_t record_bytes, const Pages& pg, const 
     a.mean_q = mean_q;
     a.mean_scale = mean_scale;
     a.status = status;
+    a.rotate = 1;
     const size_t smem = sizeof(double) * DQ_MAX_LEVELS + sizeof(int32_t) * DQ_MAX_LEVELS +
                         sizeof(float) * kLambdaSteps + sizeof(int64_t) * kEncStreams +
                         2 * sizeof(uint16_t) * kEncStreams + sizeof(int32_t) * kEncStreams +

@@ -96,6 +96,7 @@ int validate(const dq_config* c) {
     if (c->record_bytes < 9 || c->record_bytes > 2 * n + 8) return DQ_ERR_INVALID_ARG;
     if (!(c->alpha >= 1.0) || !(c->alpha <= 64.0)) return DQ_ERR_INVALID_ARG;
     if ((c->levels / 2) > (1 << (c->precision_bits - 1))) return DQ_ERR_INVALID_ARG;
+    if (c->prerotated != 0 && c->prerotated != 1) return DQ_ERR_INVALID_ARG;
     return DQ_OK;
 }
 

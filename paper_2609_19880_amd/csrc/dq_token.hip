@@ -78,7 +78,8 @@ struct TokArgs {
     int k_stride, v_stride;       // bytes per token record (multiples of 16)
     Pages pg;                     // block table of a paged cache (bt null: contiguous)
     const int32_t* seq_lens;
-    float scale_log2;             // softmax_scale * log2(e) / d
+    float scale_log2;             // softmax_scale * log2(e) / d (/ 1 for prerotated keys)
+    int rot_q, rot_out;           // keys / values rotated online (tables not prerotated)
     int32_t* ws_hdr;
     float* ws_m;
     float* ws_l;
@@ -196,6 +197,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
         a.ws_hdr[0] = a.chunk;
         a.ws_hdr[1] = a.nchunks;
         a.ws_hdr[2] = 0;          // set by the residual kernel when it runs
+        a.ws_hdr[3] = a.rot_out;  // the merge rotates the output back
     }
     const int T = min(a.seq_lens[b], a.t_cap);
     const int start = c * a.chunk;
@@ -217,7 +219,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
     float* qsum = reinterpret_cast<float*>(smem + L.qsum);
     float* qmu = reinterpret_cast<float*>(smem + L.qmu);
     uint8_t* qlimb = smem + L.qlimb;
-    rotate_query_heads(a.q + (int64_t)b * Hq * kD, Hq, Hq, wave, L.nw, lane, qt, qscale, qsum);
+    rotate_query_heads(a.q + (int64_t)b * Hq * kD, Hq, Hq, wave, L.nw, lane, qt, qscale, qsum, a.rot_q);
     __syncthreads();
     // digits of head slot r of KV head h at ((h * 32 + j / 4) * 4 + r) * 16 + j % 4 (+4, +8)
     for (int i = tid; i < Hkv * 4 * kD; i += nthr) {
@@ -595,7 +597,9 @@ int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, con
     a.v_stride = v_stride;
     a.pg = pg;
     a.seq_lens = seq_lens;
-    a.scale_log2 = scale * 1.4426950408889634f / (float)kD;
+    a.rot_q = tk->cfg.prerotated ? 0 : 1;
+    a.rot_out = tv->cfg.prerotated ? 0 : 1;
+    a.scale_log2 = scale * 1.4426950408889634f / (a.rot_q ? (float)kD : 1.0f);
     const int64_t slots = ws_slots(B, Hq, t_cap);
     a.ws_hdr = static_cast<int32_t*>(ws);
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);

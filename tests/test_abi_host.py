@@ -100,3 +100,19 @@ def test_workspace_size_grows_with_context():
     b = dq.dq_decode_workspace_bytes(16, 32, 8, 65536)
     assert 0 < a <= b
     assert dq.dq_decode_workspace_bytes(0, 32, 8, 4096) == 0
+
+
+def test_prerotated_flag_is_validated_and_leaves_tables_unchanged():
+    import ctypes
+    lib = dq._lib
+    info = lib._Info()
+    for flag, rc in ((0, dq.DQ_OK), (1, dq.DQ_OK), (2, dq.DQ_ERR_INVALID_ARG), (-1, dq.DQ_ERR_INVALID_ARG)):
+        cfg = lib._Config(128, 6, 12, 36, 1.4, flag)
+        assert lib._lib.dq_compute_tables(ctypes.byref(cfg), ctypes.byref(info), None, None, None, None,
+                                          None) == rc
+    a = dq.dq_compute_tables(128, 6, 12, 36, 1.4)[1]
+    cfg = lib._Config(128, 6, 12, 36, 1.4, 1)
+    freq = np.zeros(6, np.int32)
+    assert lib._lib.dq_compute_tables(ctypes.byref(cfg), ctypes.byref(info), freq.ctypes.data, None, None, None,
+                                      None) == dq.DQ_OK
+    assert np.array_equal(freq, a["freq"])
