@@ -107,13 +107,17 @@ def workload(name: str, variant: str = "paper", bpe: float | None = None) -> Wor
         # values per token, 331 B / 231 B containers (+ the 4-byte s, o header)
         # with 8 / 6 levels at alpha 1.4, and the 2^8-entry table of Sec. 3
         k, v = Coding(8, 335, 1.4, precision=8, n=1024), Coding(6, 235, 1.4, precision=8, n=1024)
+        if name == "b32_t32k_g8_tok":
+            # the wide-GQA shape (64 query / 8 KV heads, 8 outlier channels per
+            # key head) with the per-token coding
+            return Workload(name, 32, 32768, 64, 8, 8, k, v, streams="token")
         B, T = {"b1_t4k_tok": (1, 4096), "b16_t32k_tok": (16, 32768)}[name]
         return Workload(name, B, T, 32, 8, 4, k, v, streams="token")
     raise KeyError(name)
 
 
 WORKLOADS = ("b1_t4k", "b16_t32k", "b1_t128k", "b64_t8k", "b32_t32k_g8")
-TOKEN_WORKLOADS = ("b1_t4k_tok", "b16_t32k_tok")
+TOKEN_WORKLOADS = ("b1_t4k_tok", "b16_t32k_tok", "b32_t32k_g8_tok")
 
 
 def key_stats(seed: int, heads: int, d: int, outliers: int):

@@ -328,7 +328,7 @@ int dq_decode_attention_paged_partial(const dq_tables* k_tables, const dq_tables
  *   (rANS-decoded once per token and consumed one KV head at a time), into the
  *   workspace of dq_decode_workspace_bytes; finish with
  *   dq_decode_attention_merge (and optionally add a residual window with
- *   dq_decode_attention_residual before it).  q_heads / kv_heads <= 4;
+ *   dq_decode_attention_residual before it).  q_heads / kv_heads <= 8;
  *   k_mean_q / k_mean_scale as for dq_decode_attention.  Corrupt records set
  *   DQ_STATUS_CORRUPT.
  * Return DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_WORKSPACE or DQ_ERR_HIP.

@@ -469,7 +469,7 @@ static int token_partial(const dq_tables* tk, const dq_tables* tv, const dq::Pag
     if (!table_args_ok(tk) || !table_args_ok(tv)) return DQ_ERR_INVALID_ARG;
     if (Hkv != 1 && Hkv != 2 && Hkv != 4 && Hkv != 8) return DQ_ERR_INVALID_ARG;
     if (tk->cfg.head_dim != 128 * Hkv || tv->cfg.head_dim != 128 * Hkv) return DQ_ERR_INVALID_ARG;
-    if (B <= 0 || B > 65535 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 4) return DQ_ERR_INVALID_ARG;
+    if (B <= 0 || B > 65535 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 8) return DQ_ERR_INVALID_ARG;
     if (t_cap <= 0 || t_cap % DQ_MEAN_WINDOW) return DQ_ERR_INVALID_ARG;
     if (!q || !k_records || !k_mean_q || !k_mean_scale || !v_records || !seq_lens) return DQ_ERR_INVALID_ARG;
     if (!std::isfinite(scale)) return DQ_ERR_INVALID_ARG;

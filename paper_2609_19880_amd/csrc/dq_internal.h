@@ -171,7 +171,7 @@ int64_t attention_plan_slots(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_cap);
 int no_alloc_scratch(void** out);
 constexpr int kMaxDevices = 64;
 
-// Per-token streams over Hkv heads (table n = 128 Hkv, G = Hq / Hkv <= 4),
+// Per-token streams over Hkv heads (table n = 128 Hkv, G = Hq / Hkv <= 8),
 // records [B][t_cap][stride] in 64-token tiles, or token rows of pool pages
 // through pg; same workspace as launch_attention_partial.
 int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, const Pages& pg, const uint16_t* q,

@@ -10,8 +10,9 @@
 // (Eq. fold-key, on the matrix cores as the levels appear), the online
 // softmax update and P . v (Eq. fold-value, on the 16x16x32 matrix cores);
 // the chains then continue into the next head with their state.  All query
-// heads' accumulators live in the wavefront: per KV head, lane l holds query
-// head slot l / 16 for 8 of the 128 channels.
+// heads' accumulators live in the wavefront: per KV head and group of 4
+// query-head slots (one group for up to 4 query heads per KV head, two for up
+// to 8), lane l holds slot l / 16 of the group for 8 of the 128 channels.
 //
 // Record bytes.  Records (C bytes in S-byte slots, S a multiple of 16) are
 // stored per 64-token tile with 8-byte chunks outermost: chunk c of the tile's
@@ -43,9 +44,11 @@ namespace {
 constexpr int kD = 128;
 constexpr int kTile = 64;
 constexpr int kVSlice = 64;
-constexpr int kVRow = 80;                // bytes per row of the value and weight tiles (64 + pad)
+constexpr int kVRowT = 80;               // bytes per token row of the value tile (64 channels + pad)
 constexpr int kMaxLds = 160 * 1024;
-constexpr int kTokWaves = 12;             // wavefronts per workgroup at most
+// wavefronts per workgroup at most: 12 with up to 4 query heads per KV head
+// (168 VGPRs), 8 with up to 8 (the accumulators of 64 query heads take 128)
+__host__ __device__ constexpr int tok_waves(int HG) { return HG == 1 ? 12 : 8; }
 constexpr int kTokMaxHeads = 8;           // KV heads per stream (n <= 1024)
 constexpr int kTokMaxChunk = 2048;        // bounds the per-window q . mu table
 constexpr int kRingRow = 4 * kTile;       // bytes per ring row: one dword per lane
@@ -56,14 +59,14 @@ constexpr int kGroups = kD / 4;           // 4-step groups per head
 struct TokLayout {
     int nw;
     int lut_k, lut_v;   // 8-byte tables (the same offset when K and V share one)
-    int qlimb;          // [H_kv][32 groups][4 heads] x 16 B (three digit words)
+    int qlimb;          // [H_kv][32 groups][4 HG slots] x 16 B (three digit words)
     int qscale, qsum;   // float [H_q]
     int qmu;            // float [windows][H_q]
     int waves;          // first wavefront region
     int wave_stride;
     int ring_k, ring_v; // per wavefront
-    int vtile;          // [64 channels][kVRow]: levels of 64 tokens
-    int plimb;          // [4 heads][4 rows][kVRow]: weight digits 0..2 of 64 tokens, row 3 zero
+    int vtile;          // [64 tokens][kVRowT]: levels of a 64-channel slice
+    int plimb;          // [HG][64 tokens][16]: weight digits, byte 4 slot + digit (digit 3 zero)
     int total;
 };
 
@@ -161,19 +164,11 @@ __device__ __forceinline__ void refill2(uint32_t pbk, uint32_t& nck, uint32_t& t
     }
 }
 
-// P . v on the 16x16x32 int8 matrix cores: rows are (query-head slot,
-// digit), K is 32 tokens, columns 16 channels.  Lane l gives row l mod 16 and
-// tokens 8 (l / 16) .. + 7 of A, column l mod 16 and the same tokens of B,
-// and receives rows 4 (l / 16) .. + 3 of column l mod 16: one slot's three
-// digit sums (and the zero row) for one channel.
-__device__ __forceinline__ v4i mfma_pv(uint64_t a, uint64_t b, v4i c) {
-    return __builtin_amdgcn_mfma_i32_16x16x32_i8((long)a, (long)b, c, 0, 0, 0);
-}
-
-// Accumulators of channel block cb of slice s: one vector acc[s][cb]
-// over the KV heads, for query-head slot l / 16 and channel 64 s + 16 cb +
-// l mod 16 in lane l.  The head loop is not unrolled, so the vectors are
-// rotated by one element per head and the current head is always element 0.
+// Accumulators of channel block cb of slice s and slot group hg: one vector
+// acc[s][hg][cb] over the KV heads, for query-head slot 4 hg + l / 16 and
+// channel 64 s + 16 cb + l mod 16 in lane l.  The head loop is not unrolled,
+// so the vectors are rotated by one element per head and the current head is
+// always element 0.
 typedef float v8f __attribute__((ext_vector_type(kTokMaxHeads)));
 
 __device__ __forceinline__ v8f rot1(const v8f& v) { return v8f{v[1], v[2], v[3], v[4], v[5], v[6], v[7], v[0]}; }
@@ -185,8 +180,10 @@ __device__ __forceinline__ float lane_set(float v, int i, float x, int lane) { r
 
 // PAGED: records and key means through the block table; a separate
 // instantiation, so that the contiguous kernel carries none of its state.
-template <uint32_t LUTV, bool PAGED>
-__global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a) {
+// HG: groups of 4 query-head slots per KV head (1: G <= 4, 2: G <= 8).
+template <uint32_t LUTV, bool PAGED, int HG>
+__global__ __launch_bounds__(tok_waves(HG) * kWave) void attn_token_kernel(TokArgs a) {
+    constexpr int GS = 4 * HG;                 // query-head slots per KV head
     extern __shared__ __align__(16) uint8_t smem[];
     const TokLayout& L = a.L;
     const int G = a.G, Hkv = a.Hkv, Hq = a.Hq;
@@ -221,9 +218,9 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
     uint8_t* qlimb = smem + L.qlimb;
     rotate_query_heads(a.q + (int64_t)b * Hq * kD, Hq, Hq, wave, L.nw, lane, qt, qscale, qsum, a.rot_q);
     __syncthreads();
-    // digits of head slot r of KV head h at ((h * 32 + j / 4) * 4 + r) * 16 + j % 4 (+4, +8)
-    for (int i = tid; i < Hkv * 4 * kD; i += nthr) {
-        const int h = i / (4 * kD), r = (i / kD) % 4, j = i % kD;
+    // digits of head slot r of KV head h at ((h * 32 + j / 4) * GS + r) * 16 + j % 4 (+4, +8)
+    for (int i = tid; i < Hkv * GS * kD; i += nthr) {
+        const int h = i / (GS * kD), r = (i / kD) % GS, j = i % kD;
         const int g = h * G + r;
         int v = 0;
         if (r < G && qscale[g] > 0.f) {
@@ -232,7 +229,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
         }
         int d0, d1, d2;
         digits3(v, d0, d1, d2);
-        uint8_t* dst = qlimb + ((h * kGroups + j / 4) * 4 + r) * 16 + (j % 4);
+        uint8_t* dst = qlimb + ((h * kGroups + j / 4) * GS + r) * 16 + (j % 4);
         dst[0] = (uint8_t)d0;
         dst[4] = (uint8_t)d1;
         dst[8] = (uint8_t)d2;
@@ -275,26 +272,28 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
     const uint32_t ring_k = (uint32_t)(L.waves + wave * L.wave_stride + L.ring_k) + 4u * lane;
     const uint32_t ring_v = (uint32_t)(L.waves + wave * L.wave_stride + L.ring_v) + 4u * lane;
     uint8_t* vtile = wreg + L.vtile;
-    uint8_t* plimb = vtile + kVSlice * kVRow;   // the weight tile follows the value tile
-    // row 3 of each slot's weight digits stays zero (the prologue's query
-    // scratch overlapped it)
-    *reinterpret_cast<uint32_t*>(plimb + (4 * (lane >> 4) + 3) * kVRow + 4 * (lane & 15)) = 0u;
-    const int pslot = lane >> 4;                               // query-head slot of this lane's P . v sums
-    const int prow = (lane & 15) * kVRow + 8 * (lane >> 4);    // operand row and token offset of this lane
-    const uint32_t sel1 = (lane & 1) ? 0x03070105u : 0x06020400u;
-    const uint32_t sel2 = (lane & 2) ? 0x03020706u : 0x05040100u;
+    uint8_t* plimb = wreg + L.plimb;
+    // P . v: lane l serves slot l / 16 of each group and channel l % 16 of each
+    // 16-channel block; its tr8 reads start at token row 8 (l / 16) +
+    // (l % 16) / 2 of a 32-token block, byte 8 (l % 2) of the row's block
+    const int pslot = lane >> 4;
+    const uint32_t trow = (uint32_t)(8 * (lane >> 4) + ((lane & 15) >> 1));
+    const uint32_t a_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.plimb) + trow * 16 + 8 * (lane & 1);
+    const uint32_t b_lane = (uint32_t)(L.waves + wave * L.wave_stride + L.vtile) + trow * kVRowT + 8 * (lane & 1);
     const int pk3 = a.tk.p + 3, pv3 = a.tv.p + 3;
     const uint32_t mask8k = ((1u << a.tk.p) - 1u) << 3, mask8v = ((1u << a.tv.p) - 1u) << 3;
     const uint32_t last_k = (uint32_t)(a.k_stride / 8 - 1), last_v = (uint32_t)(a.v_stride / 8 - 1);
     const uint32_t endk = 8u * (uint32_t)a.tk.C, endv = 8u * (uint32_t)a.tv.C;
 
-    // running softmax state of query-head slot 4 h + r in lane 4 h + r
+    // running softmax state of query-head slot GS h + r in lane GS h + r
     float m_vec = -INFINITY, l_vec = 0.f, o_vec = 0.f;
-    v8f acc[2][4];
+    v8f acc[2][HG][4];
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
-        for (int cb = 0; cb < 4; ++cb) acc[s][cb] = v8f{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int hg = 0; hg < HG; ++hg)
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) acc[s][hg][cb] = v8f{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     bool corrupt = false;
     const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
 
@@ -333,10 +332,14 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
         asm volatile("" ::: "memory");
 
         for (int h = 0; h < Hkv; ++h) {
-            v4i dk[3] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
+            v4i dk[HG][3];
+#pragma unroll
+            for (int hg = 0; hg < HG; ++hg) dk[hg][0] = dk[hg][1] = dk[hg][2] = v4i{0, 0, 0, 0};
             uint32_t vlev[kGroups];
-            const uint8_t* qh = qlimb + (h * kGroups * 4 + (lane & 3)) * 16;
-            uint4 ql = *reinterpret_cast<const uint4*>(qh);   // digits of group 0; then one group ahead
+            const uint8_t* qh = qlimb + (h * kGroups * GS + (lane & 3)) * 16;
+            uint4 ql[HG];                               // digits of group 0; then one group ahead
+#pragma unroll
+            for (int hg = 0; hg < HG; ++hg) ql[hg] = *reinterpret_cast<const uint4*>(qh + hg * 4 * 16);
 #pragma unroll
             for (int grp = 0; grp < kGroups; ++grp) {
                 uint32_t k0s, k1s, k2s, k3s, v0s, v1s, v2s, v3s;
@@ -347,10 +350,14 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
                 const uint32_t lk = pack4(k0s, k1s, k2s, k3s);
                 vlev[grp] = pack4(v0s, v1s, v2s, v3s);
                 asm volatile("" : "+v"(vlev[grp]));
-                dk[0] = mfma(ql.x, lk, dk[0]);
-                dk[1] = mfma(ql.y, lk, dk[1]);
-                dk[2] = mfma(ql.z, lk, dk[2]);
-                if (grp + 1 < kGroups) ql = *reinterpret_cast<const uint4*>(qh + (grp + 1) * 4 * 16);
+#pragma unroll
+                for (int hg = 0; hg < HG; ++hg) {
+                    dk[hg][0] = mfma(ql[hg].x, lk, dk[hg][0]);
+                    dk[hg][1] = mfma(ql[hg].y, lk, dk[hg][1]);
+                    dk[hg][2] = mfma(ql[hg].z, lk, dk[hg][2]);
+                    if (grp + 1 < kGroups)
+                        ql[hg] = *reinterpret_cast<const uint4*>(qh + ((grp + 1) * GS + hg * 4) * 16);
+                }
                 if (grp & 1) {
                     refill2(pbk, nck, thrk, nk, ring_k, kr, last_k, pbv, ncv, thrv, nv, ring_v, vr, last_v);
                     refill2(pbk, nck, thrk, nk, ring_k, kr, last_k, pbv, ncv, thrv, nv, ring_v, vr, last_v);
@@ -359,14 +366,14 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
             }
 
             // ---- scores of the head's query heads and the online softmax
-            float corr[4], pscale[4];
-            int pint[4];
+            float corr[GS], pscale[GS];
+            int pint[GS];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
+            for (int r = 0; r < GS; ++r) {
                 const bool live = r < G;
                 const int g = live ? h * G + r : 0;       // slots past G take no query head
-                const int slot = h * 4 + r;
-                const float dot = combine(dk[0], dk[1], dk[2], r) * qscale[g];
+                const int slot = h * GS + r;
+                const float dot = combine(dk[r / 4][0], dk[r / 4][1], dk[r / 4][2], r % 4) * qscale[g];
                 const float score = (valid && live) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
                 const float tmax = wave_max_f32(score);
                 const float m_old = lane_get(m_vec, slot);
@@ -385,69 +392,73 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
                 const float inv = smax > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax) : 0.f;
                 pint[r] = min(4194304, (int)rintf(pw * inv));
             }
-            {
-                int dd[4][3];
+            // weight digits -> LDS, one 16-byte token row per slot group: byte
+            // 4 r + d holds digit d of slot r (byte 4 r + 3 stays zero)
+            float corr_l[HG], scale_l[HG];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) digits3(pint[r], dd[r][0], dd[r][1], dd[r][2]);
-                uint32_t wt[3];
+            for (int hg = 0; hg < HG; ++hg) {
+                uint32_t w[4];
 #pragma unroll
-                for (int d = 0; d < 3; ++d) {
-                    const uint32_t w = ((uint32_t)dd[0][d] & 0xFFu) | (((uint32_t)dd[1][d] & 0xFFu) << 8) |
-                                       (((uint32_t)dd[2][d] & 0xFFu) << 16) | ((uint32_t)dd[3][d] << 24);
-                    wt[d] = quad_transpose(w, sel1, sel2);
+                for (int r = 0; r < 4; ++r) {
+                    int d0, d1, d2;
+                    digits3(pint[4 * hg + r], d0, d1, d2);
+                    w[r] = ((uint32_t)d0 & 0xFFu) | (((uint32_t)d1 & 0xFFu) << 8) | (((uint32_t)d2 & 0xFFu) << 16);
                 }
-                // lane 4 q + i: slot i, tokens 4 q .. 4 q + 3, rows 4 i + digit
-                uint8_t* pw = plimb + (lane & 3) * 4 * kVRow + (lane >> 2) * 4;
-                *reinterpret_cast<uint32_t*>(pw) = wt[0];
-                *reinterpret_cast<uint32_t*>(pw + kVRow) = wt[1];
-                *reinterpret_cast<uint32_t*>(pw + 2 * kVRow) = wt[2];
+                *reinterpret_cast<uint4*>(plimb + hg * (kTile * 16) + lane * 16) = uint4{w[0], w[1], w[2], w[3]};
+                corr_l[hg] = pick4(corr + 4 * hg, pslot);
+                scale_l[hg] = pick4(pscale + 4 * hg, pslot);
             }
-            const float corr_l = pslot == 0 ? corr[0] : pslot == 1 ? corr[1] : pslot == 2 ? corr[2] : corr[3];
-            const float pscale_l =
-                pslot == 0 ? pscale[0] : pslot == 1 ? pscale[1] : pslot == 2 ? pscale[2] : pscale[3];
 
             // ---- P . v over two slices of 64 channels
-            uint64_t pa[2];
+            wave_sync();   // the weight rows are read by other lanes
+            uint64_t pa[HG][2];
+#pragma unroll
+            for (int hg = 0; hg < HG; ++hg)
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) pa[hg][kb] = lds_tr8(a_lane + hg * (kTile * 16) + kb * 32 * 16);
 #pragma unroll
             for (int sl = 0; sl < 2; ++sl) {
-                wave_sync();   // the previous slice / head is no longer read; the weights are written
+                if (sl) wave_sync();   // the first slice's value rows are no longer read
 #pragma unroll
-                for (int grp = 0; grp < kVSlice / 4; ++grp) {
-                    const uint32_t wt = quad_transpose(vlev[sl * (kVSlice / 4) + grp], sel1, sel2);
-                    *reinterpret_cast<uint32_t*>(vtile + (grp * 4 + (lane & 3)) * kVRow + (lane >> 2) * 4) = wt;
-                }
+                for (int q = 0; q < 4; ++q)
+                    *reinterpret_cast<uint4*>(vtile + lane * kVRowT + 16 * q) =
+                        uint4{vlev[16 * sl + 4 * q], vlev[16 * sl + 4 * q + 1], vlev[16 * sl + 4 * q + 2],
+                              vlev[16 * sl + 4 * q + 3]};
                 wave_sync();
-                if (sl == 0) {   // from the value tile's address: one base register for both tiles
-                    pa[0] = *reinterpret_cast<const uint64_t*>(vtile + prow + kVSlice * kVRow);
-                    pa[1] = *reinterpret_cast<const uint64_t*>(vtile + prow + kVSlice * kVRow + 32);
-                }
-                // all operands first, then four independent product chains
+                // all operands first, then the product chains
                 uint64_t vb[kVSlice / 16][2];
 #pragma unroll
                 for (int cb = 0; cb < kVSlice / 16; ++cb) {
-                    vb[cb][0] = *reinterpret_cast<const uint64_t*>(vtile + cb * 16 * kVRow + prow);
-                    vb[cb][1] = *reinterpret_cast<const uint64_t*>(vtile + cb * 16 * kVRow + prow + 32);
+                    vb[cb][0] = lds_tr8(b_lane + 16 * cb);
+                    vb[cb][1] = lds_tr8(b_lane + 32 * kVRowT + 16 * cb);
                 }
-                v4i dv[kVSlice / 16];
 #pragma unroll
-                for (int cb = 0; cb < kVSlice / 16; ++cb) dv[cb] = mfma_pv(pa[0], vb[cb][0], v4i{0, 0, 0, 0});
+                for (int hg = 0; hg < HG; ++hg) {
+                    v4i dv[kVSlice / 16];
 #pragma unroll
-                for (int cb = 0; cb < kVSlice / 16; ++cb) dv[cb] = mfma_pv(pa[1], vb[cb][1], dv[cb]);
+                    for (int cb = 0; cb < kVSlice / 16; ++cb) dv[cb] = mfma16(pa[hg][0], vb[cb][0], v4i{0, 0, 0, 0});
 #pragma unroll
-                for (int cb = 0; cb < kVSlice / 16; ++cb) {
-                    const float pv =
-                        ((float)dv[cb][2] * 65536.0f + (float)dv[cb][1] * 256.0f + (float)dv[cb][0]) * pscale_l;
-                    v8f t = acc[sl][cb];
-                    t[0] = t[0] * corr_l + pv;
-                    acc[sl][cb] = rot1(t);
+                    for (int cb = 0; cb < kVSlice / 16; ++cb) dv[cb] = mfma16(pa[hg][1], vb[cb][1], dv[cb]);
+#pragma unroll
+                    for (int cb = 0; cb < kVSlice / 16; ++cb) {
+                        const float pv =
+                            ((float)dv[cb][2] * 65536.0f + (float)dv[cb][1] * 256.0f + (float)dv[cb][0]) *
+                            scale_l[hg];
+                        v8f t = acc[sl][hg][cb];
+                        t[0] = t[0] * corr_l[hg] + pv;
+                        acc[sl][hg][cb] = rot1(t);
+                    }
                 }
             }
+            wave_sync();   // the next head rewrites the weight and value rows
         }
         for (int h = Hkv; h < kTokMaxHeads; ++h)
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int cb = 0; cb < 4; ++cb) acc[s][cb] = rot1(acc[s][cb]);
+                for (int hg = 0; hg < HG; ++hg)
+#pragma unroll
+                    for (int cb = 0; cb < 4; ++cb) acc[s][hg][cb] = rot1(acc[s][hg][cb]);
         // every stream ends at x = L having read no byte past its record
         corrupt |= valid && ((xk >> 3) != kRansL || pbk > endk);
         corrupt |= valid && ((xv >> 3) != kRansL || pbv > endv);
@@ -457,53 +468,56 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
 
     // ---- merge the wavefronts of the workgroup, one KV head at a time
     const int NC = a.nchunks;
-    float* mw = reinterpret_cast<float*>(smem);        // [nw][4]
-    float* lw = mw + L.nw * 4;                         // [nw][4]
-    float* aw = lw + L.nw * 4;                         // [nw][4][d]
+    float* mw = reinterpret_cast<float*>(smem);        // [nw][GS]
+    float* lw = mw + L.nw * GS;                        // [nw][GS]
+    float* aw = lw + L.nw * GS;                        // [nw][GS][d]
     for (int h = 0; h < Hkv; ++h) {
-        float av[2][4];
+        float av[2][HG][4];
 #pragma unroll
         for (int s = 0; s < 2; ++s)
 #pragma unroll
-            for (int cb = 0; cb < 4; ++cb) {
-                av[s][cb] = acc[s][cb][0];
-                acc[s][cb] = rot1(acc[s][cb]);
-            }
-        __syncthreads();   // LDS free (first head) / previous head merged
-        float ov4[4];
+            for (int hg = 0; hg < HG; ++hg)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int slot = h * 4 + r;
+                for (int cb = 0; cb < 4; ++cb) {
+                    av[s][hg][cb] = acc[s][hg][cb][0];
+                    acc[s][hg][cb] = rot1(acc[s][hg][cb]);
+                }
+        __syncthreads();   // LDS free (first head) / previous head merged
+        float ovs[GS];
+#pragma unroll
+        for (int r = 0; r < GS; ++r) {
+            const int slot = h * GS + r;
             const float mv = lane_get(m_vec, slot), lv = lane_get(l_vec, slot);
-            ov4[r] = lane_get(o_vec, slot);
+            ovs[r] = lane_get(o_vec, slot);
             if (lane == 0) {
-                mw[wave * 4 + r] = mv;
-                lw[wave * 4 + r] = lv;
+                mw[wave * GS + r] = mv;
+                lw[wave * GS + r] = lv;
             }
         }
-        {
-            const float ovt = pslot == 0 ? ov4[0] : pslot == 1 ? ov4[1] : pslot == 2 ? ov4[2] : ov4[3];
-            float* row = aw + (wave * 4 + pslot) * kD + (lane & 15);
+#pragma unroll
+        for (int hg = 0; hg < HG; ++hg) {
+            const float ovt = pick4(ovs + 4 * hg, pslot);
+            float* row = aw + (wave * GS + 4 * hg + pslot) * kD + (lane & 15);
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int cb = 0; cb < 4; ++cb) row[s * kVSlice + cb * 16] = av[s][cb] + ovt;
+                for (int cb = 0; cb < 4; ++cb) row[s * kVSlice + cb * 16] = av[s][hg][cb] + ovt;
         }
         __syncthreads();
         for (int i = tid; i < G * kD; i += nthr) {
             const int r = i / kD, j = i % kD;
             float M = -INFINITY;
-            for (int w = 0; w < L.nw; ++w) M = fmaxf(M, mw[w * 4 + r]);
-            float acc = 0.f, l = 0.f;
+            for (int w = 0; w < L.nw; ++w) M = fmaxf(M, mw[w * GS + r]);
+            float acc_o = 0.f, l = 0.f;
             for (int w = 0; w < L.nw; ++w) {
-                const float mv = mw[w * 4 + r];
+                const float mv = mw[w * GS + r];
                 if (mv == -INFINITY) continue;
                 const float e = exp2f(mv - M);
-                acc += aw[(w * 4 + r) * kD + j] * e;
-                l += lw[w * 4 + r] * e;
+                acc_o += aw[(w * GS + r) * kD + j] * e;
+                l += lw[w * GS + r] * e;
             }
             const int64_t slot = ((int64_t)b * Hq + h * G + r) * (NC + kResSlots) + c;
-            a.ws_acc[slot * kD + j] = acc;
+            a.ws_acc[slot * kD + j] = acc_o;
             if (j == 0) {
                 a.ws_m[slot] = M;
                 a.ws_l[slot] = l;
@@ -512,7 +526,7 @@ __global__ __launch_bounds__(kTokWaves * kWave) void attn_token_kernel(TokArgs a
     }
 }
 
-TokLayout tok_layout(int pk, int pv, bool shared_lut, int Hq, int Hkv, int chunk, int nw) {
+TokLayout tok_layout(int pk, int pv, bool shared_lut, int Hq, int Hkv, int chunk, int nw, int HG) {
     TokLayout L;
     int off = 0;
     L.lut_k = off;
@@ -520,7 +534,7 @@ TokLayout tok_layout(int pk, int pv, bool shared_lut, int Hq, int Hkv, int chunk
     L.lut_v = shared_lut ? L.lut_k : off;
     if (!shared_lut) off += 8 << pv;
     L.qlimb = off;
-    off += Hkv * kGroups * 4 * 16;
+    off += Hkv * kGroups * 4 * HG * 16;
     L.qscale = off;
     off += 4 * Hq;
     L.qsum = off;
@@ -532,12 +546,12 @@ TokLayout tok_layout(int pk, int pv, bool shared_lut, int Hq, int Hkv, int chunk
     L.ring_k = 0;
     L.ring_v = kRingBytes;
     L.vtile = 2 * kRingBytes;
-    L.plimb = L.vtile + kVSlice * kVRow;   // the kernel relies on this placement
-    L.wave_stride = (L.plimb + 16 * kVRow + 15) & ~15;
+    L.plimb = L.vtile + kTile * kVRowT;
+    L.wave_stride = (L.plimb + HG * kTile * 16 + 15) & ~15;
     L.nw = nw;
     // the prologue's query scratch and the epilogue's merge buffers use the
     // wavefront regions
-    const int scratch = std::max(Hq * kD * 4, nw * 4 * (kD + 2) * 4);
+    const int scratch = std::max(Hq * kD * 4, nw * 4 * HG * (kD + 2) * 4);
     L.total = L.waves + std::max(nw * L.wave_stride, scratch);
     return L;
 }
@@ -554,20 +568,33 @@ int32_t token_chunk(int32_t B, int32_t t_cap) {
 
 namespace {
 
-template <uint32_t LUTV>
+template <uint32_t LUTV, int HG>
 int launch_token_kernel(const TokArgs& a, dim3 grid, int nw, hipStream_t stream) {
     const bool paged = a.pg.bt != nullptr;
-    const void* fn = paged ? reinterpret_cast<const void*>(&attn_token_kernel<LUTV, true>)
-                           : reinterpret_cast<const void*>(&attn_token_kernel<LUTV, false>);
+    const void* fn = paged ? reinterpret_cast<const void*>(&attn_token_kernel<LUTV, true, HG>)
+                           : reinterpret_cast<const void*>(&attn_token_kernel<LUTV, false, HG>);
     if (int rc = hip_check("hipFuncSetAttribute",
                            hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
         return rc;
     const size_t smem = (size_t)a.L.total;
     if (paged)
-        attn_token_kernel<LUTV, true><<<grid, nw * kWave, smem, stream>>>(a);
+        attn_token_kernel<LUTV, true, HG><<<grid, nw * kWave, smem, stream>>>(a);
     else
-        attn_token_kernel<LUTV, false><<<grid, nw * kWave, smem, stream>>>(a);
+        attn_token_kernel<LUTV, false, HG><<<grid, nw * kWave, smem, stream>>>(a);
     return hip_check("attn_token launch", hipGetLastError());
+}
+
+template <int HG>
+int launch_token_hg(const TokArgs& a, dim3 grid, int nw, bool shared, hipStream_t stream) {
+    switch (shared ? 0u : (uint32_t)a.L.lut_v) {
+        case 0: return launch_token_kernel<0, HG>(a, grid, nw, stream);
+        case 8u << 8: return launch_token_kernel<8u << 8, HG>(a, grid, nw, stream);
+        case 8u << 9: return launch_token_kernel<8u << 9, HG>(a, grid, nw, stream);
+        case 8u << 10: return launch_token_kernel<8u << 10, HG>(a, grid, nw, stream);
+        case 8u << 11: return launch_token_kernel<8u << 11, HG>(a, grid, nw, stream);
+        case 8u << 12: return launch_token_kernel<8u << 12, HG>(a, grid, nw, stream);
+        default: return DQ_ERR_INVALID_ARG;
+    }
 }
 
 }  // namespace
@@ -606,22 +633,16 @@ int launch_attention_token_partial(const dq_tables* tk, const dq_tables* tv, con
     a.ws_m = a.ws_acc + slots * kD;
     a.ws_l = a.ws_m + slots;
     a.status = status;
-    int nw = kTokWaves;
+    if (a.G < 1 || a.G > 8) return DQ_ERR_INVALID_ARG;
+    const int HG = a.G > 4 ? 2 : 1;
+    int nw = tok_waves(HG);
     for (; nw > 0; --nw) {
-        a.L = tok_layout(a.tk.p, a.tv.p, shared, Hq, Hkv, a.chunk, nw);
+        a.L = tok_layout(a.tk.p, a.tv.p, shared, Hq, Hkv, a.chunk, nw, HG);
         if (a.L.total <= kMaxLds) break;
     }
     if (nw == 0) return DQ_ERR_INVALID_ARG;
     const dim3 grid(a.nchunks, 1, B);
-    switch (shared ? 0u : (uint32_t)a.L.lut_v) {
-        case 0: return launch_token_kernel<0>(a, grid, nw, stream);
-        case 8u << 8: return launch_token_kernel<8u << 8>(a, grid, nw, stream);
-        case 8u << 9: return launch_token_kernel<8u << 9>(a, grid, nw, stream);
-        case 8u << 10: return launch_token_kernel<8u << 10>(a, grid, nw, stream);
-        case 8u << 11: return launch_token_kernel<8u << 11>(a, grid, nw, stream);
-        case 8u << 12: return launch_token_kernel<8u << 12>(a, grid, nw, stream);
-        default: return DQ_ERR_INVALID_ARG;
-    }
+    return HG == 1 ? launch_token_hg<1>(a, grid, nw, shared, stream) : launch_token_hg<2>(a, grid, nw, shared, stream);
 }
 
 }  // namespace dq

@@ -1,8 +1,10 @@
-"""Per-token streams at the full b16_t32k_tok size, in the launch configuration
-bench.py times (--workload b16_t32k_tok): batch 16 x 32768 tokens, one
-1024-value stream per token and tensor (335 / 235-byte records in 336 / 240
-byte slots, 8 / 6 levels, p 8), one encode call per sequence, then the same
-partial + merge calls.
+"""Per-token streams at full size, in the launch configuration bench.py times
+(--workload b16_t32k_tok: batch 16 x 32768 tokens, 32 query / 8 KV heads;
+--workload b32_t32k_g8_tok: batch 32 x 32768 tokens, 64 query / 8 KV heads,
+the second query-head slot group of the kernel): one 1024-value stream per
+token and tensor (335 / 235-byte records in 336 / 240 byte slots, 8 / 6
+levels, p 8), one prefill append per tensor, then the same partial + merge
+calls.
 
 The oracle cannot re-encode 524,288 tokens in seconds, so it checks what it
 computes from the same seeded inputs:
@@ -12,8 +14,9 @@ computes from the same seeded inputs:
   means of all 8 heads bit-exact;
 * a decode step in the same launch configuration (same grid, chunking and
   wavefronts: those depend on the capacity, not on the lengths) where one
-  sequence holds 2048 tokens: its 32 query heads within 2e-3 (row-normalized)
-  of the oracle's fp64 attention over the oracle's own records;
+  sequence holds 2048 tokens: its 32 (64) query heads within 2e-3
+  (row-normalized) of the oracle's fp64 attention over the oracle's own
+  records;
 * properties of the full-length launch: no status flag, finite outputs.
 """
 
@@ -33,11 +36,11 @@ W = 128
 SEED = 0          # bench.py's default seed
 
 
-@pytest.fixture(scope="module")
-def full():
+@pytest.fixture(scope="module", params=["b16_t32k_tok", "b32_t32k_g8_tok"])
+def full(request):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
-    wl = wlmod.workload("b16_t32k_tok")
+    wl = wlmod.workload(request.param)
     dev = torch.device("cuda")
     tk, tv, cache, _ = bench.fill_cache(wl, SEED, dev)
     q, seq, out = bench.step_inputs(wl, SEED, dev)

@@ -278,7 +278,7 @@ def test_token_paged_arguments_rejected(dq):
                                                            btd.data_ptr(), max_pages, page_tokens, num_pages,
                                                            lens.data_ptr(), ctypes.c_float(1 / 128 ** 0.5),
                                                            ws.data_ptr(), ws_bytes, None, None)
-    assert attn(Hq=H * 8) == dq.DQ_ERR_INVALID_ARG           # G = 8 is not supported for per-token streams
+    assert attn(Hq=H * 16) == dq.DQ_ERR_INVALID_ARG          # at most 8 query heads per KV head
     assert attn(ws_bytes=64) == dq.DQ_ERR_WORKSPACE
     assert attn(page_tokens=100) == dq.DQ_ERR_INVALID_ARG
     torch.cuda.synchronize()

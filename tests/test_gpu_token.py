@@ -117,10 +117,12 @@ def test_token_attention_matches_oracle(dq, p):
     assert _rel_err(got[live], ref[live]) < TOL
 
 
-@pytest.mark.parametrize("H,G,Ck,Cv", [(8, 1, 335, 235), (4, 2, 170, 120), (2, 4, 88, 62), (1, 4, 44, 32)])
+@pytest.mark.parametrize("H,G,Ck,Cv", [(8, 1, 335, 235), (4, 2, 170, 120), (2, 4, 88, 62), (1, 4, 44, 32),
+                                       (8, 8, 335, 235), (4, 6, 170, 120), (2, 8, 88, 62), (1, 5, 44, 32)])
 def test_token_attention_heads_and_groups(dq, H, G, Ck, Cv):
-    """Streams of 128 H values for H = 8, 4, 2, 1 KV heads and 1, 2 or 4 query
-    heads per KV head; the GPU encoder fills the cache."""
+    """Streams of 128 H values for H = 8, 4, 2, 1 KV heads and 1 to 8 query
+    heads per KV head (above 4: two groups of query-head slots per KV head);
+    the GPU encoder fills the cache."""
     B, T = 2, 256
     n = 128 * H
     gtk, otk = _tabs(dq, n, 8, Ck)
@@ -207,7 +209,7 @@ def test_token_entry_points_reject_bad_arguments(dq):
                                                      0.088, p, ws_bytes, p, None)
 
     assert attn(g128, gtv) == dq.DQ_ERR_INVALID_ARG             # n must be 128 H
-    assert attn(gtk, gtv, Hq=64) == dq.DQ_ERR_INVALID_ARG       # G = 8 is not supported here
+    assert attn(gtk, gtv, Hq=128) == dq.DQ_ERR_INVALID_ARG      # at most 8 query heads per KV head
     assert attn(gtk, gtv, Hq=30) == dq.DQ_ERR_INVALID_ARG       # not a multiple of H
     assert attn(gtk, gtv, t_cap=200) == dq.DQ_ERR_INVALID_ARG
     assert attn(gtk, gtv, ws_bytes=16) == dq.DQ_ERR_WORKSPACE
