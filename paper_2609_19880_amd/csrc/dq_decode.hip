@@ -147,29 +147,76 @@ struct AttnArgs {
 
 
 // One step of Alg. 2 on the state kept as X = 8 x (+ up to 7 in the low bits,
-// which nothing reads).  Returns the table word (level in its top byte).
+// which nothing reads), in two halves so that the key and value chains of a
+// lane overlap: the reads of one chain are in flight while the other's
+// arithmetic runs.
 //   table address = X & (2^p - 1) << 3          (8-byte entries at lut_off)
 //   y = f (X >> (p + 3)) + (z - c) = x'          (one 24-bit multiply-add)
 //   s = ((clz(y) - 3) & 24) ^ 29 = 29 - 8 n      (n = 0, 1 or 2 bytes to read)
 //   X = alignbit(y, pair << 16, s),  Q -= 16 s   (J: step in the 16-step window,
 //                                                  a constant once unrolled)
 //
-// The pair goes straight into the high half of r (ds_read_u16_d16_hi; the low
-// half is never read).  The compiler does not emit that load, so it is
-// written out; it is issued before the table read, which is made to depend on
-// it, and LDS returns in order, so the compiler's wait for the table word
-// also covers the pair (whose only use comes after the table word's).
+// dissue requests the pair (straight into the high half of r with
+// ds_read_u16_d16_hi, which the compiler does not emit; the low half is never
+// read) and the table word.  The compiler does not see these loads, so
+// nothing may read r or e until dwait<N> has run on them: it waits until at
+// most N LDS or scalar-memory operations are outstanding.  LDS returns in
+// order, so N = the number of LDS reads issued after e in program order is
+// enough (operations the compiler adds in between only make the wait
+// stricter).  dfinish then completes the step and returns the table word
+// (level in its top byte).
 template <uint32_t LUT_OFF>
-__device__ __forceinline__ uint32_t dstep(uint32_t& X, uint32_t& Q, uint32_t mask8, int p3, int J) {
-    uint32_t laddr = X & mask8, r;
-    asm volatile("ds_read_u16_d16_hi %0, %2 offset:%3" : "=v"(r), "+v"(laddr) : "v"(Q), "i"(kPairStep * J));
-    const uint64_t e = *LDS_PTR(const uint64_t, laddr + LUT_OFF);
+__device__ __forceinline__ void dissue(uint32_t X, uint32_t Q, uint32_t mask8, int J, uint32_t& r, uint64_t& e) {
+    asm volatile("ds_read_u16_d16_hi %0, %2 offset:%4\n\t"
+                 "ds_read_b64 %1, %3 offset:%5"
+                 : "=&v"(r), "=&v"(e)
+                 : "v"(Q), "v"(X & mask8), "i"(kPairStep * J), "i"(LUT_OFF));
+}
+
+template <int N>
+__device__ __forceinline__ void dwait(uint32_t& r, uint64_t& e) {
+    asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(r), "+v"(e) : "i"(N));
+}
+
+// The query digits of one group (16 bytes at LDS address a + off, off a
+// constant once unrolled), requested under the same rule: pending until a
+// dwaitq that follows it has run.
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void qissue(uint32_t a, int off, v4u& q) {
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=&v"(q) : "v"(a), "i"(off));
+}
+
+template <int N, int HG>
+__device__ __forceinline__ void dwaitq(uint32_t& r, uint64_t& e, v4u (&q)[HG]) {
+    if constexpr (HG == 1)
+        asm volatile("s_waitcnt lgkmcnt(%3)" : "+v"(r), "+v"(e), "+v"(q[0]) : "i"(N));
+    else
+        asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(r), "+v"(e), "+v"(q[0]), "+v"(q[1]) : "i"(N));
+}
+
+__device__ __forceinline__ uint32_t dfinish(uint32_t& X, uint32_t& Q, int p3, uint32_t r, uint64_t e) {
     const uint32_t ex = (uint32_t)e, ey = (uint32_t)(e >> 32);
     const uint32_t y = __umul24(ex, X >> p3) + ey;
     const uint32_t s = (((uint32_t)__builtin_clz(y) - 3u) & 24u) ^ 29u;
     X = __builtin_amdgcn_alignbit(y, r, s);
     asm("v_mad_i32_i24 %0, %1, -16, %2" : "=v"(Q) : "v"(s), "v"(Q));
     return ex;
+}
+
+// Copies a decode table into LDS: the device table holds 8 f | m << 24 and
+// 8 (z - c), the decode step takes f | m << 24 and z - c.  Eight entries per
+// thread are requested before any is stored, so that their latencies overlap.
+__device__ __forceinline__ void stage_table(uint2* dst, const uint2* __restrict__ src, int n, int tid, int nthr) {
+    for (int i0 = tid; i0 < n; i0 += 8 * nthr) {
+        uint2 e[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (i0 + u * nthr < n) e[u] = src[i0 + u * nthr];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (i0 + u * nthr < n)
+                dst[i0 + u * nthr] = uint2{(e[u].x & 0xFF000000u) | ((e[u].x & 0x00FFFFFFu) >> 3), e[u].y >> 3};
+    }
 }
 
 // Record dwords of the lane's token (C % 4 == 0, C <= 64).
@@ -259,10 +306,11 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
 
 
     // records of the wavefront's first tile, requested before the prologue so
-    // that their latency overlaps it; each later tile's records are loaded
-    // while the wavefront decodes the one before (up to 4 query heads per KV
-    // head; with 8 the registers go to accumulators unless the workgroup has
-    // at most 8 wavefronts)
+    // that their latency overlaps it; each later tile's records are requested
+    // once the tile before has its softmax weights, and arrive while its
+    // value products are formed (up to 4 query heads per KV head; with 8 the
+    // registers go to accumulators unless the workgroup has at most 8
+    // wavefronts)
     constexpr bool kPrefetch = HG == 1 || WMAX <= 8;
     uint32_t rk[kMaxRecDwords], rv[kMaxRecDwords];
     if (kPrefetch && wave < ntiles) {
@@ -271,18 +319,30 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
         load_record(rv, a.vrec, tok, CWv);
     }
 
+    // key means of the wavefront's first window(s) of the q . mu table below,
+    // requested here for the same reason: half a wavefront per window, two
+    // windows per pass, lane l taking channels 4 (l % 32) .. + 3 of window
+    // 2 pass + l / 32.  Windows from the sequence's length on are never used:
+    // their block-table entries may be unmapped.
+    const int nwin_total = a.t_cap / DQ_MEAN_WINDOW;
+    const int w0 = start / DQ_MEAN_WINDOW;
+    const int nwin = (a.chunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1;
+    auto mean_live = [&](int wi) {
+        return wi < nwin && w0 + wi < nwin_total && (w0 + wi) * DQ_MEAN_WINDOW < T;
+    };
+    uint32_t mv0 = 0;
+    uint16_t ms0 = 0;
+    if (mean_live(2 * wave + (lane >> 5))) {
+        const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + 2 * wave + (lane >> 5), bad_page);
+        ms0 = a.kms[widx];
+        mv0 = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + 4 * (lane & 31));
+    }
+
     // ---- prologue: tables, rotated query, its digits, q . mu per window
     if (!FIXED) {
         const int Pk = 1 << a.tk.p, Pv = 1 << a.tv.p;
-        // the device table holds 8 f | m << 24 and 8 (z - c); the decode step
-        // takes f | m << 24 and z - c
-        auto unscaled = [](uint2 e) { return uint2{(e.x & 0xFF000000u) | ((e.x & 0x00FFFFFFu) >> 3), e.y >> 3}; };
-        uint2* lk = reinterpret_cast<uint2*>(smem + L.lut_k);
-        for (int i = tid; i < Pk; i += nthr) lk[i] = unscaled(a.tk.t.lut64[i]);
-        if (LUTV != 0) {
-            uint2* lv = reinterpret_cast<uint2*>(smem + LUTV);
-            for (int i = tid; i < Pv; i += nthr) lv[i] = unscaled(a.tv.t.lut64[i]);
-        }
+        stage_table(reinterpret_cast<uint2*>(smem + L.lut_k), a.tk.t.lut64, Pk, tid, nthr);
+        if (LUTV != 0) stage_table(reinterpret_cast<uint2*>(smem + LUTV), a.tv.t.lut64, Pv, tid, nthr);
     }
     float* qt = reinterpret_cast<float*>(smem + L.waves);          // [G][d] scratch
     float* qscale = reinterpret_cast<float*>(smem + L.qscale);
@@ -307,21 +367,19 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
         dst[8] = (uint8_t)d2;
         dst[12] = 0;
     }
-    const int nwin_total = a.t_cap / DQ_MEAN_WINDOW;
-    const int w0 = start / DQ_MEAN_WINDOW;
-    const int nwin = (a.chunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1;
-    // half a wavefront per window, two windows per pass: lane l takes
-    // channels 4 (l % 32) .. 4 (l % 32) + 3 of window 2 pass + l / 32
     {
         const int r = lane >> 5, c4 = 4 * (lane & 31);
-        for (int wi = 2 * wave + r; wi - r < nwin; wi += 2 * L.nw) {
+        for (int wi = 2 * wave + r, pass = 0; wi - r < nwin; wi += 2 * L.nw, ++pass) {
             float f[4] = {0.f, 0.f, 0.f, 0.f};
-            // windows from the sequence's length on are never used: their
-            // block-table entries may be unmapped
-            if (wi < nwin && w0 + wi < nwin_total && (w0 + wi) * DQ_MEAN_WINDOW < T) {
-                const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + wi, bad_page);
-                const float sc = half_bits_to_f32(a.kms[widx]);
-                const uint32_t mv = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + c4);
+            if (mean_live(wi)) {
+                uint32_t mv = mv0;
+                uint16_t ms = ms0;
+                if (pass > 0) {
+                    const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + wi, bad_page);
+                    ms = a.kms[widx];
+                    mv = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + c4);
+                }
+                const float sc = half_bits_to_f32(ms);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) f[k] = sc * (float)(int8_t)((mv >> (8 * k)) & 0xFF);
             }
@@ -398,11 +456,6 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
             build_pairs(rk, CWk, smem + pk_lane);
             build_pairs(rv, CWv, smem + pv_lane);
         }
-        if (kPrefetch && tile + L.nw < ntiles) {
-            const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, t_base + L.nw * kTile, bad_page) + lane;
-            load_record(rk, a.krec, tok, CWk);
-            load_record(rv, a.vrec, tok, CWv);
-        }
         uint32_t xk = xk0, xv = xv0;
         // the pair arrays are read back by this lane only: order the reads
         // after the writes (LDS keeps a wavefront's accesses in order)
@@ -421,15 +474,20 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
 #pragma unroll
             for (int d = 0; d < 3; ++d) dk[hg][d] = v4i{0, 0, 0, 0};
         uint32_t vlev[kD / 4];
-        // query digits: with up to 12 wavefronts per CU they are read one
-        // group ahead, so that the products do not wait for the read; with 16
-        // the others cover that wait, and reading in place keeps the
-        // registers of that case free
-        constexpr bool kAhead = HG > 1 || WMAX <= 12;
-        uint4 qla[HG];
-        if constexpr (kAhead) {
-#pragma unroll
-            for (int hg = 0; hg < HG; ++hg) qla[hg] = *reinterpret_cast<const uint4*>(qlimb + (hg * 4 + (lane & 3)) * 16);
+        // the query digits of group g are requested after the key step 4 g + 3,
+        // so that the wait for the value step 4 g + 3 covers them too
+        const uint32_t q_lane = (uint32_t)L.qlimb + (uint32_t)(lane & 3) * 16;
+        v4u qd[HG];
+        // step n of both chains: wait for its reads, finish it, request step
+        // n + 1 (pointer windows advance and are clamped between n and n + 1;
+        // a corrupt stream may run past its array, so clamp often enough
+        // that it cannot leave the workgroup's LDS (kPairSlack above the
+        // arrays), except after the last window, whose pointer is checked)
+        uint32_t rk_, rv_;
+        uint64_t ek_, ev_;
+        if (!FIXED) {
+            dissue<0>(xk, pq, mask8k, 0, rk_, ek_);
+            dissue<LUTV>(xv, pv, mask8v, 0, rv_, ev_);
         }
 #pragma unroll
         for (int grp = 0; grp < kD / 4; ++grp) {
@@ -438,48 +496,49 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
                 const int w = 1 + (FIXED ? grp / 4 : 0), sh = 8 * (grp % 4);
                 lk = spread2(__builtin_amdgcn_ubfe(ck[w], sh, 8));
                 vlev[grp] = spread2(__builtin_amdgcn_ubfe(cv[w], sh, 8));
+#pragma unroll
+                for (int hg = 0; hg < HG; ++hg)
+                    qd[hg] = *reinterpret_cast<const v4u*>(qlimb + ((grp * GP) + hg * 4 + (lane & 3)) * 16);
             } else {
-                const int j0 = 4 * (grp % kClampGroups);     // step of the pointer window
-                const uint32_t k0 = dstep<0>(xk, pq, mask8k, pk3, j0);
-                const uint32_t v0 = dstep<LUTV>(xv, pv, mask8v, pv3, j0);
-                const uint32_t k1 = dstep<0>(xk, pq, mask8k, pk3, j0 + 1);
-                const uint32_t v1 = dstep<LUTV>(xv, pv, mask8v, pv3, j0 + 1);
-                const uint32_t k2 = dstep<0>(xk, pq, mask8k, pk3, j0 + 2);
-                const uint32_t v2 = dstep<LUTV>(xv, pv, mask8v, pv3, j0 + 2);
-                const uint32_t k3 = dstep<0>(xk, pq, mask8k, pk3, j0 + 3);
-                const uint32_t v3 = dstep<LUTV>(xv, pv, mask8v, pv3, j0 + 3);
-                lk = pack4(k0, k1, k2, k3);
-                vlev[grp] = pack4(v0, v1, v2, v3);
+                uint32_t kw[4], vw[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int n = 4 * grp + u, J1 = (n + 1) % kWindow;
+                    const bool more = n + 1 < kD;
+                    dwait<2>(rk_, ek_);                  // the value reads of step n follow
+                    kw[u] = dfinish(xk, pq, pk3, rk_, ek_);
+                    if (J1 == 0) {
+                        pq += kWindow * kPairStep;
+                        if (more) pq = min(pq, pk_end);
+                    }
+                    if (u == 3) {
+                        qissue(q_lane, (grp * GP) * 16, qd[0]);
+                        if constexpr (HG == 2) qissue(q_lane, (grp * GP + 4) * 16, qd[1]);
+                    }
+                    if (more) dissue<0>(xk, pq, mask8k, J1, rk_, ek_);
+                    // the key reads of step n + 1 follow (and the digits at u = 3,
+                    // before them: this wait covers those too)
+                    if (u < 3) dwait<2>(rv_, ev_);
+                    else if (more) dwaitq<2>(rv_, ev_, qd);
+                    else dwaitq<0>(rv_, ev_, qd);
+                    vw[u] = dfinish(xv, pv, pv3, rv_, ev_);
+                    if (J1 == 0) {
+                        pv += kWindow * kPairStep;
+                        if (more) pv = min(pv, pv_end);
+                    }
+                    if (more) dissue<LUTV>(xv, pv, mask8v, J1, rv_, ev_);
+                }
+                lk = pack4(kw[0], kw[1], kw[2], kw[3]);
+                vlev[grp] = pack4(vw[0], vw[1], vw[2], vw[3]);
             }
             // pack now: left alone, the packing sinks to the value pass and the
             // four table words stay live until then
             asm volatile("" : "+v"(vlev[grp]));
 #pragma unroll
             for (int hg = 0; hg < HG; ++hg) {
-                if constexpr (kAhead) {
-                    dk[hg][0] = mfma(qla[hg].x, lk, dk[hg][0]);
-                    dk[hg][1] = mfma(qla[hg].y, lk, dk[hg][1]);
-                    dk[hg][2] = mfma(qla[hg].z, lk, dk[hg][2]);
-                    if (grp + 1 < kD / 4)
-                        qla[hg] = *reinterpret_cast<const uint4*>(qlimb + (((grp + 1) * GP) + hg * 4 + (lane & 3)) * 16);
-                } else {
-                    const uint4 ql = *reinterpret_cast<const uint4*>(qlimb + ((grp * GP) + hg * 4 + (lane & 3)) * 16);
-                    dk[hg][0] = mfma(ql.x, lk, dk[hg][0]);
-                    dk[hg][1] = mfma(ql.y, lk, dk[hg][1]);
-                    dk[hg][2] = mfma(ql.z, lk, dk[hg][2]);
-                }
-            }
-            // end of a pointer window: the registers become the pointers again;
-            // a corrupt stream may run past its array, so clamp often enough
-            // that it cannot leave the workgroup's LDS (kPairSlack above the
-            // arrays), except after the last window, whose pointer is checked
-            if (!FIXED && (grp % kClampGroups) == kClampGroups - 1) {
-                pq += kWindow * kPairStep;
-                pv += kWindow * kPairStep;
-                if (grp + 1 < kD / 4) {
-                    pq = min(pq, pk_end);
-                    pv = min(pv, pv_end);
-                }
+                dk[hg][0] = mfma(qd[hg].x, lk, dk[hg][0]);
+                dk[hg][1] = mfma(qd[hg].y, lk, dk[hg][1]);
+                dk[hg][2] = mfma(qd[hg].z, lk, dk[hg][2]);
             }
             // keep the scheduler inside one group: live ranges stay short
             __builtin_amdgcn_sched_barrier(0);
@@ -547,6 +606,12 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
             }
         }
 
+        if (kPrefetch && tile + L.nw < ntiles) {
+            const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, t_base + L.nw * kTile, bad_page) + lane;
+            load_record(rk, a.krec, tok, CWk);
+            load_record(rv, a.vrec, tok, CWv);
+        }
+
         // ---- P . v over two slices of 64 channels
         wave_sync();   // the weight rows (and, below, the value rows) are read by other lanes
         uint64_t pa[HG][2];
@@ -611,17 +676,30 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     }
     __syncthreads();
     const int NC = a.nchunks;
+    // only the wavefronts that decoded a tile hold partials; their values are
+    // all requested before the first is used (the wavefront loop unrolled to
+    // the instantiation's bound, indexes clamped)
+    const int nwa = min(L.nw, ntiles);
     for (int i = tid; i < G * kD; i += nthr) {
         const int g = i / kD, j = i % kD;
+        float mv[WMAX], av[WMAX], lv[WMAX];
+#pragma unroll
+        for (int w = 0; w < WMAX; ++w) {
+            const int ww = min(w, nwa - 1);
+            mv[w] = mw[ww * GP + g];
+            av[w] = aw[(ww * GP + g) * kD + j];
+            lv[w] = lw[ww * GP + g];
+        }
         float M = -INFINITY;
-        for (int w = 0; w < L.nw; ++w) M = fmaxf(M, mw[w * GP + g]);
+#pragma unroll
+        for (int w = 0; w < WMAX; ++w) M = fmaxf(M, mv[w]);
         float acc = 0.f, l = 0.f;
-        for (int w = 0; w < L.nw; ++w) {
-            const float mv = mw[w * GP + g];
-            if (mv == -INFINITY) continue;
-            const float e = exp2f(mv - M);
-            acc += aw[(w * GP + g) * kD + j] * e;
-            l += lw[w * GP + g] * e;
+#pragma unroll
+        for (int w = 0; w < WMAX; ++w) {
+            if (w >= nwa || mv[w] == -INFINITY) continue;
+            const float e = exp2f(mv[w] - M);
+            acc += av[w] * e;
+            l += lv[w] * e;
         }
         const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * (NC + kResSlots) + c;
         a.ws_acc[slot * kD + j] = acc;
@@ -632,15 +710,17 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     }
 }
 
-__global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restrict__ ws_hdr,
-                                                        const float* __restrict__ ws_m,
-                                                        const float* __restrict__ ws_l,
-                                                        const float* __restrict__ ws_acc,
-                                                        const int32_t* __restrict__ seq_lens,
-                                                        int Hq, int t_cap, float* __restrict__ out) {
-    __shared__ float o[kD];
-    __shared__ float red[kD];
-    const int hq = blockIdx.x, b = blockIdx.y, j = threadIdx.x;
+// One wavefront per (query head, sequence): lane l combines channels l and
+// l + 64 of every partial, so no barrier is needed anywhere.  The partials'
+// maxima and their first 8 accumulator rows are requested together, right
+// after the header.
+__global__ __launch_bounds__(kWave) void attn_merge_kernel(const int32_t* __restrict__ ws_hdr,
+                                                           const float* __restrict__ ws_m,
+                                                           const float* __restrict__ ws_l,
+                                                           const float* __restrict__ ws_acc,
+                                                           const int32_t* __restrict__ seq_lens,
+                                                           int Hq, int t_cap, float* __restrict__ out) {
+    const int hq = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
     const int chunk = ws_hdr[0], NC = ws_hdr[1], residual = min(max(ws_hdr[2], 0), kResSlots);
     const int T = max(0, min(seq_lens[b], t_cap));
     float* dst = out + ((int64_t)b * Hq + hq) * kD;
@@ -650,53 +730,63 @@ __global__ __launch_bounds__(kD) void attn_merge_kernel(const int32_t* __restric
     const int64_t base = ((int64_t)b * Hq + hq) * (NC + kResSlots);
     // partials in use: chunks 0..nc-1, then the residual slots NC..
     const int np = nc + residual;
-    float M = -INFINITY;
-    for (int i = j; i < np; i += kD) M = fmaxf(M, ws_m[base + (i < nc ? i : NC + i - nc)]);
-    red[j] = M;
-    __syncthreads();
-    for (int s2 = kD / 2; s2 > 0; s2 >>= 1) {
-        if (j < s2) red[j] = fmaxf(red[j], red[j + s2]);
-        __syncthreads();
-    }
-    M = red[0];
-    if (M == -INFINITY) {      // no token at all
-        dst[j] = 0.f;
+    auto slot_of = [&](int i) { return base + (i < nc ? i : NC + i - nc); };
+    if (np == 0) {
+        dst[lane] = 0.f;
+        dst[lane + 64] = 0.f;
         return;
     }
-    float acc = 0.f, l = 0.f;
-    // batches of 8 partials, loads unconditional on a clamped index so that
-    // they are in flight together; partials past np get weight 0
-    for (int i0 = 0; i0 < np; i0 += 8) {
-        float av[8], mv[8], lv[8];
+    // batch 0 of the accumulator rows (index clamped: loads unconditional)
+    float a0[8], a1[8], mv[8], lv[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int i = min(i0 + u, np - 1);
-            const int c = i < nc ? i : NC + i - nc;  // same for every thread of the block
-            av[u] = ws_acc[(base + c) * kD + j];
-            mv[u] = ws_m[base + c];
-            lv[u] = ws_l[base + c];
-        }
+    for (int u = 0; u < 8; ++u) {
+        const int64_t s = slot_of(min(u, np - 1));
+        a0[u] = ws_acc[s * kD + lane];
+        a1[u] = ws_acc[s * kD + lane + 64];
+        mv[u] = ws_m[s];
+        lv[u] = ws_l[s];
+    }
+    float M = -INFINITY;
+    for (int i = lane; i < np; i += kWave) M = fmaxf(M, ws_m[slot_of(i)]);
+    M = wave_max_f32(M);
+    if (M == -INFINITY) {      // no token at all
+        dst[lane] = 0.f;
+        dst[lane + 64] = 0.f;
+        return;
+    }
+    float acc0 = 0.f, acc1 = 0.f, l = 0.f;
+    for (int i0 = 0;;) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const float e = i0 + u < np ? exp2f(mv[u] - M) : 0.f;
-            acc += av[u] * e;
+            acc0 += a0[u] * e;
+            acc1 += a1[u] * e;
             l += lv[u] * e;
         }
+        i0 += 8;
+        if (i0 >= np) break;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int64_t s = slot_of(min(i0 + u, np - 1));
+            a0[u] = ws_acc[s * kD + lane];
+            a1[u] = ws_acc[s * kD + lane + 64];
+            mv[u] = ws_m[s];
+            lv[u] = ws_l[s];
+        }
     }
-    if (!ws_hdr[3]) {          // values were coded in the caller's basis
-        dst[j] = acc / l;
-        return;
+    float v0 = acc0 / l, v1 = acc1 / l;
+    if (ws_hdr[3]) {           // inverse rotation of the value basis: H v / d
+        for (int hh = 1; hh < 64; hh <<= 1) {
+            const float p0 = __shfl_xor(v0, hh), p1 = __shfl_xor(v1, hh);
+            v0 = (lane & hh) ? p0 - v0 : v0 + p0;
+            v1 = (lane & hh) ? p1 - v1 : v1 + p1;
+        }
+        const float r0 = (v0 + v1) * (1.0f / kD), r1 = (v0 - v1) * (1.0f / kD);
+        v0 = r0;
+        v1 = r1;
     }
-    o[j] = acc / l;
-    __syncthreads();
-    // inverse rotation of the value basis: H v / d
-    for (int hh = 1; hh < kD; hh <<= 1) {
-        const float mine = o[j], other = o[j ^ hh];
-        __syncthreads();
-        o[j] = (j & hh) ? (other - mine) : (mine + other);
-        __syncthreads();
-    }
-    dst[j] = o[j] * (1.0f / kD);
+    dst[lane] = v0;
+    dst[lane + 64] = v1;
 }
 
 // ------------------------------------------------------- residual window
@@ -997,7 +1087,9 @@ struct ChunkPlan {
 // about one workgroup per CU (more when the batch has more (sequence, KV head)
 // pairs than there are CUs), with chunks of kMinChunk..kMaxChunk tokens in
 // whole 64-token tiles.  Every workgroup then runs its waves over many tiles
-// and the grid ends in whole rounds of the CUs.
+// and the grid ends in whole rounds of the CUs.  At small batches and short
+// contexts the lower bound sets the grid: a 256-token chunk is four tiles,
+// one wavefront per SIMD, so that no two decode chains share issue slots.
 ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap, int num_cus) {
     ChunkPlan p;
     const int64_t pairs = (int64_t)B * Hkv;
@@ -1170,7 +1262,7 @@ int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* se
     const float* acc = reinterpret_cast<const float*>(static_cast<const uint8_t*>(ws) + kWsHeader);
     const float* m = acc + slots * kD;
     const float* l = m + slots;
-    attn_merge_kernel<<<dim3(Hq, B), kD, 0, stream>>>(hdr, m, l, acc, seq_lens, Hq, t_cap, out);
+    attn_merge_kernel<<<dim3(Hq, B), kWave, 0, stream>>>(hdr, m, l, acc, seq_lens, Hq, t_cap, out);
     return hip_check("attn_merge launch", hipGetLastError());
 }
 

@@ -20,7 +20,7 @@ constexpr int kBracketUnits = 40 * kLambdaSteps;  // hi - lo = 40 octaves
 // Slots NC .. NC + kResSlots - 1 of each (sequence, query head) hold the
 // residual window's partials, one per workgroup of its split.
 constexpr int kWsHeader = 256;
-constexpr int kMinChunk = 512;
+constexpr int kMinChunk = 256;
 constexpr int kResSlots = 4;
 inline int64_t max_chunks(int t_cap) { return (t_cap + kMinChunk - 1) / kMinChunk; }
 inline int64_t ws_slots(int B, int Hq, int t_cap) { return (int64_t)B * Hq * (max_chunks(t_cap) + kResSlots); }
@@ -154,7 +154,7 @@ size_t attention_workspace_bytes(int32_t B, int32_t Hq, int32_t Hkv, int32_t t_c
 
 // ws_slots_used: (max, sum, accumulator) slots the workspace holds, which
 // places the max and sum arrays after the accumulators; 0 = the size
-// attention_workspace_bytes allows for (512-token chunks).
+// attention_workspace_bytes allows for (chunks of kMinChunk tokens).
 int launch_attention_partial(const dq_tables* tk, const dq_tables* tv, const Pages& pg, const uint16_t* q,
                              int32_t B, int32_t Hq, int32_t Hkv, const uint8_t* krec,
                              const int8_t* kmq, const uint16_t* kms, const uint8_t* vrec,
