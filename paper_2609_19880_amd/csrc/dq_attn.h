@@ -37,11 +37,31 @@ __device__ __forceinline__ void digits3(int v, int& d0, int& d1, int& d2) {
     d2 = (v1 - d1) >> 8;
 }
 
-// Rotated query heads (unnormalized Hadamard, stages h = 1, 2, ..., 64 in
-// the order of the definition) into qt [nh][128] fp32, a wavefront per head
-// with channels l and l + 64 in lane l; qscale = max |q_rot| / 2^22 and qsum =
-// sum of q_rot per head, 0 for the slots nh .. slots - 1.  rotate = 0: keys
-// arrive in the rotated basis, and so does the query: it is taken as it is.
+// Rotates one query head held as channels l and l + 64 in lane l
+// (unnormalized Hadamard, stages h = 1, 2, ..., 64 in the order of the
+// definition) and stores it into qt[g][128] fp32, with qscale[g] = max |q_rot| /
+// 2^22 and qsum[g] = sum of q_rot.  rotate = 0: keys arrive in the rotated
+// basis, and so does the query: it is taken as it is.
+__device__ __forceinline__ void rotate_query_head(float v0, float v1, int g, int lane, float* qt, float* qscale,
+                                                  float* qsum, int rotate) {
+    float r0 = v0, r1 = v1;
+    if (rotate) {
+        hadamard_lanes(v0, v1, lane);
+        r0 = v0 + v1;
+        r1 = v0 - v1;
+    }
+    qt[g * 128 + lane] = r0;
+    qt[g * 128 + lane + 64] = r1;
+    const float mx = wave_max_f32(fmaxf(fabsf(r0), fabsf(r1)));
+    const float sm = wave_sum_f32(r0 + r1);
+    if (lane == 0) {
+        qscale[g] = mx * (1.0f / 4194304.0f);
+        qsum[g] = sm;
+    }
+}
+
+// All query heads of a workgroup, a wavefront per head: heads 0 .. nh - 1 of
+// q, and qscale = qsum = 0 for the slots nh .. slots - 1.
 __device__ __forceinline__ void rotate_query_heads(const uint16_t* q, int nh, int slots, int wave, int nw,
                                                    int lane, float* qt, float* qscale, float* qsum,
                                                    int rotate = 1) {
@@ -53,25 +73,8 @@ __device__ __forceinline__ void rotate_query_heads(const uint16_t* q, int nh, in
             }
             continue;
         }
-        float v0 = bf16_to_f32(q[g * 128 + lane]), v1 = bf16_to_f32(q[g * 128 + lane + 64]);
-        float r0 = v0, r1 = v1;
-        if (rotate) {
-            for (int hh = 1; hh < 64; hh <<= 1) {
-                const float p0 = __shfl_xor(v0, hh), p1 = __shfl_xor(v1, hh);
-                v0 = (lane & hh) ? p0 - v0 : v0 + p0;
-                v1 = (lane & hh) ? p1 - v1 : v1 + p1;
-            }
-            r0 = v0 + v1;
-            r1 = v0 - v1;
-        }
-        qt[g * 128 + lane] = r0;
-        qt[g * 128 + lane + 64] = r1;
-        const float mx = wave_max_f32(fmaxf(fabsf(r0), fabsf(r1)));
-        const float sm = wave_sum_f32(r0 + r1);
-        if (lane == 0) {
-            qscale[g] = mx * (1.0f / 4194304.0f);
-            qsum[g] = sm;
-        }
+        rotate_query_head(bf16_to_f32(q[g * 128 + lane]), bf16_to_f32(q[g * 128 + lane + 64]), g, lane, qt, qscale,
+                          qsum, rotate);
     }
 }
 

@@ -117,6 +117,54 @@ __device__ __forceinline__ float half_sum_f32(float v) {
     return v;
 }
 
+// v of lane l ^ HH (HH a power of two below 64) with no LDS traffic: DPP
+// within rows of 16 lanes, the gfx950 lane-swap instructions across them.
+template <int HH>
+__device__ __forceinline__ float xor_lane(float v, int lane) {
+    const int x = __float_as_int(v);
+    if constexpr (HH == 1) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));     // quad_perm [1,0,3,2]
+    } else if constexpr (HH == 2) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));     // quad_perm [2,3,0,1]
+    } else if constexpr (HH == 4) {
+        // lanes with bit 2 clear (banks 0 and 2 of a row) read l + 4 (row_ror:12),
+        // the others l - 4 (row_ror:4)
+        int t = __builtin_amdgcn_update_dpp(0, x, 0x12C, 0xF, 0x5, false);
+        t = __builtin_amdgcn_update_dpp(t, x, 0x124, 0xF, 0xA, false);
+        return __int_as_float(t);
+    } else if constexpr (HH == 8) {
+        return __int_as_float(__builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, false));    // row_ror:8
+    } else if constexpr (HH == 16) {
+        // odd rows of the first result hold the even rows of the source and
+        // even rows of the second the odd rows
+        const auto r = __builtin_amdgcn_permlane16_swap((unsigned)x, (unsigned)x, false, false);
+        return __uint_as_float((lane & 16) ? r[0] : r[1]);
+    } else {
+        static_assert(HH == 32, "xor_lane: HH in 1, 2, 4, ..., 32");
+        const auto r = __builtin_amdgcn_permlane32_swap((unsigned)x, (unsigned)x, false, false);
+        return __uint_as_float((lane & 32) ? r[0] : r[1]);
+    }
+}
+
+template <int HH>
+__device__ __forceinline__ void hadamard_stage(float& v0, float& v1, int lane) {
+    const float p0 = xor_lane<HH>(v0, lane), p1 = xor_lane<HH>(v1, lane);
+    v0 = (lane & HH) ? p0 - v0 : v0 + p0;
+    v1 = (lane & HH) ? p1 - v1 : v1 + p1;
+}
+
+// Stages h = 1, 2, ..., 32 of the unnormalized Hadamard transform of a
+// 128-vector held as channels l (v0) and l + 64 (v1) in lane l, in the order
+// of the definition; stage 64 is (v0 + v1, v0 - v1), left to the caller.
+__device__ __forceinline__ void hadamard_lanes(float& v0, float& v1, int lane) {
+    hadamard_stage<1>(v0, v1, lane);
+    hadamard_stage<2>(v0, v1, lane);
+    hadamard_stage<4>(v0, v1, lane);
+    hadamard_stage<8>(v0, v1, lane);
+    hadamard_stage<16>(v0, v1, lane);
+    hadamard_stage<32>(v0, v1, lane);
+}
+
 __device__ __forceinline__ int wave_sum_i32(int v) { return wave_sum(v); }
 
 __device__ __forceinline__ float wave_sum_f32(float v) { return wave_sum(v); }

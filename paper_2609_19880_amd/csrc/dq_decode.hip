@@ -204,18 +204,28 @@ __device__ __forceinline__ uint32_t dfinish(uint32_t& X, uint32_t& Q, int p3, ui
 }
 
 // Copies a decode table into LDS: the device table holds 8 f | m << 24 and
-// 8 (z - c), the decode step takes f | m << 24 and z - c.  Eight entries per
-// thread are requested before any is stored, so that their latencies overlap.
+// 8 (z - c), the decode step takes f | m << 24 and z - c.  Entries i0 + u nthr
+// (u < 8) are requested by stage_load and stored by stage_store, so that the
+// eight latencies overlap (and overlap whatever runs in between);
+// stage_table copies entries i0 + 8 nthr on, eight per thread at a time.
+__device__ __forceinline__ void stage_load(uint2 (&e)[8], const uint2* __restrict__ src, int n, int i0, int nthr) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+        if (i0 + u * nthr < n) e[u] = src[i0 + u * nthr];
+}
+
+__device__ __forceinline__ void stage_store(uint2* dst, const uint2 (&e)[8], int n, int i0, int nthr) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+        if (i0 + u * nthr < n)
+            dst[i0 + u * nthr] = uint2{(e[u].x & 0xFF000000u) | ((e[u].x & 0x00FFFFFFu) >> 3), e[u].y >> 3};
+}
+
 __device__ __forceinline__ void stage_table(uint2* dst, const uint2* __restrict__ src, int n, int tid, int nthr) {
-    for (int i0 = tid; i0 < n; i0 += 8 * nthr) {
+    for (int i0 = tid + 8 * nthr; i0 < n; i0 += 8 * nthr) {
         uint2 e[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (i0 + u * nthr < n) e[u] = src[i0 + u * nthr];
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (i0 + u * nthr < n)
-                dst[i0 + u * nthr] = uint2{(e[u].x & 0xFF000000u) | ((e[u].x & 0x00FFFFFFu) >> 3), e[u].y >> 3};
+        stage_load(e, src, n, i0, nthr);
+        stage_store(dst, e, n, i0, nthr);
     }
 }
 
@@ -297,60 +307,118 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
         a.ws_hdr[2] = 0;          // set by the residual kernel when it runs
         a.ws_hdr[3] = a.rot_out;
     }
-    const int T = min(a.seq_lens[b], a.t_cap);
+    // ---- the prologue's loads, all in flight together: the tables and the
+    //      query heads (neither depends on the sequence's length), then the
+    //      first tile's records and key means
+    const int hq0 = h * G;
+    uint2 lut_e[8], lutv_e[8];
+    if (!FIXED) {
+        stage_load(lut_e, a.tk.t.lut64, 1 << a.tk.p, tid, nthr);
+        if (LUTV != 0) stage_load(lutv_e, a.tv.t.lut64, 1 << a.tv.p, tid, nthr);
+    }
+    // wavefront g < G rotates query head g (channels l and l + 64 in lane l)
+    uint16_t qb0 = 0, qb1 = 0;
+    if (wave < G) {
+        const uint16_t* qh = a.q + ((int64_t)b * a.Hq + hq0 + wave) * kD;
+        qb0 = qh[lane];
+        qb1 = qh[lane + 64];
+    }
+    // records of the wavefront's first tile and key means of the first
+    // window(s) of the q . mu table below.  In a contiguous cache every row
+    // below t_cap exists, so they are requested before the sequence's length
+    // is known (rows past it are loaded and not used); through a block table
+    // only rows below the length may be looked up, so they wait for it.
+    //   records: each later tile's records are requested once the tile before
+    //     has its softmax weights, and arrive while its value products are
+    //     formed (up to 4 query heads per KV head; with 8 the registers go to
+    //     accumulators unless the workgroup has at most 8 wavefronts); a
+    //     wavefront that turns out to have no tile may load one it does not
+    //     use
+    //   key means: half a wavefront per window, two windows per pass, lane l
+    //     of wavefront nw - 1 - mw taking channels 4 (l % 32) .. + 3 of window
+    //     2 (mw + pass nw) + l / 32 (the last wavefronts: the first ones form
+    //     the query digits meanwhile)
     const int start = c * a.chunk;
-    if (start >= T) return;   // the merge ignores chunks past the length
-    const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
+    const bool paged = a.pg.bt != nullptr;
     const int Ck = RWK ? 4 * RWK : a.tk.C, Cv = RWV ? 4 * RWV : a.tv.C, CWk = Ck / 4, CWv = Cv / 4;
-    bool bad_page = false;
-
-
-    // records of the wavefront's first tile, requested before the prologue so
-    // that their latency overlaps it; each later tile's records are requested
-    // once the tile before has its softmax weights, and arrive while its
-    // value products are formed (up to 4 query heads per KV head; with 8 the
-    // registers go to accumulators unless the workgroup has at most 8
-    // wavefronts)
     constexpr bool kPrefetch = HG == 1 || WMAX <= 8;
     uint32_t rk[kMaxRecDwords], rv[kMaxRecDwords];
-    if (kPrefetch && wave < ntiles) {
-        const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, start + wave * kTile, bad_page) + lane;
-        load_record(rk, a.krec, tok, CWk);
-        load_record(rv, a.vrec, tok, CWv);
-    }
-
-    // key means of the wavefront's first window(s) of the q . mu table below,
-    // requested here for the same reason: half a wavefront per window, two
-    // windows per pass, lane l taking channels 4 (l % 32) .. + 3 of window
-    // 2 pass + l / 32.  Windows from the sequence's length on are never used:
-    // their block-table entries may be unmapped.
     const int nwin_total = a.t_cap / DQ_MEAN_WINDOW;
     const int w0 = start / DQ_MEAN_WINDOW;
     const int nwin = (a.chunk + DQ_MEAN_WINDOW - 1) / DQ_MEAN_WINDOW + 1;
+    const int mwave = L.nw - 1 - wave;
+    const int mwin = 2 * mwave + (lane >> 5);            // this lane's first window
+    uint32_t mv0 = 0;
+    uint16_t ms0 = 0;
+    bool bad_page = false;
+    if (!paged) {
+        if (kPrefetch && wave * kTile < a.chunk) {
+            const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, min(start + wave * kTile, a.t_cap - kTile),
+                                           bad_page) + lane;
+            load_record(rk, a.krec, tok, CWk);
+            load_record(rv, a.vrec, tok, CWv);
+        }
+        if (mwin < nwin && w0 + mwin < nwin_total) {
+            const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + mwin, bad_page);
+            ms0 = a.kms[widx];
+            mv0 = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + 4 * (lane & 31));
+        }
+    }
+    const int T = min(a.seq_lens[b], a.t_cap);
+    if (start >= T) return;   // the merge ignores chunks past the length
+    const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
+    // windows from the sequence's length on are never used
     auto mean_live = [&](int wi) {
         return wi < nwin && w0 + wi < nwin_total && (w0 + wi) * DQ_MEAN_WINDOW < T;
     };
-    uint32_t mv0 = 0;
-    uint16_t ms0 = 0;
-    if (mean_live(2 * wave + (lane >> 5))) {
-        const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + 2 * wave + (lane >> 5), bad_page);
-        ms0 = a.kms[widx];
-        mv0 = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + 4 * (lane & 31));
+    if (paged) {
+        if (kPrefetch) {
+            const int ft = min(wave, ntiles - 1);
+            const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, start + ft * kTile, bad_page) + lane;
+            load_record(rk, a.krec, tok, CWk);
+            load_record(rv, a.vrec, tok, CWv);
+        }
+        if (mean_live(mwin)) {
+            const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + mwin, bad_page);
+            ms0 = a.kms[widx];
+            mv0 = *reinterpret_cast<const uint32_t*>(a.kmq + widx * kD + 4 * (lane & 31));
+        }
     }
 
     // ---- prologue: tables, rotated query, its digits, q . mu per window
     if (!FIXED) {
         const int Pk = 1 << a.tk.p, Pv = 1 << a.tv.p;
+        stage_store(reinterpret_cast<uint2*>(smem + L.lut_k), lut_e, Pk, tid, nthr);
         stage_table(reinterpret_cast<uint2*>(smem + L.lut_k), a.tk.t.lut64, Pk, tid, nthr);
-        if (LUTV != 0) stage_table(reinterpret_cast<uint2*>(smem + LUTV), a.tv.t.lut64, Pv, tid, nthr);
+        if (LUTV != 0) {
+            stage_store(reinterpret_cast<uint2*>(smem + LUTV), lutv_e, Pv, tid, nthr);
+            stage_table(reinterpret_cast<uint2*>(smem + LUTV), a.tv.t.lut64, Pv, tid, nthr);
+        }
     }
     float* qt = reinterpret_cast<float*>(smem + L.waves);          // [G][d] scratch
     float* qscale = reinterpret_cast<float*>(smem + L.qscale);
     float* qsum = reinterpret_cast<float*>(smem + L.qsum);
     float* qmu = reinterpret_cast<float*>(smem + L.qmu);
     uint8_t* qlimb = smem + L.qlimb;
-    const int hq0 = h * G;
-    rotate_query_heads(a.q + ((int64_t)b * a.Hq + hq0) * kD, G, GP, wave, L.nw, lane, qt, qscale, qsum, a.rot_q);
+    // (a workgroup with fewer wavefronts than head slots loads the other
+    // heads here; the first head of a wavefront needs no wait on the records)
+    if (wave < G) {
+        // consumed here, not where loaded: a wait there would hold back the
+        // loads behind it
+        uint32_t w0 = qb0, w1 = qb1;
+        asm volatile("" : "+v"(w0), "+v"(w1));
+        rotate_query_head(bf16_to_f32((uint16_t)w0), bf16_to_f32((uint16_t)w1), wave, lane, qt, qscale, qsum,
+                          a.rot_q);
+    }
+    else if (wave < GP && lane == 0) qscale[wave] = qsum[wave] = 0.f;
+    for (int g = wave + L.nw; g < GP; g += L.nw) {
+        if (g >= G) {
+            if (lane == 0) qscale[g] = qsum[g] = 0.f;
+            continue;
+        }
+        const uint16_t* qh = a.q + ((int64_t)b * a.Hq + hq0 + g) * kD;
+        rotate_query_head(bf16_to_f32(qh[lane]), bf16_to_f32(qh[lane + 64]), g, lane, qt, qscale, qsum, a.rot_q);
+    }
     __syncthreads();
     for (int i = tid; i < GP * kD; i += nthr) {
         const int g = i / kD, j = i % kD;
@@ -369,7 +437,7 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     }
     {
         const int r = lane >> 5, c4 = 4 * (lane & 31);
-        for (int wi = 2 * wave + r, pass = 0; wi - r < nwin; wi += 2 * L.nw, ++pass) {
+        for (int wi = 2 * mwave + r, pass = 0; wi - r < nwin; wi += 2 * L.nw, ++pass) {
             float f[4] = {0.f, 0.f, 0.f, 0.f};
             if (mean_live(wi)) {
                 uint32_t mv = mv0;
@@ -676,30 +744,33 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     }
     __syncthreads();
     const int NC = a.nchunks;
-    // only the wavefronts that decoded a tile hold partials; their values are
-    // all requested before the first is used (the wavefront loop unrolled to
-    // the instantiation's bound, indexes clamped)
+    // only the wavefronts that decoded a tile hold partials; they are read in
+    // blocks of four whose loads are in flight together (indexes clamped)
     const int nwa = min(L.nw, ntiles);
     for (int i = tid; i < G * kD; i += nthr) {
         const int g = i / kD, j = i % kD;
-        float mv[WMAX], av[WMAX], lv[WMAX];
-#pragma unroll
-        for (int w = 0; w < WMAX; ++w) {
-            const int ww = min(w, nwa - 1);
-            mv[w] = mw[ww * GP + g];
-            av[w] = aw[(ww * GP + g) * kD + j];
-            lv[w] = lw[ww * GP + g];
-        }
         float M = -INFINITY;
+        for (int w0 = 0; w0 < nwa; w0 += 4) {
 #pragma unroll
-        for (int w = 0; w < WMAX; ++w) M = fmaxf(M, mv[w]);
+            for (int u = 0; u < 4; ++u) M = fmaxf(M, mw[min(w0 + u, nwa - 1) * GP + g]);
+        }
         float acc = 0.f, l = 0.f;
+        for (int w0 = 0; w0 < nwa; w0 += 4) {
+            float mv[4], av[4], lv[4];
 #pragma unroll
-        for (int w = 0; w < WMAX; ++w) {
-            if (w >= nwa || mv[w] == -INFINITY) continue;
-            const float e = exp2f(mv[w] - M);
-            acc += av[w] * e;
-            l += lv[w] * e;
+            for (int u = 0; u < 4; ++u) {
+                const int ww = min(w0 + u, nwa - 1);
+                mv[u] = mw[ww * GP + g];
+                av[u] = aw[(ww * GP + g) * kD + j];
+                lv[u] = lw[ww * GP + g];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (w0 + u >= nwa || mv[u] == -INFINITY) continue;
+                const float e = exp2f(mv[u] - M);
+                acc += av[u] * e;
+                l += lv[u] * e;
+            }
         }
         const int64_t slot = ((int64_t)b * a.Hq + hq0 + g) * (NC + kResSlots) + c;
         a.ws_acc[slot * kD + j] = acc;
@@ -776,11 +847,7 @@ __global__ __launch_bounds__(kWave) void attn_merge_kernel(const int32_t* __rest
     }
     float v0 = acc0 / l, v1 = acc1 / l;
     if (ws_hdr[3]) {           // inverse rotation of the value basis: H v / d
-        for (int hh = 1; hh < 64; hh <<= 1) {
-            const float p0 = __shfl_xor(v0, hh), p1 = __shfl_xor(v1, hh);
-            v0 = (lane & hh) ? p0 - v0 : v0 + p0;
-            v1 = (lane & hh) ? p1 - v1 : v1 + p1;
-        }
+        hadamard_lanes(v0, v1, lane);
         const float r0 = (v0 + v1) * (1.0f / kD), r1 = (v0 - v1) * (1.0f / kD);
         v0 = r0;
         v1 = r1;
@@ -962,11 +1029,7 @@ __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
         }
         float r0 = v0, r1 = v1;
         if (rotate) {
-            for (int hh = 1; hh < 64; hh <<= 1) {
-                const float p0 = __shfl_xor(v0, hh), p1 = __shfl_xor(v1, hh);
-                v0 = (lane & hh) ? p0 - v0 : v0 + p0;
-                v1 = (lane & hh) ? p1 - v1 : v1 + p1;
-            }
+            hadamard_lanes(v0, v1, lane);
             r0 = v0 + v1;
             r1 = v0 - v1;
         }
