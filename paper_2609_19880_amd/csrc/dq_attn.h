@@ -41,23 +41,26 @@ __device__ __forceinline__ void digits3(int v, int& d0, int& d1, int& d2) {
 // (unnormalized Hadamard, stages h = 1, 2, ..., 64 in the order of the
 // definition) and stores it into qt[g][128] fp32, with qscale[g] = max |q_rot| /
 // 2^22 and qsum[g] = sum of q_rot.  rotate = 0: keys arrive in the rotated
-// basis, and so does the query: it is taken as it is.
-__device__ __forceinline__ void rotate_query_head(float v0, float v1, int g, int lane, float* qt, float* qscale,
-                                                  float* qsum, int rotate) {
-    float r0 = v0, r1 = v1;
+// basis, and so does the query: it is taken as it is.  v0, v1 end as the
+// rotated channels; returns qscale[g].
+__device__ __forceinline__ float rotate_query_head(float& v0, float& v1, int g, int lane, float* qt, float* qscale,
+                                                   float* qsum, int rotate) {
     if (rotate) {
         hadamard_lanes(v0, v1, lane);
-        r0 = v0 + v1;
-        r1 = v0 - v1;
+        const float r0 = v0 + v1, r1 = v0 - v1;
+        v0 = r0;
+        v1 = r1;
     }
-    qt[g * 128 + lane] = r0;
-    qt[g * 128 + lane + 64] = r1;
-    const float mx = wave_max_f32(fmaxf(fabsf(r0), fabsf(r1)));
-    const float sm = wave_sum_f32(r0 + r1);
+    qt[g * 128 + lane] = v0;
+    qt[g * 128 + lane + 64] = v1;
+    const float mx = wave_max_f32(fmaxf(fabsf(v0), fabsf(v1)));
+    const float sm = wave_sum_f32(v0 + v1);
+    const float qs = mx * (1.0f / 4194304.0f);
     if (lane == 0) {
-        qscale[g] = mx * (1.0f / 4194304.0f);
+        qscale[g] = qs;
         qsum[g] = sm;
     }
+    return qs;
 }
 
 // All query heads of a workgroup, a wavefront per head: heads 0 .. nh - 1 of
@@ -73,8 +76,8 @@ __device__ __forceinline__ void rotate_query_heads(const uint16_t* q, int nh, in
             }
             continue;
         }
-        rotate_query_head(bf16_to_f32(q[g * 128 + lane]), bf16_to_f32(q[g * 128 + lane + 64]), g, lane, qt, qscale,
-                          qsum, rotate);
+        float v0 = bf16_to_f32(q[g * 128 + lane]), v1 = bf16_to_f32(q[g * 128 + lane + 64]);
+        rotate_query_head(v0, v1, g, lane, qt, qscale, qsum, rotate);
     }
 }
 

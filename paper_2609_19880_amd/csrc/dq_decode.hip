@@ -311,10 +311,16 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     //      query heads (neither depends on the sequence's length), then the
     //      first tile's records and key means
     const int hq0 = h * G;
+    // the tables go through the wavefronts that do not rotate a query head
+    // when those can hold every entry in registers (8 per thread), else
+    // through all of them
+    const int Pk = 1 << a.tk.p, Pv = LUTV != 0 ? 1 << a.tv.p : 0;
+    const int tw0 = (L.nw - G) * kWave * 8 >= max(Pk, Pv) ? G : 0;
+    const int ttid = tid - tw0 * kWave, tthr = nthr - tw0 * kWave;
     uint2 lut_e[8], lutv_e[8];
-    if (!FIXED) {
-        stage_load(lut_e, a.tk.t.lut64, 1 << a.tk.p, tid, nthr);
-        if (LUTV != 0) stage_load(lutv_e, a.tv.t.lut64, 1 << a.tv.p, tid, nthr);
+    if (!FIXED && wave >= tw0) {
+        stage_load(lut_e, a.tk.t.lut64, Pk, ttid, tthr);
+        if (LUTV != 0) stage_load(lutv_e, a.tv.t.lut64, Pv, ttid, tthr);
     }
     // wavefront g < G rotates query head g (channels l and l + 64 in lane l)
     uint16_t qb0 = 0, qb1 = 0;
@@ -386,13 +392,12 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     }
 
     // ---- prologue: tables, rotated query, its digits, q . mu per window
-    if (!FIXED) {
-        const int Pk = 1 << a.tk.p, Pv = 1 << a.tv.p;
-        stage_store(reinterpret_cast<uint2*>(smem + L.lut_k), lut_e, Pk, tid, nthr);
-        stage_table(reinterpret_cast<uint2*>(smem + L.lut_k), a.tk.t.lut64, Pk, tid, nthr);
+    if (!FIXED && wave >= tw0) {
+        stage_store(reinterpret_cast<uint2*>(smem + L.lut_k), lut_e, Pk, ttid, tthr);
+        stage_table(reinterpret_cast<uint2*>(smem + L.lut_k), a.tk.t.lut64, Pk, ttid, tthr);
         if (LUTV != 0) {
-            stage_store(reinterpret_cast<uint2*>(smem + LUTV), lutv_e, Pv, tid, nthr);
-            stage_table(reinterpret_cast<uint2*>(smem + LUTV), a.tv.t.lut64, Pv, tid, nthr);
+            stage_store(reinterpret_cast<uint2*>(smem + LUTV), lutv_e, Pv, ttid, tthr);
+            stage_table(reinterpret_cast<uint2*>(smem + LUTV), a.tv.t.lut64, Pv, ttid, tthr);
         }
     }
     float* qt = reinterpret_cast<float*>(smem + L.waves);          // [G][d] scratch
@@ -400,41 +405,52 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     float* qsum = reinterpret_cast<float*>(smem + L.qsum);
     float* qmu = reinterpret_cast<float*>(smem + L.qmu);
     uint8_t* qlimb = smem + L.qlimb;
-    // (a workgroup with fewer wavefronts than head slots loads the other
-    // heads here; the first head of a wavefront needs no wait on the records)
+    // wavefront g rotates query head g and forms its digits from the
+    // registers (slots past G get zero digits); a workgroup with fewer
+    // wavefronts than head slots loads the other heads here, the first head
+    // of a wavefront needs no wait on the records
+    auto head_digits = [&](float r0, float r1, float qs, int g) {
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+            const int j = lane + 64 * hh;
+            int v = 0;
+            if (qs > 0.f) {
+                v = (int)rintf((hh ? r1 : r0) / qs);
+                v = max(-4194304, min(4194304, v));
+            }
+            int d0, d1, d2;
+            digits3(v, d0, d1, d2);
+            uint8_t* dst = qlimb + ((j / 4) * GP + g) * 16 + (j % 4);
+            dst[0] = (uint8_t)d0;
+            dst[4] = (uint8_t)d1;
+            dst[8] = (uint8_t)d2;
+            dst[12] = 0;
+        }
+    };
     if (wave < G) {
         // consumed here, not where loaded: a wait there would hold back the
         // loads behind it
         uint32_t w0 = qb0, w1 = qb1;
         asm volatile("" : "+v"(w0), "+v"(w1));
-        rotate_query_head(bf16_to_f32((uint16_t)w0), bf16_to_f32((uint16_t)w1), wave, lane, qt, qscale, qsum,
-                          a.rot_q);
+        float v0 = bf16_to_f32((uint16_t)w0), v1 = bf16_to_f32((uint16_t)w1);
+        const float qs = rotate_query_head(v0, v1, wave, lane, qt, qscale, qsum, a.rot_q);
+        head_digits(v0, v1, qs, wave);
+    } else if (wave < GP) {
+        if (lane == 0) qscale[wave] = qsum[wave] = 0.f;
+        head_digits(0.f, 0.f, 0.f, wave);
     }
-    else if (wave < GP && lane == 0) qscale[wave] = qsum[wave] = 0.f;
     for (int g = wave + L.nw; g < GP; g += L.nw) {
         if (g >= G) {
             if (lane == 0) qscale[g] = qsum[g] = 0.f;
+            head_digits(0.f, 0.f, 0.f, g);
             continue;
         }
         const uint16_t* qh = a.q + ((int64_t)b * a.Hq + hq0 + g) * kD;
-        rotate_query_head(bf16_to_f32(qh[lane]), bf16_to_f32(qh[lane + 64]), g, lane, qt, qscale, qsum, a.rot_q);
+        float v0 = bf16_to_f32(qh[lane]), v1 = bf16_to_f32(qh[lane + 64]);
+        const float qs = rotate_query_head(v0, v1, g, lane, qt, qscale, qsum, a.rot_q);
+        head_digits(v0, v1, qs, g);
     }
     __syncthreads();
-    for (int i = tid; i < GP * kD; i += nthr) {
-        const int g = i / kD, j = i % kD;
-        int v = 0;
-        if (g < G && qscale[g] > 0.f) {
-            v = (int)rintf(qt[g * kD + j] / qscale[g]);
-            v = max(-4194304, min(4194304, v));
-        }
-        int d0, d1, d2;
-        digits3(v, d0, d1, d2);
-        uint8_t* dst = qlimb + ((j / 4) * GP + g) * 16 + (j % 4);
-        dst[0] = (uint8_t)d0;
-        dst[4] = (uint8_t)d1;
-        dst[8] = (uint8_t)d2;
-        dst[12] = 0;
-    }
     {
         const int r = lane >> 5, c4 = 4 * (lane & 31);
         for (int wi = 2 * mwave + r, pass = 0; wi - r < nwin; wi += 2 * L.nw, ++pass) {
@@ -451,15 +467,25 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
 #pragma unroll
                 for (int k = 0; k < 4; ++k) f[k] = sc * (float)(int8_t)((mv >> (8 * k)) & 0xFF);
             }
+            // every head slot at once, without branches (rows of slots past G
+            // hold no query: their sums are replaced by 0), so that the LDS
+            // reads and the half-wavefront sums of the slots overlap
+            float sg[GP];
 #pragma unroll
             for (int g = 0; g < GP; ++g) {
+                const float4 qv = *reinterpret_cast<const float4*>(qt + g * kD + c4);
                 float s = 0.f;
-                if (g < G) {
+                s = s + qv.x * f[0];
+                s = s + qv.y * f[1];
+                s = s + qv.z * f[2];
+                s = s + qv.w * f[3];
+                sg[g] = s;
+            }
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) s = s + qt[g * kD + c4 + k] * f[k];
-                    s = half_sum_f32(s);
-                }
-                if ((lane & 31) == 31 && wi < nwin) qmu[wi * GP + g] = s;
+            for (int g = 0; g < GP; ++g) sg[g] = half_sum_f32(sg[g]);
+            if ((lane & 31) == 31 && wi < nwin) {
+#pragma unroll
+                for (int g = 0; g < GP; ++g) qmu[wi * GP + g] = g < G ? sg[g] : 0.f;
             }
         }
     }
@@ -624,31 +650,44 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
         const float* qm = qmu + ((t / DQ_MEAN_WINDOW) - w0) * GP;
         float pscale[GP], corrs[GP];
         int pint[GP];
+        // four query heads at a time, their tile maxima reduced together
 #pragma unroll
-        for (int hg = 0; hg < HG; ++hg)
+        for (int hg = 0; hg < HG; ++hg) {
+            float score[4], tmax[4], pw[4], smax[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int g = 4 * hg + r;
                 const float dot = combine(dk[hg][0], dk[hg][1], dk[hg][2], r) * qscale[g];
-                const float score = (valid && g < G) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
-                const float tmax = wave_max_f32(score);
-                const float mn = fmaxf(m_run[g], tmax);
+                score[r] = (valid && g < G) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
+                tmax[r] = score[r];
+            }
+            wave_max4_f32(tmax);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int g = 4 * hg + r;
+                const float mn = fmaxf(m_run[g], tmax[r]);
                 // v_exp_f32 directly: arguments are <= 0 and results that would
                 // be denormal may flush to zero
                 const float corr = (m_run[g] == -INFINITY || mn == -INFINITY) ? (m_run[g] == mn ? 1.f : 0.f)
                                                                                : __builtin_amdgcn_exp2f(m_run[g] - mn);
-                const float p = (score == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(score - mn);
+                const float p = (score[r] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(score[r] - mn);
                 l_part[g] = l_part[g] * corr + p;
                 acco[g] = acco[g] * corr + p * ov;
                 corrs[g] = corr;
                 m_run[g] = mn;
-                const float pw = p * sv;                 // >= 0: scales are non-negative
-                const float smax = wave_max_f32(pw);
-                pscale[g] = smax * (1.0f / 4194304.0f);
-                // 22-bit fixed point of pw relative to the tile maximum
-                const float inv = smax > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax) : 0.f;
-                pint[g] = min(4194304, (int)rintf(pw * inv));
+                pw[r] = p * sv;                          // >= 0: scales are non-negative
+                smax[r] = pw[r];
             }
+            wave_max4_f32(smax);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int g = 4 * hg + r;
+                pscale[g] = smax[r] * (1.0f / 4194304.0f);
+                // 22-bit fixed point of pw relative to the tile maximum
+                const float inv = smax[r] > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax[r]) : 0.f;
+                pint[g] = min(4194304, (int)rintf(pw[r] * inv));
+            }
+        }
         // weight digits -> LDS, one 16-byte token row per slot group: byte
         // 4 r + d holds digit d of slot r (byte 4 r + 3 stays zero)
 #pragma unroll
