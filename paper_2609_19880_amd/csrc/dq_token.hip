@@ -98,32 +98,86 @@ struct TokArgs {
 //   r = b_pos << 24 | b_pos+1 << 16 | b_pos+2 << 8 | b_pos+3 (byte reverse)
 // r >> (29 - sh) puts the sh bits to shift in at bits 3 and up; what lands in
 // the low three bits of X is never read.  Each step reads at most 2 bytes, so
-// the second step's bytes are r << sh of the first.  Returns the two table
-// words (levels in their top bytes).
+// the second step's bytes are r << sh of the first.
+//
+// The two steps are split so that the key and value chains of a lane
+// overlap: tissue_a requests the ring dwords and the first table word,
+// tfinish_a completes the first step, tissue_b requests the second table
+// word, tfinish_b completes the second step.  The compiler does not see the
+// requested loads, so nothing may read their results until a twait<N> has run
+// on them: it waits until at most N LDS or scalar-memory operations are
+// outstanding (LDS returns in order; N counts the LDS reads issued after the
+// awaited one, and operations the compiler adds in between only make the wait
+// stricter).  The finish steps return the table words (levels in their top
+// bytes).
+struct TChain {
+    uint32_t X, pb, w;
+    uint64_t rr, e;      // pending: ring dwords (lo, hi), table word
+};
+
 template <uint32_t LUT_OFF>
-__device__ __forceinline__ void tstep2(uint32_t& X, uint32_t& pb, uint32_t ring_lane, uint32_t mask8, int p3,
-                                       uint32_t& e0, uint32_t& e1) {
+__device__ __forceinline__ void tissue_a(TChain& c, uint32_t ring_lane, uint32_t mask8) {
     uint32_t addr;
-    asm("v_lshl_add_u32 %0, %1, 8, %2" : "=v"(addr) : "v"(__builtin_amdgcn_ubfe(pb, 5, 3)), "v"(ring_lane));
-    const uint32_t lo = *LDS_PTR(const uint32_t, addr);
-    const uint32_t hi = *LDS_PTR(const uint32_t, addr + kRingRow);
-    const uint32_t w = __builtin_amdgcn_perm(0u, __builtin_amdgcn_alignbit(hi, lo, pb), 0x00010203u);
+    asm("v_lshl_add_u32 %0, %1, 8, %2" : "=v"(addr) : "v"(__builtin_amdgcn_ubfe(c.pb, 5, 3)), "v"(ring_lane));
+    asm volatile("ds_read2st64_b32 %0, %2 offset1:1\n\t"
+                 "ds_read_b64 %1, %3 offset:%4"
+                 : "=&v"(c.rr), "=&v"(c.e)
+                 : "v"(addr), "v"(c.X & mask8), "i"(LUT_OFF));
+}
 
-    const uint64_t ea = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
-    const uint32_t ya = __umul24((uint32_t)ea, X >> p3) + (uint32_t)(ea >> 32);
-    const uint32_t sha = (uint32_t)__builtin_clz(ya) & 24u;
-    const uint32_t qa = w >> (sha ^ 29u);
-    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(ya), "v"(sha), "v"(qa));
+template <uint32_t LUT_OFF>
+__device__ __forceinline__ void tissue_b(TChain& c, uint32_t mask8) {
+    asm volatile("ds_read_b64 %0, %1 offset:%2" : "=&v"(c.e) : "v"(c.X & mask8), "i"(LUT_OFF));
+}
 
-    const uint32_t wb = w << sha;
-    const uint64_t eb = *LDS_PTR(const uint64_t, (X & mask8) + LUT_OFF);
-    const uint32_t yb = __umul24((uint32_t)eb, X >> p3) + (uint32_t)(eb >> 32);
-    const uint32_t shb = (uint32_t)__builtin_clz(yb) & 24u;
-    const uint32_t qb = wb >> (shb ^ 29u);
-    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(X) : "v"(yb), "v"(shb), "v"(qb));
-    asm("v_add3_u32 %0, %1, %2, %3" : "=v"(pb) : "v"(pb), "v"(sha), "v"(shb));
-    e0 = (uint32_t)ea;
-    e1 = (uint32_t)eb;
+template <int N>
+__device__ __forceinline__ void twait_a(TChain& c) {
+    asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(c.rr), "+v"(c.e) : "i"(N));
+}
+
+template <int N>
+__device__ __forceinline__ void twait_b(TChain& c) {
+    asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(c.e) : "i"(N));
+}
+
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
+// The query digits of one group (16 bytes at LDS address a + off, off a
+// constant once unrolled), requested under the same rule: pending until a
+// twait_bq that follows it has run.
+__device__ __forceinline__ void qissue(uint32_t a, int off, v4u& q) {
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=&v"(q) : "v"(a), "i"(off));
+}
+
+template <int N, int HG>
+__device__ __forceinline__ void twait_bq(TChain& c, v4u (&q)[HG]) {
+    if constexpr (HG == 1)
+        asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(c.e), "+v"(q[0]) : "i"(N));
+    else
+        asm volatile("s_waitcnt lgkmcnt(%3)" : "+v"(c.e), "+v"(q[0]), "+v"(q[1]) : "i"(N));
+}
+
+// sh of the first step, kept for the second
+__device__ __forceinline__ uint32_t tfinish_a(TChain& c, int p3, uint32_t& sh) {
+    const uint32_t lo = (uint32_t)c.rr, hi = (uint32_t)(c.rr >> 32);
+    const uint32_t w = __builtin_amdgcn_perm(0u, __builtin_amdgcn_alignbit(hi, lo, c.pb), 0x00010203u);
+    const uint32_t ea = (uint32_t)c.e;
+    const uint32_t y = __umul24(ea, c.X >> p3) + (uint32_t)(c.e >> 32);
+    sh = (uint32_t)__builtin_clz(y) & 24u;
+    const uint32_t q = w >> (sh ^ 29u);
+    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(c.X) : "v"(y), "v"(sh), "v"(q));
+    c.w = w << sh;
+    return ea;
+}
+
+__device__ __forceinline__ uint32_t tfinish_b(TChain& c, int p3, uint32_t sha) {
+    const uint32_t eb = (uint32_t)c.e;
+    const uint32_t y = __umul24(eb, c.X >> p3) + (uint32_t)(c.e >> 32);
+    const uint32_t sh = (uint32_t)__builtin_clz(y) & 24u;
+    const uint32_t q = c.w >> (sh ^ 29u);
+    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(c.X) : "v"(y), "v"(sh), "v"(q));
+    asm("v_add3_u32 %0, %1, %2, %3" : "=v"(c.pb) : "v"(c.pb), "v"(sha), "v"(sh));
+    return eb;
 }
 
 // rec: the lane's first chunk (tile + 8 lane); chunks are 512 bytes apart.
@@ -322,8 +376,10 @@ __global__ __launch_bounds__(tok_waves(HG) * kWave) void attn_token_kernel(TokAr
         put_chunk(ring_v, 3, v3);
         uint32_t nck = 4, ncv = 4;
         uint32_t thrk = 8u * (8u * 4u - 20u) - 1u, thrv = thrk;
-        uint32_t xk = k0.y << 3, xv = v0.y << 3;
-        uint32_t pbk = 64, pbv = 64;                // payload starts at byte 8
+        TChain ck, cv;
+        ck.X = k0.y << 3;
+        cv.X = v0.y << 3;
+        ck.pb = cv.pb = 64;                         // payload starts at byte 8
         const float sk = half_lo(k0.x), ok = half_hi(k0.x);
         const float sv = half_lo(v0.x), ov = half_hi(v0.x);
         const float* qm = qmu + ((t / DQ_MEAN_WINDOW) - w0) * Hq;
@@ -336,31 +392,61 @@ __global__ __launch_bounds__(tok_waves(HG) * kWave) void attn_token_kernel(TokAr
 #pragma unroll
             for (int hg = 0; hg < HG; ++hg) dk[hg][0] = dk[hg][1] = dk[hg][2] = v4i{0, 0, 0, 0};
             uint32_t vlev[kGroups];
-            const uint8_t* qh = qlimb + (h * kGroups * GS + (lane & 3)) * 16;
-            uint4 ql[HG];                               // digits of group 0; then one group ahead
-#pragma unroll
-            for (int hg = 0; hg < HG; ++hg) ql[hg] = *reinterpret_cast<const uint4*>(qh + hg * 4 * 16);
+            // the digits of group g are requested in its last step pair, so
+            // that the wait for the value step covers them too
+            const uint32_t q_lane = (uint32_t)L.qlimb + (uint32_t)(h * kGroups * GS + (lane & 3)) * 16;
+            v4u qd[HG];
+            // steps in blocks of 8 (two groups): the rings are refilled after
+            // each block, so the block's last reads are awaited (and the next
+            // block's requested) after the refill; inside a block, step pair u
+            // of both chains: wait for the key chain's first reads (the value
+            // chain's follow: 2), finish, request its second table word; the
+            // same for the value chain (the key chain's word follows: 1); then
+            // the second steps (1, and 2 or 0 at the block's end)
 #pragma unroll
             for (int grp = 0; grp < kGroups; ++grp) {
-                uint32_t k0s, k1s, k2s, k3s, v0s, v1s, v2s, v3s;
-                tstep2<0>(xk, pbk, ring_k, mask8k, pk3, k0s, k1s);
-                tstep2<LUTV>(xv, pbv, ring_v, mask8v, pv3, v0s, v1s);
-                tstep2<0>(xk, pbk, ring_k, mask8k, pk3, k2s, k3s);
-                tstep2<LUTV>(xv, pbv, ring_v, mask8v, pv3, v2s, v3s);
-                const uint32_t lk = pack4(k0s, k1s, k2s, k3s);
-                vlev[grp] = pack4(v0s, v1s, v2s, v3s);
+                if ((grp & 1) == 0) {
+                    tissue_a<0>(ck, ring_k, mask8k);
+                    tissue_a<LUTV>(cv, ring_v, mask8v);
+                }
+                uint32_t kw[4], vw[4];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const bool more = !((grp & 1) && u == 1);
+                    uint32_t shk, shv;
+                    twait_a<2>(ck);
+                    kw[2 * u] = tfinish_a(ck, pk3, shk);
+                    tissue_b<0>(ck, mask8k);
+                    twait_a<1>(cv);
+                    vw[2 * u] = tfinish_a(cv, pv3, shv);
+                    tissue_b<LUTV>(cv, mask8v);
+                    twait_b<1>(ck);
+                    kw[2 * u + 1] = tfinish_b(ck, pk3, shk);
+                    if (u == 1) {
+                        qissue(q_lane, (grp * GS) * 16, qd[0]);
+                        if constexpr (HG == 2) qissue(q_lane, (grp * GS + 4) * 16, qd[1]);
+                    }
+                    if (more) tissue_a<0>(ck, ring_k, mask8k);
+                    if (u == 0) twait_b<2>(cv);
+                    else if (more) twait_bq<2>(cv, qd);
+                    else twait_bq<0>(cv, qd);
+                    vw[2 * u + 1] = tfinish_b(cv, pv3, shv);
+                    if (more) tissue_a<LUTV>(cv, ring_v, mask8v);
+                }
+                const uint32_t lk = pack4(kw[0], kw[1], kw[2], kw[3]);
+                vlev[grp] = pack4(vw[0], vw[1], vw[2], vw[3]);
                 asm volatile("" : "+v"(vlev[grp]));
 #pragma unroll
                 for (int hg = 0; hg < HG; ++hg) {
-                    dk[hg][0] = mfma(ql[hg].x, lk, dk[hg][0]);
-                    dk[hg][1] = mfma(ql[hg].y, lk, dk[hg][1]);
-                    dk[hg][2] = mfma(ql[hg].z, lk, dk[hg][2]);
-                    if (grp + 1 < kGroups)
-                        ql[hg] = *reinterpret_cast<const uint4*>(qh + ((grp + 1) * GS + hg * 4) * 16);
+                    dk[hg][0] = mfma(qd[hg].x, lk, dk[hg][0]);
+                    dk[hg][1] = mfma(qd[hg].y, lk, dk[hg][1]);
+                    dk[hg][2] = mfma(qd[hg].z, lk, dk[hg][2]);
                 }
                 if (grp & 1) {
-                    refill2(pbk, nck, thrk, nk, ring_k, kr, last_k, pbv, ncv, thrv, nv, ring_v, vr, last_v);
-                    refill2(pbk, nck, thrk, nk, ring_k, kr, last_k, pbv, ncv, thrv, nv, ring_v, vr, last_v);
+                    refill2(ck.pb, nck, thrk, nk, ring_k, kr, last_k, cv.pb, ncv, thrv, nv, ring_v, vr, last_v);
+                    refill2(ck.pb, nck, thrk, nk, ring_k, kr, last_k, cv.pb, ncv, thrv, nv, ring_v, vr, last_v);
+                    // the next block's ring reads come after these writes
+                    asm volatile("" ::: "memory");
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -368,29 +454,45 @@ __global__ __launch_bounds__(tok_waves(HG) * kWave) void attn_token_kernel(TokAr
             // ---- scores of the head's query heads and the online softmax
             float corr[GS], pscale[GS];
             int pint[GS];
+            // four slots at a time, their tile maxima reduced together
 #pragma unroll
-            for (int r = 0; r < GS; ++r) {
-                const bool live = r < G;
-                const int g = live ? h * G + r : 0;       // slots past G take no query head
-                const int slot = h * GS + r;
-                const float dot = combine(dk[r / 4][0], dk[r / 4][1], dk[r / 4][2], r % 4) * qscale[g];
-                const float score = (valid && live) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
-                const float tmax = wave_max_f32(score);
-                const float m_old = lane_get(m_vec, slot);
-                const float mn = fmaxf(m_old, tmax);
-                corr[r] = (m_old == -INFINITY || mn == -INFINITY) ? (m_old == mn ? 1.f : 0.f)
-                                                                  : __builtin_amdgcn_exp2f(m_old - mn);
-                const float p = (score == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(score - mn);
-                const float lt = wave_sum_f32(p);
-                const float ot = wave_sum_f32(p * ov);
-                m_vec = lane_set(m_vec, slot, mn, lane);
-                l_vec = lane_set(l_vec, slot, lane_get(l_vec, slot) * corr[r] + lt, lane);
-                o_vec = lane_set(o_vec, slot, lane_get(o_vec, slot) * corr[r] + ot, lane);
-                const float pw = p * sv;                 // >= 0: scales are non-negative
-                const float smax = wave_max_f32(pw);
-                pscale[r] = smax * (1.0f / 4194304.0f);
-                const float inv = smax > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax) : 0.f;
-                pint[r] = min(4194304, (int)rintf(pw * inv));
+            for (int hg = 0; hg < HG; ++hg) {
+                float score[4], tmax[4], pw[4], smax[4];
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int r = 4 * hg + rr;
+                    const bool live = r < G;
+                    const int g = live ? h * G + r : 0;       // slots past G take no query head
+                    const float dot = combine(dk[hg][0], dk[hg][1], dk[hg][2], rr) * qscale[g];
+                    score[rr] = (valid && live) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
+                    tmax[rr] = score[rr];
+                }
+                wave_max4_f32(tmax);
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int r = 4 * hg + rr;
+                    const int slot = h * GS + r;
+                    const float m_old = lane_get(m_vec, slot);
+                    const float mn = fmaxf(m_old, tmax[rr]);
+                    corr[r] = (m_old == -INFINITY || mn == -INFINITY) ? (m_old == mn ? 1.f : 0.f)
+                                                                      : __builtin_amdgcn_exp2f(m_old - mn);
+                    const float p = (score[rr] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(score[rr] - mn);
+                    const float lt = wave_sum_f32(p);
+                    const float ot = wave_sum_f32(p * ov);
+                    m_vec = lane_set(m_vec, slot, mn, lane);
+                    l_vec = lane_set(l_vec, slot, lane_get(l_vec, slot) * corr[r] + lt, lane);
+                    o_vec = lane_set(o_vec, slot, lane_get(o_vec, slot) * corr[r] + ot, lane);
+                    pw[rr] = p * sv;                          // >= 0: scales are non-negative
+                    smax[rr] = pw[rr];
+                }
+                wave_max4_f32(smax);
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int r = 4 * hg + rr;
+                    pscale[r] = smax[rr] * (1.0f / 4194304.0f);
+                    const float inv = smax[rr] > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax[rr]) : 0.f;
+                    pint[r] = min(4194304, (int)rintf(pw[rr] * inv));
+                }
             }
             // weight digits -> LDS, one 16-byte token row per slot group: byte
             // 4 r + d holds digit d of slot r (byte 4 r + 3 stays zero)
@@ -460,8 +562,8 @@ __global__ __launch_bounds__(tok_waves(HG) * kWave) void attn_token_kernel(TokAr
 #pragma unroll
                     for (int cb = 0; cb < 4; ++cb) acc[s][hg][cb] = rot1(acc[s][hg][cb]);
         // every stream ends at x = L having read no byte past its record
-        corrupt |= valid && ((xk >> 3) != kRansL || pbk > endk);
-        corrupt |= valid && ((xv >> 3) != kRansL || pbv > endv);
+        corrupt |= valid && ((ck.X >> 3) != kRansL || ck.pb > endk);
+        corrupt |= valid && ((cv.X >> 3) != kRansL || cv.pb > endv);
     }
     if (__any(corrupt) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_CORRUPT);
     if (PAGED && __any(bad_page) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_PAGE);
