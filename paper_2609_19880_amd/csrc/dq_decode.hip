@@ -821,9 +821,13 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
 }
 
 // One wavefront per (query head, sequence): lane l combines channels l and
-// l + 64 of every partial, so no barrier is needed anywhere.  The partials'
-// maxima and their first 8 accumulator rows are requested together, right
-// after the header.
+// l + 64 of every partial, so no barrier is needed anywhere.  Lane i holds
+// the maximum and sum of partial i (of the first 64); the accumulator rows
+// of up to kMergeBatch partials are requested together with them, right
+// after the header: one memory round trip for the usual counts (b1_t128k: 32
+// chunks + 4 residual slots), a further one per batch beyond.
+constexpr int kMergeBatch = 32;
+
 __global__ __launch_bounds__(kWave) void attn_merge_kernel(const int32_t* __restrict__ ws_hdr,
                                                            const float* __restrict__ ws_m,
                                                            const float* __restrict__ ws_l,
@@ -846,42 +850,53 @@ __global__ __launch_bounds__(kWave) void attn_merge_kernel(const int32_t* __rest
         dst[lane + 64] = 0.f;
         return;
     }
-    // batch 0 of the accumulator rows (index clamped: loads unconditional)
-    float a0[8], a1[8], mv[8], lv[8];
+    // every load of the first round at once (indexes clamped: unconditional)
+    const int64_t sl = slot_of(min(lane, np - 1));
+    const float m_lane = lane < np ? ws_m[sl] : -INFINITY;
+    const float l_lane = lane < np ? ws_l[sl] : 0.f;
+    float a0[kMergeBatch], a1[kMergeBatch];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < kMergeBatch; ++u) {
         const int64_t s = slot_of(min(u, np - 1));
         a0[u] = ws_acc[s * kD + lane];
         a1[u] = ws_acc[s * kD + lane + 64];
-        mv[u] = ws_m[s];
-        lv[u] = ws_l[s];
     }
-    float M = -INFINITY;
-    for (int i = lane; i < np; i += kWave) M = fmaxf(M, ws_m[slot_of(i)]);
+    float M = m_lane;
+    for (int i = lane + kWave; i < np; i += kWave) M = fmaxf(M, ws_m[slot_of(i)]);
     M = wave_max_f32(M);
     if (M == -INFINITY) {      // no token at all
         dst[lane] = 0.f;
         dst[lane + 64] = 0.f;
         return;
     }
-    float acc0 = 0.f, acc1 = 0.f, l = 0.f;
+    // weight of partial i: lane i for the first 64, computed in place beyond
+    const float e_lane = lane < np ? exp2f(m_lane - M) : 0.f;
+    float l = wave_sum_f32(l_lane * e_lane);
+    float acc0 = 0.f, acc1 = 0.f;
     for (int i0 = 0;;) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const float e = i0 + u < np ? exp2f(mv[u] - M) : 0.f;
+        for (int u = 0; u < kMergeBatch; ++u) {
+            const int i = i0 + u;
+            float e = 0.f;
+            if (i < np) {
+                if (i < kWave) {
+                    e = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(e_lane), i));
+                } else {
+                    const int64_t s = slot_of(i);
+                    e = exp2f(ws_m[s] - M);
+                    l += ws_l[s] * e;
+                }
+            }
             acc0 += a0[u] * e;
             acc1 += a1[u] * e;
-            l += lv[u] * e;
         }
-        i0 += 8;
+        i0 += kMergeBatch;
         if (i0 >= np) break;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < kMergeBatch; ++u) {
             const int64_t s = slot_of(min(i0 + u, np - 1));
             a0[u] = ws_acc[s * kD + lane];
             a1[u] = ws_acc[s * kD + lane + 64];
-            mv[u] = ws_m[s];
-            lv[u] = ws_l[s];
         }
     }
     float v0 = acc0 / l, v1 = acc1 / l;
