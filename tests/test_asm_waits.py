@@ -78,7 +78,7 @@ def check_function(body):
         if s == ";;#ASMEND":
             in_asm = False
             continue
-        if not line[:1].isspace() and s.endswith(":"):   # a label: control may arrive from elsewhere
+        if not line[:1].isspace() and s.split(";")[0].strip().endswith(":"):   # a label: control may arrive from elsewhere
             if pending:
                 problems.append((no, "label while asm reads are pending", s))
                 pending = []
@@ -108,7 +108,7 @@ def check_function(body):
 
 
 def _fn(lines):
-    return [l if l.endswith(":") else "\t" + l for l in lines]
+    return [l if l.split(";")[0].strip().endswith(":") else "\t" + l for l in lines]
 
 
 def test_checker_catches_planted_mistakes():
@@ -128,6 +128,8 @@ def test_checker_catches_planted_mistakes():
     assert not ok(read + ["v_mfma_i32_4x4x4_16b_i8 a[0:3], v9, v[2:3], a[0:3]"])
     assert not ok(read + ["s_cbranch_scc1 .LBB0_2", "s_waitcnt lgkmcnt(0)"])
     assert not ok(read + [".LBB0_2:", "s_waitcnt lgkmcnt(0)"])
+    assert not ok(read + [".LBB0_3:                                ; =>This Inner Loop Header: Depth=1",
+                          "s_waitcnt lgkmcnt(0)"])
     # registers elsewhere are free to use
     assert ok(read + ["v_mov_b32 v9, v4", "s_waitcnt lgkmcnt(0)"] + use)
 
