@@ -583,6 +583,12 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
             dissue<0>(xk, pq, mask8k, 0, rk_, ek_);
             dissue<LUTV>(xv, pv, mask8v, 0, rv_, ev_);
         }
+        // A wavefront in the decode runs at a raised priority: its two
+        // dependent chains issue first whenever they are ready, and the
+        // softmax, P . v and pair building of the other wavefronts, which have
+        // more independent work, fill the slots in between (7 % less time at
+        // 16 wavefronts than at one priority for all).
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int grp = 0; grp < kD / 4; ++grp) {
             uint32_t lk;
@@ -643,6 +649,7 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
             corrupt |= valid && ((xv >> 3) != kRansL || pv > pv_end);
         }
 
+        __builtin_amdgcn_s_setprio(0);
         // ---- scores (Eq. fold-key) and online softmax; the value scale is
         //      folded into the weight (Eq. fold-value)
         const float sk = half_lo(hk0), ok = half_hi(hk0);
