@@ -444,7 +444,10 @@ __global__ __launch_bounds__(tok_waves(HG) * kWave) void attn_token_kernel(TokAr
                 }
                 if (grp & 1) {
                     refill2(ck.pb, nck, thrk, nk, ring_k, kr, last_k, cv.pb, ncv, thrv, nv, ring_v, vr, last_v);
-                    refill2(ck.pb, nck, thrk, nk, ring_k, kr, last_k, cv.pb, ncv, thrv, nv, ring_v, vr, last_v);
+                    // a second chunk only where a lane is still short (rare): the
+                    // test is one wavefront vote, so blocks where none is skip it
+                    if (__any(ck.pb > thrk || cv.pb > thrv))
+                        refill2(ck.pb, nck, thrk, nk, ring_k, kr, last_k, cv.pb, ncv, thrv, nv, ring_v, vr, last_v);
                     // the next block's ring reads come after these writes
                     asm volatile("" ::: "memory");
                 }
