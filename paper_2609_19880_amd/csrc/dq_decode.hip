@@ -927,7 +927,8 @@ __global__ __launch_bounds__(kWave) void attn_merge_kernel(const int32_t* __rest
 constexpr int kResThreads = 256;
 constexpr int kMaxResidual = 256;
 constexpr int kMaxGroup = 8;
-constexpr int kResPart = kMaxResidual / kResSlots;   // tokens per workgroup (64)
+constexpr int kResWaves = 2;                          // wavefronts per part
+constexpr int kResWaveTokens = kMaxResidual / kResSlots / kResWaves;   // at most 32 per wavefront
 
 struct ResArgs {
     const uint16_t* q;
@@ -943,21 +944,136 @@ struct ResArgs {
     float* ws_acc;
 };
 
-// One workgroup per (part, KV head, sequence); the r residual tokens of a
-// sequence are cut into kResSlots parts of ceil(r / kResSlots) <= 64 tokens.
-// Every key and value row of the part is requested at the
-// start (one memory round trip); then the logits of the G query heads, the
-// softmax statistics of the part, the weighted sum of its raw values, and the
-// rotation H of that sum so that the merge's inverse rotation H / d returns it
-// (H H = d I); without that rotation when the values were coded in the
-// caller's basis (the merge then leaves the output as it is).  The result is
-// one more split-K partial, in slot NC + i; a part without tokens writes
-// m = -inf and zeros.
-__global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
-    __shared__ __align__(16) float qs[kMaxGroup][kD];
-    __shared__ float sc[kMaxGroup][kResPart];
-    __shared__ float pq[kResThreads / 32][kMaxGroup][kD];
-    __shared__ float stat[2][kMaxGroup];
+// Maximum and sum over each row of 16 lanes; every lane of the row ends with
+// the row's result.
+__device__ __forceinline__ float row_max_f32(float v) {
+    v = fmaxf(v, dpp_step<0xB1, 0xF>(v));    // quad_perm [1, 0, 3, 2]
+    v = fmaxf(v, dpp_step<0x4E, 0xF>(v));    // quad_perm [2, 3, 0, 1]
+    v = fmaxf(v, dpp_step<0x141, 0xF>(v));   // row_half_mirror
+    return fmaxf(v, dpp_step<0x140, 0xF>(v));   // row_mirror
+}
+__device__ __forceinline__ float row_sum_f32(float v) {
+    v += dpp_step<0xB1, 0xF>(v);
+    v += dpp_step<0x4E, 0xF>(v);
+    v += dpp_step<0x141, 0xF>(v);
+    return v + dpp_step<0x140, 0xF>(v);
+}
+
+// bf16 pairs a . b + c in fp32 (v_dot2c_f32_bf16)
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c,
+                                           false);
+}
+
+// Softmax partial of nw <= NT raw tokens (ring positions ring0 + i, wrapping
+// at r_cap) for the G query heads of KV head h, in one wavefront:
+// * logits: lane l takes tokens l % 16 (+ 16) and channels 32 (l / 16) .. + 31,
+//   bf16 pair products summed in fp32, then summed over the four rows with
+//   lane swaps; every row then holds every logit;
+// * statistics per head over the row (DPP), weights to p_lds[g][token];
+// * values: lane l takes channels 2 l and 2 l + 1 of every token and the
+//   weights from LDS (one broadcast read per 4 tokens and head).
+// Every load is requested before the first is used (one memory round trip).
+template <int NT>
+__device__ __forceinline__ void residual_wave(const ResArgs& a, int b, int h, int ring0, int nw, int lane,
+                                              float (*p_lds)[kResWaveTokens], float (&acc)[kMaxGroup][2],
+                                              float (&mx)[kMaxGroup], float (&sm)[kMaxGroup]) {
+    constexpr int NS = NT / 16;
+    const int G = a.G, ti = lane & 15, cq = lane >> 4;
+    const int64_t row0 = ((int64_t)b * a.Hkv + h) * a.r_cap;
+    auto row = [&](int i) {           // ring slot of token min(i, nw - 1) (ring0 + i < 2 r_cap)
+        const int s = ring0 + min(i, nw - 1);
+        return row0 + (s < a.r_cap ? s : s - a.r_cap);
+    };
+    uint4 kr[NS][4];
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+        const uint4* src = reinterpret_cast<const uint4*>(a.rk + row(ti + 16 * j) * kD + 32 * cq);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) kr[j][u] = src[u];
+    }
+    uint4 qr[kMaxGroup][4];
+#pragma unroll
+    for (int g = 0; g < kMaxGroup; ++g) {
+        if (g < G) {
+            const uint4* src = reinterpret_cast<const uint4*>(a.q + ((int64_t)b * a.Hq + h * G + g) * kD + 32 * cq);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) qr[g][u] = src[u];
+        }
+    }
+    uint32_t vr[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) vr[t] = *reinterpret_cast<const uint32_t*>(a.rv + row(t) * kD + 2 * lane);
+
+#pragma unroll
+    for (int g = 0; g < kMaxGroup; ++g) {
+        if (g < G) {
+            float s[NS];
+#pragma unroll
+            for (int j = 0; j < NS; ++j) {
+                float d = 0.f;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    d = dot2_bf16(qr[g][u].x, kr[j][u].x, d);
+                    d = dot2_bf16(qr[g][u].y, kr[j][u].y, d);
+                    d = dot2_bf16(qr[g][u].z, kr[j][u].z, d);
+                    d = dot2_bf16(qr[g][u].w, kr[j][u].w, d);
+                }
+                d += xor_lane<16>(d, lane);
+                d += xor_lane<32>(d, lane);
+                s[j] = ti + 16 * j < nw ? d * a.scale_log2 : -INFINITY;
+            }
+            float m = s[0];
+#pragma unroll
+            for (int j = 1; j < NS; ++j) m = fmaxf(m, s[j]);
+            m = row_max_f32(m);
+            float l = 0.f;
+#pragma unroll
+            for (int j = 0; j < NS; ++j) {
+                s[j] = exp2f(s[j] - m);
+                l += s[j];
+                if (cq == 0) p_lds[g][ti + 16 * j] = s[j];
+            }
+            mx[g] = m;
+            sm[g] = row_sum_f32(l);
+        }
+    }
+    // the weights were written by lanes of this wavefront, whose LDS
+    // operations complete in order
+    wave_sync();
+#pragma unroll
+    for (int g = 0; g < kMaxGroup; ++g) acc[g][0] = acc[g][1] = 0.f;
+#pragma unroll
+    for (int t4 = 0; t4 < NT; t4 += 4) {
+#pragma unroll
+        for (int g = 0; g < kMaxGroup; ++g) {
+            if (g < G) {
+                const float4 p = *reinterpret_cast<const float4*>(&p_lds[g][t4]);
+                const float pw[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[g][0] += pw[e] * __uint_as_float(vr[t4 + e] << 16);
+                    acc[g][1] += pw[e] * __uint_as_float(vr[t4 + e] & 0xFFFF0000u);
+                }
+            }
+        }
+    }
+}
+
+// One workgroup of two wavefronts per (part, KV head, sequence); the r
+// residual tokens of a sequence are cut into kResSlots parts of
+// ceil(r / kResSlots) <= 64 tokens, and each part into two halves, one per
+// wavefront (residual_wave).  The second wavefront hands its maxima, sums and
+// weighted values to the first through LDS, which merges them, rotates the
+// sum by H so that the merge's inverse rotation H / d returns it (H H = d I;
+// not when the values were coded in the caller's basis: the merge then leaves
+// the output as it is) and writes one more split-K partial, in slot NC + part.
+// A part without tokens writes m = -inf and zeros.
+__global__ __launch_bounds__(kResWaves * kWave) void attn_residual_kernel(ResArgs a) {
+    __shared__ __align__(16) float p_lds[kResWaves][kMaxGroup][kResWaveTokens];
+    __shared__ float2 x_acc[kMaxGroup][kWave];
+    __shared__ float x_m[kMaxGroup], x_l[kMaxGroup];
     const int part = blockIdx.x, h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
     const int lane = tid & (kWave - 1), wave = tid / kWave;
     const int G = a.G, NC = a.ws_hdr[1], rotate = a.ws_hdr[3];
@@ -966,140 +1082,78 @@ __global__ __launch_bounds__(kResThreads) void attn_residual_kernel(ResArgs a) {
     const int ps = (r + kResSlots - 1) / kResSlots;
     const int t0 = part * ps;
     const int n = max(0, min(ps, r - t0));
-    const int hq0 = h * G;
-    const int64_t slot0 = ((int64_t)b * a.Hq + hq0) * (NC + kResSlots) + NC + part;
+    const int64_t slot0 = ((int64_t)b * a.Hq + h * G) * (NC + kResSlots) + NC + part;
     if (n == 0) {
-        for (int i = tid; i < G * kD; i += kResThreads) {
-            const int g = i / kD, j = i % kD;
-            const int64_t slot = slot0 + (int64_t)g * (NC + kResSlots);
-            a.ws_acc[slot * kD + j] = 0.f;
-            if (j == 0) {
-                a.ws_m[slot] = -INFINITY;
-                a.ws_l[slot] = 0.f;
+        if (wave == 0) {
+            for (int g = 0; g < G; ++g) {
+                const int64_t slot = slot0 + (int64_t)g * (NC + kResSlots);
+                *reinterpret_cast<float2*>(&a.ws_acc[slot * kD + 2 * lane]) = float2{0.f, 0.f};
+                if (lane == 0) {
+                    a.ws_m[slot] = -INFINITY;
+                    a.ws_l[slot] = 0.f;
+                }
             }
         }
         return;
     }
-    const int first = max(0, a.seq_lens[b]) % a.r_cap;
-    const int64_t row0 = ((int64_t)b * a.Hkv + h) * a.r_cap;
-    // ring slot of token i < n of the part (first + t0 + i < 2 r_cap)
-    auto ring = [&](int i) {
-        const int s = first + t0 + i;
-        return s < a.r_cap ? s : s - a.r_cap;
-    };
-
-    // ---- every load of the workgroup in flight together: thread tid takes
-    //      channels 32 (tid % 4) .. + 31 of key row tid / 4, and channels
-    //      4 (tid % 32) .. + 3 of value rows 8 (tid / 32) .. + 7 (rows past the
-    //      part read its last token and are given weight 0)
-    const int kt = tid >> 2, kc = 32 * (tid & 3);
-    const int vc = 4 * (tid & 31), vg = tid >> 5;
-    uint4 kr[4];
-    {
-        const uint4* src = reinterpret_cast<const uint4*>(a.rk + (row0 + ring(min(kt, n - 1))) * kD + kc);
+    // halves: the first wavefront takes ceil(n / 2) >= 1 tokens, the second the rest
+    const int nh = (n + 1) / 2;
+    const int nw = wave ? n - nh : nh;
+    const int ring0 = max(0, a.seq_lens[b]) % a.r_cap + t0 + (wave ? nh : 0);
+    float acc[kMaxGroup][2], mx[kMaxGroup], sm[kMaxGroup];
+    if (nw > 16) {
+        residual_wave<32>(a, b, h, ring0, nw, lane, p_lds[wave], acc, mx, sm);
+    } else if (nw > 0) {
+        residual_wave<16>(a, b, h, ring0, nw, lane, p_lds[wave], acc, mx, sm);
+    } else {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) kr[u] = src[u];
-    }
-    uint2 vr[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-        vr[u] = *reinterpret_cast<const uint2*>(a.rv + (row0 + ring(min(8 * vg + u, n - 1))) * kD + vc);
-    for (int i = tid; i < G * kD; i += kResThreads)
-        qs[i / kD][i % kD] = bf16_to_f32(a.q[((int64_t)b * a.Hq + hq0) * kD + i]);
-    __syncthreads();
-
-    // ---- logits: quarter dot products, summed over the lane quad
-    {
-        float dot[kMaxGroup];
-#pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g) dot[g] = 0.f;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const uint32_t ww[4] = {kr[u].x, kr[u].y, kr[u].z, kr[u].w};
-#pragma unroll
-            for (int g = 0; g < kMaxGroup; ++g) {
-                if (g < G) {
-                    const float4 qa = *reinterpret_cast<const float4*>(&qs[g][kc + 8 * u]);
-                    const float4 qb = *reinterpret_cast<const float4*>(&qs[g][kc + 8 * u + 4]);
-                    const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        dot[g] += qv[e] * __uint_as_float((e & 1) ? (ww[e >> 1] & 0xFFFF0000u) : (ww[e >> 1] << 16));
-                }
-            }
+        for (int g = 0; g < kMaxGroup; ++g) {
+            acc[g][0] = acc[g][1] = 0.f;
+            mx[g] = -INFINITY;
+            sm[g] = 0.f;
         }
+    }
+    if (wave == 1) {
 #pragma unroll
         for (int g = 0; g < kMaxGroup; ++g) {
             if (g < G) {
-                float v = dot[g];
-                v += dpp_step<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
-                v += dpp_step<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
-                if ((tid & 3) == 0) sc[g][kt] = kt < n ? v * a.scale_log2 : -INFINITY;
-            }
-        }
-    }
-    __syncthreads();
-    // ---- softmax statistics of the part, a wavefront per head
-    for (int g = wave; g < G; g += kResThreads / kWave) {
-        const float v = sc[g][lane];
-        const float mx = wave_max(v);
-        const float p = lane < n ? exp2f(v - mx) : 0.f;
-        sc[g][lane] = p;
-        const float sum = wave_sum_f32(p);
-        if (lane == 0) {
-            stat[0][g] = mx;
-            stat[1][g] = sum;
-        }
-    }
-    __syncthreads();
-    // ---- weighted values: 8 tokens x 4 channels per thread
-    {
-        float acc[kMaxGroup][4];
-#pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g)
-#pragma unroll
-            for (int k = 0; k < 4; ++k) acc[g][k] = 0.f;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int t = 8 * vg + u;
-            const float v[4] = {__uint_as_float(vr[u].x << 16), __uint_as_float(vr[u].x & 0xFFFF0000u),
-                                __uint_as_float(vr[u].y << 16), __uint_as_float(vr[u].y & 0xFFFF0000u)};
-#pragma unroll
-            for (int g = 0; g < kMaxGroup; ++g) {
-                if (g < G) {
-                    const float w = t < n ? sc[g][t] : 0.f;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) acc[g][k] += w * v[k];
+                x_acc[g][lane] = float2{acc[g][0], acc[g][1]};
+                if (lane == 0) {
+                    x_m[g] = mx[g];
+                    x_l[g] = sm[g];
                 }
             }
         }
-#pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g)
-            if (g < G)
-                *reinterpret_cast<float4*>(&pq[vg][g][vc]) = float4{acc[g][0], acc[g][1], acc[g][2], acc[g][3]};
     }
     __syncthreads();
-    // ---- sum of the 8 token groups and the rotation H, a wavefront per head
-    //      (channels l and l + 64 in lane l, stages h = 1, 2, ..., 64)
-    for (int g = wave; g < G; g += kResThreads / kWave) {
-        float v0 = 0.f, v1 = 0.f;
+    if (wave == 1) return;
 #pragma unroll
-        for (int k = 0; k < kResThreads / 32; ++k) {
-            v0 += pq[k][g][lane];
-            v1 += pq[k][g][lane + 64];
-        }
-        float r0 = v0, r1 = v1;
-        if (rotate) {
-            hadamard_lanes(v0, v1, lane);
-            r0 = v0 + v1;
-            r1 = v0 - v1;
-        }
-        const int64_t slot = slot0 + (int64_t)g * (NC + kResSlots);
-        a.ws_acc[slot * kD + lane] = r0;
-        a.ws_acc[slot * kD + lane + 64] = r1;
-        if (lane == 0) {
-            a.ws_m[slot] = stat[0][g];
-            a.ws_l[slot] = stat[1][g];
+    for (int g = 0; g < kMaxGroup; ++g) {
+        if (g < G) {
+            // the first wavefront holds at least one token: M is finite
+            const float m1 = x_m[g], M = fmaxf(mx[g], m1);
+            const float e0 = exp2f(mx[g] - M), e1 = exp2f(m1 - M);
+            const float2 o = x_acc[g][lane];
+            float v0 = acc[g][0] * e0 + o.x * e1, v1 = acc[g][1] * e0 + o.y * e1;
+            if (rotate) {
+                // channels 2 l (v0) and 2 l + 1 (v1): stage h = 1 inside the
+                // lane, stages h = 2, 4, ..., 64 between lanes l and l ^ h / 2
+                const float w0 = v0 + v1, w1 = v0 - v1;
+                v0 = w0;
+                v1 = w1;
+                hadamard_stage<1>(v0, v1, lane);
+                hadamard_stage<2>(v0, v1, lane);
+                hadamard_stage<4>(v0, v1, lane);
+                hadamard_stage<8>(v0, v1, lane);
+                hadamard_stage<16>(v0, v1, lane);
+                hadamard_stage<32>(v0, v1, lane);
+            }
+            const int64_t slot = slot0 + (int64_t)g * (NC + kResSlots);
+            *reinterpret_cast<float2*>(&a.ws_acc[slot * kD + 2 * lane]) = float2{v0, v1};
+            if (lane == 0) {
+                a.ws_m[slot] = M;
+                a.ws_l[slot] = sm[g] * e0 + x_l[g] * e1;
+            }
         }
     }
 }
@@ -1410,7 +1464,7 @@ int launch_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t 
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
     a.ws_m = a.ws_acc + slots * kD;
     a.ws_l = a.ws_m + slots;
-    attn_residual_kernel<<<dim3(kResSlots, Hkv, B), kResThreads, 0, stream>>>(a);
+    attn_residual_kernel<<<dim3(kResSlots, Hkv, B), kResWaves * kWave, 0, stream>>>(a);
     return hip_check("attn_residual launch", hipGetLastError());
 }
 

@@ -121,6 +121,55 @@ def test_attention_over_ring_and_compressed_tokens(dq):
     assert _rel_err(got[[0, 2, 4]], ref0[[0, 2, 4]]) < TOL
 
 
+@pytest.mark.parametrize("G", [1, 2, 8])
+def test_residual_query_groups(dq, G):
+    """1, 2 and 8 query heads per KV head; residual lengths that give every
+    part an odd count, one token, or halves of 1..32 tokens per wavefront."""
+    wl = wlmod.workload("b1_t4k")
+    otk = tables.build_tables(128, wl.k.levels, wl.k.precision, wl.k.alpha, wl.k.record_bytes)
+    otv = tables.build_tables(128, wl.v.levels, wl.v.precision, wl.v.alpha, wl.v.record_bytes)
+    gtk = dq.Tables(128, wl.k.levels, wl.k.precision, wl.k.record_bytes, wl.k.alpha)
+    gtv = dq.Tables(128, wl.v.levels, wl.v.precision, wl.v.record_bytes, wl.v.alpha)
+    B, Hkv, t_cap, r_cap = 6, 2, 256, 256
+    comp = [128, 0, 256, 128, 0, 256]
+    res = [255, 1, 5, 64, 129, 0]
+    T = max(c + r for c, r in zip(comp, res))
+    w2 = wlmod.Workload("ring_g", B, T, Hkv * G, Hkv, G, wl.k, wl.v)
+    k, v, q = wlmod.make_k(w2, 50 + G), wlmod.make_v(w2, 50 + G), wlmod.make_q(w2, 50 + G)
+    kb, vb, qb = wlmod.bf16_bits(k), wlmod.bf16_bits(v), wlmod.bf16_bits(q)
+    records_k = torch.zeros((B, Hkv, t_cap, wl.k.record_bytes), dtype=torch.uint8, device=DEV)
+    records_v = torch.zeros((B, Hkv, t_cap, wl.v.record_bytes), dtype=torch.uint8, device=DEV)
+    mean_q = torch.zeros((B, Hkv, t_cap // 128, 128), dtype=torch.int8, device=DEV)
+    mean_s = torch.zeros((B, Hkv, t_cap // 128), dtype=torch.int16, device=DEV)
+    res_k = torch.full((B, Hkv, r_cap, 128), 30.0, dtype=torch.bfloat16, device=DEV)
+    res_v = torch.full_like(res_k, -50.0)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    kd, vd = k.to(DEV), v.to(DEV)
+    for b in range(B):
+        n = comp[b]
+        if n:
+            dq.dq_encode_kv(gtk, kd[b:b + 1, :n], 0, t_cap, records_k[b:b + 1], mean_q[b:b + 1], mean_s[b:b + 1],
+                            status)
+            dq.dq_encode_kv(gtv, vd[b:b + 1, :n], 0, t_cap, records_v[b:b + 1], None, None, status)
+        for i in range(res[b]):
+            slot = (n + i) % r_cap
+            res_k[b, :, slot] = kd[b, n + i]
+            res_v[b, :, slot] = vd[b, n + i]
+    seq = torch.tensor(comp, dtype=torch.int32, device=DEV)
+    rl = torch.tensor(res, dtype=torch.int32, device=DEV)
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, Hkv * G, Hkv, t_cap), dtype=torch.uint8, device=DEV)
+    out = torch.empty((B, Hkv * G, 128), dtype=torch.float32, device=DEV)
+    qd = q.to(DEV)
+    dq.dq_decode_attention_partial(gtk, gtv, qd, records_k, mean_q, mean_s, records_v, seq, ws, status=status)
+    dq.dq_decode_attention_residual(qd, res_k, res_v, seq, rl, t_cap, ws)
+    dq.dq_decode_attention_merge(B, Hkv * G, Hkv, seq, t_cap, ws, out)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    got = out.cpu().numpy().astype(np.float64)
+    ref = _oracle(qb, kb, vb, comp, res, otk, otv, G)
+    assert _rel_err(got, ref) < TOL
+
+
 @pytest.mark.parametrize("r_cap", [1, 3, 37, 130])
 def test_residual_small_and_odd_rings(dq, r_cap):
     """Rings of any capacity up to 256: each of the four partial slots covers a
