@@ -95,6 +95,9 @@ def _args():
                     help="also time the fixed-width comparator (App. B: 36-byte INT2 records of the same workload)")
     ap.add_argument("--residual", type=int, default=0,
                     help="also attend over this many raw BF16 tokens per sequence (residual window, <= 255)")
+    ap.add_argument("--residual-two-call", action="store_true",
+                    help="with --residual: the window as its own launch before the merge, instead of the "
+                         "one-launch window + merge")
     return ap.parse_args()
 
 
@@ -508,14 +511,19 @@ def main():
         ring = (rk, rv, rl)
 
     calls = [lambda: cache.partial(q, seq)]
-    if ring is not None:
+    if ring is not None and a.residual_two_call:
         calls.append(lambda: dq.dq_decode_attention_residual(q, ring[0], ring[1], seq, ring[2], T, cache.workspace))
-    calls.append(lambda: cache.merge(seq, out))
+        calls.append(lambda: cache.merge(seq, out))
+    elif ring is not None:
+        calls.append(lambda: dq.dq_decode_attention_merge_residual(q, ring[0], ring[1], seq, ring[2], T,
+                                                                   cache.workspace, out))
+    else:
+        calls.append(lambda: cache.merge(seq, out))
     step_ms, per_call, wall, settle = time_steps(calls, a.steps, a.warmup, graph=a.graph)
     if int(cache.status.item()):
         raise RuntimeError(f"decode status {int(cache.status.item())}")
     partial_ms, merge_ms = per_call[0], per_call[-1]
-    residual_ms = per_call[1] if ring is not None else 0.0
+    residual_ms = per_call[1] if ring is not None and a.residual_two_call else 0.0
 
     # algorithmic bytes of one partial launch: per (token, KV head) the two
     # records plus the amortized INT8 key mean and its fp16 scale (per token
@@ -578,9 +586,12 @@ def main():
             "valu_insts_per_launch": counters[1],
             "valu_lane_ops_per_symbol": counters[1] * 64 / n_symbols},
         "merge_ms": merge_ms,
-        "residual": None if ring is None else {
-            "tokens_per_sequence": a.residual, "ms": residual_ms,
-            "gbs": B * Hkv * a.residual * d * 2 * 2 / (residual_ms * 1e-3) / 1e9},
+        "residual": None if ring is None else (
+            {"tokens_per_sequence": a.residual, "form": "own launch, then the merge", "ms": residual_ms,
+             "gbs": B * Hkv * a.residual * d * 2 * 2 / (residual_ms * 1e-3) / 1e9}
+            if a.residual_two_call else
+            {"tokens_per_sequence": a.residual, "form": "one launch with the merge (merge_ms)",
+             "window_bytes": B * Hkv * a.residual * d * 2 * 2}),
         "wall_ms_per_step": wall * 1e3 / a.steps,
         "step_launch": "graph replay" if a.graph else "eager",
         "symbols_per_s": n_symbols / (step_ms * 1e-3),

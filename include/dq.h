@@ -246,7 +246,8 @@ int dq_decode_attention_merge(int32_t batch, int32_t q_heads, int32_t kv_heads,
  * into the workspace: call it after dq_decode_attention_partial and before
  * dq_decode_attention_merge, with the same sizes and workspace; the merge then
  * attends over the compressed tokens and the residual tokens together
- * (a sequence with neither gives 0).  head_dim is 128; q_heads / kv_heads <= 8.
+ * (a sequence with neither gives 0).  head_dim is 128; q_heads / kv_heads <= 8;
+ * q, res_k and res_v 16-byte aligned.
  * Returns DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_WORKSPACE or DQ_ERR_HIP.
  */
 int dq_decode_attention_residual(const uint16_t* q, int32_t batch, int32_t q_heads,
@@ -255,6 +256,23 @@ int dq_decode_attention_residual(const uint16_t* q, int32_t batch, int32_t q_hea
                                  const int32_t* res_lens, int32_t r_cap, int32_t t_cap,
                                  float softmax_scale, void* workspace,
                                  size_t workspace_bytes, void* stream);
+
+/*
+ * The residual window and the merge in one launch (Sec. 5.1, Alg. 2): after
+ * dq_decode_attention_partial (or any other _partial call) with the same
+ * sizes and workspace, writes `out` as dq_decode_attention_residual followed
+ * by dq_decode_attention_merge would (equal up to fp32 rounding order), one
+ * kernel instead of two.  The workspace is read, not written, so the
+ * residual slots it holds for the two-call form are ignored.  Arguments as
+ * for the two calls; q 16-byte aligned (as for dq_decode_attention_residual).
+ * Returns DQ_OK, DQ_ERR_INVALID_ARG, DQ_ERR_WORKSPACE or DQ_ERR_HIP.
+ */
+int dq_decode_attention_merge_residual(const uint16_t* q, int32_t batch, int32_t q_heads,
+                                       int32_t kv_heads, const uint16_t* res_k,
+                                       const uint16_t* res_v, const int32_t* seq_lens,
+                                       const int32_t* res_lens, int32_t r_cap, int32_t t_cap,
+                                       float softmax_scale, const void* workspace,
+                                       size_t workspace_bytes, float* out, void* stream);
 
 /*
  * Appends one token per sequence to its ring: k_new, v_new bf16

@@ -9,7 +9,8 @@ Entry points (same names as the C ABI in ``include/dq.h``):
     dq_compute_tables, dq_build_tables, dq_encode_kv,
     dq_decode_workspace_bytes, dq_decode_attention, dq_decode_attention_no_alloc,
     dq_decode_attention_partial, dq_decode_attention_merge, dq_decode_attention_residual,
-    dq_residual_append, dq_residual_commit, dq_bf16_decode_attention_partial, dq_encode_kv_paged,
+    dq_decode_attention_merge_residual, dq_residual_append, dq_residual_commit,
+    dq_bf16_decode_attention_partial, dq_encode_kv_paged,
     dq_decode_attention_paged_partial, dq_token_record_stride, dq_encode_kv_token,
     dq_decode_attention_token_partial, dq_fixed_bits, dq_encode_kv_fixed,
     dq_decode_attention_fixed_partial, dq_decode_symbols, dq_strerror, dq_last_error
@@ -22,6 +23,7 @@ from ._lib import (  # noqa: F401
     dq_compute_tables, dq_build_tables, dq_encode_kv, dq_decode_workspace_bytes,
     dq_decode_attention, dq_decode_attention_no_alloc, DQ_NO_ALLOC_SCRATCH_BYTES,
     dq_decode_attention_partial, dq_decode_attention_merge, dq_decode_attention_residual,
+    dq_decode_attention_merge_residual,
     dq_residual_append, dq_residual_commit,
     dq_bf16_decode_attention_partial, dq_encode_kv_paged, dq_decode_attention_paged_partial,
     dq_token_record_stride, token_records_shape, dq_encode_kv_token, dq_decode_attention_token_partial,

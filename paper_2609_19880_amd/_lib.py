@@ -85,6 +85,9 @@ def _load():
     lib.dq_decode_attention_residual.argtypes = [P, I32, I32, I32, P, P, P, P, I32, I32, ctypes.c_float,
                                                  P, SZ, P]
     lib.dq_decode_attention_residual.restype = ctypes.c_int
+    lib.dq_decode_attention_merge_residual.argtypes = [P, I32, I32, I32, P, P, P, P, I32, I32, ctypes.c_float,
+                                                       P, SZ, P, P]
+    lib.dq_decode_attention_merge_residual.restype = ctypes.c_int
     lib.dq_encode_kv_paged.argtypes = [P, P, I64, I64, I64, I32, I32, I32, I32, P, I32, I32, I32, P, P, P, P, P]
     lib.dq_encode_kv_paged.restype = ctypes.c_int
     lib.dq_decode_attention_paged_partial.argtypes = [P, P, P, I32, I32, I32, P, P, P, P, P, I32, I32, I32, P,
@@ -347,6 +350,25 @@ def dq_decode_attention_residual(q, res_k, res_v, seq_lens, res_lens, t_cap: int
                                            _ptr(workspace), workspace.numel() * workspace.element_size(),
                                            _stream(stream))
     _check(rc, "dq_decode_attention_residual")
+
+
+def dq_decode_attention_merge_residual(q, res_k, res_v, seq_lens, res_lens, t_cap: int, workspace, out,
+                                       softmax_scale=None, stream=None):
+    """Residual window and merge in one launch: after any _partial call, writes
+    out fp32 [B, Hq, d] as dq_decode_attention_residual + _merge would."""
+    import torch
+    B, Hkv, r_cap, d = _ring_args(res_k, res_v, seq_lens, res_lens)
+    _need(q.is_cuda and q.dtype == torch.bfloat16 and q.is_contiguous() and q.dim() == 3
+          and q.shape[0] == B and q.shape[2] == d, "q")
+    Hq = q.shape[1]
+    _need(out.is_cuda and out.dtype == torch.float32 and out.is_contiguous()
+          and tuple(out.shape) == (B, Hq, 128), "out")
+    scale = (1.0 / d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    rc = _lib.dq_decode_attention_merge_residual(_ptr(q), B, Hq, Hkv, _ptr(res_k), _ptr(res_v), _ptr(seq_lens),
+                                                 _ptr(res_lens), r_cap, int(t_cap), ctypes.c_float(scale),
+                                                 _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                                 _ptr(out), _stream(stream))
+    _check(rc, "dq_decode_attention_merge_residual")
 
 
 def _pool_args(tables, record_pool, block_table, mean_q_pool=None, mean_scale_pool=None):

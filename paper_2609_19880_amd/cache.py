@@ -196,7 +196,6 @@ class StreamingKVCache:
         if out is None:
             out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
         c.partial(q, self.seq_lens, softmax_scale)
-        _lib.dq_decode_attention_residual(q, self.res_k, self.res_v, self.seq_lens, self.res_lens, c.t_cap,
-                                          c.workspace, softmax_scale=softmax_scale)
-        _lib.dq_decode_attention_merge(c.batch, c.q_heads, c.kv_heads, self.seq_lens, c.t_cap, c.workspace, out)
+        _lib.dq_decode_attention_merge_residual(q, self.res_k, self.res_v, self.seq_lens, self.res_lens, c.t_cap,
+                                                c.workspace, out, softmax_scale=softmax_scale)
         return out

@@ -1158,6 +1158,148 @@ __global__ __launch_bounds__(kResWaves * kWave) void attn_residual_kernel(ResArg
     }
 }
 
+// ------------------------------------------- merge with the residual window
+//
+// The residual window and the merge in one launch: a workgroup of eight
+// wavefronts per (KV head, sequence).  Wavefront w takes half w % 2 of part
+// w / 2 of the window (residual_wave, the same split as attn_residual_kernel)
+// and leaves its maxima, sums and weighted values in LDS; after the one
+// barrier, wavefront g merges query head g of the group: the chunk partials
+// of the compressed tokens (their rows requested at the start, so they arrive
+// while the window is computed), rotated back by H / d when the values were
+// rotated online, and the eight window partials, which are in the original
+// basis already.  The residual slots of the workspace are not used.
+constexpr int kMrWaves = kResSlots * kResWaves;   // 8: halves of the window's parts, then query heads
+constexpr int kMrBatch = 8;                       // chunk rows per memory round trip
+
+struct MergeResArgs {
+    ResArgs r;
+    int t_cap;
+    float* out;
+};
+
+__global__ __launch_bounds__(kMrWaves * kWave) void attn_merge_residual_kernel(MergeResArgs ma) {
+    const ResArgs& a = ma.r;
+    __shared__ __align__(16) float p_lds[kMrWaves][kMaxGroup][kResWaveTokens];
+    __shared__ __align__(16) float r_acc[kMrWaves][kMaxGroup][kD];
+    __shared__ float r_m[kMrWaves][kMaxGroup], r_l[kMrWaves][kMaxGroup];
+    const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int lane = tid & (kWave - 1), wave = tid / kWave;
+    const int G = a.G, chunk = a.ws_hdr[0], NC = a.ws_hdr[1], rotate = a.ws_hdr[3];
+
+    // ---- the chunk partials of query head h G + wave, requested first
+    const int T = max(0, min(a.seq_lens[b], ma.t_cap));
+    const int nc = min(NC, (T + chunk - 1) / chunk);
+    const int64_t base = ((int64_t)b * a.Hq + h * G + wave) * (NC + kResSlots);
+    float m_lane = -INFINITY, l_lane = 0.f, a0[kMrBatch], a1[kMrBatch];
+    if (wave < G) {
+        if (lane < nc) {
+            m_lane = a.ws_m[base + lane];
+            l_lane = a.ws_l[base + lane];
+        }
+#pragma unroll
+        for (int u = 0; u < kMrBatch; ++u) {
+            const int64_t s = base + min(u, max(nc - 1, 0));
+            a0[u] = a.ws_acc[s * kD + lane];
+            a1[u] = a.ws_acc[s * kD + lane + 64];
+        }
+    }
+
+    // ---- the window: half (wave % 2) of part (wave / 2)
+    {
+        const int part = wave >> 1, half = wave & 1;
+        const int r = max(0, min(a.res_lens[b], a.r_cap));
+        const int ps = (r + kResSlots - 1) / kResSlots;
+        const int t0 = part * ps;
+        const int n = max(0, min(ps, r - t0));
+        const int nh = (n + 1) / 2;
+        const int nw = half ? n - nh : nh;
+        const int ring0 = max(0, a.seq_lens[b]) % a.r_cap + t0 + (half ? nh : 0);
+        float acc[kMaxGroup][2], mx[kMaxGroup], sm[kMaxGroup];
+        if (nw > 16) {
+            residual_wave<32>(a, b, h, ring0, nw, lane, p_lds[wave], acc, mx, sm);
+        } else if (nw > 0) {
+            residual_wave<16>(a, b, h, ring0, nw, lane, p_lds[wave], acc, mx, sm);
+        } else {
+#pragma unroll
+            for (int g = 0; g < kMaxGroup; ++g) {
+                acc[g][0] = acc[g][1] = 0.f;
+                mx[g] = -INFINITY;
+                sm[g] = 0.f;
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < kMaxGroup; ++g) {
+            if (g < G) {
+                *reinterpret_cast<float2*>(&r_acc[wave][g][2 * lane]) = float2{acc[g][0], acc[g][1]};
+                if (lane == 0) {
+                    r_m[wave][g] = mx[g];
+                    r_l[wave][g] = sm[g];
+                }
+            }
+        }
+    }
+    __syncthreads();
+    if (wave >= G) return;
+
+    // ---- merge of query head g: lane l holds channels l and l + 64
+    const int g = wave;
+    float* dst = ma.out + ((int64_t)b * a.Hq + h * G + g) * kD;
+    float M = m_lane;
+    for (int i = lane + kWave; i < nc; i += kWave) M = fmaxf(M, a.ws_m[base + i]);
+    M = wave_max_f32(M);
+#pragma unroll
+    for (int w = 0; w < kMrWaves; ++w) M = fmaxf(M, r_m[w][g]);
+    if (M == -INFINITY) {      // no token at all
+        dst[lane] = 0.f;
+        dst[lane + 64] = 0.f;
+        return;
+    }
+    const float e_lane = lane < nc ? exp2f(m_lane - M) : 0.f;
+    float l = wave_sum_f32(l_lane * e_lane);
+    float c0 = 0.f, c1 = 0.f;
+    for (int i0 = 0; i0 < nc; i0 += kMrBatch) {
+        if (i0) {
+#pragma unroll
+            for (int u = 0; u < kMrBatch; ++u) {
+                const int64_t s = base + min(i0 + u, nc - 1);
+                a0[u] = a.ws_acc[s * kD + lane];
+                a1[u] = a.ws_acc[s * kD + lane + 64];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kMrBatch; ++u) {
+            const int i = i0 + u;
+            if (i < nc) {
+                float e;
+                if (i < kWave) {
+                    e = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(e_lane), i));
+                } else {
+                    e = exp2f(a.ws_m[base + i] - M);
+                    l += a.ws_l[base + i] * e;
+                }
+                c0 += a0[u] * e;
+                c1 += a1[u] * e;
+            }
+        }
+    }
+    if (rotate) {              // the chunks' values were rotated: H v / d
+        hadamard_lanes(c0, c1, lane);
+        const float r0 = (c0 + c1) * (1.0f / kD), r1 = (c0 - c1) * (1.0f / kD);
+        c0 = r0;
+        c1 = r1;
+    }
+#pragma unroll
+    for (int w = 0; w < kMrWaves; ++w) {
+        const float e = exp2f(r_m[w][g] - M);     // 0 for a half without tokens
+        l += r_l[w][g] * e;
+        c0 += r_acc[w][g][lane] * e;
+        c1 += r_acc[w][g][lane + 64] * e;
+    }
+    dst[lane] = c0 / l;
+    dst[lane + 64] = c1 / l;
+}
+
 // One new token per sequence into its ring slot; block per sequence.
 __global__ __launch_bounds__(kResThreads) void residual_append_kernel(const uint16_t* __restrict__ k_new,
                                                                       const uint16_t* __restrict__ v_new,
@@ -1466,6 +1608,33 @@ int launch_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t 
     a.ws_l = a.ws_m + slots;
     attn_residual_kernel<<<dim3(kResSlots, Hkv, B), kResWaves * kWave, 0, stream>>>(a);
     return hip_check("attn_residual launch", hipGetLastError());
+}
+
+int launch_attention_merge_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                                    const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
+                                    const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
+                                    void* ws, float* out, hipStream_t stream) {
+    const int64_t slots = ws_slots(B, Hq, t_cap);
+    MergeResArgs m;
+    ResArgs& a = m.r;
+    a.q = q;
+    a.rk = res_k;
+    a.rv = res_v;
+    a.seq_lens = seq_lens;
+    a.res_lens = res_lens;
+    a.r_cap = r_cap;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.G = Hq / Hkv;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.ws_hdr = static_cast<int32_t*>(ws);
+    a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
+    a.ws_m = a.ws_acc + slots * kD;
+    a.ws_l = a.ws_m + slots;
+    m.t_cap = t_cap;
+    m.out = out;
+    attn_merge_residual_kernel<<<dim3(Hkv, B), kMrWaves * kWave, 0, stream>>>(m);
+    return hip_check("attn_merge_residual launch", hipGetLastError());
 }
 
 int launch_residual_append(const uint16_t* k_new, const uint16_t* v_new, int32_t B, int32_t Hkv,

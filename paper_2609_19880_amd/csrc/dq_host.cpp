@@ -567,18 +567,44 @@ int dq_decode_attention_no_alloc(const dq_tables* tk, const dq_tables* tv, const
     return dq::launch_attention_merge(B, Hq, Hkv, seq_lens, t_cap, ws, out, s, slots);
 }
 
-int dq_decode_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
-                                 const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
-                                 const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
-                                 void* ws, size_t ws_bytes, void* stream) {
+// Shared checks of the residual-window calls (the window kernels read q, the
+// key rows and the value rows in 16- and 4-byte pieces).
+static int check_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, const uint16_t* res_k,
+                          const uint16_t* res_v, const int32_t* seq_lens, const int32_t* res_lens, int32_t r_cap,
+                          int32_t t_cap, float scale, const void* ws, size_t ws_bytes) {
     if (B <= 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv || Hq / Hkv > 8 || B > 65535 || Hkv > 65535)
         return DQ_ERR_INVALID_ARG;
     if (t_cap <= 0 || t_cap % DQ_MEAN_WINDOW || r_cap <= 0 || r_cap > 256) return DQ_ERR_INVALID_ARG;
     if (!q || !res_k || !res_v || !seq_lens || !res_lens || !std::isfinite(scale)) return DQ_ERR_INVALID_ARG;
-    if ((reinterpret_cast<uintptr_t>(res_k) | reinterpret_cast<uintptr_t>(res_v)) & 15) return DQ_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(res_k) | reinterpret_cast<uintptr_t>(res_v) |
+         reinterpret_cast<uintptr_t>(q)) & 15)
+        return DQ_ERR_INVALID_ARG;
     if (!ws || ws_bytes < dq::attention_workspace_bytes(B, Hq, Hkv, t_cap, 128)) return DQ_ERR_WORKSPACE;
+    return DQ_OK;
+}
+
+int dq_decode_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                                 const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
+                                 const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
+                                 void* ws, size_t ws_bytes, void* stream) {
+    const int rc = check_residual(q, B, Hq, Hkv, res_k, res_v, seq_lens, res_lens, r_cap, t_cap, scale, ws,
+                                  ws_bytes);
+    if (rc != DQ_OK) return rc;
     return dq::launch_attention_residual(q, B, Hq, Hkv, res_k, res_v, seq_lens, res_lens, r_cap, t_cap, scale,
                                          ws, static_cast<hipStream_t>(stream));
+}
+
+int dq_decode_attention_merge_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                                       const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
+                                       const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
+                                       const void* ws, size_t ws_bytes, float* out, void* stream) {
+    const int rc = check_residual(q, B, Hq, Hkv, res_k, res_v, seq_lens, res_lens, r_cap, t_cap, scale, ws,
+                                  ws_bytes);
+    if (rc != DQ_OK) return rc;
+    if (!out) return DQ_ERR_INVALID_ARG;
+    return dq::launch_attention_merge_residual(q, B, Hq, Hkv, res_k, res_v, seq_lens, res_lens, r_cap, t_cap,
+                                               scale, const_cast<void*>(ws), out,
+                                               static_cast<hipStream_t>(stream));
 }
 
 int dq_bf16_decode_attention_partial(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, const uint16_t* k,

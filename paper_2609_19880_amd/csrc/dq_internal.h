@@ -200,6 +200,10 @@ int launch_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t 
                               const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
                               const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
                               void* ws, hipStream_t stream);
+int launch_attention_merge_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv,
+                                    const uint16_t* res_k, const uint16_t* res_v, const int32_t* seq_lens,
+                                    const int32_t* res_lens, int32_t r_cap, int32_t t_cap, float scale,
+                                    void* ws, float* out, hipStream_t stream);
 int launch_residual_append(const uint16_t* k_new, const uint16_t* v_new, int32_t B, int32_t Hkv,
                            uint16_t* res_k, uint16_t* res_v, const int32_t* seq_lens, int32_t* res_lens,
                            int32_t r_cap, uint32_t* status, hipStream_t stream);

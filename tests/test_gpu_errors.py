@@ -81,6 +81,33 @@ def test_attention_rejects_short_workspace(dq, bufs):
     assert rc == dq.DQ_ERR_INVALID_ARG
 
 
+def test_residual_calls_reject_bad_arguments(dq, bufs):
+    """The window calls (two-call and one-launch forms): misaligned q or ring,
+    ring capacity above 256, short workspace, missing output."""
+    lib = dq._lib._lib
+    need = dq.dq_decode_workspace_bytes(1, 4, 1, 256)
+
+    def res(q_off=0, rk_off=0, r_cap=128, ws_bytes=need):
+        return lib.dq_decode_attention_residual(
+            ctypes.c_void_p(bufs[0].data_ptr() + q_off), 1, 4, 1, ctypes.c_void_p(bufs[1].data_ptr() + rk_off),
+            _p(bufs[2]), _p(bufs[5]), _p(bufs[4]), r_cap, 256, ctypes.c_float(0.088), _p(bufs[6]), ws_bytes, None)
+
+    def fused(q_off=0, rk_off=0, r_cap=128, ws_bytes=need, out=True):
+        return lib.dq_decode_attention_merge_residual(
+            ctypes.c_void_p(bufs[0].data_ptr() + q_off), 1, 4, 1, ctypes.c_void_p(bufs[1].data_ptr() + rk_off),
+            _p(bufs[2]), _p(bufs[5]), _p(bufs[4]), r_cap, 256, ctypes.c_float(0.088), _p(bufs[6]), ws_bytes,
+            _p(bufs[3]) if out else None, None)
+
+    for call in (res, fused):
+        assert call(q_off=2) == dq.DQ_ERR_INVALID_ARG
+        assert call(rk_off=8) == dq.DQ_ERR_INVALID_ARG
+        assert call(r_cap=257) == dq.DQ_ERR_INVALID_ARG
+        assert call(r_cap=0) == dq.DQ_ERR_INVALID_ARG
+        assert call(ws_bytes=need - 1) == dq.DQ_ERR_WORKSPACE
+    assert fused(out=False) == dq.DQ_ERR_INVALID_ARG
+    torch.cuda.synchronize()
+
+
 def test_encode_rejects_bad_ranges(dq, bufs):
     t = dq.Tables(128, 6, 12, 36, 1.4)
     lib = dq._lib._lib

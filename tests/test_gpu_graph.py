@@ -33,7 +33,7 @@ def _capture(step):
     return g
 
 
-def _check_replays(wl, cache, lens, extra=None, zero_rows=()):
+def _check_replays(wl, cache, lens, extra=None, zero_rows=(), finish=None):
     dev = torch.device("cuda")
     q, _, out = bench.step_inputs(wl, SEED, dev)
     seq = torch.tensor(lens, dtype=torch.int32, device=dev)
@@ -43,7 +43,10 @@ def _check_replays(wl, cache, lens, extra=None, zero_rows=()):
         cache.partial(qq, seq)
         if extra is not None:
             extra(qq)
-        cache.merge(seq, oo)
+        if finish is not None:
+            finish(qq, oo)
+        else:
+            cache.merge(seq, oo)
 
     g = _capture(lambda: step(static_q, static_out))
     for i in range(REPLAYS):
@@ -90,6 +93,23 @@ def test_graph_replay_with_residual_window(head_cache):
     _check_replays(wl, cache, lens,
                    extra=lambda qq: dq.dq_decode_attention_residual(qq, rk, rv, seq, rl, cache.t_cap,
                                                                     cache.workspace))
+
+
+def test_graph_replay_merge_with_residual_window(head_cache):
+    """The one-launch window + merge in the captured step."""
+    wl, cache = head_cache
+    dev = torch.device("cuda")
+    B, Hkv, d = wl.batch, wl.kv_heads, wl.head_dim
+    g = torch.Generator(device=dev)
+    g.manual_seed(SEED + 1)
+    rk = torch.randn((B, Hkv, 256, d), generator=g, device=dev).to(torch.bfloat16)
+    rv = torch.randn((B, Hkv, 256, d), generator=g, device=dev).to(torch.bfloat16)
+    lens = [4096, 1000, 0, 2113]
+    seq = torch.tensor(lens, dtype=torch.int32, device=dev)
+    rl = torch.tensor([255, 128, 5, 0], dtype=torch.int32, device=dev)
+    _check_replays(wl, cache, lens,
+                   finish=lambda qq, oo: dq.dq_decode_attention_merge_residual(qq, rk, rv, seq, rl, cache.t_cap,
+                                                                               cache.workspace, oo))
 
 
 def test_graph_replay_per_token_streams():

@@ -33,6 +33,19 @@ def _rel_err(got, ref):
     return float(np.max(np.abs(got - ref) / np.maximum(scale, 1e-30)))
 
 
+def _fused(dq, qd, res_k, res_v, seq, rl, t_cap, ws, two_call):
+    """The one-launch window + merge over the chunk partials already in ws:
+    returns its output; it must equal the two-call form up to fp32 rounding
+    order (the window's sum skips the H, H / d round trip)."""
+    out = torch.full(tuple(two_call.shape), float("nan"), dtype=torch.float32, device=DEV)
+    dq.dq_decode_attention_merge_residual(qd, res_k, res_v, seq, rl, t_cap, ws, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(got))
+    assert _rel_err(got, two_call) < 1e-5
+    return got
+
+
 def _oracle(q_bits, k_bits, v_bits, comp_lens, res_lens, otk, otv, G):
     """Oracle attention for sequences whose first comp_lens[b] tokens are
     encoded (window by window, as the cache does) and whose next res_lens[b]
@@ -110,6 +123,9 @@ def test_attention_over_ring_and_compressed_tokens(dq):
     assert np.all(got[3] == 0.0)          # neither compressed nor residual tokens
     live = [0, 1, 2, 4]
     assert _rel_err(got[live], ref[live]) < TOL
+    fused = _fused(dq, qd, res_k, res_v, seq, rl, t_cap, ws, got)
+    assert np.all(fused[3] == 0.0)
+    assert _rel_err(fused[live], ref[live]) < TOL
 
     # without the residual call the same workspace attends over the compressed tokens only
     dq.dq_decode_attention_partial(gtk, gtv, qd, records_k, mean_q, mean_s, records_v, seq, ws, status=status)
@@ -168,6 +184,7 @@ def test_residual_query_groups(dq, G):
     got = out.cpu().numpy().astype(np.float64)
     ref = _oracle(qb, kb, vb, comp, res, otk, otv, G)
     assert _rel_err(got, ref) < TOL
+    assert _rel_err(_fused(dq, qd, res_k, res_v, seq, rl, t_cap, ws, got), ref) < TOL
 
 
 @pytest.mark.parametrize("r_cap", [1, 3, 37, 130])
@@ -221,9 +238,12 @@ def test_residual_small_and_odd_rings(dq, r_cap):
     ref = _oracle(qb, kb, vb, comp, res, otk, otv, G)
     live = [b for b in range(B) if comp[b] + res[b] > 0]
     assert _rel_err(got[live], ref[live]) < TOL
+    fused = _fused(dq, qd, res_k, res_v, seq, rl, t_cap, ws, got)
+    assert _rel_err(fused[live], ref[live]) < TOL
     for b in range(B):
         if comp[b] + res[b] == 0:
             assert np.all(got[b] == 0.0)
+            assert np.all(fused[b] == 0.0)
 
 
 def test_streaming_cache_matches_oracle(dq):
