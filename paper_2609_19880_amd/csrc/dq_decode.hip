@@ -194,6 +194,12 @@ __device__ __forceinline__ void dwaitq(uint32_t& r, uint64_t& e, v4u (&q)[HG]) {
         asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(r), "+v"(e), "+v"(q[0]), "+v"(q[1]) : "i"(N));
 }
 
+// The query digits alone (a single chain whose next reads stay in flight).
+template <int N>
+__device__ __forceinline__ void dwaitq1(v4u& q) {
+    asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(q) : "i"(N));
+}
+
 __device__ __forceinline__ uint32_t dfinish(uint32_t& X, uint32_t& Q, int p3, uint32_t r, uint64_t e) {
     const uint32_t ex = (uint32_t)e, ey = (uint32_t)(e >> 32);
     const uint32_t y = __umul24(ex, X >> p3) + ey;
@@ -291,7 +297,9 @@ __device__ __forceinline__ uint32_t spread2(uint32_t x) {
 // FIXED: the fixed-width comparator at matched storage; levels come straight
 // from the record words (no tables, no byte pairs, no rANS state).
 // WMAX: the wavefront bound of the instantiation (max_waves, or 8).
-template <int HG, uint32_t LUTV, int RWP, bool FIXED, int WMAX>
+// SPLIT: one tile per pair of wavefronts, keys and values decoded by
+// different wavefronts (chunks of at most nw / 2 tiles: small batches).
+template <int HG, uint32_t LUTV, int RWP, bool FIXED, int WMAX, bool SPLIT = false>
 __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) {
     constexpr int RWK = RWP >> 8, RWV = RWP & 0xFF;
     constexpr int GP = 4 * HG;
@@ -357,12 +365,17 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     uint32_t mv0 = 0;
     uint16_t ms0 = 0;
     bool bad_page = false;
+    // the wavefront's first tile (SPLIT: its pair's tile, keys in the even
+    // wavefront with the value header, values in the odd one)
+    const int ptile = SPLIT ? wave >> 1 : wave;
+    const bool load_k = !SPLIT || !(wave & 1), load_v = !SPLIT || (wave & 1);
     if (!paged) {
-        if (kPrefetch && wave * kTile < a.chunk) {
-            const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, min(start + wave * kTile, a.t_cap - kTile),
+        if (kPrefetch && ptile * kTile < a.chunk) {
+            const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, min(start + ptile * kTile, a.t_cap - kTile),
                                            bad_page) + lane;
-            load_record(rk, a.krec, tok, CWk);
-            load_record(rv, a.vrec, tok, CWv);
+            if (load_k) load_record(rk, a.krec, tok, CWk);
+            if (load_v) load_record(rv, a.vrec, tok, CWv);
+            else rv[0] = *reinterpret_cast<const uint32_t*>(a.vrec + tok * (CWv * 4));
         }
         if (mwin < nwin && w0 + mwin < nwin_total) {
             const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + mwin, bad_page);
@@ -379,10 +392,11 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     };
     if (paged) {
         if (kPrefetch) {
-            const int ft = min(wave, ntiles - 1);
+            const int ft = min(ptile, ntiles - 1);
             const int64_t tok = record_row(a.pg, a.Hkv, a.t_cap, b, h, start + ft * kTile, bad_page) + lane;
-            load_record(rk, a.krec, tok, CWk);
-            load_record(rv, a.vrec, tok, CWv);
+            if (load_k) load_record(rk, a.krec, tok, CWk);
+            if (load_v) load_record(rv, a.vrec, tok, CWv);
+            else rv[0] = *reinterpret_cast<const uint32_t*>(a.vrec + tok * (CWv * 4));
         }
         if (mean_live(mwin)) {
             const int64_t widx = window_index(a.pg, a.Hkv, a.t_cap, b, h, w0 + mwin, bad_page);
@@ -525,8 +539,173 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
 #pragma unroll
         for (int cb = 0; cb < 4; ++cb) acc[0][hg][cb] = acc[1][hg][cb] = 0.f;
     bool corrupt = false;
+    float l_tot[GP], o_tot[GP];
 
-    for (int tile = wave; tile < ntiles; tile += L.nw) {
+    if constexpr (SPLIT) {
+        // One tile per pair of wavefronts: the even wavefront decodes the
+        // keys, forms the scores and the softmax weights and leaves their
+        // digits (its weight-digit tile) and the tile's statistics in its LDS
+        // region; the odd one decodes the values meanwhile and, after the
+        // barrier, forms P . v with its partner's weights.  Each chain then
+        // has its SIMD to itself: a step waits only for its own two LDS reads
+        // (two chains in one wavefront take a third longer per tile, which
+        // bounds the latency when one wavefront runs per SIMD).
+        static_assert(HG == 1 && !FIXED, "split tiles: up to 4 query heads, entropy-coded records");
+        const int tile = wave >> 1, role = wave & 1;
+        // [0, GP) weight scale of each slot, then maxima, sums, offset sums
+        float* kx = reinterpret_cast<float*>(smem + L.waves + (wave & ~1) * L.wave_stride + L.vtile);
+        uint32_t vlev[kD / 4];
+        const int t_base = start + tile * kTile;
+        const int t = t_base + lane;
+        const bool valid = t < T;
+        uint32_t rr_;
+        uint64_t ee_;
+        if (tile < ntiles && role == 0) {
+            const uint32_t hk0 = rk[0], hv0 = rv[0];
+            uint32_t xk = rk[1] << 3;
+            build_pairs(rk, CWk, smem + pk_lane);
+            asm volatile("" ::: "memory");
+            uint32_t pq = pk_lane;
+            const uint32_t pk_end = pk_lane + (uint32_t)((Ck - kPayloadOffset) * kPairRow);
+            v4i dk[3];
+#pragma unroll
+            for (int d = 0; d < 3; ++d) dk[d] = v4i{0, 0, 0, 0};
+            const uint32_t q_lane = (uint32_t)L.qlimb + (uint32_t)(lane & 3) * 16;
+            v4u qd;
+            dissue<0>(xk, pq, mask8k, 0, rr_, ee_);
+#pragma unroll
+            for (int grp = 0; grp < kD / 4; ++grp) {
+                uint32_t kw[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int n = 4 * grp + u, J1 = (n + 1) % kWindow;
+                    const bool more = n + 1 < kD;
+                    dwait<0>(rr_, ee_);
+                    kw[u] = dfinish(xk, pq, pk3, rr_, ee_);
+                    if (J1 == 0) {
+                        pq += kWindow * kPairStep;
+                        if (more) pq = min(pq, pk_end);
+                    }
+                    if (u == 3) qissue(q_lane, (grp * GP) * 16, qd);
+                    if (more) dissue<0>(xk, pq, mask8k, J1, rr_, ee_);
+                }
+                const uint32_t lk = pack4(kw[0], kw[1], kw[2], kw[3]);
+                // the digits were requested before the next step's two reads
+                if (grp + 1 < kD / 4) dwaitq1<2>(qd);
+                else dwaitq1<0>(qd);
+                dk[0] = mfma(qd.x, lk, dk[0]);
+                dk[1] = mfma(qd.y, lk, dk[1]);
+                dk[2] = mfma(qd.z, lk, dk[2]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            corrupt |= valid && ((xk >> 3) != kRansL || pq > pk_end);
+            // scores (Eq. fold-key) and the tile's softmax; the value scale is
+            // folded into the weight (Eq. fold-value)
+            const float sk = half_lo(hk0), ok = half_hi(hk0);
+            const float sv = half_lo(hv0), ov = half_hi(hv0);
+            const float* qm = qmu + ((t / DQ_MEAN_WINDOW) - w0) * GP;
+            float score[4], tmax[4], pw[4], smax[4], lp[4], op[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float dot = combine(dk[0], dk[1], dk[2], r) * qscale[r];
+                score[r] = (valid && r < G) ? (sk * dot + ok * qsum[r] + qm[r]) * a.scale_log2 : -INFINITY;
+                tmax[r] = score[r];
+            }
+            wave_max4_f32(tmax);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float p = (score[r] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(score[r] - tmax[r]);
+                lp[r] = p;
+                op[r] = p * ov;
+                pw[r] = p * sv;
+                smax[r] = pw[r];
+            }
+            wave_max4_f32(smax);
+            uint32_t wd[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float inv = smax[r] > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax[r]) : 0.f;
+                const int pint = min(4194304, (int)rintf(pw[r] * inv));
+                int d0, d1, d2;
+                digits3(pint, d0, d1, d2);
+                wd[r] = ((uint32_t)d0 & 0xFFu) | (((uint32_t)d1 & 0xFFu) << 8) | (((uint32_t)d2 & 0xFFu) << 16);
+                l_tot[r] = wave_sum_f32(lp[r]);
+                o_tot[r] = wave_sum_f32(op[r]);
+            }
+            *reinterpret_cast<uint4*>(plimb + lane * 16) = uint4{wd[0], wd[1], wd[2], wd[3]};
+            if (lane == 0) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    kx[r] = smax[r] * (1.0f / 4194304.0f);
+                    kx[GP + r] = tmax[r];
+                    kx[2 * GP + r] = l_tot[r];
+                    kx[3 * GP + r] = o_tot[r];
+                }
+            }
+        } else if (tile < ntiles) {
+            uint32_t xv = rv[1] << 3;
+            build_pairs(rv, CWv, smem + pv_lane);
+            asm volatile("" ::: "memory");
+            uint32_t pv = pv_lane;
+            const uint32_t pv_end = pv_lane + (uint32_t)((Cv - kPayloadOffset) * kPairRow);
+            dissue<LUTV>(xv, pv, mask8v, 0, rr_, ee_);
+#pragma unroll
+            for (int grp = 0; grp < kD / 4; ++grp) {
+                uint32_t vw[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int n = 4 * grp + u, J1 = (n + 1) % kWindow;
+                    const bool more = n + 1 < kD;
+                    dwait<0>(rr_, ee_);
+                    vw[u] = dfinish(xv, pv, pv3, rr_, ee_);
+                    if (J1 == 0) {
+                        pv += kWindow * kPairStep;
+                        if (more) pv = min(pv, pv_end);
+                    }
+                    if (more) dissue<LUTV>(xv, pv, mask8v, J1, rr_, ee_);
+                }
+                vlev[grp] = pack4(vw[0], vw[1], vw[2], vw[3]);
+                asm volatile("" : "+v"(vlev[grp]));
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            corrupt |= valid && ((xv >> 3) != kRansL || pv > pv_end);
+        }
+        __syncthreads();   // the weights and statistics of every pair are in LDS
+        if (tile < ntiles && role == 1) {
+            // ---- P . v with the partner's weight digits, two slices of 64 channels
+            const uint32_t a_pair = a_lane - (uint32_t)L.wave_stride;
+            uint64_t pa[2];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) pa[kb] = lds_tr8(a_pair + kb * 32 * 16);
+            const float scale_l = pick4(kx, slot);
+#pragma unroll
+            for (int g = 0; g < GP; ++g) {
+                m_run[g] = kx[GP + g];
+                l_tot[g] = kx[2 * GP + g];
+                o_tot[g] = kx[3 * GP + g];
+            }
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl) {
+                if (sl) wave_sync();   // the first slice's value rows are no longer read
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq)
+                    *reinterpret_cast<uint4*>(vtile + lane * kVRowT + 16 * qq) =
+                        uint4{vlev[16 * sl + 4 * qq], vlev[16 * sl + 4 * qq + 1], vlev[16 * sl + 4 * qq + 2],
+                              vlev[16 * sl + 4 * qq + 3]};
+                wave_sync();
+#pragma unroll
+                for (int cb = 0; cb < 4; ++cb) {
+                    const uint64_t b0 = lds_tr8(b_lane + 16 * cb);
+                    const uint64_t b1 = lds_tr8(b_lane + 32 * kVRowT + 16 * cb);
+                    v4i d = mfma16(pa[0], b0, v4i{0, 0, 0, 0});
+                    d = mfma16(pa[1], b1, d);
+                    acc[sl][0][cb] = ((float)d[2] * 65536.0f + (float)d[1] * 256.0f + (float)d[0]) * scale_l;
+                }
+            }
+        }
+    }
+
+    for (int tile = SPLIT ? ntiles : wave; tile < ntiles; tile += L.nw) {
         const int t_base = start + tile * kTile;
         const int t = t_base + lane;
         const bool valid = t < T;
@@ -760,32 +939,37 @@ __global__ __launch_bounds__(WMAX * kWave) void attn_partial_kernel(AttnArgs a) 
     if (__any(corrupt) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_CORRUPT);
     if (__any(bad_page) && lane == 0 && a.status) atomicOr(a.status, DQ_STATUS_PAGE);
 
-    // ---- merge the wavefronts of the workgroup
-    float l_tot[GP], o_tot[GP];
+    // ---- merge the wavefronts of the workgroup (SPLIT: the pairs, whose
+    //      statistics the value wavefront has read from its partner)
+    if constexpr (!SPLIT) {
 #pragma unroll
-    for (int g = 0; g < GP; ++g) {
-        l_tot[g] = wave_sum_f32(l_part[g]);
-        o_tot[g] = wave_sum_f32(acco[g]);
+        for (int g = 0; g < GP; ++g) {
+            l_tot[g] = wave_sum_f32(l_part[g]);
+            o_tot[g] = wave_sum_f32(acco[g]);
+        }
     }
     __syncthreads();   // every wavefront is done with LDS
     float* mw = reinterpret_cast<float*>(smem);        // [nw][GP]
     float* lw = mw + L.nw * GP;                        // [nw][GP]
     float* aw = lw + L.nw * GP;                        // [nw][GP][d]
+    if (!SPLIT || ((wave & 1) && (wave >> 1) < ntiles)) {
+        const int ws = SPLIT ? wave >> 1 : wave;
 #pragma unroll
-    for (int g = 0; g < GP; ++g) {
-        if (lane == 0) {
-            mw[wave * GP + g] = m_run[g];
-            lw[wave * GP + g] = l_tot[g];
+        for (int g = 0; g < GP; ++g) {
+            if (lane == 0) {
+                mw[ws * GP + g] = m_run[g];
+                lw[ws * GP + g] = l_tot[g];
+            }
         }
-    }
 #pragma unroll
-    for (int hg = 0; hg < HG; ++hg) {
-        const float o_l = pick4(o_tot + 4 * hg, slot);
-        float* row = aw + (wave * GP + 4 * hg + slot) * kD + (lane & 15);
+        for (int hg = 0; hg < HG; ++hg) {
+            const float o_l = pick4(o_tot + 4 * hg, slot);
+            float* row = aw + (ws * GP + 4 * hg + slot) * kD + (lane & 15);
 #pragma unroll
-        for (int cb = 0; cb < 4; ++cb) {
-            row[16 * cb] = acc[0][hg][cb] + o_l;
-            row[kVSlice + 16 * cb] = acc[1][hg][cb] + o_l;
+            for (int cb = 0; cb < 4; ++cb) {
+                row[16 * cb] = acc[0][hg][cb] + o_l;
+                row[kVSlice + 16 * cb] = acc[1][hg][cb] + o_l;
+            }
         }
     }
     __syncthreads();
@@ -1452,15 +1636,16 @@ bool attention_supports(const dq_tables* tk, const dq_tables* tv) {
     return true;
 }
 
-template <int HG, uint32_t LUTV, int RWP, bool FIXED, int WMAX>
+template <int HG, uint32_t LUTV, int RWP, bool FIXED, int WMAX, bool SPLIT = false>
 static int launch_w(AttnArgs& a, dim3 grid, hipStream_t stream) {
     if (a.L.nw > WMAX) return DQ_ERR_INVALID_ARG;
+    if (SPLIT && 2 * ((a.chunk + kTile - 1) / kTile) > a.L.nw) return DQ_ERR_INVALID_ARG;
     if (int rc = hip_check("hipFuncSetAttribute",
                            hipFuncSetAttribute(
-                               reinterpret_cast<const void*>(&attn_partial_kernel<HG, LUTV, RWP, FIXED, WMAX>),
+                               reinterpret_cast<const void*>(&attn_partial_kernel<HG, LUTV, RWP, FIXED, WMAX, SPLIT>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, a.L.total)))
         return rc;
-    attn_partial_kernel<HG, LUTV, RWP, FIXED, WMAX><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
+    attn_partial_kernel<HG, LUTV, RWP, FIXED, WMAX, SPLIT><<<grid, a.L.nw * kWave, a.L.total, stream>>>(a);
     return hip_check("attn_partial launch", hipGetLastError());
 }
 
@@ -1469,6 +1654,10 @@ static int launch_w(AttnArgs& a, dim3 grid, hipStream_t stream) {
 template <int HG, uint32_t LUTV, int RWP, bool FIXED = false>
 static int launch_rw(AttnArgs& a, dim3 grid, hipStream_t stream) {
     constexpr int W = max_waves(HG, RWP);
+    // chunks of at most nw / 2 tiles (small batches, short contexts): keys and
+    // values in different wavefronts (one shared table, equal record lengths)
+    if constexpr (HG == 1 && LUTV == 0 && !FIXED && RWP != 0 && (RWP >> 8) == (RWP & 0xFF))
+        if (2 * ((a.chunk + kTile - 1) / kTile) <= a.L.nw) return launch_w<HG, LUTV, RWP, FIXED, W, true>(a, grid, stream);
     if constexpr (HG == 2 && W > 8)
         if (a.L.nw <= 8) return launch_w<HG, LUTV, RWP, FIXED, 8>(a, grid, stream);
     return launch_w<HG, LUTV, RWP, FIXED, W>(a, grid, stream);

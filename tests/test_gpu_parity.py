@@ -224,8 +224,29 @@ def _upload_cache(dq, wl, krec, mq, ms, vrec):
             torch.from_numpy(ms.view(np.int16)).to(DEV), torch.from_numpy(vrec).to(DEV))
 
 
-def _gpu_attention(dq, gtk, gtv, q, kr, mq, ms, vr, lens, Hq):
+def _pad_capacity(kr, mq, ms, vr, t_cap):
+    """The same cache in buffers of capacity t_cap (zero rows past the old
+    one).  The chunk plan follows the capacity, not the lengths: on a 256-CU
+    device a capacity of 32 x 1024 tokens per (sequence, KV head) pair gives
+    1024-token chunks (16 tiles), which one wavefront per tile decodes with
+    both chains (the split form takes chunks of at most half as many tiles
+    as a workgroup has wavefronts)."""
+    def pad(x, n):
+        shape = list(x.shape)
+        shape[2] = n
+        y = torch.zeros(shape, dtype=x.dtype, device=x.device)
+        y[:, :, :x.shape[2]] = x
+        return y
+    return pad(kr, t_cap), pad(mq, t_cap // 128), pad(ms, t_cap // 128), pad(vr, t_cap)
+
+
+JOINT_CAP = 32768     # b1_t4k-like batches: 1024-token chunks, the two-chain form
+
+
+def _gpu_attention(dq, gtk, gtv, q, kr, mq, ms, vr, lens, Hq, t_cap=None):
     B = q.shape[0]
+    if t_cap is not None:
+        kr, mq, ms, vr = _pad_capacity(kr, mq, ms, vr, t_cap)
     Hkv, t_cap = kr.shape[1], kr.shape[2]
     out = torch.empty((B, Hq, 128), dtype=torch.float32, device=DEV)
     ws = torch.empty(dq.dq_decode_workspace_bytes(B, Hq, Hkv, t_cap), dtype=torch.uint8, device=DEV)
@@ -236,9 +257,10 @@ def _gpu_attention(dq, gtk, gtv, q, kr, mq, ms, vr, lens, Hq):
     return out.cpu().numpy().astype(np.float64), int(status.item())
 
 
-@pytest.mark.parametrize("variant", ["paper", "literal"])
-def test_attention_small_workload(dq, variant):
-    """Full b1_t4k workload: batch 1, 32/8 heads, 4096 tokens."""
+@pytest.mark.parametrize("variant,cap", [("paper", None), ("literal", None), ("paper", JOINT_CAP)])
+def test_attention_small_workload(dq, variant, cap):
+    """Full b1_t4k workload: batch 1, 32/8 heads, 4096 tokens (keys and values
+    in separate wavefronts; in larger buffers, with both chains in one)."""
     wl = wlmod.workload("b1_t4k", variant)
     gtk, otk = _tabs(dq, wl.k)
     gtv, otv = _tabs(dq, wl.v)
@@ -248,13 +270,17 @@ def test_attention_small_workload(dq, variant):
     krec, mq, ms, _ = kv.encode_keys(k, otk)
     vrec, _ = kv.encode_values(v, otv)
     ref = _oracle_attention(wlmod.bf16_bits(q), krec, mq, ms, vrec, otk, otv, [4096], wl.gqa)
-    got, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl, krec, mq, ms, vrec), [4096], wl.q_heads)
+    got, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl, krec, mq, ms, vrec), [4096], wl.q_heads,
+                             t_cap=cap)
     assert st == 0
     assert _rel_err(got, ref) < TOL
 
 
-def test_attention_ragged_lengths(dq):
-    """Lengths 0, 1, 63, 64, 65, 127, 128, 129, 300, 512 in one batch."""
+@pytest.mark.parametrize("cap", [None, 4096])
+def test_attention_ragged_lengths(dq, cap):
+    """Lengths 0, 1, 63, 64, 65, 127, 128, 129, 300, 512 in one batch; in
+    buffers of 512 tokens (split form) and of 4096 (1024-token chunks, both
+    chains in one wavefront)."""
     wl = wlmod.workload("b1_t4k")
     gtk, otk = _tabs(dq, wl.k)
     gtv, otv = _tabs(dq, wl.v)
@@ -265,7 +291,8 @@ def test_attention_ragged_lengths(dq):
     q = wlmod.make_q(wl, 11, batch=B)
     krec, mq, ms, _ = kv.encode_keys(k, otk)
     vrec, _ = kv.encode_values(v, otv)
-    got, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl, krec, mq, ms, vrec), lens, wl.q_heads)
+    got, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl, krec, mq, ms, vrec), lens, wl.q_heads,
+                             t_cap=cap)
     assert st == 0
     assert np.all(got[0] == 0.0)
     ref = _oracle_attention(wlmod.bf16_bits(q)[1:], krec[1:], mq[1:], ms[1:], vrec[1:], otk, otv, lens[1:], wl.gqa)
@@ -292,10 +319,13 @@ def test_attention_gqa_groups(dq, G):
     assert _rel_err(got, ref) < TOL
 
 
-@pytest.mark.parametrize("C,G", [(32, 4), (36, 8), (48, 4), (64, 4), (64, 8)])
-def test_attention_record_lengths(dq, C, G):
+@pytest.mark.parametrize("C,G,cap", [(32, 4, None), (36, 8, None), (48, 4, None), (64, 4, None), (64, 8, None),
+                                     (32, 4, 65536), (48, 4, 65536), (64, 4, 65536)])
+def test_attention_record_lengths(dq, C, G, cap):
     """Equal key/value record lengths of the 2.0 / 2.25 / 3.0 / 4.0 bits-per-
-    element budgets (paper level counts), 4 and 8 query heads per KV head."""
+    element budgets (paper level counts), 4 and 8 query heads per KV head;
+    with 4, also in buffers of 65536 tokens (2048-token chunks, both chains
+    in one wavefront)."""
     coding = wlmod.Coding(levels=wlmod.PAPER_LEVELS[C], record_bytes=C, alpha=1.4)
     gtk, otk = _tabs(dq, coding)
     B, T, Hkv = 2, 1536, 2
@@ -307,12 +337,14 @@ def test_attention_record_lengths(dq, C, G):
     vrec, _ = kv.encode_values(v, otk)
     lens = [1536, 1000]
     ref = _oracle_attention(wlmod.bf16_bits(q), krec, mq, ms, vrec, otk, otk, lens, G)
-    got, st = _gpu_attention(dq, gtk, gtk, q, *_upload_cache(dq, wl, krec, mq, ms, vrec), lens, Hkv * G)
+    got, st = _gpu_attention(dq, gtk, gtk, q, *_upload_cache(dq, wl, krec, mq, ms, vrec), lens, Hkv * G,
+                             t_cap=cap)
     assert st == 0
     assert _rel_err(got, ref) < TOL
 
 
-def test_attention_flags_corrupt_record(dq):
+@pytest.mark.parametrize("cap", [None, JOINT_CAP])
+def test_attention_flags_corrupt_record(dq, cap):
     wl = wlmod.workload("b1_t4k")
     gtk, otk = _tabs(dq, wl.k)
     gtv, otv = _tabs(dq, wl.v)
@@ -322,13 +354,21 @@ def test_attention_flags_corrupt_record(dq):
     krec, mq, ms, _ = kv.encode_keys(k, otk)
     vrec, _ = kv.encode_values(v, otv)
     vrec[0, 3, 17, 5] ^= 0x40
-    _, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl, krec, mq, ms, vrec), [256], wl.q_heads)
+    _, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl, krec, mq, ms, vrec), [256], wl.q_heads,
+                           t_cap=cap)
+    assert st & dq.DQ_STATUS_CORRUPT
+    # the same in a key record
+    vrec[0, 3, 17, 5] ^= 0x40
+    krec1 = krec.copy()
+    krec1[0, 5, 40, 5] ^= 0x40
+    _, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl, krec1, mq, ms, vrec), [256], wl.q_heads,
+                           t_cap=cap)
     assert st & dq.DQ_STATUS_CORRUPT
     # a corrupt record past the sequence length is never read
     krec2 = krec.copy()
     krec2[0, 0, 200, 6] ^= 0x40
-    vrec[0, 3, 17, 5] ^= 0x40
-    _, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl, krec2, mq, ms, vrec), [128], wl.q_heads)
+    _, st = _gpu_attention(dq, gtk, gtv, q, *_upload_cache(dq, wl, krec2, mq, ms, vrec), [128], wl.q_heads,
+                           t_cap=cap)
     assert st == 0
 
 
