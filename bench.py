@@ -484,6 +484,8 @@ def main():
 
     wl = wlmod.workload(a.workload, a.variant, a.bpe) if a.workload == "b1_t128k" else \
         wlmod.workload(a.workload, a.variant)
+    # the committed counter summaries hold for the workload's own precision
+    own_precision = a.precision is None or (a.precision == wl.k.precision and a.precision == wl.v.precision)
     if a.precision is not None:
         from dataclasses import replace
         wl = replace(wl, k=replace(wl.k, precision=a.precision), v=replace(wl.v, precision=a.precision))
@@ -538,10 +540,10 @@ def main():
     n_symbols = 2 * B * T * Hkv * d
     achieved = alg_bytes / (partial_ms * 1e-3) / 1e9
     tokens_s = B * (T + a.residual) / (step_ms * 1e-3)
-    counters = None if a.precision not in (None, 12) else counter_figures(wl.name, a.variant)
+    counters = counter_figures(wl.name, a.variant) if own_precision else None
     traffic = counters[0] if counters else None
     n_streams = 2 * B * T if tok else 2 * B * T * Hkv
-    enc_vps = None if a.precision not in (None, 12) else encode_valu_per_stream(wl, a.variant)
+    enc_vps = encode_valu_per_stream(wl, a.variant) if own_precision else None
 
     rec = {
         "metric": METRIC,
