@@ -49,6 +49,7 @@ constexpr int kMaxLds = 160 * 1024;
 // wavefronts per workgroup at most: 12 with up to 4 query heads per KV head
 // (168 VGPRs), 8 with up to 8 (the accumulators of 64 query heads take 128)
 __host__ __device__ constexpr int tok_waves(int HG) { return HG == 1 ? 12 : 8; }
+constexpr int kTokSplitWaves = 8;          // split tiles: 4 pairs of wavefronts (at most 256 VGPRs)
 constexpr int kTokMaxHeads = 8;           // KV heads per stream (n <= 1024)
 constexpr int kTokMaxChunk = 2048;        // bounds the per-window q . mu table
 constexpr int kRingRow = 4 * kTile;       // bytes per ring row: one dword per lane
@@ -218,6 +219,78 @@ __device__ __forceinline__ void refill2(uint32_t pbk, uint32_t& nck, uint32_t& t
     }
 }
 
+// One chunk for one ring (keys and values decoded by separate wavefronts).
+__device__ __forceinline__ void refill1(uint32_t pb, uint32_t& nc, uint32_t& thr, uint2& nxt, uint32_t ring,
+                                        const uint8_t* rec, uint32_t last) {
+    if (pb > thr) {
+        put_chunk(ring, nc, nxt);
+        ++nc;
+        thr += 64u;
+        nxt = load_chunk(rec, nc, last);
+    }
+}
+
+// The query digits alone (a single chain whose next reads stay in flight).
+template <int N>
+__device__ __forceinline__ void twait_q(v4u& q) {
+    asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(q) : "i"(N));
+}
+
+// The 128 steps of one KV head on a single chain (the wavefront decodes only
+// the keys or only the values of its tile): per step pair the ring dwords
+// and the first table word, then the second table word, each awaited before
+// it is used; the ring is refilled after every block of 8 steps, whose last
+// reads come after the refill's writes.  Keys (KEYS): the query digits of
+// group g are requested in its last step pair and the q . k products formed
+// as the levels appear; values: the packed levels are returned in vlev.
+template <uint32_t LUT, bool KEYS>
+__device__ __forceinline__ void chain_head(TChain& c, uint32_t ring, uint32_t mask8, int p3, uint32_t& nc,
+                                           uint32_t& thr, uint2& nxt, const uint8_t* rec, uint32_t last,
+                                           uint32_t q_lane, v4i (&dk)[3], uint32_t (&vlev)[kGroups]) {
+    v4u qd;
+#pragma unroll
+    for (int grp = 0; grp < kGroups; ++grp) {
+        if ((grp & 1) == 0) tissue_a<LUT>(c, ring, mask8);
+        uint32_t w[4];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const bool more = !((grp & 1) && u == 1);
+            uint32_t sh;
+            twait_a<0>(c);
+            w[2 * u] = tfinish_a(c, p3, sh);
+            tissue_b<LUT>(c, mask8);
+            if (KEYS && u == 1) {
+                qissue(q_lane, (grp * 4) * 16, qd);
+                twait_b<1>(c);
+            } else {
+                twait_b<0>(c);
+            }
+            w[2 * u + 1] = tfinish_b(c, p3, sh);
+            if (more) tissue_a<LUT>(c, ring, mask8);
+        }
+        const uint32_t lev = pack4(w[0], w[1], w[2], w[3]);
+        if constexpr (KEYS) {
+            // the digits were requested before the next pair's two reads
+            if (grp & 1) twait_q<0>(qd);
+            else twait_q<2>(qd);
+            dk[0] = mfma(qd.x, lev, dk[0]);
+            dk[1] = mfma(qd.y, lev, dk[1]);
+            dk[2] = mfma(qd.z, lev, dk[2]);
+        } else {
+            vlev[grp] = lev;
+            asm volatile("" : "+v"(vlev[grp]));
+        }
+        if (grp & 1) {
+            refill1(c.pb, nc, thr, nxt, ring, rec, last);
+            // a second chunk only where a lane is still short (rare)
+            if (__any(c.pb > thr)) refill1(c.pb, nc, thr, nxt, ring, rec, last);
+            // the next block's ring reads come after these writes
+            asm volatile("" ::: "memory");
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 // Accumulators of channel block cb of slice s and slot group hg: one vector
 // acc[s][hg][cb] over the KV heads, for query-head slot 4 hg + l / 16 and
 // channel 64 s + 16 cb + l mod 16 in lane l.  The head loop is not unrolled,
@@ -235,8 +308,10 @@ __device__ __forceinline__ float lane_set(float v, int i, float x, int lane) { r
 // PAGED: records and key means through the block table; a separate
 // instantiation, so that the contiguous kernel carries none of its state.
 // HG: groups of 4 query-head slots per KV head (1: G <= 4, 2: G <= 8).
-template <uint32_t LUTV, bool PAGED, int HG>
-__global__ __launch_bounds__(tok_waves(HG) * kWave) void attn_token_kernel(TokArgs a) {
+// SPLIT: one tile per pair of wavefronts, keys and values decoded by
+// different wavefronts (chunks of at most nw / 2 tiles: small batches).
+template <uint32_t LUTV, bool PAGED, int HG, bool SPLIT = false>
+__global__ __launch_bounds__((SPLIT ? kTokSplitWaves : tok_waves(HG)) * kWave) void attn_token_kernel(TokArgs a) {
     constexpr int GS = 4 * HG;                 // query-head slots per KV head
     extern __shared__ __align__(16) uint8_t smem[];
     const TokLayout& L = a.L;
@@ -351,7 +426,177 @@ __global__ __launch_bounds__(tok_waves(HG) * kWave) void attn_token_kernel(TokAr
     bool corrupt = false;
     const int ntiles = (min(a.chunk, T - start) + kTile - 1) / kTile;
 
-    for (int tile = wave; tile < ntiles; tile += L.nw) {
+    if constexpr (SPLIT) {
+        // One tile per pair of wavefronts.  Per KV head the even wavefront
+        // decodes the keys alone and forms the scores and the softmax weights
+        // (their digits in one of two weight tiles of its region, the slots'
+        // corrections and weight scales beside them), while the odd one
+        // decodes the values alone; after the head's barrier the odd one forms
+        // P . v with its partner's weights, while the even one goes on to the
+        // next head (whose weights go to the other tile).  At the end the even
+        // wavefront hands its softmax statistics to the odd one, which alone
+        // then holds the pair's partial.
+        static_assert(HG == 1 && !PAGED, "split tiles: up to 4 query heads, contiguous records");
+        const int tile = wave >> 1, role = wave & 1;
+        const bool has = tile < ntiles;
+        const uint32_t kreg = (uint32_t)(L.waves + (wave & ~1) * L.wave_stride);
+        // in the key wavefront's value-tile area: weight tile 1, then
+        // [2][GS] corrections, [2][GS] weight scales, and the statistics
+        float* kx = reinterpret_cast<float*>(smem + kreg + L.vtile + kTile * 16);
+        const int t_base = start + tile * kTile;
+        const int t = t_base + lane;
+        const bool valid = t < T;
+        const int64_t row0 = (int64_t)b * a.t_cap + t_base;
+        const uint8_t* rec = role ? a.vrec + row0 * a.v_stride + 8 * lane : a.krec + row0 * a.k_stride + 8 * lane;
+        const uint32_t last = role ? last_v : last_k;
+        const uint32_t ring = role ? ring_v : ring_k;
+        const uint32_t mask8 = role ? mask8v : mask8k;
+        const int p3 = role ? pv3 : pk3;
+        TChain ch;
+        uint32_t nc = 4, thr = 8u * (8u * 4u - 20u) - 1u;
+        uint2 nxt{0u, 0u};
+        float sk = 0.f, ok = 0.f, sv = 0.f, ov = 0.f;
+        if (has) {
+            const uint2 c0 = load_chunk(rec, 0, last), c1 = load_chunk(rec, 1, last), c2 = load_chunk(rec, 2, last),
+                        c3 = load_chunk(rec, 3, last);
+            nxt = load_chunk(rec, 4, last);
+            // the key wavefront also needs the value record's scale and offset
+            const uint32_t vh = role ? c0.x : load_chunk(a.vrec + row0 * a.v_stride + 8 * lane, 0, last_v).x;
+            put_chunk(ring, 0, c0);
+            put_chunk(ring, 1, c1);
+            put_chunk(ring, 2, c2);
+            put_chunk(ring, 3, c3);
+            ch.X = c0.y << 3;
+            ch.pb = 64;                             // payload starts at byte 8
+            sk = half_lo(c0.x);
+            ok = half_hi(c0.x);
+            sv = half_lo(vh);
+            ov = half_hi(vh);
+            asm volatile("" ::: "memory");
+        }
+        const float* qm = qmu + ((t / DQ_MEAN_WINDOW) - w0) * Hq;
+        for (int h = 0; h < Hkv; ++h) {
+            v4i dk[3] = {v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}, v4i{0, 0, 0, 0}};
+            uint32_t vlev[kGroups];
+            const int buf = h & 1;
+            if (has && role == 0) {
+                const uint32_t q_lane = (uint32_t)L.qlimb + (uint32_t)(h * kGroups * GS + (lane & 3)) * 16;
+                chain_head<0, true>(ch, ring, mask8, p3, nc, thr, nxt, rec, last, q_lane, dk, vlev);
+                // scores of the head's query heads and the online softmax
+                float score[4], tmax[4], pw[4], smax[4], corr[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const bool live = r < G;
+                    const int g = live ? h * G + r : 0;
+                    const float dot = combine(dk[0], dk[1], dk[2], r) * qscale[g];
+                    score[r] = (valid && live) ? (sk * dot + ok * qsum[g] + qm[g]) * a.scale_log2 : -INFINITY;
+                    tmax[r] = score[r];
+                }
+                wave_max4_f32(tmax);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int slot = h * GS + r;
+                    const float m_old = lane_get(m_vec, slot);
+                    const float mn = fmaxf(m_old, tmax[r]);
+                    corr[r] = (m_old == -INFINITY || mn == -INFINITY) ? (m_old == mn ? 1.f : 0.f)
+                                                                     : __builtin_amdgcn_exp2f(m_old - mn);
+                    const float p = (score[r] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(score[r] - mn);
+                    const float lt = wave_sum_f32(p);
+                    const float ot = wave_sum_f32(p * ov);
+                    m_vec = lane_set(m_vec, slot, mn, lane);
+                    l_vec = lane_set(l_vec, slot, lane_get(l_vec, slot) * corr[r] + lt, lane);
+                    o_vec = lane_set(o_vec, slot, lane_get(o_vec, slot) * corr[r] + ot, lane);
+                    pw[r] = p * sv;
+                    smax[r] = pw[r];
+                }
+                wave_max4_f32(smax);
+                uint32_t wd[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float inv = smax[r] > 0.f ? 4194304.0f * __builtin_amdgcn_rcpf(smax[r]) : 0.f;
+                    const int pint = min(4194304, (int)rintf(pw[r] * inv));
+                    int d0, d1, d2;
+                    digits3(pint, d0, d1, d2);
+                    wd[r] = ((uint32_t)d0 & 0xFFu) | (((uint32_t)d1 & 0xFFu) << 8) | (((uint32_t)d2 & 0xFFu) << 16);
+                }
+                uint8_t* wt = smem + kreg + (buf ? L.vtile : L.plimb);
+                *reinterpret_cast<uint4*>(wt + lane * 16) = uint4{wd[0], wd[1], wd[2], wd[3]};
+                if (lane == 0) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        kx[buf * GS + r] = corr[r];
+                        kx[2 * GS + buf * GS + r] = smax[r] * (1.0f / 4194304.0f);
+                    }
+                }
+            } else if (has) {
+                chain_head<LUTV, false>(ch, ring, mask8, p3, nc, thr, nxt, rec, last, 0u, dk, vlev);
+            }
+            __syncthreads();   // the weights of the head are in LDS
+            if (has && role == 1) {
+                // ---- P . v over two slices of 64 channels, the partner's weights
+                const uint32_t a_pair = kreg + (uint32_t)(buf ? L.vtile : L.plimb) + trow * 16 + 8 * (lane & 1);
+                uint64_t pa[2];
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) pa[kb] = lds_tr8(a_pair + kb * 32 * 16);
+                const float corr_l = pick4(kx + buf * GS, pslot);
+                const float scale_l = pick4(kx + 2 * GS + buf * GS, pslot);
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) {
+                    if (sl) wave_sync();   // the first slice's value rows are no longer read
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        *reinterpret_cast<uint4*>(vtile + lane * kVRowT + 16 * q) =
+                            uint4{vlev[16 * sl + 4 * q], vlev[16 * sl + 4 * q + 1], vlev[16 * sl + 4 * q + 2],
+                                  vlev[16 * sl + 4 * q + 3]};
+                    wave_sync();
+                    uint64_t vb[kVSlice / 16][2];
+#pragma unroll
+                    for (int cb = 0; cb < kVSlice / 16; ++cb) {
+                        vb[cb][0] = lds_tr8(b_lane + 16 * cb);
+                        vb[cb][1] = lds_tr8(b_lane + 32 * kVRowT + 16 * cb);
+                    }
+                    v4i dv[kVSlice / 16];
+#pragma unroll
+                    for (int cb = 0; cb < kVSlice / 16; ++cb) dv[cb] = mfma16(pa[0], vb[cb][0], v4i{0, 0, 0, 0});
+#pragma unroll
+                    for (int cb = 0; cb < kVSlice / 16; ++cb) dv[cb] = mfma16(pa[1], vb[cb][1], dv[cb]);
+#pragma unroll
+                    for (int cb = 0; cb < kVSlice / 16; ++cb) {
+                        const float pv =
+                            ((float)dv[cb][2] * 65536.0f + (float)dv[cb][1] * 256.0f + (float)dv[cb][0]) * scale_l;
+                        v8f tv = acc[sl][0][cb];
+                        tv[0] = tv[0] * corr_l + pv;
+                        acc[sl][0][cb] = rot1(tv);
+                    }
+                }
+                wave_sync();   // the next head rewrites the value rows
+            }
+        }
+        for (int h = Hkv; h < kTokMaxHeads; ++h)
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+                for (int cb = 0; cb < 4; ++cb) acc[sl][0][cb] = rot1(acc[sl][0][cb]);
+        // every stream ends at x = L having read no byte past its record
+        if (has) corrupt |= valid && ((ch.X >> 3) != kRansL || ch.pb > (role ? endv : endk));
+        // the softmax statistics go to the value wavefront
+        float* kst = kx + 4 * GS;
+        if (has && role == 0) {
+            kst[lane] = m_vec;
+            kst[kWave + lane] = l_vec;
+            kst[2 * kWave + lane] = o_vec;
+        }
+        __syncthreads();
+        if (has && role == 1) {
+            m_vec = kst[lane];
+            l_vec = kst[kWave + lane];
+            o_vec = kst[2 * kWave + lane];
+        } else {
+            m_vec = -INFINITY;
+        }
+    }
+
+    for (int tile = SPLIT ? ntiles : wave; tile < ntiles; tile += L.nw) {
         const int t_base = start + tile * kTile;
         const int t = t_base + lane;               // < t_cap: tiles lie inside the capacity
         const bool valid = t < T;
@@ -683,6 +928,22 @@ namespace {
 template <uint32_t LUTV, int HG>
 int launch_token_kernel(const TokArgs& a, dim3 grid, int nw, hipStream_t stream) {
     const bool paged = a.pg.bt != nullptr;
+    // chunks of at most 4 tiles (small batches, short contexts): keys and
+    // values in different wavefronts (contiguous records, up to 4 query heads,
+    // when LDS holds 8 wavefronts)
+    if constexpr (HG == 1) {
+        TokArgs s = a;
+        s.L = tok_layout(a.tk.p, a.tv.p, a.L.lut_v == a.L.lut_k, a.Hq, a.Hkv, a.chunk, kTokSplitWaves, 1);
+        // (two 4096-entry tables leave no room for 8 wavefronts: both chains in one)
+        if (!paged && 2 * ((a.chunk + kTile - 1) / kTile) <= kTokSplitWaves && s.L.total <= kMaxLds) {
+            const void* fn = reinterpret_cast<const void*>(&attn_token_kernel<LUTV, false, 1, true>);
+            if (int rc = hip_check("hipFuncSetAttribute",
+                                   hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, s.L.total)))
+                return rc;
+            attn_token_kernel<LUTV, false, 1, true><<<grid, kTokSplitWaves * kWave, (size_t)s.L.total, stream>>>(s);
+            return hip_check("attn_token launch", hipGetLastError());
+        }
+    }
     const void* fn = paged ? reinterpret_cast<const void*>(&attn_token_kernel<LUTV, true, HG>)
                            : reinterpret_cast<const void*>(&attn_token_kernel<LUTV, false, HG>);
     if (int rc = hip_check("hipFuncSetAttribute",

@@ -87,8 +87,26 @@ def test_token_encode_bit_exact(dq, p):
     assert np.array_equal(gms.cpu().numpy().view(np.uint16), ms.view(np.uint16))
 
 
-@pytest.mark.parametrize("p", [12, 8])
-def test_token_attention_matches_oracle(dq, p):
+def _pad_tok(grk, gmq, gms, grv, cap):
+    """The same cache in buffers of capacity cap (zero tiles past the old
+    one).  The chunk plan follows the capacity: small capacities give chunks
+    of at most 4 tiles, whose keys and values separate wavefronts decode; a
+    capacity of 64 x 1024 tokens per sequence gives larger chunks, decoded
+    with both chains in one wavefront."""
+    def pad(x, n):
+        shape = list(x.shape)
+        shape[1 if x.dim() == 5 else 2] = n
+        y = torch.zeros(shape, dtype=x.dtype, device=x.device)
+        if x.dim() == 5:
+            y[:, :x.shape[1]] = x
+        else:
+            y[:, :, :x.shape[2]] = x
+        return y
+    return pad(grk, cap // 64), pad(gmq, cap // 128), pad(gms, cap // 128), pad(grv, cap // 64)
+
+
+@pytest.mark.parametrize("p,cap", [(12, None), (8, None), (8, 65536)])
+def test_token_attention_matches_oracle(dq, p, cap):
     H, G, B, T = 8, 4, 4, 384
     gtk, otk = _tabs(dq, 1024, 8, 335, p)
     gtv, otv = _tabs(dq, 1024, 6, 235, p)
@@ -102,12 +120,15 @@ def test_token_attention_matches_oracle(dq, p):
     gmq = torch.from_numpy(mq).to(DEV)
     gms = torch.from_numpy(ms.view(np.int16)).to(DEV)
     seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
-    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, T), dtype=torch.uint8, device=DEV)
+    if cap is not None:
+        grk, gmq, gms, grv = _pad_tok(grk, gmq, gms, grv, cap)
+    tc = cap or T
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, tc), dtype=torch.uint8, device=DEV)
     out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
     status = torch.zeros(1, dtype=torch.int32, device=DEV)
     qd = q.to(DEV)
     dq.dq_decode_attention_token_partial(gtk, gtv, qd, grk, gmq, gms, grv, seq, ws, status=status)
-    dq.dq_decode_attention_merge(B, H * G, H, seq, T, ws, out)
+    dq.dq_decode_attention_merge(B, H * G, H, seq, tc, ws, out)
     torch.cuda.synchronize()
     assert int(status.item()) == 0
     got = out.cpu().numpy().astype(np.float64)
@@ -117,12 +138,16 @@ def test_token_attention_matches_oracle(dq, p):
     assert _rel_err(got[live], ref[live]) < TOL
 
 
-@pytest.mark.parametrize("H,G,Ck,Cv", [(8, 1, 335, 235), (4, 2, 170, 120), (2, 4, 88, 62), (1, 4, 44, 32),
-                                       (8, 8, 335, 235), (4, 6, 170, 120), (2, 8, 88, 62), (1, 5, 44, 32)])
-def test_token_attention_heads_and_groups(dq, H, G, Ck, Cv):
+@pytest.mark.parametrize("H,G,Ck,Cv,cap", [(8, 1, 335, 235, None), (4, 2, 170, 120, None), (2, 4, 88, 62, None),
+                                           (1, 4, 44, 32, None), (8, 8, 335, 235, None), (4, 6, 170, 120, None),
+                                           (2, 8, 88, 62, None), (1, 5, 44, 32, None),
+                                           (8, 1, 335, 235, 131072), (2, 4, 88, 62, 131072)])
+def test_token_attention_heads_and_groups(dq, H, G, Ck, Cv, cap):
     """Streams of 128 H values for H = 8, 4, 2, 1 KV heads and 1 to 8 query
     heads per KV head (above 4: two groups of query-head slots per KV head);
-    the GPU encoder fills the cache."""
+    the GPU encoder fills the cache.  Up to 4 query heads, also in buffers of
+    131072 tokens (chunks of more than 4 tiles: both chains in one
+    wavefront)."""
     B, T = 2, 256
     n = 128 * H
     gtk, otk = _tabs(dq, n, 8, Ck)
@@ -141,19 +166,24 @@ def test_token_attention_heads_and_groups(dq, H, G, Ck, Cv):
     dq.dq_encode_kv_token(gtv, v.to(DEV), 0, T, grv, None, None, status)
     lens = [T, 129]
     seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
-    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, T), dtype=torch.uint8, device=DEV)
-    out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
-    dq.dq_decode_attention_token_partial(gtk, gtv, q.to(DEV), grk, gmq, gms, grv, seq, ws, status=status)
-    dq.dq_decode_attention_merge(B, H * G, H, seq, T, ws, out)
     torch.cuda.synchronize()
-    assert int(status.item()) == 0
     assert np.array_equal(grk.cpu().numpy(), to_tiles(krec, Sk))
     assert np.array_equal(grv.cpu().numpy(), to_tiles(vrec, Sv))
+    if cap is not None:
+        grk, gmq, gms, grv = _pad_tok(grk, gmq, gms, grv, cap)
+    tc = cap or T
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, tc), dtype=torch.uint8, device=DEV)
+    out = torch.empty((B, H * G, 128), dtype=torch.float32, device=DEV)
+    dq.dq_decode_attention_token_partial(gtk, gtv, q.to(DEV), grk, gmq, gms, grv, seq, ws, status=status)
+    dq.dq_decode_attention_merge(B, H * G, H, seq, tc, ws, out)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
     ref = _oracle_attention(wlmod.bf16_bits(q), krec, mq, ms, vrec, otk, otv, lens, H, G)
     assert _rel_err(out.cpu().numpy().astype(np.float64), ref) < TOL
 
 
-def test_token_attention_flags_corrupt_record_and_is_deterministic(dq):
+@pytest.mark.parametrize("cap", [None, 65536])
+def test_token_attention_flags_corrupt_record_and_is_deterministic(dq, cap):
     H, G, B, T = 8, 4, 2, 256
     gtk, otk = _tabs(dq, 1024, 8, 335)
     gtv, otv = _tabs(dq, 1024, 6, 235)
@@ -165,7 +195,10 @@ def test_token_attention_flags_corrupt_record_and_is_deterministic(dq):
     grv = torch.from_numpy(to_tiles(vrec, Sv)).to(DEV)
     gmq = torch.from_numpy(mq).to(DEV)
     gms = torch.from_numpy(ms.view(np.int16)).to(DEV)
-    seq = torch.tensor([T, 200], dtype=torch.int32, device=DEV)
+    if cap is not None:
+        grk, gmq, gms, grv = _pad_tok(grk, gmq, gms, grv, cap)
+    T = cap or T
+    seq = torch.tensor([256, 200], dtype=torch.int32, device=DEV)
     ws = torch.empty(dq.dq_decode_workspace_bytes(B, H * G, H, T), dtype=torch.uint8, device=DEV)
     outs = []
     for _ in range(2):
