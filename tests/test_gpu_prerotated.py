@@ -147,6 +147,12 @@ def test_prerotated_values_with_residual_window(dq):
     ref = attention.attention_with_residual(kv.bf16_to_f64(wlmod.bf16_bits(q)), k_rot, v_rot, seq_l, rk_o, rv_o,
                                             res_l, G, 1 / np.sqrt(D), rotate_v=False)
     assert _rel_err(out.cpu().numpy().astype(np.float64), ref) < TOL
+    # the one-launch window + merge over the same chunk partials
+    out1 = torch.empty_like(out)
+    dq.dq_decode_attention_merge_residual(qd, rk.to(DEV), rv.to(DEV), seq, res, T, cache.workspace, out1)
+    torch.cuda.synchronize()
+    assert _rel_err(out1.cpu().numpy().astype(np.float64), ref) < TOL
+    assert _rel_err(out1.cpu().numpy().astype(np.float64), out.cpu().numpy().astype(np.float64)) < 1e-5
 
 
 def test_prerotated_per_token_streams(dq):

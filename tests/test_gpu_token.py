@@ -313,6 +313,11 @@ def test_token_streams_with_residual_window(dq):
     ref = attention.attention_with_residual(kv.bf16_to_f64(wlmod.bf16_bits(q)), k_rot, v_rot, comp, res_k, res_v,
                                             res, G, 1 / np.sqrt(128))
     assert _rel_err(out.cpu().numpy().astype(np.float64), ref) < TOL
+    # the one-launch window + merge over the same chunk partials
+    out1 = torch.empty_like(out)
+    dq.dq_decode_attention_merge_residual(qd, rk, rv, seq, rl, t_cap, ws, out1)
+    torch.cuda.synchronize()
+    assert _rel_err(out1.cpu().numpy().astype(np.float64), ref) < TOL
 
 
 def _oracle_stream(q_bits, kb, vb, comp, res, otk, otv, H, G):
