@@ -436,7 +436,7 @@ __global__ __launch_bounds__((SPLIT ? kTokSplitWaves : tok_waves(HG)) * kWave) v
         // next head (whose weights go to the other tile).  At the end the even
         // wavefront hands its softmax statistics to the odd one, which alone
         // then holds the pair's partial.
-        static_assert(HG == 1 && !PAGED, "split tiles: up to 4 query heads, contiguous records");
+        static_assert(HG == 1, "split tiles: up to 4 query heads");
         const int tile = wave >> 1, role = wave & 1;
         const bool has = tile < ntiles;
         const uint32_t kreg = (uint32_t)(L.waves + (wave & ~1) * L.wave_stride);
@@ -446,7 +446,9 @@ __global__ __launch_bounds__((SPLIT ? kTokSplitWaves : tok_waves(HG)) * kWave) v
         const int t_base = start + tile * kTile;
         const int t = t_base + lane;
         const bool valid = t < T;
-        const int64_t row0 = (int64_t)b * a.t_cap + t_base;
+        // a tile never straddles a page
+        const int64_t row0 = !has ? 0 : PAGED ? token_row(a.pg, a.t_cap, b, t_base, bad_page)
+                                              : (int64_t)b * a.t_cap + t_base;
         const uint8_t* rec = role ? a.vrec + row0 * a.v_stride + 8 * lane : a.krec + row0 * a.k_stride + 8 * lane;
         const uint32_t last = role ? last_v : last_k;
         const uint32_t ring = role ? ring_v : ring_k;
@@ -929,18 +931,22 @@ template <uint32_t LUTV, int HG>
 int launch_token_kernel(const TokArgs& a, dim3 grid, int nw, hipStream_t stream) {
     const bool paged = a.pg.bt != nullptr;
     // chunks of at most 4 tiles (small batches, short contexts): keys and
-    // values in different wavefronts (contiguous records, up to 4 query heads,
-    // when LDS holds 8 wavefronts)
+    // values in different wavefronts (up to 4 query heads, when LDS holds 8
+    // wavefronts)
     if constexpr (HG == 1) {
         TokArgs s = a;
         s.L = tok_layout(a.tk.p, a.tv.p, a.L.lut_v == a.L.lut_k, a.Hq, a.Hkv, a.chunk, kTokSplitWaves, 1);
         // (two 4096-entry tables leave no room for 8 wavefronts: both chains in one)
-        if (!paged && 2 * ((a.chunk + kTile - 1) / kTile) <= kTokSplitWaves && s.L.total <= kMaxLds) {
-            const void* fn = reinterpret_cast<const void*>(&attn_token_kernel<LUTV, false, 1, true>);
+        if (2 * ((a.chunk + kTile - 1) / kTile) <= kTokSplitWaves && s.L.total <= kMaxLds) {
+            const void* fn = paged ? reinterpret_cast<const void*>(&attn_token_kernel<LUTV, true, 1, true>)
+                                   : reinterpret_cast<const void*>(&attn_token_kernel<LUTV, false, 1, true>);
             if (int rc = hip_check("hipFuncSetAttribute",
                                    hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, s.L.total)))
                 return rc;
-            attn_token_kernel<LUTV, false, 1, true><<<grid, kTokSplitWaves * kWave, (size_t)s.L.total, stream>>>(s);
+            if (paged)
+                attn_token_kernel<LUTV, true, 1, true><<<grid, kTokSplitWaves * kWave, (size_t)s.L.total, stream>>>(s);
+            else
+                attn_token_kernel<LUTV, false, 1, true><<<grid, kTokSplitWaves * kWave, (size_t)s.L.total, stream>>>(s);
             return hip_check("attn_token launch", hipGetLastError());
         }
     }
