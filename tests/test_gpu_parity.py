@@ -320,12 +320,13 @@ def test_attention_gqa_groups(dq, G):
 
 
 @pytest.mark.parametrize("C,G,cap", [(32, 4, None), (36, 8, None), (48, 4, None), (64, 4, None), (64, 8, None),
-                                     (32, 4, 65536), (48, 4, 65536), (64, 4, 65536)])
+                                     (36, 1, None), (36, 2, None),
+                                     (32, 4, 65536), (48, 4, 65536), (64, 4, 65536), (36, 2, 65536)])
 def test_attention_record_lengths(dq, C, G, cap):
     """Equal key/value record lengths of the 2.0 / 2.25 / 3.0 / 4.0 bits-per-
-    element budgets (paper level counts), 4 and 8 query heads per KV head;
-    with 4, also in buffers of 65536 tokens (2048-token chunks, both chains
-    in one wavefront)."""
+    element budgets (paper level counts), 1, 2, 4 and 8 query heads per KV
+    head; up to 4 also in buffers of 65536 tokens (2048-token chunks, both
+    chains in one wavefront)."""
     coding = wlmod.Coding(levels=wlmod.PAPER_LEVELS[C], record_bytes=C, alpha=1.4)
     gtk, otk = _tabs(dq, coding)
     B, T, Hkv = 2, 1536, 2
