@@ -1024,9 +1024,12 @@ __global__ __launch_bounds__(kWave) void attn_merge_kernel(const int32_t* __rest
                                                            const float* __restrict__ ws_l,
                                                            const float* __restrict__ ws_acc,
                                                            const int32_t* __restrict__ seq_lens,
-                                                           int Hq, int t_cap, float* __restrict__ out) {
+                                                           int Hq, int t_cap, int nc_max, float* __restrict__ out) {
     const int hq = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
-    const int chunk = ws_hdr[0], NC = ws_hdr[1], residual = min(max(ws_hdr[2], 0), kResSlots);
+    // the header's chunk count is bounded by the workspace's capacity, so a
+    // workspace no partial call wrote cannot send the reads past it
+    const int chunk = max(ws_hdr[0], 1), NC = min(max(ws_hdr[1], 1), nc_max);
+    const int residual = min(max(ws_hdr[2], 0), kResSlots);
     const int T = max(0, min(seq_lens[b], t_cap));
     float* dst = out + ((int64_t)b * Hq + hq) * kD;
     // the chunks that hold tokens, then the residual window's slots (a part
@@ -1122,6 +1125,7 @@ struct ResArgs {
     const int32_t* res_lens;     // residual tokens per sequence
     int r_cap, Hq, Hkv, G;
     float scale_log2;            // softmax_scale * log2(e): logits of raw keys
+    int nc_max;                  // chunk slots per query head the workspace holds
     int32_t* ws_hdr;
     float* ws_m;
     float* ws_l;
@@ -1260,7 +1264,7 @@ __global__ __launch_bounds__(kResWaves * kWave) void attn_residual_kernel(ResArg
     __shared__ float x_m[kMaxGroup], x_l[kMaxGroup];
     const int part = blockIdx.x, h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
     const int lane = tid & (kWave - 1), wave = tid / kWave;
-    const int G = a.G, NC = a.ws_hdr[1], rotate = a.ws_hdr[3];
+    const int G = a.G, NC = min(max(a.ws_hdr[1], 1), a.nc_max), rotate = a.ws_hdr[3];
     if ((part | h | b) == 0 && tid == 0) a.ws_hdr[2] = kResSlots;
     const int r = max(0, min(a.res_lens[b], a.r_cap));
     const int ps = (r + kResSlots - 1) / kResSlots;
@@ -1369,7 +1373,8 @@ __global__ __launch_bounds__(kMrWaves * kWave) void attn_merge_residual_kernel(M
     __shared__ float r_m[kMrWaves][kMaxGroup], r_l[kMrWaves][kMaxGroup];
     const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
     const int lane = tid & (kWave - 1), wave = tid / kWave;
-    const int G = a.G, chunk = a.ws_hdr[0], NC = a.ws_hdr[1], rotate = a.ws_hdr[3];
+    const int G = a.G, chunk = max(a.ws_hdr[0], 1), NC = min(max(a.ws_hdr[1], 1), a.nc_max);
+    const int rotate = a.ws_hdr[3];
 
     // ---- the chunk partials of query head h G + wave, requested first
     const int T = max(0, min(a.seq_lens[b], ma.t_cap));
@@ -1771,7 +1776,8 @@ int launch_attention_merge(int32_t B, int32_t Hq, int32_t Hkv, const int32_t* se
     const float* acc = reinterpret_cast<const float*>(static_cast<const uint8_t*>(ws) + kWsHeader);
     const float* m = acc + slots * kD;
     const float* l = m + slots;
-    attn_merge_kernel<<<dim3(Hq, B), kWave, 0, stream>>>(hdr, m, l, acc, seq_lens, Hq, t_cap, out);
+    const int nc_max = (int)(slots / ((int64_t)B * Hq)) - kResSlots;
+    attn_merge_kernel<<<dim3(Hq, B), kWave, 0, stream>>>(hdr, m, l, acc, seq_lens, Hq, t_cap, nc_max, out);
     return hip_check("attn_merge launch", hipGetLastError());
 }
 
@@ -1791,6 +1797,7 @@ int launch_attention_residual(const uint16_t* q, int32_t B, int32_t Hq, int32_t 
     a.Hkv = Hkv;
     a.G = Hq / Hkv;
     a.scale_log2 = scale * 1.4426950408889634f;
+    a.nc_max = (int)(slots / ((int64_t)B * Hq)) - kResSlots;
     a.ws_hdr = static_cast<int32_t*>(ws);
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
     a.ws_m = a.ws_acc + slots * kD;
@@ -1816,6 +1823,7 @@ int launch_attention_merge_residual(const uint16_t* q, int32_t B, int32_t Hq, in
     a.Hkv = Hkv;
     a.G = Hq / Hkv;
     a.scale_log2 = scale * 1.4426950408889634f;
+    a.nc_max = (int)(slots / ((int64_t)B * Hq)) - kResSlots;
     a.ws_hdr = static_cast<int32_t*>(ws);
     a.ws_acc = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kWsHeader);
     a.ws_m = a.ws_acc + slots * kD;

@@ -108,6 +108,31 @@ def test_residual_calls_reject_bad_arguments(dq, bufs):
     torch.cuda.synchronize()
 
 
+def test_merge_reads_inside_a_workspace_no_partial_wrote(dq):
+    """A workspace whose header no partial call wrote (every byte 0x7F: a
+    chunk count and size of 0x7F7F7F7F): the merge, the window and the
+    one-launch window + merge bound the chunk count by the workspace's own
+    capacity, so they read inside it and return."""
+    lib = dq._lib._lib
+    B, Hq, Hkv, t_cap, r_cap = 2, 8, 2, 512, 128
+    need = dq.dq_decode_workspace_bytes(B, Hq, Hkv, t_cap)
+    ws = torch.full((need,), 0x7F, dtype=torch.uint8, device="cuda")
+    seq = torch.tensor([500, 37], dtype=torch.int32, device="cuda")
+    rl = torch.tensor([100, 3], dtype=torch.int32, device="cuda")
+    q = torch.zeros((B, Hq, 128), dtype=torch.bfloat16, device="cuda")
+    rk = torch.zeros((B, Hkv, r_cap, 128), dtype=torch.bfloat16, device="cuda")
+    out = torch.zeros((B, Hq, 128), dtype=torch.float32, device="cuda")
+    assert lib.dq_decode_attention_merge(B, Hq, Hkv, _p(seq), t_cap, _p(ws), need, _p(out), None) == dq.DQ_OK
+    torch.cuda.synchronize()
+    assert lib.dq_decode_attention_merge_residual(_p(q), B, Hq, Hkv, _p(rk), _p(rk), _p(seq), _p(rl), r_cap, t_cap,
+                                                  ctypes.c_float(0.088), _p(ws), need, _p(out), None) == dq.DQ_OK
+    torch.cuda.synchronize()
+    assert lib.dq_decode_attention_residual(_p(q), B, Hq, Hkv, _p(rk), _p(rk), _p(seq), _p(rl), r_cap, t_cap,
+                                            ctypes.c_float(0.088), _p(ws), need, None) == dq.DQ_OK
+    assert lib.dq_decode_attention_merge(B, Hq, Hkv, _p(seq), t_cap, _p(ws), need, _p(out), None) == dq.DQ_OK
+    torch.cuda.synchronize()
+
+
 def test_encode_rejects_bad_ranges(dq, bufs):
     t = dq.Tables(128, 6, 12, 36, 1.4)
     lib = dq._lib._lib
