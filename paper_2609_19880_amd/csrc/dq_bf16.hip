@@ -264,7 +264,7 @@ __global__ __launch_bounds__(kThreads) void bf16_partial_kernel(B16Args a) {
 
 // Chunks: about six workgroups per CU but at most 64 chunks per sequence
 // (the merge reads up to 64 partials in one pass, one per lane), in whole
-// workgroup passes of 128 tokens, at least kMinChunk and at most kMaxChunkB
+// workgroup passes of 128 tokens, at least kMinChunkHead and at most kMaxChunkB
 // tokens.
 int launch_bf16_partial(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, const uint16_t* k,
                         const uint16_t* v, const int32_t* seq_lens, int32_t t_cap, float scale, void* ws,
@@ -273,7 +273,7 @@ int launch_bf16_partial(const uint16_t* q, int32_t B, int32_t Hq, int32_t Hkv, c
     int64_t nc = std::max<int64_t>((t_cap + kMaxChunkB - 1) / kMaxChunkB,
                                    std::min<int64_t>((6 * cu_count() + pairs - 1) / pairs, 64));
     int chunk = (int)((t_cap + nc - 1) / nc);
-    chunk = std::max(((chunk + kPass - 1) / kPass) * kPass, kMinChunk);
+    chunk = std::max(((chunk + kPass - 1) / kPass) * kPass, kMinChunkHead);
     B16Args a;
     a.q = q;
     a.k = k;

@@ -1594,18 +1594,20 @@ struct ChunkPlan {
 
 // Few, large chunks: one workgroup fits per CU (LDS), so the grid is sized to
 // about one workgroup per CU (more when the batch has more (sequence, KV head)
-// pairs than there are CUs), with chunks of kMinChunk..kMaxChunk tokens in
+// pairs than there are CUs), with chunks of kMinChunkHead..kMaxChunk tokens in
 // whole 64-token tiles.  Every workgroup then runs its waves over many tiles
 // and the grid ends in whole rounds of the CUs.  At small batches and short
 // contexts the lower bound sets the grid: a 256-token chunk is four tiles,
-// one wavefront per SIMD, so that no two decode chains share issue slots.
+// whose keys and values eight wavefronts decode apart (two per SIMD);
+// smaller chunks would double the partials the merge reads for no shorter
+// chain.
 ChunkPlan chunk_plan(int B, int Hq, int Hkv, int t_cap, int num_cus) {
     ChunkPlan p;
     const int64_t pairs = (int64_t)B * Hkv;
     int64_t nc = std::max<int64_t>((t_cap + kMaxChunk - 1) / kMaxChunk, (num_cus + pairs - 1) / pairs);
     int chunk = (int)((t_cap + nc - 1) / nc);
     chunk = ((chunk + kTile - 1) / kTile) * kTile;
-    chunk = std::max(chunk, kMinChunk);
+    chunk = std::max(chunk, kMinChunkHead);
     chunk = std::min(chunk, kMaxChunk);
     p.chunk = chunk;
     p.nchunks = (t_cap + chunk - 1) / chunk;

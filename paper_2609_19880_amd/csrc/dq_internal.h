@@ -16,11 +16,13 @@ constexpr int kBracketUnits = 40 * kLambdaSteps;  // hi - lo = 40 octaves
 
 // Split-K attention workspace: a 256-byte header (chunk size, chunk count NC,
 // residual slots written), then fp32 acc [B][Hq][NC + kResSlots][d], m and l
-// [B][Hq][NC + kResSlots], sized for chunks of at least kMinChunk tokens.
-// Slots NC .. NC + kResSlots - 1 of each (sequence, query head) hold the
-// residual window's partials, one per workgroup of its split.
+// [B][Hq][NC + kResSlots], sized for chunks of at least kMinChunk tokens
+// (per-token streams; the per-head and BF16 kernels take chunks of at least
+// kMinChunkHead).  Slots NC .. NC + kResSlots - 1 of each (sequence, query
+// head) hold the residual window's partials, one per workgroup of its split.
 constexpr int kWsHeader = 256;
-constexpr int kMinChunk = 256;
+constexpr int kMinChunk = 128;
+constexpr int kMinChunkHead = 256;
 constexpr int kResSlots = 4;
 inline int64_t max_chunks(int t_cap) { return (t_cap + kMinChunk - 1) / kMinChunk; }
 inline int64_t ws_slots(int B, int Hq, int t_cap) { return (int64_t)B * Hq * (max_chunks(t_cap) + kResSlots); }

@@ -917,6 +917,10 @@ TokLayout tok_layout(int pk, int pv, bool shared_lut, int Hq, int Hkv, int chunk
 
 }  // namespace
 
+// At least one workgroup per CU where the batch allows it, chunks of at most
+// kTokMaxChunk tokens and at least kMinChunk (two tiles: at batch 1 a
+// token's 1024-step chains bound the time, so more, smaller workgroups
+// shorten it, one decoding wavefront per SIMD).
 int32_t token_chunk(int32_t B, int32_t t_cap) {
     const int64_t nc = std::max<int64_t>((t_cap + kTokMaxChunk - 1) / kTokMaxChunk, (cu_count() + B - 1) / B);
     int chunk = (int)((t_cap + nc - 1) / nc);
