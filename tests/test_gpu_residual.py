@@ -302,3 +302,53 @@ def test_ring_overflow_and_commit_flags(dq):
     torch.cuda.synchronize()
     assert int(status.item()) & dq.DQ_STATUS_WINDOW          # the second ring holds only 4
     assert seq.tolist() == [128, 0] and rl.tolist() == [r_cap - 128, 4]
+
+
+@pytest.mark.parametrize("G", [1, 3, 4, 8])
+def test_fused_merge_many_chunks(dq, G):
+    """The one-launch window + merge over many chunk partials: 128 and 78
+    chunks of 256 tokens, so that a query head's rows arrive in many batches
+    after the first and its maxima outnumber the lanes of a wavefront; 1, 3, 4
+    and 8 query heads per KV head (at G < 8 some wavefronts only compute the
+    window).  Checked against the two-call form (residual kernel, then the
+    plain merge)."""
+    wl = wlmod.workload("b1_t4k")
+    gtk = dq.Tables(128, wl.k.levels, wl.k.precision, wl.k.record_bytes, wl.k.alpha)
+    gtv = dq.Tables(128, wl.v.levels, wl.v.precision, wl.v.record_bytes, wl.v.alpha)
+    B, Hkv, t_cap, r_cap = 2, 1, 32768, 256
+    comp = [32768, 19968]
+    res = [128, 37]
+    T = max(c + r for c, r in zip(comp, res))
+    w2 = wlmod.Workload("many_chunks", B, T, Hkv * G, Hkv, G, wl.k, wl.v)
+    k, v, q = wlmod.make_k(w2, 70 + G), wlmod.make_v(w2, 70 + G), wlmod.make_q(w2, 70 + G)
+    records_k = torch.zeros((B, Hkv, t_cap, wl.k.record_bytes), dtype=torch.uint8, device=DEV)
+    records_v = torch.zeros((B, Hkv, t_cap, wl.v.record_bytes), dtype=torch.uint8, device=DEV)
+    mean_q = torch.zeros((B, Hkv, t_cap // 128, 128), dtype=torch.int8, device=DEV)
+    mean_s = torch.zeros((B, Hkv, t_cap // 128), dtype=torch.int16, device=DEV)
+    res_k = torch.zeros((B, Hkv, r_cap, 128), dtype=torch.bfloat16, device=DEV)
+    res_v = torch.zeros_like(res_k)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    kd, vd = k.to(DEV), v.to(DEV)
+    for b in range(B):
+        n = comp[b]
+        dq.dq_encode_kv(gtk, kd[b:b + 1, :n], 0, t_cap, records_k[b:b + 1], mean_q[b:b + 1], mean_s[b:b + 1],
+                        status)
+        dq.dq_encode_kv(gtv, vd[b:b + 1, :n], 0, t_cap, records_v[b:b + 1], None, None, status)
+        slots = [(n + i) % r_cap for i in range(res[b])]
+        res_k[b, :, slots] = kd[b, n:n + res[b]].transpose(0, 1)
+        res_v[b, :, slots] = vd[b, n:n + res[b]].transpose(0, 1)
+    seq = torch.tensor(comp, dtype=torch.int32, device=DEV)
+    rl = torch.tensor(res, dtype=torch.int32, device=DEV)
+    ws = torch.empty(dq.dq_decode_workspace_bytes(B, Hkv * G, Hkv, t_cap), dtype=torch.uint8, device=DEV)
+    out = torch.empty((B, Hkv * G, 128), dtype=torch.float32, device=DEV)
+    qd = q.to(DEV)
+    dq.dq_decode_attention_partial(gtk, gtv, qd, records_k, mean_q, mean_s, records_v, seq, ws, status=status)
+    dq.dq_decode_attention_residual(qd, res_k, res_v, seq, rl, t_cap, ws)
+    dq.dq_decode_attention_merge(B, Hkv * G, Hkv, seq, t_cap, ws, out)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    hdr = ws[:8].view(torch.int32).cpu().tolist()
+    assert hdr[1] >= 64              # 128 chunks of 256 tokens on 256 CUs
+    got = out.cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(got))
+    _fused(dq, qd, res_k, res_v, seq, rl, t_cap, ws, got)
